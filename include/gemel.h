@@ -1,0 +1,266 @@
+/*
+ * gemel.h - C ABI of libgemel: batched inference of a workload of vision
+ * CNNs whose merged layers keep one weight copy in GPU memory.
+ *
+ * Model merging (GEMEL, arXiv 2201.07705, Section 4): layers that are
+ * architecturally identical across models (same type and same type-specific
+ * properties; Section 4.1) may be shared so that a single copy of the
+ * layer's definition and weights serves every model that includes it.
+ * Layer outputs are never shared, because models may watch different
+ * videos. Merging therefore changes where weights live, not what each model
+ * computes: a model's outputs after merging equal that model evaluated
+ * alone with the shared layers holding the group source's weights.
+ *
+ * Execution scheme of this library: every merged conv/FC layer runs ONCE
+ * over the concatenated frame batches of all active models that share it
+ * (one weight read, one launch); unmerged layers run per model. With a
+ * weight budget, the weights that do not fit stay in pinned host memory and
+ * are copied in on a side stream for every inference round (the paper's
+ * edge boxes swap models over PCIe, Section 3.2; Section 5.4 and Appendix
+ * A.4 load only layers not already resident and never evict shared ones).
+ *
+ * General conventions
+ *  - Every call returns a gemel_status: 0 on success, a negative code on
+ *    failure. No C++ exception and no abort crosses the ABI.
+ *  - Host-side validation (pointers, shapes, merge rules) happens before any
+ *    HIP call, so invalid arguments never touch the device; on any error the
+ *    context is left exactly as it was before the call.
+ *  - A context is bound to one device and is not thread-safe: calls on one
+ *    context must be serialised by the caller. Separate contexts are
+ *    independent.
+ *  - gemel_last_error(ctx) returns a NUL-terminated description of the last
+ *    failure on ctx (or, with ctx == NULL, of the last gemel_create failure
+ *    on this thread). The string is owned by the library.
+ */
+#ifndef GEMEL_H
+#define GEMEL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct gemel_ctx gemel_ctx;
+typedef int32_t gemel_status;
+
+enum {
+    GEMEL_OK = 0,
+    GEMEL_EINVAL = -1,        /* bad pointer, enum, id or count            */
+    GEMEL_ENOMEM = -2,        /* host or device allocation failed          */
+    GEMEL_ESHAPE = -3,        /* inconsistent layer or tensor shapes       */
+    GEMEL_ENOTMERGEABLE = -4, /* group members not architecturally equal   */
+    GEMEL_EBUDGET = -5,       /* weight budget too small to run at all     */
+    GEMEL_EDEVICE = -6,       /* HIP runtime / device failure              */
+    GEMEL_ESTATE = -7         /* call not valid in the context's state     */
+};
+
+/* Arithmetic/storage type of a context. */
+enum { GEMEL_F32 = 0, GEMEL_BF16 = 1 };
+
+/* Layer types. */
+enum {
+    GEMEL_OP_CONV = 0,       /* 2-D convolution (+ optional BN, act, residual) */
+    GEMEL_OP_FC = 1,         /* fully connected on the NCHW-flattened input    */
+    GEMEL_OP_MAXPOOL = 2,    /* kh x kw window, stride, pad (pad = -inf)       */
+    GEMEL_OP_AVGPOOL = 3,    /* global average pool over H x W                 */
+    GEMEL_OP_UPSAMPLE2X = 4, /* nearest-neighbour 2x                           */
+    GEMEL_OP_CONCAT = 5      /* channels [src0, src1]; both multiples of 8     */
+};
+
+enum { GEMEL_ACT_NONE = 0, GEMEL_ACT_RELU = 1, GEMEL_ACT_LEAKY = 2 };
+
+/* Where a residual is added relative to the activation. */
+enum {
+    GEMEL_RES_ADD_THEN_ACT = 0, /* y = act(z + r)   (ResNet blocks)  */
+    GEMEL_RES_ACT_THEN_ADD = 1  /* y = act(z) + r   (Darknet blocks) */
+};
+
+/*
+ * One layer of a model, in topological order (every producer index is
+ * smaller than the layer's own index).
+ *
+ *  op           GEMEL_OP_*
+ *  src0, src1   producer layer index; -1 = the model input. src1 is used by
+ *               CONCAT only (must be -1 otherwise).
+ *  cin, cout    CONV: input/output channels. FC: flattened input features
+ *               (C*H*W of the producer) and output features. Pools,
+ *               upsample, concat: cin = producer channels, cout = output
+ *               channels.
+ *  kh, kw, stride, pad   CONV and MAXPOOL window (kh == kw).
+ *  act, act_slope        activation applied by CONV/FC (slope for LEAKY).
+ *  res_src, res_mode     CONV only: layer whose output (same shape as this
+ *               layer's) is added, -1 = none; GEMEL_RES_*.
+ *  is_output    nonzero: the layer's output is returned by gemel_infer.
+ *  weight       CONV: float32 [cout][cin][kh][kw] (PyTorch OIHW). FC:
+ *               float32 [cout][cin], cin in the producer's NCHW flatten
+ *               order. NULL for other ops.
+ *  bias         float32 [cout] or NULL.
+ *  bn_*         batch norm applied to the conv output: float32 [cout] each,
+ *               y = gamma * (z - mean) / sqrt(var + eps) + beta. All four
+ *               NULL = no batch norm. CONV only.
+ *
+ * The library copies every array during gemel_register_model; the caller
+ * may free them when the call returns.
+ */
+typedef struct gemel_layer_desc {
+    int32_t op;
+    int32_t src0, src1;
+    int32_t cin, cout;
+    int32_t kh, kw, stride, pad;
+    int32_t act;
+    float act_slope;
+    int32_t res_src, res_mode;
+    int32_t is_output;
+    const float *weight;
+    const float *bias;
+    const float *bn_gamma, *bn_beta, *bn_mean, *bn_var;
+    float bn_eps;
+} gemel_layer_desc;
+
+/* One appearance of a layer: (model id, layer index inside that model). */
+typedef struct gemel_member {
+    int32_t model_id;
+    int32_t layer;
+} gemel_member;
+
+/*
+ * A group (Section 5.3): all appearances of one layer that share a single
+ * copy. members[0] is the weight source; every other member uses its
+ * weights, bias and batch norm. The paper seeds a merged group from one
+ * member's weights; taking the first member makes the choice deterministic.
+ */
+typedef struct gemel_group {
+    int32_t n_members;
+    const gemel_member *members;
+} gemel_group;
+
+/*
+ * Create a context on HIP device `device`.
+ *  dtype              GEMEL_F32 (float32 everywhere) or GEMEL_BF16 (bf16
+ *                     weights and activations, float32 accumulation and
+ *                     epilogue, float32 outputs).
+ *  hbm_weight_budget  bytes of device memory that weights may occupy
+ *                     (resident copies plus the swap staging buffers);
+ *                     0 = unlimited. Weights beyond the budget stay in
+ *                     pinned host memory and are streamed in every round.
+ * No device memory is touched until the first gemel_infer.
+ * Errors: EINVAL (null out, bad dtype, negative device), ENOMEM.
+ */
+gemel_status gemel_create(gemel_ctx **out, int32_t device, int32_t dtype,
+                          uint64_t hbm_weight_budget);
+
+/*
+ * Register a model (a DNN supplied with a query, Section 5.1) and copy its
+ * weights into the library's host master copy, converted to the kernel
+ * layout (bf16 round-to-nearest-even for GEMEL_BF16; conv KRSC; FC columns
+ * permuted to the internal NHWC flatten order; batch norm and bias folded
+ * into a float32 per-channel scale/shift, never into the weights).
+ *  in_c, in_h, in_w   frame shape; frames are float32 NCHW.
+ *  *out_model_id      receives the model id (0, 1, 2, ... in call order).
+ * Errors: EINVAL (null pointers, bad enums, bad producer index), ESHAPE
+ * (channels or sizes inconsistent with the producers), ESTATE.
+ */
+gemel_status gemel_register_model(gemel_ctx *ctx,
+                                  const gemel_layer_desc *layers,
+                                  int32_t n_layers, int32_t in_c,
+                                  int32_t in_h, int32_t in_w,
+                                  int32_t *out_model_id);
+
+/*
+ * Install a sharing map: after the call every group's members use one copy
+ * of members[0]'s parameters. Replaces the previous map entirely (calling
+ * it again with the same groups is a no-op; n_groups == 0 unmerges all).
+ * Members must be architecturally identical to members[0] (Section 4.1:
+ * same type and type-specific properties: op, cin, cout, kh, kw, stride,
+ * pad, bias and batch-norm presence; weights may differ), appear in at most
+ * one group, and name registered models and valid layers.
+ * Errors: EINVAL, ENOTMERGEABLE (no state change on any error).
+ */
+gemel_status gemel_merge(gemel_ctx *ctx, const gemel_group *groups,
+                         int32_t n_groups);
+
+/*
+ * Run one inference round over `n_models` registered models.
+ *  model_ids   distinct model ids; their order does not change any output.
+ *  frames      per model: device pointer to float32 NCHW
+ *              [n_frames[i]][in_c][in_h][in_w].
+ *  n_frames    per model frame count (>= 0; 0 skips the model).
+ *  outputs     flattened: for each model in model_ids order, one device
+ *              pointer per is_output layer in layer order, caller-allocated
+ *              float32. Conv outputs are NCHW [n][cout][H][W]; FC outputs
+ *              [n][cout] (gemel_output_shape gives the dims).
+ *  hip_stream  hipStream_t to enqueue on (NULL = the null stream).
+ * Stream-ordered: the call enqueues work and returns; all buffers must stay
+ * valid until the stream passes this point. Argument errors are returned
+ * synchronously without enqueuing anything; an asynchronous device fault
+ * surfaces as EDEVICE on this or a later call.
+ * Errors: EINVAL, ESHAPE, ENOMEM, EBUDGET, EDEVICE.
+ */
+gemel_status gemel_infer(gemel_ctx *ctx, const int32_t *model_ids,
+                         int32_t n_models, const void *const *frames,
+                         const int32_t *n_frames, void *const *outputs,
+                         void *hip_stream);
+
+/* Number of output layers of a model. Errors: EINVAL. */
+gemel_status gemel_model_outputs(gemel_ctx *ctx, int32_t model_id,
+                                 int32_t *n_outputs);
+
+/*
+ * Shape of output `output_idx` of a model for `n_frames` frames: dims =
+ * {n, C, H, W} for conv-type outputs, {n, C, 1, 1} for FC outputs.
+ * Errors: EINVAL.
+ */
+gemel_status gemel_output_shape(gemel_ctx *ctx, int32_t model_id,
+                                int32_t output_idx, int32_t n_frames,
+                                int64_t dims[4]);
+
+/* Keys of gemel_query. Byte counts are device bytes of stored parameters
+ * (weights in kernel layout plus float32 scale/shift). */
+enum {
+    GEMEL_Q_UNMERGED_BYTES = 0, /* all registered layers, nothing shared  */
+    GEMEL_Q_MERGED_BYTES = 1,   /* one copy per merged group              */
+    GEMEL_Q_RESIDENT_BYTES = 2, /* weights kept resident in device memory */
+    GEMEL_Q_PEAK_BYTES = 3,     /* high-water mark: resident + staging    */
+    GEMEL_Q_STREAMED_BYTES = 4, /* host->device weight bytes per round    */
+    GEMEL_Q_ACTIVATION_BYTES = 5, /* activation arena of the last plan    */
+    GEMEL_Q_LAUNCHES = 6,       /* kernel launches per round, last plan   */
+    GEMEL_Q_N_MODELS = 7,       /* registered models                      */
+    GEMEL_Q_GRAPH_REPLAYS = 8   /* rounds served by a replayed HIP graph  */
+};
+
+/* Read a counter. Errors: EINVAL (unknown key, null val). */
+gemel_status gemel_query(gemel_ctx *ctx, int32_t key, int64_t *val);
+
+/* Tunables and test hooks of gemel_set_option. */
+enum {
+    GEMEL_OPT_USE_GRAPH = 0,     /* 1 (default): replay a captured HIP graph
+                                    when frames/outputs pointers repeat    */
+    GEMEL_OPT_SWAP_SLOT_BYTES = 1, /* staging slot size (default 32 MiB)   */
+    GEMEL_OPT_SWAP_SLOTS = 2,    /* number of staging slots (default 3)    */
+    GEMEL_OPT_FAIL_COPY_AT = 3,  /* test hook: the n-th (1-based) swap copy
+                                    issued from now fails; 0 = off         */
+    GEMEL_OPT_SPLIT_MERGED = 4,  /* 1: run merged layers per model (one
+                                    launch per member, same single weight
+                                    copy); 0 (default): one launch         */
+    GEMEL_OPT_WEIGHT_BUDGET = 5  /* replace the hbm_weight_budget given to
+                                    gemel_create (bytes, 0 = unlimited)    */
+};
+
+/* Set an option; takes effect at the next gemel_infer. Errors: EINVAL. */
+gemel_status gemel_set_option(gemel_ctx *ctx, int32_t key, int64_t value);
+
+/* Description of the last error (see general conventions). */
+const char *gemel_last_error(const gemel_ctx *ctx);
+
+/* Synchronise the device, free all device and host resources. ctx may be
+ * NULL. Errors: EDEVICE if a pending device fault is found (resources are
+ * released regardless). */
+gemel_status gemel_destroy(gemel_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GEMEL_H */

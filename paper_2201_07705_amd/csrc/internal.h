@@ -1,0 +1,157 @@
+// Internal state of a gemel context: registry of models and parameter
+// blobs, device placement of the weights, and cached execution plans.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <map>
+#include <memory>
+#include <string>
+#include <vector>
+
+#include "gemel.h"
+#include "kargs.h"
+#include "kernels.h"
+
+namespace gemel {
+
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// One stored copy of a conv/FC layer's parameters in kernel layout:
+// weights [rows][k] (rows = physical output channels, k = kh*kw*cin_p for a
+// conv, producer NHWC-flat size for an FC) and fp32 scale/shift [rows]
+// holding bias and batch norm folded together.
+struct Blob {
+    int64_t rows = 0, k = 0;
+    size_t elem = 2;                 // bytes per weight element
+    std::vector<uint8_t> w;          // host master copy
+    std::vector<float> scale, shift;
+    size_t w_bytes() const { return w.size(); }
+    size_t aff_bytes() const { return 2 * scale.size() * sizeof(float); }
+    size_t bytes() const { return w_bytes() + aff_bytes(); }
+    // placement (valid while the context's weights are materialised)
+    void *w_dev = nullptr;           // resident weights, null if streamed
+    float *aff_dev = nullptr;        // scale[rows] then shift[rows], resident
+    uint8_t *w_pinned = nullptr;     // pinned host copy of a streamed blob
+    int users = 0;                   // registered layers using this copy
+};
+
+struct Layer {
+    int op = 0, src0 = -1, src1 = -1, cin = 0, cout = 0, kh = 1, kw = 1;
+    int stride = 1, pad = 0, act = 0, res = -1, res_mode = 0, is_output = 0;
+    float slope = 0.f;
+    bool has_bias = false, has_bn = false;
+    int in_c = 0, in_h = 0, in_w = 0, in_cp = 0;  // src0 tensor
+    int src1_cp = 0;                              // concat: src1 channels
+    int out_c = 0, out_h = 0, out_w = 0, out_cp = 0;
+    std::shared_ptr<Blob> own;   // this layer's own parameters
+    std::shared_ptr<Blob> eff;   // parameters in use (own or a group source's)
+    int group = -1;              // index of the merge group containing it
+    int out_index = -1;          // position among the model's outputs
+    int consumers = 0;           // layers that read this layer's output
+};
+
+struct Model {
+    int id = 0;
+    int in_c = 0, in_h = 0, in_w = 0, in_cp = 0;
+    std::vector<Layer> layers;
+    std::vector<int> outputs;    // layer indices of the outputs
+};
+
+// A caller pointer patched into an argument block at every call.
+struct Patch {
+    enum Kind { FRAMES = 0, OUTPUT = 1 } kind;
+    int slot;        // model slot within the plan
+    int out_idx;     // output number (OUTPUT)
+    int seg;         // segment index inside the argument block
+};
+
+enum LaunchType {
+    L_PACK, L_CONV_BF16, L_CONV_F32, L_CONV_REDUCE, L_FC_BF16, L_FC_F32, L_FC_REDUCE,
+    L_MAXPOOL, L_AVGPOOL, L_UPSAMPLE, L_CONCAT, L_EXPORT
+};
+
+struct Launch {
+    LaunchType type;
+    int tile = 0;
+    bool bf16 = true;
+    ConvArgs conv{};
+    ReduceArgs red{};
+    FcArgs fc{};
+    EwArgs ew{};
+    std::vector<Patch> patches;
+    // weight streaming: >= 0 when the weights come from a staging slot
+    int chunk = -1;
+};
+
+// A chunk of a streamed blob: weight rows [row0, row0 + nrows).
+struct Chunk {
+    Blob *blob;
+    int64_t row0, nrows;
+    size_t bytes() const { return (size_t)(nrows * blob->k) * blob->elem; }
+};
+
+struct Plan {
+    std::vector<int> model_ids, n_frames;  // active models (key)
+    std::vector<int> out_base;             // first output index per slot
+    std::vector<Launch> launches;
+    std::vector<Chunk> chunks;             // streamed chunks, consumption order
+    void *arena = nullptr;
+    size_t arena_bytes = 0;
+    float *partial = nullptr;
+    size_t partial_bytes = 0;
+    size_t streamed_bytes = 0;
+    // HIP graph of the launch sequence for one set of caller pointers
+    hipGraphExec_t graph = nullptr;
+    std::vector<const void *> graph_frames;
+    std::vector<void *> graph_outputs;
+    hipStream_t graph_stream = nullptr;
+};
+
+struct Options {
+    int use_graph = 1;
+    int64_t slot_bytes = 32ll << 20;
+    int slots = 3;
+    int64_t fail_copy_at = 0;
+    int split_merged = 0;
+};
+
+}  // namespace gemel
+
+struct gemel_ctx {
+    int device = 0;
+    int dtype = GEMEL_BF16;
+    uint64_t budget = 0;
+    std::vector<std::unique_ptr<gemel::Model>> models;
+    std::vector<std::vector<gemel_member>> groups;
+    gemel::Options opt;
+    std::string err;
+    // device state
+    bool dev_ready = false;
+    bool weights_ready = false;      // placement matches registry + groups
+    hipStream_t side = nullptr;      // weight-copy stream
+    std::vector<hipEvent_t> ev_copied, ev_free;
+    void *wpool = nullptr;           // resident weights + all scale/shift
+    size_t wpool_bytes = 0;
+    void *staging = nullptr;         // slots x slot_bytes
+    int staging_slots = 0;
+    int64_t staging_slot_bytes = 0;
+    std::vector<std::shared_ptr<gemel::Blob>> placed;  // blobs of the pool
+    size_t resident_bytes = 0, peak_bytes = 0;
+    int64_t copies_issued = 0;
+    int64_t graph_replays = 0;
+    std::map<std::vector<int>, std::unique_ptr<gemel::Plan>> plans;
+    gemel::Plan *last_plan = nullptr;
+};
+
+namespace gemel {
+gemel_status fail(gemel_ctx *ctx, gemel_status code, const std::string &msg);
+gemel_status materialise(gemel_ctx *ctx);
+void release_device(gemel_ctx *ctx);
+void drop_plans(gemel_ctx *ctx);
+gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models,
+                 const void *const *frames, const int32_t *n_frames, void *const *outputs,
+                 hipStream_t stream);
+size_t unmerged_bytes(const gemel_ctx *ctx);
+size_t merged_bytes(const gemel_ctx *ctx);
+}  // namespace gemel

@@ -1,0 +1,445 @@
+// Merged-batch convolution kernels for gfx950.
+//
+// conv_bf16: implicit GEMM C[M][N] = A[M][K] * B[N][K]^T on bf16 MFMA
+// (v_mfma_f32_16x16x32_bf16, fp32 accumulation).
+//   M = frames of every model in the launch x Ho x Wo  (rows of all merged
+//       models, concatenated; each model's rows read its own tensor)
+//   N = output channels, K = kh * kw * Cin (Cin-fastest, matching KRSC
+//       weights and NHWC activations, so every 8-element K chunk is one
+//       16-byte load).
+// A workgroup of 4 waves computes a BM x BN tile; A (im2col gathered on the
+// fly) and B (the single shared weight copy) tiles of depth 64 are
+// double-buffered in LDS, so one weight tile is reused by the rows of every
+// model that shares the layer. The epilogue stages the fp32 tile through
+// LDS and applies per-channel scale/shift (bias and batch norm), the
+// residual (before or after the activation) and ReLU / leaky ReLU, then
+// writes bf16 NHWC with 16-byte stores (or fp32 NCHW for model outputs).
+// With k_splits > 1 each split writes fp32 partial sums instead and
+// conv_reduce applies the epilogue.
+//
+// conv_f32: direct convolution in fp32 FMA (no reduced-precision products)
+// for float32 contexts.
+#include <hip/hip_runtime.h>
+
+#include "kargs.h"
+#include "kernels.h"
+
+namespace gemel {
+
+typedef unsigned short u16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf2f(u16 h) {
+    return __uint_as_float((uint32_t)h << 16);
+}
+__device__ __forceinline__ u16 f2bf(float f) {
+    return __builtin_bit_cast(u16, (__bf16)f);
+}
+__device__ __forceinline__ float act_fn(float y, int act, float slope) {
+    if (act == 1) return fmaxf(y, 0.f);
+    if (act == 2) return y > 0.f ? y : y * slope;
+    return y;
+}
+__device__ __forceinline__ float epi(float z, float r, int has_res,
+                                     int res_mode, int act, float slope) {
+    if (!has_res) return act_fn(z, act, slope);
+    if (res_mode == 0) return act_fn(z + r, act, slope);
+    return act_fn(z, act, slope) + r;
+}
+
+// Segment of GEMM row gm: the last segment whose m_start <= gm.
+template <typename Args>
+__device__ __forceinline__ int seg_of_row(const Args &a, int gm) {
+    int s = 0;
+    for (int i = 1; i < a.nseg; ++i) s += (gm >= a.seg[i].m_start) ? 1 : 0;
+    return s;
+}
+
+// Scalars of the fused epilogue.
+struct Epi {
+    int out_cs, cout, act, res_mode, has_res, HWo;
+    float slope;
+};
+template <typename Args>
+__device__ __forceinline__ Epi epi_of(const Args &a, int HWo) {
+    Epi e;
+    e.out_cs = a.out_cs; e.cout = a.cout; e.act = a.act; e.res_mode = a.res_mode;
+    e.has_res = a.has_res; e.HWo = HWo; e.slope = a.slope;
+    return e;
+}
+
+// Epilogue of 8 consecutive channels [gn, gn+8) of row gm into NHWC bf16.
+__device__ __forceinline__ void store8_nhwc_bf16(const ConvSeg &sg, const Epi &e,
+                                                 int gm, int gn, const float *v) {
+    const size_t off = (size_t)(gm - sg.m_start) * e.out_cs + gn;
+    const float4 sc0 = *(const float4 *)(sg.scale + gn);
+    const float4 sc1 = *(const float4 *)(sg.scale + gn + 4);
+    const float4 sh0 = *(const float4 *)(sg.shift + gn);
+    const float4 sh1 = *(const float4 *)(sg.shift + gn + 4);
+    const float sc[8] = {sc0.x, sc0.y, sc0.z, sc0.w, sc1.x, sc1.y, sc1.z, sc1.w};
+    const float sh[8] = {sh0.x, sh0.y, sh0.z, sh0.w, sh1.x, sh1.y, sh1.z, sh1.w};
+    u16 rv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (e.has_res) {
+        const uint4 r4 = *(const uint4 *)((const u16 *)sg.res + off);
+        const u16 *rp = (const u16 *)&r4;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) rv[j] = rp[j];
+    }
+    uint4 o;
+    u16 *op = (u16 *)&o;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const float z = v[j] * sc[j] + sh[j];
+        op[j] = f2bf(epi(z, bf2f(rv[j]), e.has_res, e.res_mode, e.act, e.slope));
+    }
+    *(uint4 *)((u16 *)sg.out + off) = o;
+}
+
+// Epilogue of 8 consecutive channels of row gm into NHWC fp32.
+__device__ __forceinline__ void store8_nhwc_f32(const ConvSeg &sg, const Epi &e,
+                                                int gm, int gn, const float *v) {
+    const size_t off = (size_t)(gm - sg.m_start) * e.out_cs + gn;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const float r = e.has_res ? ((const float *)sg.res)[off + j] : 0.f;
+        const float z = v[j] * sg.scale[gn + j] + sg.shift[gn + j];
+        ((float *)sg.out)[off + j] = epi(z, r, e.has_res, e.res_mode, e.act, e.slope);
+    }
+}
+
+// Epilogue of one element into a caller-owned fp32 NCHW output.
+template <bool BF16>
+__device__ __forceinline__ void store1_nchw_f32(const ConvSeg &sg, const Epi &e,
+                                                int gm, int gn, float v) {
+    if (gn >= e.cout) return;
+    const int lr = gm - sg.m_start;
+    const int f = lr / e.HWo, pix = lr - f * e.HWo;
+    float r = 0.f;
+    if (e.has_res) {
+        const size_t roff = (size_t)lr * e.out_cs + gn;
+        r = BF16 ? bf2f(((const u16 *)sg.res)[roff]) : ((const float *)sg.res)[roff];
+    }
+    const float z = v * sg.scale[gn] + sg.shift[gn];
+    ((float *)sg.out)[((size_t)f * e.cout + gn) * e.HWo + pix] =
+        epi(z, r, e.has_res, e.res_mode, e.act, e.slope);
+}
+
+template <int BM, int BN>
+__global__ __launch_bounds__(256, 2) void conv_bf16_kernel(const ConvArgs a) {
+    constexpr int BK = CONV_BK;
+    constexpr int LDA = BK + 8;            // +16 B per row: conflict-free b128
+    constexpr int WM = BM / 2, WN = BN / 2;
+    constexpr int FM = WM / 16, FN = WN / 16;
+    constexpr int AP = BM / 32, BP = BN / 32;  // 16-byte loads per thread
+    constexpr int LDC = BN + 4;
+    constexpr int SMEM_AB = 2 * (BM + BN) * LDA * 2;
+    constexpr int SMEM_C = BM * LDC * 4;
+    constexpr int SMEM = SMEM_AB > SMEM_C ? SMEM_AB : SMEM_C;
+    __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM];
+    u16 *const sAB = (u16 *)smem;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int tiles_n = (a.N + BN - 1) / BN;
+    const int tm = blockIdx.x / tiles_n, tn = blockIdx.x - tm * tiles_n;
+    const int k_begin = blockIdx.y * a.k_per_split;
+    const int k_end = min(a.K, k_begin + a.k_per_split);
+    const int HWo = a.Ho * a.Wo;
+    const size_t frame_elems = (size_t)a.H * a.W * a.in_cs;
+
+    // ---- loader set-up: thread owns K chunk q of rows r0 + 32 j ----
+    const int q = tid & 7, r0 = tid >> 3;
+    const u16 *abase[AP];
+    int ahi[AP], awi[AP];
+#pragma unroll
+    for (int j = 0; j < AP; ++j) {
+        const int gm = tm * BM + r0 + 32 * j;
+        abase[j] = (const u16 *)a.seg[0].in;
+        ahi[j] = -(1 << 28);
+        awi[j] = 0;
+        if (gm < a.M) {
+            const int s = seg_of_row(a, gm);
+            const int fr = gm / HWo;
+            const int pix = gm - fr * HWo;
+            const int ho = pix / a.Wo, wo = pix - (pix / a.Wo) * a.Wo;
+            abase[j] = (const u16 *)a.seg[s].in + (size_t)(fr - a.seg[s].f_start) * frame_elems;
+            ahi[j] = ho * a.stride - a.pad;
+            awi[j] = wo * a.stride - a.pad;
+        }
+    }
+    const u16 *bbase[BP];
+    bool bok[BP];
+#pragma unroll
+    for (int j = 0; j < BP; ++j) {
+        const int gn = tn * BN + r0 + 32 * j;
+        bok[j] = gn < a.N;
+        bbase[j] = (const u16 *)a.w + (size_t)(bok[j] ? gn : 0) * a.K;
+    }
+    // (r, s, c) of this thread's chunk at depth k
+    int k = k_begin + q * 8;
+    int c, r, s;
+    {
+        const int rs = k / a.Cin;
+        c = k - rs * a.Cin;
+        r = rs / a.kw;
+        s = rs - r * a.kw;
+    }
+
+    uint4 ra[AP], rb[BP];
+    auto gload = [&]() {
+        const bool kok = k < k_end;
+#pragma unroll
+        for (int j = 0; j < AP; ++j) {
+            const int hi = ahi[j] + r, wi = awi[j] + s;
+            if (kok && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W)
+                ra[j] = *(const uint4 *)(abase[j] + ((size_t)(hi * a.W + wi) * a.in_cs + c));
+            else
+                ra[j] = make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < BP; ++j)
+            rb[j] = (kok && bok[j]) ? *(const uint4 *)(bbase[j] + k) : make_uint4(0, 0, 0, 0);
+    };
+    auto advance = [&]() {
+        k += BK;
+        c += BK;
+        while (c >= a.Cin) {
+            c -= a.Cin;
+            if (++s == a.kw) { s = 0; ++r; }
+        }
+    };
+    auto sstore = [&](int stage) {
+        u16 *As = sAB + stage * (BM + BN) * LDA;
+        u16 *Bs = As + BM * LDA;
+#pragma unroll
+        for (int j = 0; j < AP; ++j) *(uint4 *)(As + (r0 + 32 * j) * LDA + q * 8) = ra[j];
+#pragma unroll
+        for (int j = 0; j < BP; ++j) *(uint4 *)(Bs + (r0 + 32 * j) * LDA + q * 8) = rb[j];
+    };
+
+    f32x4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int nk = (k_end - k_begin + BK - 1) / BK;
+    gload();
+    sstore(0);
+    __syncthreads();
+    for (int it = 0; it < nk; ++it) {
+        const bool more = it + 1 < nk;
+        if (more) {
+            advance();
+            gload();
+        }
+        const u16 *As = sAB + (it & 1) * (BM + BN) * LDA;
+        const u16 *Bs = As + BM * LDA;
+#pragma unroll
+        for (int kk = 0; kk < BK / 32; ++kk) {
+            bf16x8 af[FM], bfr[FN];
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+                af[i] = *(const bf16x8 *)(As + (wm * WM + i * 16 + (lane & 15)) * LDA + kk * 32 + (lane >> 4) * 8);
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+                bfr[j] = *(const bf16x8 *)(Bs + (wn * WN + j * 16 + (lane & 15)) * LDA + kk * 32 + (lane >> 4) * 8);
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        }
+        if (more) sstore((it + 1) & 1);
+        __syncthreads();
+    }
+
+    // ---- epilogue: fp32 tile through LDS ----
+    float *Cs = (float *)smem;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                Cs[(wm * WM + i * 16 + (lane >> 4) * 4 + v) * LDC + wn * WN + j * 16 + (lane & 15)] = acc[i][j][v];
+    __syncthreads();
+
+    constexpr int CH = BN / 8;            // 8-channel chunks per row
+    if (a.k_splits > 1) {
+        float *P = a.partial + (size_t)blockIdx.y * a.M * a.N;
+        for (int item = tid; item < BM * CH; item += 256) {
+            const int row = item / CH, ch = item - (item / CH) * CH;
+            const int gm = tm * BM + row, gn = tn * BN + ch * 8;
+            if (gm >= a.M || gn >= a.N) continue;
+            const float *src = Cs + row * LDC + ch * 8;
+            float4 *dst = (float4 *)(P + (size_t)gm * a.N + gn);
+            dst[0] = *(const float4 *)src;
+            dst[1] = *(const float4 *)(src + 4);
+        }
+        return;
+    }
+    const Epi e = epi_of(a, HWo);
+    if (a.out_mode == OUT_NHWC) {
+        for (int item = tid; item < BM * CH; item += 256) {
+            const int row = item / CH, ch = item - (item / CH) * CH;
+            const int gm = tm * BM + row, gn = tn * BN + ch * 8;
+            if (gm >= a.M || gn >= a.N) continue;
+            float v[8];
+            const float4 v0 = *(const float4 *)(Cs + row * LDC + ch * 8);
+            const float4 v1 = *(const float4 *)(Cs + row * LDC + ch * 8 + 4);
+            v[0] = v0.x; v[1] = v0.y; v[2] = v0.z; v[3] = v0.w;
+            v[4] = v1.x; v[5] = v1.y; v[6] = v1.z; v[7] = v1.w;
+            store8_nhwc_bf16(a.seg[seg_of_row(a, gm)], e, gm, gn, v);
+        }
+    } else {
+        // fp32 NCHW: consecutive threads take consecutive rows of a column
+        for (int item = tid; item < BM * BN; item += 256) {
+            const int col = item / BM, row = item - (item / BM) * BM;
+            const int gm = tm * BM + row, gn = tn * BN + col;
+            if (gm >= a.M || gn >= a.N) continue;
+            store1_nchw_f32<true>(a.seg[seg_of_row(a, gm)], e, gm, gn, Cs[row * LDC + col]);
+        }
+    }
+}
+
+// Split-K reduction: sum the partial tiles, then the same epilogue.
+template <bool BF16>
+__global__ __launch_bounds__(256) void conv_reduce_kernel(const ReduceArgs ra) {
+    const int item = blockIdx.x * 256 + threadIdx.x;
+    const int chunks = ra.N / 8;
+    if (item >= ra.M * chunks) return;
+    const int gm = item / chunks, gn = (item - gm * chunks) * 8;
+    float v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int sp = 0; sp < ra.splits; ++sp) {
+        const float *p = ra.partial + ((size_t)sp * ra.M + gm) * ra.N + gn;
+        const float4 p0 = *(const float4 *)p, p1 = *(const float4 *)(p + 4);
+        v[0] += p0.x; v[1] += p0.y; v[2] += p0.z; v[3] += p0.w;
+        v[4] += p1.x; v[5] += p1.y; v[6] += p1.z; v[7] += p1.w;
+    }
+    const Epi e = epi_of(ra, ra.HWo);
+    const ConvSeg &sg = ra.seg[seg_of_row(ra, gm)];
+    if (ra.out_mode == OUT_NHWC) {
+        if (BF16)
+            store8_nhwc_bf16(sg, e, gm, gn, v);
+        else
+            store8_nhwc_f32(sg, e, gm, gn, v);
+    } else {
+        for (int j = 0; j < 8; ++j) store1_nchw_f32<BF16>(sg, e, gm, gn + j, v[j]);
+    }
+}
+
+// Direct fp32 convolution: one thread per output element (row gm, col gn).
+__global__ __launch_bounds__(256) void conv_f32_kernel(const ConvArgs a) {
+    const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= (long)a.M * a.N) return;
+    const int gm = (int)(idx / a.N), gn = (int)(idx - (long)gm * a.N);
+    const int HWo = a.Ho * a.Wo;
+    const int s = seg_of_row(a, gm);
+    const ConvSeg &sg = a.seg[s];
+    const int fr = gm / HWo, pix = gm - fr * HWo;
+    const int ho = pix / a.Wo, wo = pix - ho * a.Wo;
+    const float *in = (const float *)sg.in + (size_t)(fr - sg.f_start) * a.H * a.W * a.in_cs;
+    const float *w = (const float *)a.w + (size_t)gn * a.K;
+    float acc = 0.f;
+    for (int r = 0; r < a.kh; ++r) {
+        const int hi = ho * a.stride - a.pad + r;
+        if (hi < 0 || hi >= a.H) continue;
+        for (int q = 0; q < a.kw; ++q) {
+            const int wi = wo * a.stride - a.pad + q;
+            if (wi < 0 || wi >= a.W) continue;
+            const float *ip = in + (size_t)(hi * a.W + wi) * a.in_cs;
+            const float *wp = w + (r * a.kw + q) * a.Cin;
+            for (int cc = 0; cc < a.Cin; ++cc) acc = fmaf(ip[cc], wp[cc], acc);
+        }
+    }
+    const Epi e = epi_of(a, HWo);
+    if (a.out_mode == OUT_NHWC) {
+        const size_t off = (size_t)(gm - sg.m_start) * a.out_cs + gn;
+        const float r = a.has_res ? ((const float *)sg.res)[off] : 0.f;
+        const float z = acc * sg.scale[gn] + sg.shift[gn];
+        ((float *)sg.out)[off] = epi(z, r, a.has_res, a.res_mode, a.act, a.slope);
+    } else {
+        store1_nchw_f32<false>(sg, e, gm, gn, acc);
+    }
+}
+
+int conv_tile_bm(int tile) {
+    switch (tile) {
+    case TILE_128x128: return 128;
+    case TILE_128x64: return 128;
+    case TILE_64x64: return 64;
+    case TILE_256x128: return 256;
+    }
+    return 0;
+}
+int conv_tile_bn(int tile) {
+    switch (tile) {
+    case TILE_128x128: return 128;
+    case TILE_128x64: return 64;
+    case TILE_64x64: return 64;
+    case TILE_256x128: return 128;
+    }
+    return 0;
+}
+
+static bool conv_args_ok(const ConvArgs &a) {
+    if (a.M <= 0 || a.N <= 0 || a.K <= 0 || a.nseg < 1 || a.nseg > GEMEL_MAX_SEG) return false;
+    if (a.N % 8 || a.K % 8 || a.Cin % 8 || a.in_cs < a.Cin || a.in_cs % 8) return false;
+    if (a.K != a.kh * a.kw * a.Cin || a.out_cs < a.N || a.out_cs % 8) return false;
+    if (a.Ho <= 0 || a.Wo <= 0 || a.H <= 0 || a.W <= 0) return false;
+    if (a.seg[0].m_start != 0) return false;
+    for (int i = 0; i < a.nseg; ++i) {
+        if (!a.seg[i].in || !a.seg[i].scale || !a.seg[i].shift) return false;
+        if (a.k_splits <= 1 && !a.seg[i].out) return false;
+        if (a.has_res && !a.seg[i].res) return false;
+        if (i && a.seg[i].m_start < a.seg[i - 1].m_start) return false;
+        if (a.seg[i].m_start != a.seg[i].f_start * a.Ho * a.Wo) return false;
+    }
+    if (a.k_splits > 1 && (!a.partial || a.k_per_split % CONV_BK)) return false;
+    if (a.k_per_split <= 0 || (long)a.k_per_split * a.k_splits < a.K) return false;
+    if (a.out_mode == OUT_NCHW_F32 && a.cout > a.N) return false;
+    return true;
+}
+
+hipError_t launch_conv_bf16(const ConvArgs &a, int tile, hipStream_t st) {
+    if (!conv_args_ok(a)) return hipErrorInvalidValue;
+    const int bm = conv_tile_bm(tile), bn = conv_tile_bn(tile);
+    if (!bm) return hipErrorInvalidValue;
+    const long tiles = (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn);
+    if (tiles > 0x7fffffffL) return hipErrorInvalidValue;
+    dim3 grid((unsigned)tiles, (unsigned)a.k_splits), block(256);
+    switch (tile) {
+    case TILE_128x128: hipLaunchKernelGGL((conv_bf16_kernel<128, 128>), grid, block, 0, st, a); break;
+    case TILE_128x64: hipLaunchKernelGGL((conv_bf16_kernel<128, 64>), grid, block, 0, st, a); break;
+    case TILE_64x64: hipLaunchKernelGGL((conv_bf16_kernel<64, 64>), grid, block, 0, st, a); break;
+    case TILE_256x128: hipLaunchKernelGGL((conv_bf16_kernel<256, 128>), grid, block, 0, st, a); break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_conv_f32(const ConvArgs &a, hipStream_t st) {
+    if (!conv_args_ok(a) || a.k_splits != 1) return hipErrorInvalidValue;
+    const long n = (long)a.M * a.N;
+    dim3 grid((unsigned)((n + 255) / 256)), block(256);
+    hipLaunchKernelGGL(conv_f32_kernel, grid, block, 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_conv_reduce(const ReduceArgs &a, bool bf16, hipStream_t st) {
+    if (a.M <= 0 || a.N <= 0 || a.N % 8 || a.splits < 1 || !a.partial || a.nseg < 1 || a.nseg > GEMEL_MAX_SEG)
+        return hipErrorInvalidValue;
+    for (int i = 0; i < a.nseg; ++i)
+        if (!a.seg[i].out || !a.seg[i].scale || !a.seg[i].shift || (a.has_res && !a.seg[i].res))
+            return hipErrorInvalidValue;
+    const long n = (long)a.M * (a.N / 8);
+    dim3 grid((unsigned)((n + 255) / 256)), block(256);
+    if (bf16)
+        hipLaunchKernelGGL(conv_reduce_kernel<true>, grid, block, 0, st, a);
+    else
+        hipLaunchKernelGGL(conv_reduce_kernel<false>, grid, block, 0, st, a);
+    return hipGetLastError();
+}
+
+}  // namespace gemel

@@ -1,0 +1,186 @@
+// Fully connected layers for small frame counts (M <= 64 frames).
+//
+// An FC layer at a few frames is a weight-streaming problem: every weight
+// byte is read once and used M times, far below the MFMA ridge point, so
+// the kernel is organised for HBM bandwidth. Each wave owns 16 output
+// neurons and a slice of K; every lane streams 64 contiguous bytes of one
+// weight row per step (4 lanes cover 256 contiguous bytes of a row) and the
+// same K positions of up to 16 frames, and v_mfma_f32_16x16x32_bf16 does the
+// multiply-adds (weights as the 16-row A operand, frames as the 16-column B
+// operand; the K order inside a step is the same for A and B, so any order
+// is correct). K is split over blockIdx.y so that enough waves are in flight
+// to saturate HBM; partial sums go to a [splits][M][N] fp32 buffer and
+// fc_reduce applies bias, activation and the store. With one split the
+// epilogue is applied directly.
+#include <hip/hip_runtime.h>
+
+#include "kargs.h"
+#include "kernels.h"
+
+namespace gemel {
+
+typedef unsigned short u16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float fc_bf2f(u16 h) { return __uint_as_float((uint32_t)h << 16); }
+__device__ __forceinline__ u16 fc_f2bf(float f) { return __builtin_bit_cast(u16, (__bf16)f); }
+__device__ __forceinline__ float fc_act(float y, int act, float slope) {
+    if (act == 1) return fmaxf(y, 0.f);
+    if (act == 2) return y > 0.f ? y : y * slope;
+    return y;
+}
+
+// Segment holding launch frame f: the last one with f_start <= f.
+__device__ __forceinline__ int fc_seg(const FcArgs &a, int f) {
+    int s = 0;
+    for (int i = 1; i < a.nseg; ++i) s += (f >= a.seg[i].f_start) ? 1 : 0;
+    return s;
+}
+
+__device__ __forceinline__ void fc_store(const FcArgs &a, int f, int n, float acc, bool bf16) {
+    const FcSeg &sg = a.seg[fc_seg(a, f)];
+    const int lf = f - sg.f_start;
+    const float y = fc_act(acc * sg.scale[n] + sg.shift[n], a.act, a.slope);
+    if (a.out_mode == OUT_NHWC) {
+        if (bf16)
+            ((u16 *)sg.out)[(size_t)lf * a.out_cs + n] = fc_f2bf(y);
+        else
+            ((float *)sg.out)[(size_t)lf * a.out_cs + n] = y;
+    } else if (n < a.cout) {
+        ((float *)sg.out)[(size_t)lf * a.cout + n] = y;
+    }
+}
+
+template <int MB>  // frame blocks of 16
+__global__ __launch_bounds__(256) void fc_bf16_kernel(const FcArgs a) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int n0 = blockIdx.x * 64 + wave * 16;
+    const int k_begin = blockIdx.y * a.k_per_split;
+    const int k_end = min(a.K, k_begin + a.k_per_split);
+    const int row = n0 + (lane & 15);
+    const int g = lane >> 4;
+    const bool row_ok = row < a.N;
+    const u16 *wrow = (const u16 *)a.w + (size_t)(row_ok ? row : 0) * a.K;
+    const u16 *xrow[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+        const int f = mb * 16 + (lane & 15);
+        xrow[mb] = nullptr;
+        if (f < a.M) {
+            const FcSeg &sg = a.seg[fc_seg(a, f)];
+            xrow[mb] = (const u16 *)sg.in + (size_t)(f - sg.f_start) * a.K;
+        }
+    }
+    f32x4 acc[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    if (n0 < a.N) {
+        for (int k = k_begin; k < k_end; k += 128) {
+            uint4 wv[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int kk = k + g * 32 + j * 8;
+                wv[j] = (row_ok && kk < k_end) ? *(const uint4 *)(wrow + kk) : make_uint4(0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+                uint4 xv[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int kk = k + g * 32 + j * 8;
+                    xv[j] = (xrow[mb] && kk < k_end) ? *(const uint4 *)(xrow[mb] + kk) : make_uint4(0, 0, 0, 0);
+                }
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(bf16x8, wv[j]), __builtin_bit_cast(bf16x8, xv[j]), acc[mb], 0, 0, 0);
+            }
+        }
+    }
+    // D[neuron = n0 + 4 g + v][frame = mb*16 + lane%16]
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+        const int f = mb * 16 + (lane & 15);
+        if (f >= a.M) continue;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int n = n0 + g * 4 + v;
+            if (n >= a.N) continue;
+            if (a.k_splits > 1)
+                a.partial[((size_t)blockIdx.y * a.M + f) * a.N + n] = acc[mb][v];
+            else
+                fc_store(a, f, n, acc[mb][v], true);
+        }
+    }
+}
+
+// float32 FC: one thread per (frame, neuron), fp32 FMA over K.
+__global__ __launch_bounds__(256) void fc_f32_kernel(const FcArgs a) {
+    const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= (long)a.M * a.N) return;
+    const int f = (int)(idx / a.N), n = (int)(idx - (long)f * a.N);
+    const FcSeg &sg = a.seg[fc_seg(a, f)];
+    const float *x = (const float *)sg.in + (size_t)(f - sg.f_start) * a.K;
+    const float *w = (const float *)a.w + (size_t)n * a.K;
+    float acc = 0.f;
+    for (int k = 0; k < a.K; ++k) acc = fmaf(x[k], w[k], acc);
+    fc_store(a, f, n, acc, false);
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void fc_reduce_kernel(const FcArgs a) {
+    const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= (long)a.M * a.N) return;
+    const int f = (int)(idx / a.N), n = (int)(idx - (long)f * a.N);
+    float acc = 0.f;
+    for (int s = 0; s < a.k_splits; ++s) acc += a.partial[((size_t)s * a.M + f) * a.N + n];
+    fc_store(a, f, n, acc, BF16);
+}
+
+static bool fc_args_ok(const FcArgs &a) {
+    if (a.M <= 0 || a.N <= 0 || a.K <= 0 || a.nseg < 1 || a.nseg > GEMEL_MAX_SEG) return false;
+    if (a.N % 8 || a.K % 8 || a.k_splits < 1 || a.k_per_split <= 0) return false;
+    if ((long)a.k_splits * a.k_per_split < a.K) return false;
+    if (a.out_mode == OUT_NHWC && a.out_cs < a.N) return false;
+    if (a.out_mode == OUT_NCHW_F32 && a.cout > a.N) return false;
+    if (a.seg[0].f_start != 0) return false;
+    for (int i = 0; i < a.nseg; ++i)
+        if (!a.seg[i].in || !a.seg[i].out || !a.seg[i].scale || !a.seg[i].shift) return false;
+    if (a.k_splits > 1 && !a.partial) return false;
+    return true;
+}
+
+hipError_t launch_fc_bf16(const FcArgs &a, hipStream_t st) {
+    if (!fc_args_ok(a) || a.M > 64 || (a.k_splits > 1 && a.k_per_split % 128)) return hipErrorInvalidValue;
+    dim3 grid((unsigned)((a.N + 63) / 64), (unsigned)a.k_splits), block(256);
+    const int mb = (a.M + 15) / 16;
+    switch (mb) {
+    case 1: hipLaunchKernelGGL(fc_bf16_kernel<1>, grid, block, 0, st, a); break;
+    case 2: hipLaunchKernelGGL(fc_bf16_kernel<2>, grid, block, 0, st, a); break;
+    case 3: hipLaunchKernelGGL(fc_bf16_kernel<3>, grid, block, 0, st, a); break;
+    default: hipLaunchKernelGGL(fc_bf16_kernel<4>, grid, block, 0, st, a); break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_fc_f32(const FcArgs &a, hipStream_t st) {
+    if (!fc_args_ok(a) || a.k_splits != 1) return hipErrorInvalidValue;
+    const long n = (long)a.M * a.N;
+    hipLaunchKernelGGL(fc_f32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_fc_reduce(const FcArgs &a, bool bf16, hipStream_t st) {
+    if (!fc_args_ok(a) || a.k_splits < 2) return hipErrorInvalidValue;
+    const long n = (long)a.M * a.N;
+    dim3 grid((unsigned)((n + 255) / 256)), block(256);
+    if (bf16)
+        hipLaunchKernelGGL(fc_reduce_kernel<true>, grid, block, 0, st, a);
+    else
+        hipLaunchKernelGGL(fc_reduce_kernel<false>, grid, block, 0, st, a);
+    return hipGetLastError();
+}
+
+}  // namespace gemel

@@ -1,0 +1,96 @@
+// Kernel argument blocks shared by the host planner and the HIP kernels.
+//
+// Activations are NHWC with a channel count padded to a multiple of 8
+// ("physical" channels; padded channels hold zeros). A merged launch covers
+// the concatenated frames of several models: GEMM row m belongs to segment
+// s when seg[s].m_start <= m < seg[s+1].m_start, and each segment carries
+// its own input, residual, output and scale/shift pointers, so the models'
+// tensors can live anywhere while the weight tile is shared by all rows.
+#pragma once
+#include <stdint.h>
+
+#define GEMEL_MAX_SEG 16
+
+enum { OUT_NHWC = 0, OUT_NCHW_F32 = 1, OUT_PARTIAL_F32 = 2 };
+
+struct ConvSeg {
+    const void *in;       // NHWC [frames][H][W][in_cs], frame 0 of the segment
+    const void *res;      // NHWC [frames][Ho][Wo][out_cs] or null
+    void *out;            // NHWC [frames][Ho][Wo][out_cs] or NCHW f32 final
+    const float *scale;   // [N] per output channel
+    const float *shift;   // [N]
+    int32_t m_start;      // first GEMM row (= first frame * Ho * Wo)
+    int32_t f_start;      // first frame of the segment in the launch
+};
+
+struct ConvArgs {
+    const void *w;        // [N][K], k = (r * kw + s) * Cin + c
+    int32_t M, N, K;      // rows = frames*Ho*Wo, cols = out channels, depth
+    int32_t H, W, Cin;    // input spatial size, physical input channels
+    int32_t in_cs;        // input pixel stride in elements (>= Cin)
+    int32_t Ho, Wo;
+    int32_t kh, kw, stride, pad;
+    int32_t out_cs;       // output pixel stride (NHWC) in elements
+    int32_t cout;         // logical output channels (NCHW f32 stores)
+    int32_t act;
+    float slope;
+    int32_t res_mode;     // 0: act(z + r), 1: act(z) + r
+    int32_t has_res;
+    int32_t out_mode;     // OUT_NHWC or OUT_NCHW_F32
+    int32_t nseg;
+    int32_t k_splits;     // >1: write fp32 partials to `partial`
+    int32_t k_per_split;  // depth handled by one split (multiple of BK)
+    float *partial;       // [k_splits][M][N] when k_splits > 1
+    ConvSeg seg[GEMEL_MAX_SEG];
+};
+
+// Split-K reduction + epilogue over partial sums [splits][M][N].
+struct ReduceArgs {
+    const float *partial;
+    int32_t M, N, splits;
+    int32_t HWo;          // rows per frame
+    int32_t out_cs, cout;
+    int32_t act;
+    float slope;
+    int32_t res_mode, has_res, out_mode, nseg;
+    ConvSeg seg[GEMEL_MAX_SEG];
+};
+
+struct FcSeg {
+    const void *in;       // [frames][K] (the producer tensor, NHWC-flat)
+    void *out;            // [frames][out_cs] internal, or [frames][cout] f32
+    const float *scale, *shift;
+    int32_t f_start;      // first frame of the segment in the launch
+};
+
+struct FcArgs {
+    const void *w;        // [N][K]
+    int32_t M, N, K;      // frames, out features (physical), in features
+    int32_t out_cs, cout;
+    int32_t act;
+    float slope;
+    int32_t out_mode;     // OUT_NHWC (internal) or OUT_NCHW_F32 (final)
+    int32_t nseg;
+    int32_t k_splits, k_per_split;
+    float *partial;       // [k_splits][M][N]
+    FcSeg seg[GEMEL_MAX_SEG];
+};
+
+struct EwSeg {
+    const void *in0;
+    const void *in1;
+    void *out;
+    int32_t frames;
+};
+
+// Element-wise / pooling / layout kernels, one segment per model.
+struct EwArgs {
+    int32_t H, W, C;      // input spatial size and physical channels (in0)
+    int32_t C1;           // concat: physical channels of in1
+    int32_t Ho, Wo, Co;   // output size and physical channels
+    int32_t k, stride, pad;
+    int32_t c_logical;    // pack: logical input channels; export: cout
+    int32_t nseg;
+    int32_t max_frames;
+    EwSeg seg[GEMEL_MAX_SEG];
+};

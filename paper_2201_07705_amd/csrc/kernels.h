@@ -1,0 +1,35 @@
+// Host-side launchers of the HIP kernels. Each launcher checks on the host
+// that the argument block matches what its kernel and grid assume and
+// returns hipErrorInvalidValue instead of launching otherwise.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include "kargs.h"
+
+namespace gemel {
+
+// Tile configurations of the bf16 implicit-GEMM convolution.
+enum ConvTile { TILE_128x128 = 0, TILE_128x64 = 1, TILE_64x64 = 2, TILE_256x128 = 3 };
+int conv_tile_bm(int tile);
+int conv_tile_bn(int tile);
+constexpr int CONV_BK = 64;
+
+hipError_t launch_conv_bf16(const ConvArgs &a, int tile, hipStream_t st);
+hipError_t launch_conv_f32(const ConvArgs &a, hipStream_t st);
+// Split-K reduction + fused epilogue (bf16 or f32 internal activations).
+hipError_t launch_conv_reduce(const ReduceArgs &a, bool bf16, hipStream_t st);
+
+hipError_t launch_fc_bf16(const FcArgs &a, hipStream_t st);
+hipError_t launch_fc_f32(const FcArgs &a, hipStream_t st);
+hipError_t launch_fc_reduce(const FcArgs &a, bool bf16, hipStream_t st);
+
+// Input pack: caller NCHW f32 -> NHWC physical channels (bf16 or f32).
+hipError_t launch_pack(const EwArgs &a, bool bf16, hipStream_t st);
+hipError_t launch_maxpool(const EwArgs &a, bool bf16, hipStream_t st);
+hipError_t launch_avgpool(const EwArgs &a, bool bf16, hipStream_t st);
+hipError_t launch_upsample2x(const EwArgs &a, bool bf16, hipStream_t st);
+hipError_t launch_concat(const EwArgs &a, bool bf16, hipStream_t st);
+// Internal NHWC tensor -> caller NCHW f32 output.
+hipError_t launch_export(const EwArgs &a, bool bf16, hipStream_t st);
+
+}  // namespace gemel

@@ -1,0 +1,831 @@
+// Device placement of weights, execution plans and the inference round.
+//
+// Placement (materialise): every distinct parameter copy in use (one per
+// merged group, one per unmerged layer) is either resident in one device
+// pool or, when a weight budget does not fit, kept in pinned host memory
+// and streamed through a ring of staging slots every round. Merged copies
+// are made resident first: they serve several models (the paper's edge
+// scheduler never evicts layers still needed by other models, Appendix
+// A.4); the remaining budget is filled largest-first.
+//
+// Plan: for one set of (model, frame count) the layers of all models
+// become launch nodes. The members of a merge group that agree on input
+// shape and epilogue form ONE node (one launch over their concatenated
+// frames, reading the single shared weight copy); every other layer is a
+// node of its own. Nodes run in a topological order of their dependencies.
+// Activations live in one arena whose offsets are assigned from tensor
+// lifetimes (tensors whose lifetimes overlap never share bytes).
+//
+// Round: the plan's launches are enqueued on the caller's stream (or a
+// captured HIP graph of them is replayed). Streamed weights are copied on a
+// side stream: copy i waits for the consumer of the chunk that last used
+// its slot, and consumer i waits for copy i.
+#include <algorithm>
+#include <cstring>
+#include <numeric>
+#include <queue>
+#include <set>
+
+#include "internal.h"
+
+namespace gemel {
+
+#define HIPCHK(call, what)                                                                   \
+    do {                                                                                     \
+        hipError_t e_ = (call);                                                              \
+        if (e_ != hipSuccess)                                                                \
+            return fail(ctx, GEMEL_EDEVICE, std::string(what) + ": " + hipGetErrorString(e_)); \
+    } while (0)
+
+namespace {
+
+struct DeviceScope {
+    int prev = -1;
+    explicit DeviceScope(int d) {
+        if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+        (void)hipSetDevice(d);
+    }
+    ~DeviceScope() {
+        if (prev >= 0) (void)hipSetDevice(prev);
+    }
+};
+
+gemel_status ensure_device(gemel_ctx *ctx) {
+    if (ctx->dev_ready) return GEMEL_OK;
+    int n = 0;
+    HIPCHK(hipGetDeviceCount(&n), "hipGetDeviceCount");
+    if (ctx->device >= n) return fail(ctx, GEMEL_EINVAL, "device index beyond the visible devices");
+    HIPCHK(hipSetDevice(ctx->device), "hipSetDevice");
+    hipDeviceProp_t prop;
+    HIPCHK(hipGetDeviceProperties(&prop, ctx->device), "hipGetDeviceProperties");
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return fail(ctx, GEMEL_EDEVICE, std::string("libgemel is built for gfx950; device is ") + prop.gcnArchName);
+    HIPCHK(hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking), "hipStreamCreate");
+    ctx->dev_ready = true;
+    return GEMEL_OK;
+}
+
+void free_placement(gemel_ctx *ctx) {
+    for (auto &b : ctx->placed) {
+        if (b->w_pinned) (void)hipHostFree(b->w_pinned);
+        b->w_pinned = nullptr;
+        b->w_dev = nullptr;
+        b->aff_dev = nullptr;
+    }
+    ctx->placed.clear();
+    if (ctx->wpool) (void)hipFree(ctx->wpool);
+    if (ctx->staging) (void)hipFree(ctx->staging);
+    ctx->wpool = ctx->staging = nullptr;
+    ctx->wpool_bytes = 0;
+    for (auto e : ctx->ev_copied) (void)hipEventDestroy(e);
+    for (auto e : ctx->ev_free) (void)hipEventDestroy(e);
+    ctx->ev_copied.clear();
+    ctx->ev_free.clear();
+    ctx->staging_slots = 0;
+    ctx->resident_bytes = 0;
+    ctx->weights_ready = false;
+}
+
+}  // namespace
+
+void drop_plans(gemel_ctx *ctx) {
+    if (!ctx->plans.empty()) (void)hipDeviceSynchronize();
+    for (auto &kv : ctx->plans) {
+        Plan &p = *kv.second;
+        if (p.graph) (void)hipGraphExecDestroy(p.graph);
+        if (p.arena) (void)hipFree(p.arena);
+        if (p.partial) (void)hipFree(p.partial);
+    }
+    ctx->plans.clear();
+    ctx->last_plan = nullptr;
+}
+
+void release_device(gemel_ctx *ctx) {
+    drop_plans(ctx);
+    free_placement(ctx);
+    if (ctx->side) (void)hipStreamDestroy(ctx->side);
+    ctx->side = nullptr;
+    ctx->dev_ready = false;
+}
+
+gemel_status materialise(gemel_ctx *ctx) {
+    if (ctx->weights_ready) return GEMEL_OK;
+    gemel_status st = ensure_device(ctx);
+    if (st) return st;
+    drop_plans(ctx);
+    free_placement(ctx);
+
+    // distinct copies in use, in registration order, with their user counts
+    std::vector<std::shared_ptr<Blob>> blobs;
+    std::set<Blob *> seen;
+    for (auto &m : ctx->models)
+        for (auto &l : m->layers)
+            if (l.eff) {
+                if (seen.insert(l.eff.get()).second) {
+                    l.eff->users = 0;
+                    blobs.push_back(l.eff);
+                }
+                l.eff->users++;
+            }
+    size_t w_total = 0, aff_total = 0, max_final = 0;
+    for (auto &b : blobs) {
+        w_total += (size_t)round_up((int64_t)b->w_bytes(), 256);
+        aff_total += (size_t)round_up((int64_t)b->aff_bytes(), 256);
+    }
+    for (auto &m : ctx->models)
+        for (auto &l : m->layers)
+            if (l.eff && l.is_output && l.consumers == 0) max_final = std::max(max_final, l.eff->w_bytes());
+
+    std::vector<char> resident(blobs.size(), 1);
+    size_t staging_bytes = 0;
+    int slots = 0;
+    int64_t slot_bytes = 0;
+    if (ctx->budget && w_total + aff_total > ctx->budget) {
+        slots = ctx->opt.slots;
+        slot_bytes = std::max<int64_t>(ctx->opt.slot_bytes, round_up((int64_t)max_final, 256));
+        staging_bytes = (size_t)slots * (size_t)slot_bytes;
+        if (aff_total + staging_bytes > ctx->budget)
+            return fail(ctx, GEMEL_EBUDGET, "weight budget smaller than scale/shift vectors plus staging slots");
+        size_t avail = ctx->budget - aff_total - staging_bytes;
+        std::vector<size_t> order(blobs.size());
+        std::iota(order.begin(), order.end(), 0);
+        std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) {
+            const bool sa = blobs[a]->users > 1, sb = blobs[b]->users > 1;
+            if (sa != sb) return sa;
+            return blobs[a]->w_bytes() > blobs[b]->w_bytes();
+        });
+        std::fill(resident.begin(), resident.end(), 0);
+        for (size_t i : order) {
+            const size_t need = (size_t)round_up((int64_t)blobs[i]->w_bytes(), 256);
+            if (need <= avail) {
+                resident[i] = 1;
+                avail -= need;
+            }
+        }
+        for (size_t i = 0; i < blobs.size(); ++i)
+            if (!resident[i] && blobs[i]->k * (int64_t)blobs[i]->elem * 8 > slot_bytes)
+                return fail(ctx, GEMEL_EBUDGET, "a weight row block does not fit one staging slot");
+    }
+
+    size_t pool = aff_total;
+    for (size_t i = 0; i < blobs.size(); ++i)
+        if (resident[i]) pool += (size_t)round_up((int64_t)blobs[i]->w_bytes(), 256);
+    if (hipMalloc(&ctx->wpool, pool) != hipSuccess) {
+        ctx->wpool = nullptr;
+        (void)hipGetLastError();
+        return fail(ctx, GEMEL_ENOMEM, "device allocation of the weight pool failed");
+    }
+    ctx->wpool_bytes = pool;
+    size_t off = 0;
+    for (size_t i = 0; i < blobs.size(); ++i) {
+        Blob &b = *blobs[i];
+        ctx->placed.push_back(blobs[i]);
+        b.aff_dev = (float *)((char *)ctx->wpool + off);
+        hipError_t e = hipMemcpy(b.aff_dev, b.scale.data(), b.scale.size() * 4, hipMemcpyHostToDevice);
+        if (e == hipSuccess)
+            e = hipMemcpy(b.aff_dev + b.rows, b.shift.data(), b.shift.size() * 4, hipMemcpyHostToDevice);
+        off += (size_t)round_up((int64_t)b.aff_bytes(), 256);
+        if (e == hipSuccess && resident[i]) {
+            b.w_dev = (char *)ctx->wpool + off;
+            e = hipMemcpy(b.w_dev, b.w.data(), b.w_bytes(), hipMemcpyHostToDevice);
+            off += (size_t)round_up((int64_t)b.w_bytes(), 256);
+        } else if (e == hipSuccess) {
+            e = hipHostMalloc((void **)&b.w_pinned, b.w_bytes(), hipHostMallocDefault);
+            if (e == hipSuccess) std::memcpy(b.w_pinned, b.w.data(), b.w_bytes());
+            else b.w_pinned = nullptr;
+        }
+        if (e != hipSuccess) {
+            free_placement(ctx);
+            return fail(ctx, GEMEL_ENOMEM, std::string("placing weights: ") + hipGetErrorString(e));
+        }
+    }
+    if (slots) {
+        if (hipMalloc(&ctx->staging, staging_bytes) != hipSuccess) {
+            ctx->staging = nullptr;
+            free_placement(ctx);
+            return fail(ctx, GEMEL_ENOMEM, "device allocation of the staging slots failed");
+        }
+        ctx->staging_slots = slots;
+        ctx->staging_slot_bytes = slot_bytes;
+        ctx->ev_copied.resize((size_t)slots);
+        ctx->ev_free.resize((size_t)slots);
+        for (int i = 0; i < slots; ++i) {
+            if (hipEventCreateWithFlags(&ctx->ev_copied[(size_t)i], hipEventDisableTiming) != hipSuccess ||
+                hipEventCreateWithFlags(&ctx->ev_free[(size_t)i], hipEventDisableTiming) != hipSuccess) {
+                free_placement(ctx);
+                return fail(ctx, GEMEL_EDEVICE, "event creation failed");
+            }
+        }
+    }
+    size_t res_w = 0;
+    for (size_t i = 0; i < blobs.size(); ++i)
+        if (resident[i]) res_w += blobs[i]->bytes();
+        else res_w += blobs[i]->aff_bytes();
+    ctx->resident_bytes = res_w;
+    ctx->peak_bytes = std::max(ctx->peak_bytes, pool + staging_bytes);
+    ctx->weights_ready = true;
+    return GEMEL_OK;
+}
+
+// ----------------------------------------------------------------------------
+// plan construction
+// ----------------------------------------------------------------------------
+namespace {
+
+struct TRef {
+    int slot, layer;  // layer -1 = the slot's packed input
+    bool operator<(const TRef &o) const { return slot != o.slot ? slot < o.slot : layer < o.layer; }
+};
+
+struct Tensor {
+    size_t bytes = 0;
+    int first = 0, last = 0;
+    size_t off = 0;
+};
+
+struct Node {
+    int op;
+    std::vector<std::pair<int, int>> mem;  // (slot, layer)
+};
+
+bool direct_output(const Layer &l) {
+    return l.is_output && l.consumers == 0 && (l.op == GEMEL_OP_CONV || l.op == GEMEL_OP_FC);
+}
+
+// Launch configuration of a bf16 implicit-GEMM conv of size M x N x K.
+void pick_conv_config(int64_t M, int64_t N, int64_t K, int &tile, int &splits, int &kps) {
+    tile = N <= 64 ? TILE_128x64 : TILE_128x128;
+    const int64_t bm = conv_tile_bm(tile), bn = conv_tile_bn(tile);
+    const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+    splits = 1;
+    if (tiles < 512) {
+        const int64_t want = (512 + tiles - 1) / tiles;
+        const int64_t maxs = std::max<int64_t>(1, K / (4 * CONV_BK));
+        splits = (int)std::min(want, maxs);
+    }
+    kps = (int)round_up((K + splits - 1) / splits, CONV_BK);
+    splits = (int)((K + kps - 1) / kps);
+}
+
+void pick_fc_config(int64_t N, int64_t K, int &splits, int &kps) {
+    const int64_t blocks = (N + 63) / 64;
+    const int64_t want = (1024 + blocks - 1) / blocks;
+    const int64_t maxs = std::max<int64_t>(1, K / 1024);
+    splits = (int)std::max<int64_t>(1, std::min(want, maxs));
+    kps = (int)round_up((K + splits - 1) / splits, 128);
+    splits = (int)((K + kps - 1) / kps);
+}
+
+}  // namespace
+
+static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, const std::vector<int> &nfr,
+                               Plan &P) {
+    const bool bf16 = ctx->dtype == GEMEL_BF16;
+    const size_t esz = bf16 ? 2 : 4;
+    const int S = (int)ids.size();
+    P.model_ids = ids;
+    P.n_frames = nfr;
+    P.out_base.resize((size_t)S);
+    for (int s = 0, ob = 0; s < S; ++s) {
+        P.out_base[(size_t)s] = ob;
+        ob += (int)ctx->models[(size_t)ids[(size_t)s]]->outputs.size();
+    }
+    auto model = [&](int s) -> const Model & { return *ctx->models[(size_t)ids[(size_t)s]]; };
+    auto layer = [&](int s, int l) -> const Layer & { return model(s).layers[(size_t)l]; };
+
+    // ---- nodes: merged groups batched when compatible ----
+    std::vector<Node> nodes;
+    std::map<std::vector<int64_t>, int> group_node;
+    std::vector<std::vector<int>> node_of((size_t)S);
+    for (int s = 0; s < S; ++s) {
+        const Model &m = model(s);
+        node_of[(size_t)s].assign(m.layers.size(), -1);
+        for (int l = 0; l < (int)m.layers.size(); ++l) {
+            const Layer &L = m.layers[(size_t)l];
+            int nid = -1;
+            if (L.group >= 0 && !ctx->opt.split_merged) {
+                std::vector<int64_t> key = {L.group, L.in_h, L.in_w, L.in_c, L.act,
+                                            (int64_t)(L.slope * 1e6f), L.res >= 0, L.res_mode,
+                                            direct_output(L), L.src1_cp};
+                auto it = group_node.find(key);
+                if (it != group_node.end() && nodes[(size_t)it->second].mem.size() < GEMEL_MAX_SEG) {
+                    nid = it->second;
+                } else {
+                    nid = (int)nodes.size();
+                    nodes.push_back(Node{L.op, {}});
+                    group_node[key] = nid;
+                }
+            } else {
+                nid = (int)nodes.size();
+                nodes.push_back(Node{L.op, {}});
+            }
+            nodes[(size_t)nid].mem.push_back({s, l});
+            node_of[(size_t)s][(size_t)l] = nid;
+        }
+    }
+
+    // ---- topological order of nodes (Kahn); dissolve merged nodes on a cycle ----
+    auto topo = [&](std::vector<int> &order) -> bool {
+        const size_t n = nodes.size();
+        std::vector<std::set<int>> out(n);
+        std::vector<int> indeg(n, 0);
+        for (size_t v = 0; v < n; ++v)
+            for (auto [s, l] : nodes[v].mem) {
+                const Layer &L = layer(s, l);
+                for (int p : {L.src0, L.src1, L.res}) {
+                    if (p < 0) continue;
+                    const int u = node_of[(size_t)s][(size_t)p];
+                    if (u != (int)v && out[(size_t)u].insert((int)v).second) indeg[v]++;
+                }
+            }
+        auto key = [&](int v) {
+            auto [s, l] = nodes[(size_t)v].mem[0];
+            return std::make_pair(l, s);
+        };
+        auto cmp = [&](int a, int b) { return key(a) > key(b); };
+        std::priority_queue<int, std::vector<int>, decltype(cmp)> q(cmp);
+        for (size_t v = 0; v < n; ++v)
+            if (!indeg[v]) q.push((int)v);
+        order.clear();
+        while (!q.empty()) {
+            const int v = q.top();
+            q.pop();
+            order.push_back(v);
+            for (int w : out[(size_t)v])
+                if (--indeg[(size_t)w] == 0) q.push(w);
+        }
+        return order.size() == n;
+    };
+    std::vector<int> order;
+    if (!topo(order)) {
+        std::vector<Node> single;
+        for (auto &nd : nodes)
+            for (auto &mb : nd.mem) {
+                node_of[(size_t)mb.first][(size_t)mb.second] = (int)single.size();
+                single.push_back(Node{nd.op, {mb}});
+            }
+        nodes.swap(single);
+        if (!topo(order)) return fail(ctx, GEMEL_ESTATE, "internal: layer graph has a cycle");
+    }
+
+    // ---- tensors and lifetimes: step 0 = pack, node steps 1.., exports last ----
+    std::map<TRef, Tensor> T;
+    const int last_step = (int)order.size() + 1;
+    for (int s = 0; s < S; ++s) {
+        const Model &m = model(s);
+        Tensor t;
+        t.bytes = (size_t)nfr[(size_t)s] * m.in_h * m.in_w * m.in_cp * esz;
+        t.first = t.last = 0;
+        T[{s, -1}] = t;
+    }
+    for (int step = 0; step < (int)order.size(); ++step)
+        for (auto [s, l] : nodes[(size_t)order[(size_t)step]].mem) {
+            const Layer &L = layer(s, l);
+            if (!direct_output(L)) {
+                Tensor t;
+                t.bytes = (size_t)nfr[(size_t)s] * L.out_h * L.out_w * L.out_cp * esz;
+                t.first = step + 1;
+                t.last = L.is_output ? last_step : step + 1;
+                T[{s, l}] = t;
+            }
+        }
+    auto touch = [&](int s, int p, int step) {
+        auto it = T.find({s, p});
+        if (it != T.end()) it->second.last = std::max(it->second.last, step);
+    };
+    for (int step = 0; step < (int)order.size(); ++step)
+        for (auto [s, l] : nodes[(size_t)order[(size_t)step]].mem) {
+            const Layer &L = layer(s, l);
+            touch(s, L.src0, step + 1);
+            if (L.op == GEMEL_OP_CONCAT) touch(s, L.src1, step + 1);
+            if (L.res >= 0) touch(s, L.res, step + 1);
+        }
+    // offsets: largest first, lowest gap among lifetime-overlapping tensors
+    std::vector<Tensor *> tv;
+    for (auto &kv : T)
+        if (kv.second.bytes) tv.push_back(&kv.second);
+    std::stable_sort(tv.begin(), tv.end(), [](Tensor *a, Tensor *b) { return a->bytes > b->bytes; });
+    std::vector<Tensor *> placed;
+    size_t arena = 0;
+    for (Tensor *t : tv) {
+        std::vector<std::pair<size_t, size_t>> busy;
+        for (Tensor *o : placed)
+            if (!(o->last < t->first || t->last < o->first)) busy.push_back({o->off, o->off + o->bytes});
+        std::sort(busy.begin(), busy.end());
+        size_t cand = 0;
+        for (auto &b : busy) {
+            if (cand + t->bytes <= b.first) break;
+            cand = std::max(cand, (size_t)round_up((int64_t)b.second, 256));
+        }
+        t->off = cand;
+        arena = std::max(arena, cand + (size_t)round_up((int64_t)t->bytes, 256));
+        placed.push_back(t);
+    }
+    P.arena_bytes = arena;
+    if (arena && hipMalloc(&P.arena, arena) != hipSuccess) {
+        P.arena = nullptr;
+        (void)hipGetLastError();
+        return fail(ctx, GEMEL_ENOMEM, "device allocation of the activation arena failed");
+    }
+    auto tptr = [&](int s, int l) -> void * {
+        auto it = T.find({s, l});
+        if (it == T.end() || !it->second.bytes) return nullptr;
+        return (char *)P.arena + it->second.off;
+    };
+
+    // ---- launches ----
+    size_t partial_need = 0;
+    // input pack, grouped by input shape, at most GEMEL_MAX_SEG models each
+    {
+        std::map<std::vector<int>, std::vector<int>> by_shape;
+        for (int s = 0; s < S; ++s) {
+            const Model &m = model(s);
+            by_shape[{m.in_c, m.in_h, m.in_w, m.in_cp}].push_back(s);
+        }
+        for (auto &kv : by_shape)
+            for (size_t b = 0; b < kv.second.size(); b += GEMEL_MAX_SEG) {
+                Launch L;
+                L.type = L_PACK;
+                L.bf16 = bf16;
+                EwArgs &a = L.ew;
+                a.H = kv.first[1]; a.W = kv.first[2]; a.Co = kv.first[3]; a.c_logical = kv.first[0];
+                a.nseg = 0;
+                for (size_t i = b; i < std::min(kv.second.size(), b + GEMEL_MAX_SEG); ++i) {
+                    const int s = kv.second[i];
+                    EwSeg &sg = a.seg[a.nseg];
+                    sg.in0 = nullptr;
+                    sg.in1 = nullptr;
+                    sg.out = tptr(s, -1);
+                    sg.frames = nfr[(size_t)s];
+                    a.max_frames = std::max(a.max_frames, sg.frames);
+                    L.patches.push_back({Patch::FRAMES, s, 0, a.nseg});
+                    a.nseg++;
+                }
+                P.launches.push_back(L);
+            }
+    }
+    auto in_ptr = [&](int s, int p) { return p < 0 ? tptr(s, -1) : tptr(s, p); };
+
+    for (int step = 0; step < (int)order.size(); ++step) {
+        const Node &nd = nodes[(size_t)order[(size_t)step]];
+        const auto [s0, l0] = nd.mem[0];
+        const Layer &L0 = layer(s0, l0);
+        if (L0.op == GEMEL_OP_CONV || L0.op == GEMEL_OP_FC) {
+            Blob *blob = L0.eff.get();
+            int64_t M = 0;
+            for (auto [s, l] : nd.mem) M += (int64_t)nfr[(size_t)s] * layer(s, l).out_h * layer(s, l).out_w;
+            const bool direct = direct_output(L0);
+            const bool fc_small = L0.op == GEMEL_OP_FC && bf16 && M <= 64;
+            const bool fc_f32 = L0.op == GEMEL_OP_FC && !bf16;
+            // weight chunks: a resident blob is one chunk with no copy
+            std::vector<std::pair<int64_t, int64_t>> rows;  // (row0, nrows)
+            if (blob->w_dev) {
+                rows.push_back({0, blob->rows});
+            } else {
+                const int64_t row_bytes = blob->k * (int64_t)blob->elem;
+                int64_t per = ctx->staging_slot_bytes / row_bytes;
+                per = per >= 128 ? per / 128 * 128 : per / 8 * 8;
+                if (direct && per < blob->rows)
+                    return fail(ctx, GEMEL_EBUDGET, "an output layer's weights exceed one staging slot");
+                for (int64_t r0 = 0; r0 < blob->rows; r0 += per) rows.push_back({r0, std::min(per, blob->rows - r0)});
+            }
+            for (auto [row0, nrows] : rows) {
+                Launch Lc;
+                Lc.bf16 = bf16;
+                if (!blob->w_dev) {
+                    Lc.chunk = (int)P.chunks.size();
+                    P.chunks.push_back(Chunk{blob, row0, nrows});
+                    P.streamed_bytes += P.chunks.back().bytes();
+                }
+                const void *wptr = blob->w_dev ? (const void *)((const char *)blob->w_dev) : nullptr;
+                if (fc_small || fc_f32) {
+                    FcArgs &a = Lc.fc;
+                    a.w = wptr;
+                    a.M = (int)M; a.N = (int)nrows; a.K = (int)blob->k;
+                    a.out_cs = L0.out_cp; a.cout = L0.out_c;
+                    a.act = L0.act; a.slope = L0.slope;
+                    a.out_mode = direct ? OUT_NCHW_F32 : OUT_NHWC;
+                    a.nseg = 0;
+                    int f = 0;
+                    for (auto [s, l] : nd.mem) {
+                        if (!nfr[(size_t)s]) continue;
+                        FcSeg &sg = a.seg[a.nseg];
+                        sg.in = in_ptr(s, layer(s, l).src0);
+                        sg.out = direct ? nullptr : (void *)((char *)tptr(s, l) + row0 * esz);
+                        sg.scale = blob->aff_dev + row0;
+                        sg.shift = blob->aff_dev + blob->rows + row0;
+                        sg.f_start = f;
+                        if (direct) Lc.patches.push_back({Patch::OUTPUT, s, layer(s, l).out_index, a.nseg});
+                        f += nfr[(size_t)s];
+                        a.nseg++;
+                    }
+                    if (fc_f32) {
+                        a.k_splits = 1;
+                        a.k_per_split = a.K;
+                        Lc.type = L_FC_F32;
+                    } else {
+                        pick_fc_config(a.N, a.K, a.k_splits, a.k_per_split);
+                        Lc.type = L_FC_BF16;
+                        if (a.k_splits > 1)
+                            partial_need = std::max(partial_need, (size_t)a.k_splits * a.M * a.N * 4);
+                    }
+                    P.launches.push_back(Lc);
+                    if (Lc.type == L_FC_BF16 && a.k_splits > 1) {
+                        Launch R = Lc;
+                        R.type = L_FC_REDUCE;
+                        R.chunk = -1;
+                        P.launches.push_back(R);
+                    }
+                    continue;
+                }
+                ConvArgs &a = Lc.conv;
+                a.w = wptr;
+                a.M = (int)M; a.N = (int)nrows; a.K = (int)blob->k;
+                if (L0.op == GEMEL_OP_CONV) {
+                    a.H = L0.in_h; a.W = L0.in_w; a.Cin = L0.in_cp; a.in_cs = L0.in_cp;
+                    a.Ho = L0.out_h; a.Wo = L0.out_w;
+                    a.kh = L0.kh; a.kw = L0.kw; a.stride = L0.stride; a.pad = L0.pad;
+                } else {  // FC over many frames: a 1x1 conv on a 1x1 map with Cin = K
+                    a.H = a.W = 1; a.Cin = a.in_cs = (int)blob->k;
+                    a.Ho = a.Wo = 1;
+                    a.kh = a.kw = 1; a.stride = 1; a.pad = 0;
+                }
+                a.out_cs = L0.out_cp;
+                a.cout = direct ? std::min<int>((int)nrows, L0.out_c - (int)row0) : L0.out_c;
+                a.act = L0.act; a.slope = L0.slope;
+                a.res_mode = L0.res_mode; a.has_res = L0.res >= 0;
+                a.out_mode = direct ? OUT_NCHW_F32 : OUT_NHWC;
+                a.nseg = 0;
+                int f = 0;
+                for (auto [s, l] : nd.mem) {
+                    if (!nfr[(size_t)s]) continue;
+                    const Layer &L = layer(s, l);
+                    ConvSeg &sg = a.seg[a.nseg];
+                    sg.in = in_ptr(s, L.src0);
+                    sg.res = L.res >= 0 ? (const void *)((char *)tptr(s, L.res) + row0 * esz) : nullptr;
+                    sg.out = direct ? nullptr : (void *)((char *)tptr(s, l) + row0 * esz);
+                    sg.scale = blob->aff_dev + row0;
+                    sg.shift = blob->aff_dev + blob->rows + row0;
+                    sg.f_start = f;
+                    sg.m_start = f * L.out_h * L.out_w;
+                    if (direct) Lc.patches.push_back({Patch::OUTPUT, s, L.out_index, a.nseg});
+                    f += nfr[(size_t)s];
+                    a.nseg++;
+                }
+                if (!a.nseg) continue;
+                if (bf16) {
+                    pick_conv_config(a.M, a.N, a.K, Lc.tile, a.k_splits, a.k_per_split);
+                    Lc.type = L_CONV_BF16;
+                } else {
+                    a.k_splits = 1;
+                    a.k_per_split = a.K;
+                    Lc.type = L_CONV_F32;
+                }
+                P.launches.push_back(Lc);
+                if (a.k_splits > 1) {
+                    partial_need = std::max(partial_need, (size_t)a.k_splits * a.M * a.N * 4);
+                    Launch R;
+                    R.type = L_CONV_REDUCE;
+                    R.bf16 = bf16;
+                    R.patches = Lc.patches;
+                    ReduceArgs &r = R.red;
+                    r.M = a.M; r.N = a.N; r.splits = a.k_splits; r.HWo = a.Ho * a.Wo;
+                    r.out_cs = a.out_cs; r.cout = a.cout; r.act = a.act; r.slope = a.slope;
+                    r.res_mode = a.res_mode; r.has_res = a.has_res; r.out_mode = a.out_mode;
+                    r.nseg = a.nseg;
+                    for (int i = 0; i < a.nseg; ++i) r.seg[i] = a.seg[i];
+                    P.launches.push_back(R);
+                }
+            }
+            continue;
+        }
+        // memory-bound ops: one launch with one segment per member
+        Launch Le;
+        Le.bf16 = bf16;
+        EwArgs &a = Le.ew;
+        a.H = L0.in_h; a.W = L0.in_w; a.C = L0.in_cp;
+        a.Ho = L0.out_h; a.Wo = L0.out_w; a.Co = L0.out_cp;
+        a.k = L0.kh; a.stride = L0.stride; a.pad = L0.pad;
+        a.C1 = L0.src1_cp;
+        a.nseg = 0;
+        for (auto [s, l] : nd.mem) {
+            if (!nfr[(size_t)s]) continue;
+            const Layer &L = layer(s, l);
+            EwSeg &sg = a.seg[a.nseg++];
+            sg.in0 = in_ptr(s, L.src0);
+            sg.in1 = L.op == GEMEL_OP_CONCAT ? in_ptr(s, L.src1) : nullptr;
+            sg.out = tptr(s, l);
+            sg.frames = nfr[(size_t)s];
+            a.max_frames = std::max(a.max_frames, sg.frames);
+        }
+        if (!a.nseg) continue;
+        switch (L0.op) {
+        case GEMEL_OP_MAXPOOL: Le.type = L_MAXPOOL; break;
+        case GEMEL_OP_AVGPOOL: Le.type = L_AVGPOOL; break;
+        case GEMEL_OP_UPSAMPLE2X: Le.type = L_UPSAMPLE; break;
+        default: Le.type = L_CONCAT; break;
+        }
+        P.launches.push_back(Le);
+    }
+    // outputs that are also read internally (or not conv/fc): export to NCHW f32
+    for (int s = 0; s < S; ++s) {
+        const Model &m = model(s);
+        for (int l : m.outputs) {
+            const Layer &L = m.layers[(size_t)l];
+            if (direct_output(L)) continue;
+            Launch Le;
+            Le.type = L_EXPORT;
+            Le.bf16 = bf16;
+            EwArgs &a = Le.ew;
+            a.H = L.out_h; a.W = L.out_w; a.C = L.out_cp; a.c_logical = L.out_c;
+            a.nseg = 1;
+            a.seg[0].in0 = tptr(s, l);
+            a.seg[0].in1 = nullptr;
+            a.seg[0].out = nullptr;
+            a.seg[0].frames = nfr[(size_t)s];
+            a.max_frames = a.seg[0].frames;
+            Le.patches.push_back({Patch::OUTPUT, s, L.out_index, 0});
+            P.launches.push_back(Le);
+        }
+    }
+    if (partial_need) {
+        if (hipMalloc((void **)&P.partial, partial_need) != hipSuccess) {
+            P.partial = nullptr;
+            (void)hipGetLastError();
+            return fail(ctx, GEMEL_ENOMEM, "device allocation of the split-K buffer failed");
+        }
+        P.partial_bytes = partial_need;
+        for (auto &L : P.launches) {
+            L.conv.partial = P.partial;
+            L.red.partial = P.partial;
+            L.fc.partial = P.partial;
+        }
+    }
+    return GEMEL_OK;
+}
+
+// ----------------------------------------------------------------------------
+// inference round
+// ----------------------------------------------------------------------------
+namespace {
+
+struct CallPtrs {
+    std::vector<const void *> frames;  // per slot
+    std::vector<void *> outputs;       // per slot output, flattened by slot
+};
+
+hipError_t launch_one(Launch &L, const CallPtrs &cp, const Plan &P, void *wptr, hipStream_t st) {
+    for (const Patch &p : L.patches) {
+        if (p.kind == Patch::FRAMES) {
+            L.ew.seg[p.seg].in0 = cp.frames[(size_t)p.slot];
+        } else {
+            void *o = cp.outputs[(size_t)(P.out_base[(size_t)p.slot] + p.out_idx)];
+            switch (L.type) {
+            case L_CONV_BF16:
+            case L_CONV_F32: L.conv.seg[p.seg].out = o; break;
+            case L_CONV_REDUCE: L.red.seg[p.seg].out = o; break;
+            case L_FC_BF16:
+            case L_FC_F32:
+            case L_FC_REDUCE: L.fc.seg[p.seg].out = o; break;
+            default: L.ew.seg[p.seg].out = o; break;
+            }
+        }
+    }
+    if (wptr) {
+        L.conv.w = wptr;
+        L.fc.w = wptr;
+    }
+    switch (L.type) {
+    case L_PACK: return launch_pack(L.ew, L.bf16, st);
+    case L_CONV_BF16: return launch_conv_bf16(L.conv, L.tile, st);
+    case L_CONV_F32: return launch_conv_f32(L.conv, st);
+    case L_CONV_REDUCE: return launch_conv_reduce(L.red, L.bf16, st);
+    case L_FC_BF16: return launch_fc_bf16(L.fc, st);
+    case L_FC_F32: return launch_fc_f32(L.fc, st);
+    case L_FC_REDUCE: return launch_fc_reduce(L.fc, L.bf16, st);
+    case L_MAXPOOL: return launch_maxpool(L.ew, L.bf16, st);
+    case L_AVGPOOL: return launch_avgpool(L.ew, L.bf16, st);
+    case L_UPSAMPLE: return launch_upsample2x(L.ew, L.bf16, st);
+    case L_CONCAT: return launch_concat(L.ew, L.bf16, st);
+    case L_EXPORT: return launch_export(L.ew, L.bf16, st);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+static gemel_status enqueue(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStream_t st) {
+    const int nslots = ctx->staging_slots;
+    const int nch = (int)P.chunks.size();
+    int next_copy = 0;
+    auto slot_ptr = [&](int c) { return (char *)ctx->staging + (size_t)(c % nslots) * ctx->staging_slot_bytes; };
+    auto issue_copies = [&](int upto) -> gemel_status {
+        for (; next_copy < nch && next_copy <= upto; ++next_copy) {
+            const Chunk &ch = P.chunks[(size_t)next_copy];
+            const int slot = next_copy % nslots;
+            ctx->copies_issued++;
+            if (ctx->opt.fail_copy_at && ctx->copies_issued == ctx->opt.fail_copy_at) {
+                ctx->opt.fail_copy_at = 0;
+                return fail(ctx, GEMEL_EDEVICE, "injected failure of a weight copy");
+            }
+            HIPCHK(hipStreamWaitEvent(ctx->side, ctx->ev_free[(size_t)slot], 0), "hipStreamWaitEvent");
+            HIPCHK(hipMemcpyAsync(slot_ptr(next_copy), ch.blob->w_pinned + (size_t)(ch.row0 * ch.blob->k) * ch.blob->elem,
+                                  ch.bytes(), hipMemcpyHostToDevice, ctx->side),
+                   "hipMemcpyAsync (weight swap-in)");
+            HIPCHK(hipEventRecord(ctx->ev_copied[(size_t)slot], ctx->side), "hipEventRecord");
+        }
+        return GEMEL_OK;
+    };
+    if (nch) {
+        gemel_status s = issue_copies(nslots - 1);
+        if (s) return s;
+    }
+    for (Launch &L : P.launches) {
+        void *wptr = nullptr;
+        if (L.chunk >= 0) {
+            gemel_status s = issue_copies(L.chunk + nslots - 1);
+            if (s) return s;
+            HIPCHK(hipStreamWaitEvent(st, ctx->ev_copied[(size_t)(L.chunk % nslots)], 0), "hipStreamWaitEvent");
+            wptr = slot_ptr(L.chunk);
+        }
+        hipError_t e = launch_one(L, cp, P, wptr, st);
+        if (e != hipSuccess) return fail(ctx, GEMEL_EDEVICE, std::string("kernel launch: ") + hipGetErrorString(e));
+        if (L.chunk >= 0) HIPCHK(hipEventRecord(ctx->ev_free[(size_t)(L.chunk % nslots)], st), "hipEventRecord");
+    }
+    return GEMEL_OK;
+}
+
+gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, const void *const *frames,
+                 const int32_t *n_frames, void *const *outputs, hipStream_t stream) {
+    // canonical slot order: active models sorted by id
+    std::vector<std::pair<int, int>> act;  // (model id, caller index)
+    std::vector<int> caller_out_base((size_t)n_models);
+    for (int i = 0, ob = 0; i < n_models; ++i) {
+        caller_out_base[(size_t)i] = ob;
+        ob += (int)ctx->models[(size_t)model_ids[i]]->outputs.size();
+        if (n_frames[i] > 0) act.push_back({model_ids[i], i});
+    }
+    if (act.empty()) return GEMEL_OK;
+    std::sort(act.begin(), act.end());
+    std::vector<int> ids, nfr, key;
+    for (auto [id, ci] : act) {
+        ids.push_back(id);
+        nfr.push_back(n_frames[ci]);
+        key.push_back(id);
+        key.push_back(n_frames[ci]);
+    }
+    DeviceScope scope(ctx->device);
+    gemel_status st = materialise(ctx);
+    if (st) return st;
+    auto it = ctx->plans.find(key);
+    if (it == ctx->plans.end()) {
+        auto P = std::make_unique<Plan>();
+        st = build_plan(ctx, ids, nfr, *P);
+        if (st) {
+            if (P->arena) (void)hipFree(P->arena);
+            if (P->partial) (void)hipFree(P->partial);
+            return st;
+        }
+        it = ctx->plans.emplace(key, std::move(P)).first;
+    }
+    Plan &P = *it->second;
+    ctx->last_plan = &P;
+    CallPtrs cp;
+    for (auto [id, ci] : act) {
+        cp.frames.push_back(frames[ci]);
+        const int no = (int)ctx->models[(size_t)id]->outputs.size();
+        for (int o = 0; o < no; ++o) cp.outputs.push_back(outputs[caller_out_base[(size_t)ci] + o]);
+    }
+    const bool graphable = ctx->opt.use_graph && P.chunks.empty() && stream != nullptr;
+    if (!graphable) return enqueue(ctx, P, cp, stream);
+    if (P.graph && P.graph_stream == stream && P.graph_frames == cp.frames && P.graph_outputs == cp.outputs) {
+        HIPCHK(hipGraphLaunch(P.graph, stream), "hipGraphLaunch");
+        ctx->graph_replays++;
+        return GEMEL_OK;
+    }
+    if (P.graph) {
+        (void)hipGraphExecDestroy(P.graph);
+        P.graph = nullptr;
+    }
+    HIPCHK(hipStreamBeginCapture(stream, hipStreamCaptureModeThreadLocal), "hipStreamBeginCapture");
+    st = enqueue(ctx, P, cp, stream);
+    hipGraph_t g = nullptr;
+    hipError_t ec = hipStreamEndCapture(stream, &g);
+    if (st) {
+        if (g) (void)hipGraphDestroy(g);
+        return st;
+    }
+    if (ec != hipSuccess) return fail(ctx, GEMEL_EDEVICE, std::string("hipStreamEndCapture: ") + hipGetErrorString(ec));
+    hipGraphExec_t ex = nullptr;
+    ec = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    if (ec != hipSuccess) return fail(ctx, GEMEL_EDEVICE, std::string("hipGraphInstantiate: ") + hipGetErrorString(ec));
+    P.graph = ex;
+    P.graph_stream = stream;
+    P.graph_frames = cp.frames;
+    P.graph_outputs = cp.outputs;
+    HIPCHK(hipGraphLaunch(P.graph, stream), "hipGraphLaunch");
+    return GEMEL_OK;
+}
+
+}  // namespace gemel

@@ -1,0 +1,268 @@
+"""ctypes binding of libgemel (include/gemel.h): the same entry points,
+argument marshalling only. Every layer of every model runs in the HIP
+kernels of libgemel.so; there is no Python or CPU fallback: importing this
+module without the built library raises.
+
+``Context`` wraps the calls for Python callers: layers are given as dicts
+(op, src0, src1, cin, cout, kh, kw, stride, pad, act, res, res_mode, out;
+see workloads/zoo.py for the format) with per-layer parameter dicts
+(w, b, bn = (gamma, beta, mean, var, eps)); device buffers and streams come
+from torch.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libgemel.so")
+
+# status codes
+OK, EINVAL, ENOMEM, ESHAPE, ENOTMERGEABLE, EBUDGET, EDEVICE, ESTATE = \
+    0, -1, -2, -3, -4, -5, -6, -7
+STATUS_NAMES = {0: "OK", -1: "EINVAL", -2: "ENOMEM", -3: "ESHAPE",
+                -4: "ENOTMERGEABLE", -5: "EBUDGET", -6: "EDEVICE",
+                -7: "ESTATE"}
+F32, BF16 = 0, 1
+OP = {"conv": 0, "fc": 1, "maxpool": 2, "avgpool": 3, "upsample": 4,
+      "concat": 5}
+ACT = {"none": 0, "relu": 1, "leaky": 2}
+RES_MODE = {"add_act": 0, "act_add": 1}
+LEAKY_SLOPE = 0.1
+
+Q_UNMERGED_BYTES, Q_MERGED_BYTES, Q_RESIDENT_BYTES, Q_PEAK_BYTES, \
+    Q_STREAMED_BYTES, Q_ACTIVATION_BYTES, Q_LAUNCHES, Q_N_MODELS, \
+    Q_GRAPH_REPLAYS = range(9)
+OPT_USE_GRAPH, OPT_SWAP_SLOT_BYTES, OPT_SWAP_SLOTS, OPT_FAIL_COPY_AT, \
+    OPT_SPLIT_MERGED, OPT_WEIGHT_BUDGET = range(6)
+
+EXPORTED = ("gemel_create", "gemel_register_model", "gemel_merge",
+            "gemel_infer", "gemel_model_outputs", "gemel_output_shape",
+            "gemel_query", "gemel_set_option", "gemel_last_error",
+            "gemel_destroy")
+
+_fp = ctypes.POINTER(ctypes.c_float)
+
+
+class LayerDesc(ctypes.Structure):
+    _fields_ = [("op", ctypes.c_int32), ("src0", ctypes.c_int32),
+                ("src1", ctypes.c_int32), ("cin", ctypes.c_int32),
+                ("cout", ctypes.c_int32), ("kh", ctypes.c_int32),
+                ("kw", ctypes.c_int32), ("stride", ctypes.c_int32),
+                ("pad", ctypes.c_int32), ("act", ctypes.c_int32),
+                ("act_slope", ctypes.c_float), ("res_src", ctypes.c_int32),
+                ("res_mode", ctypes.c_int32), ("is_output", ctypes.c_int32),
+                ("weight", _fp), ("bias", _fp), ("bn_gamma", _fp),
+                ("bn_beta", _fp), ("bn_mean", _fp), ("bn_var", _fp),
+                ("bn_eps", ctypes.c_float)]
+
+
+class Member(ctypes.Structure):
+    _fields_ = [("model_id", ctypes.c_int32), ("layer", ctypes.c_int32)]
+
+
+class Group(ctypes.Structure):
+    _fields_ = [("n_members", ctypes.c_int32),
+                ("members", ctypes.POINTER(Member))]
+
+
+class GemelError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"{STATUS_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def lib():
+    """Load libgemel.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with "
+                "`python -m paper_2201_07705_amd.build` (no fallback exists)")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+        L.gemel_create.argtypes = [ctypes.POINTER(vp), i32, i32,
+                                   ctypes.c_uint64]
+        L.gemel_register_model.argtypes = [vp, ctypes.POINTER(LayerDesc), i32,
+                                           i32, i32, i32,
+                                           ctypes.POINTER(i32)]
+        L.gemel_merge.argtypes = [vp, ctypes.POINTER(Group), i32]
+        L.gemel_infer.argtypes = [vp, ctypes.POINTER(i32), i32,
+                                  ctypes.POINTER(vp), ctypes.POINTER(i32),
+                                  ctypes.POINTER(vp), vp]
+        L.gemel_model_outputs.argtypes = [vp, i32, ctypes.POINTER(i32)]
+        L.gemel_output_shape.argtypes = [vp, i32, i32, i32,
+                                         ctypes.POINTER(i64)]
+        L.gemel_query.argtypes = [vp, i32, ctypes.POINTER(i64)]
+        L.gemel_set_option.argtypes = [vp, i32, i64]
+        L.gemel_last_error.argtypes = [vp]
+        L.gemel_last_error.restype = ctypes.c_char_p
+        L.gemel_destroy.argtypes = [vp]
+        for name in EXPORTED:
+            if name != "gemel_last_error":
+                getattr(L, name).restype = ctypes.c_int32
+        _lib = L
+    return _lib
+
+
+def _fptr(a):
+    return None if a is None else a.ctypes.data_as(_fp)
+
+
+def layer_descs(layers, params):
+    """Marshal layer dicts + parameter dicts into a LayerDesc array. Returns
+    (array, keepalive list of the float32 arrays it points into)."""
+    arr = (LayerDesc * len(layers))()
+    keep = []
+    for i, (l, p) in enumerate(zip(layers, params)):
+        d = arr[i]
+        d.op = OP[l["op"]]
+        d.src0, d.src1 = l["src0"], l.get("src1", -1)
+        d.cin, d.cout = l["cin"], l["cout"]
+        d.kh, d.kw = l.get("kh", 1), l.get("kw", 1)
+        d.stride, d.pad = l.get("stride", 1), l.get("pad", 0)
+        d.act = ACT[l.get("act", "none")]
+        d.act_slope = LEAKY_SLOPE if l.get("act") == "leaky" else 0.0
+        d.res_src = l.get("res", -1)
+        d.res_mode = RES_MODE[l.get("res_mode", "add_act")]
+        d.is_output = 1 if l.get("out") else 0
+        if p is not None:
+            w = np.ascontiguousarray(p["w"], np.float32)
+            keep.append(w)
+            d.weight = _fptr(w)
+            if p.get("b") is not None:
+                b = np.ascontiguousarray(p["b"], np.float32)
+                keep.append(b)
+                d.bias = _fptr(b)
+            if p.get("bn") is not None:
+                g, be, mu, var, eps = p["bn"]
+                vs = [np.ascontiguousarray(v, np.float32)
+                      for v in (g, be, mu, var)]
+                keep.extend(vs)
+                d.bn_gamma, d.bn_beta, d.bn_mean, d.bn_var = \
+                    [_fptr(v) for v in vs]
+                d.bn_eps = eps
+    return arr, keep
+
+
+class Context:
+    """One libgemel context on one device."""
+
+    def __init__(self, device=0, dtype="bf16", budget=0):
+        self._h = ctypes.c_void_p()
+        st = lib().gemel_create(ctypes.byref(self._h), device,
+                                BF16 if dtype == "bf16" else F32, budget)
+        if st != OK:
+            raise GemelError(st, lib().gemel_last_error(None).decode())
+        self.dtype = dtype
+        self.device = device
+        self._in_shape = {}
+        self._out_ops = {}
+
+    # -- raw calls (status returned, message on failure) --
+    def _check(self, st):
+        if st != OK:
+            raise GemelError(st, lib().gemel_last_error(self._h).decode())
+        return st
+
+    def register_model(self, layers, params, in_chw):
+        arr, keep = layer_descs(layers, params)
+        mid = ctypes.c_int32(-1)
+        self._check(lib().gemel_register_model(
+            self._h, arr, len(layers), in_chw[0], in_chw[1], in_chw[2],
+            ctypes.byref(mid)))
+        del keep
+        self._in_shape[mid.value] = tuple(in_chw)
+        self._out_ops[mid.value] = [l["op"] for l in layers if l.get("out")]
+        return mid.value
+
+    def merge(self, groups):
+        """groups: list of lists of (model_id, layer_index); first = source."""
+        n = len(groups)
+        garr = (Group * max(n, 1))()
+        keep = []
+        for i, g in enumerate(groups):
+            m = (Member * len(g))(*[Member(a, b) for a, b in g])
+            keep.append(m)
+            garr[i].n_members = len(g)
+            garr[i].members = ctypes.cast(m, ctypes.POINTER(Member))
+        self._check(lib().gemel_merge(self._h, garr, n))
+
+    def n_outputs(self, model_id):
+        n = ctypes.c_int32()
+        self._check(lib().gemel_model_outputs(self._h, model_id,
+                                              ctypes.byref(n)))
+        return n.value
+
+    def output_shape(self, model_id, idx, n_frames):
+        dims = (ctypes.c_int64 * 4)()
+        self._check(lib().gemel_output_shape(self._h, model_id, idx,
+                                             n_frames, dims))
+        if self._out_ops.get(model_id, [None] * (idx + 1))[idx] == "fc":
+            return (n_frames, dims[1])
+        return (n_frames, dims[1], dims[2], dims[3])
+
+    def query(self, key):
+        v = ctypes.c_int64()
+        self._check(lib().gemel_query(self._h, key, ctypes.byref(v)))
+        return v.value
+
+    def set_option(self, key, value):
+        self._check(lib().gemel_set_option(self._h, key, value))
+
+    def infer_raw(self, model_ids, frame_ptrs, n_frames, out_ptrs, stream):
+        n = len(model_ids)
+        ids = (ctypes.c_int32 * n)(*model_ids)
+        fp = (ctypes.c_void_p * n)(*frame_ptrs)
+        nf = (ctypes.c_int32 * n)(*n_frames)
+        op = (ctypes.c_void_p * max(len(out_ptrs), 1))(*out_ptrs)
+        return lib().gemel_infer(self._h, ids, n, fp, nf, op,
+                                 ctypes.c_void_p(stream))
+
+    def close(self):
+        if self._h:
+            st = lib().gemel_destroy(self._h)
+            self._h = ctypes.c_void_p()
+            if st != OK:
+                raise GemelError(st, "destroy found a device fault")
+
+    def __del__(self):
+        try:
+            if self._h:
+                lib().gemel_destroy(self._h)
+        except Exception:
+            pass
+
+    # -- torch conveniences --
+    def alloc_outputs(self, model_ids, n_frames, device="cuda"):
+        import torch
+        outs = []
+        for mid, n in zip(model_ids, n_frames):
+            outs.append([torch.empty(self.output_shape(mid, i, n),
+                                     dtype=torch.float32, device=device)
+                         for i in range(self.n_outputs(mid))])
+        return outs
+
+    def infer(self, model_ids, frames, stream=None, outputs=None):
+        """frames: list of float32 NCHW cuda tensors, one per model id.
+        Returns (and fills) per-model lists of float32 output tensors."""
+        import torch
+        n_frames = [int(f.shape[0]) for f in frames]
+        for f in frames:
+            assert f.dtype == torch.float32 and f.is_cuda and \
+                f.is_contiguous()
+        if outputs is None:
+            outputs = self.alloc_outputs(model_ids, n_frames,
+                                         frames[0].device)
+        out_ptrs = [t.data_ptr() for o in outputs for t in o]
+        s = stream if stream is not None else torch.cuda.current_stream()
+        self._check(self.infer_raw(model_ids, [f.data_ptr() for f in frames],
+                                   n_frames, out_ptrs, s.cuda_stream))
+        return outputs

@@ -1,0 +1,141 @@
+"""Layer-level parity of the HIP kernels against the oracle, through the C
+ABI: single conv/FC/pool/routing layers and small graphs, chosen to span
+several tiles, ragged M/N/K tails, split-K, padded channel counts, both
+residual orders, the NHWC internal store and the NCHW fp32 output store,
+and merged launches whose segments carry different frame counts."""
+
+import numpy as np
+import pytest
+
+from harness import GpuWorkload, compare, log, oracle_outputs
+from workloads.configs import ModelSpec, Workload
+
+pytestmark = pytest.mark.gpu
+
+BF16_LAYER_TOL = 1e-2   # one or two bf16 roundings of the activations
+F32_LAYER_TOL = 1e-4
+
+
+def L(name, op, src0, **kw):
+    d = dict(name=name, op=op, src0=src0, src1=-1, cin=0, cout=0, kh=1, kw=1,
+             stride=1, pad=0, act="none", res=-1, res_mode="add_act",
+             bias=False, bn=False, out=False)
+    d.update(kw)
+    return d
+
+
+def conv(name, src, cin, cout, k, s=1, p=0, **kw):
+    return L(name, "conv", src, cin=cin, cout=cout, kh=k, kw=k, stride=s,
+             pad=p, **kw)
+
+
+def run_case(layers_per_model, in_chw, frames, dtype, groups=(), seed=7,
+             tol=None, dist="normal"):
+    models = [ModelSpec(f"m{i}", "custom", lay, n, in_chw)
+              for i, (lay, n) in enumerate(zip(layers_per_model, frames))]
+    wl = Workload(f"case{seed}", seed, dtype, models, list(groups), dist)
+    params = [wl.params(i) for i in range(len(models))]
+    fr = [wl.frames(i) for i in range(len(models))]
+    g = GpuWorkload(wl, params)
+    try:
+        got = g.run(fr)
+    finally:
+        g.close()
+    ref = oracle_outputs(wl, params, fr)
+    tol = tol or (BF16_LAYER_TOL if dtype == "bf16" else F32_LAYER_TOL)
+    return compare(wl, got, ref, tol=tol, check_argmax=False)
+
+
+CONV_CASES = [
+    # cin, cout, k, stride, pad, hw, frames
+    (3, 64, 7, 2, 3, 64, 2),
+    (64, 64, 3, 1, 1, 20, 3),
+    (64, 256, 1, 1, 0, 14, 2),
+    (128, 96, 3, 2, 1, 15, 2),
+    (256, 255, 1, 1, 0, 13, 2),
+    (512, 512, 3, 1, 1, 7, 2),
+    (32, 64, 3, 2, 1, 33, 1),
+    (16, 40, 3, 1, 1, 9, 5),
+    (1024, 64, 1, 1, 0, 5, 3),
+]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("case", CONV_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_conv_layer_output_store(dtype, case):
+    cin, cout, k, s, p, hw, n = case
+    log(f"conv {case} {dtype}")
+    lay = [conv("c", -1, cin, cout, k, s, p, bias=True, act="relu", out=True)]
+    run_case([lay], (cin, hw, hw), [n], dtype)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("case", CONV_CASES[:6], ids=lambda c: "x".join(map(str, c)))
+def test_conv_layer_internal_store_and_export(dtype, case):
+    cin, cout, k, s, p, hw, n = case
+    log(f"conv+export {case} {dtype}")
+    lay = [conv("c", -1, cin, cout, k, s, p, bn=True, act="leaky"),
+           L("copy", "maxpool", 0, cin=cout, cout=cout, kh=1, kw=1, out=True)]
+    run_case([lay], (cin, hw, hw), [n], dtype)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("act,mode", [("relu", "add_act"), ("leaky", "act_add"),
+                                      ("none", "add_act")])
+def test_conv_residual_orders(dtype, act, mode):
+    log(f"residual {act} {mode} {dtype}")
+    lay = [conv("a", -1, 32, 64, 3, 1, 1, bn=True, act="relu"),
+           conv("b", 0, 64, 64, 3, 1, 1, bn=True, act=act, res=0,
+                res_mode=mode),
+           conv("c", 1, 64, 128, 1, 1, 0, bias=True, act="relu", out=True)]
+    run_case([lay], (32, 17, 17), [3], dtype)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("frames", [1, 3, 8, 20, 80])
+def test_fc_stack_small_and_large_batches(dtype, frames):
+    log(f"fc stack frames={frames} {dtype}")
+    # NCHW flatten of a 64 x 7 x 7 map, two FC layers (internal + output)
+    lay = [conv("c", -1, 8, 64, 3, 1, 1, bias=True, act="relu"),
+           L("fc1", "fc", 0, cin=64 * 49, cout=520, bias=True, act="relu"),
+           L("fc2", "fc", 1, cin=520, cout=1000, bias=True, out=True)]
+    run_case([lay], (8, 7, 7), [frames], dtype)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_pools(dtype):
+    log(f"pools {dtype}")
+    lay = [conv("c", -1, 3, 64, 3, 2, 1, bn=True, act="relu"),
+           L("mp3", "maxpool", 0, cin=64, cout=64, kh=3, kw=3, stride=2,
+             pad=1),
+           L("mp2", "maxpool", 1, cin=64, cout=64, kh=2, kw=2, stride=2),
+           L("gap", "avgpool", 2, cin=64, cout=64),
+           L("fc", "fc", 3, cin=64, cout=10, bias=True, out=True)]
+    run_case([lay], (3, 57, 57), [4], dtype)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_upsample_concat_route(dtype):
+    log(f"route {dtype}")
+    lay = [conv("a", -1, 8, 32, 3, 2, 1, bn=True, act="leaky"),   # 16x16
+           conv("b", 0, 32, 64, 3, 2, 1, bn=True, act="leaky"),   # 8x8
+           conv("r", 1, 64, 16, 1, 1, 0, bn=True, act="leaky"),
+           L("up", "upsample", 2, cin=16, cout=16),                # 16x16
+           L("cat", "concat", 3, src1=0, cin=16, cout=48),
+           conv("o", 4, 48, 255, 1, 1, 0, bias=True, out=True),
+           conv("o2", 1, 64, 24, 3, 1, 1, bias=True, out=True)]
+    run_case([lay], (8, 32, 32), [3], dtype)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_merged_segments_with_different_frame_counts(dtype):
+    log(f"merged segments {dtype}")
+    body = [conv("c1", -1, 3, 32, 3, 1, 1, bn=True, act="relu"),
+            conv("c2", 0, 32, 64, 3, 2, 1, bn=True, act="relu"),
+            conv("c3", 1, 64, 64, 3, 1, 1, bn=True, act="relu", res=1),
+            L("gap", "avgpool", 2, cin=64, cout=64)]
+    heads = [L("fc", "fc", 3, cin=64, cout=c, bias=True, out=True)
+             for c in (10, 37, 5)]
+    models = [body + [h] for h in heads]
+    groups = [[(0, i), (1, i), (2, i)] for i in range(4)]
+    run_case(models, (3, 24, 24), [2, 5, 1], dtype, groups)

@@ -1,0 +1,96 @@
+"""End-to-end parity of the merged workloads against the oracle.
+
+Reduced-resolution variants are checked on every output element (the
+oracle finishes them in seconds); the full-size workloads run in the same
+launch configuration as the benchmark and are checked on sampled frames:
+the oracle evaluates only the sampled frames (frames are independent, so
+the outputs of a frame do not depend on the other frames in the batch)."""
+
+import numpy as np
+import pytest
+
+from harness import GpuWorkload, compare, log, oracle_outputs
+from workloads import configs
+
+pytestmark = pytest.mark.gpu
+
+
+def _full_check(wl, budget=0, tag=""):
+    params = [wl.params(i) for i in range(len(wl.models))]
+    fr = [wl.frames(i) for i in range(len(wl.models))]
+    log(f"{tag}: gpu run")
+    g = GpuWorkload(wl, params, budget=budget)
+    try:
+        got = g.run(fr)
+    finally:
+        g.close()
+    log(f"{tag}: oracle")
+    ref = oracle_outputs(wl, params, fr)
+    e = compare(wl, got, ref, tag=tag)
+    log(f"{tag}: worst normwise error {e:.3e}")
+
+
+def _sampled_check(wl, pick, budget=0, tag=""):
+    """GPU on every frame; oracle on frames ``pick(model_index, n)``."""
+    params = [wl.params(i) for i in range(len(wl.models))]
+    fr = [wl.frames(i) for i in range(len(wl.models))]
+    log(f"{tag}: gpu run ({wl.total_frames()} frames)")
+    g = GpuWorkload(wl, params, budget=budget)
+    try:
+        got = g.run(fr)
+    finally:
+        g.close()
+    idx = [pick(i, m.n_frames) for i, m in enumerate(wl.models)]
+    log(f"{tag}: oracle on frames {idx}")
+    sub = [f[i] for f, i in zip(fr, idx)]
+    ref = oracle_outputs(wl, params, sub)
+    got_sub = [[o[i] for o in outs] for outs, i in zip(got, idx)]
+    e = compare(wl, got_sub, ref, tag=tag)
+    log(f"{tag}: worst normwise error {e:.3e}")
+
+
+def test_tiny2_fp32_full():
+    _full_check(configs.tiny2(), tag="tiny2")
+
+
+def test_tiny2_fp32_more_frames():
+    _full_check(configs.tiny2(res=40, frames=7), tag="tiny2-40px")
+
+
+def test_resnet18x2_reduced():
+    _full_check(configs.resnet18x2(res=96, frames=3), tag="r18x2-96px")
+
+
+def test_resnet18x2_full_size_sampled():
+    _sampled_check(configs.resnet18x2(),
+                   lambda i, n: [0, n - 1] if i == 0 else [1, 2],
+                   tag="r18x2")
+
+
+def test_r50_vgg16_reduced():
+    _full_check(configs.r50x2_vgg16x2(res=64, frames=2), tag="r50vgg-64px")
+
+
+def test_r50_vgg16_full_size_sampled():
+    _sampled_check(configs.r50x2_vgg16x2(),
+                   lambda i, n: [(3 * i) % n, n - 1 - i],
+                   tag="r50vgg")
+
+
+def test_yolov3x3_reduced():
+    _full_check(configs.yolov3x3(res=96, frames=2), tag="yolo-96px")
+
+
+def test_yolov3x3_full_size_sampled():
+    _sampled_check(configs.yolov3x3(), lambda i, n: [(i + 1) % n],
+                   tag="yolo")
+
+
+def test_mix8_reduced_with_budget():
+    _full_check(configs.mix8_budget40(res=32, frames=2), budget="auto",
+                tag="mix8-32px")
+
+
+def test_mix8_full_size_sampled_with_budget():
+    _sampled_check(configs.mix8_budget40(), lambda i, n: [(5 * i) % n],
+                   budget="auto", tag="mix8")
