@@ -78,15 +78,39 @@ class GemelError(RuntimeError):
 _lib = None
 
 
+def _hip_runtimes():
+    """Paths of every HIP runtime library mapped into this process."""
+    paths = set()
+    try:
+        with open("/proc/self/maps") as f:
+            for line in f:
+                if "libamdhip64" in line:
+                    paths.add(os.path.realpath(line.split()[-1]))
+    except OSError:
+        pass
+    return paths
+
+
 def lib():
-    """Load libgemel.so (raises if it has not been built)."""
+    """Load libgemel.so (raises if it has not been built).
+
+    torch brings its own HIP runtime whose soname equals the system one; it
+    is loaded first so that libgemel binds to the same runtime instance
+    (two HIP runtimes in one process do not share the device)."""
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(
                 f"{LIB_PATH} is missing: build it with "
                 "`python -m paper_2201_07705_amd.build` (no fallback exists)")
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         L = ctypes.CDLL(LIB_PATH)
+        rts = _hip_runtimes()
+        if len(rts) > 1:
+            raise RuntimeError(f"two HIP runtimes are loaded: {sorted(rts)}")
         vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
         L.gemel_create.argtypes = [ctypes.POINTER(vp), i32, i32,
                                    ctypes.c_uint64]
