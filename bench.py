@@ -1,0 +1,198 @@
+#!/usr/bin/env python3
+"""Merged multi-model inference throughput on one MI355X.
+
+One step is one inference round of a merged workload: every model's frame
+batch goes through the whole hot path (input pack, merged and per-model
+convs with fused epilogues, pools, routing, FC heads, fp32 outputs) in one
+gemel_infer call, inputs already resident in HBM. The default workload is
+two ResNet-50 sharing stem + layer1..3 and two VGG-16 sharing all convs, 8
+frames each at 3x224x224 (the ResNet-50 configuration named by the
+throughput target); --config selects any other workload.
+
+Prints one JSON line: whole-job frames/s, ms per step, the roofline of the
+dominant kernel family (HIP-event timings collected by the library with
+profiling on, in a separate pass after the timed region), and the CPU
+oracle timed on a bounded sample of the same workload.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("merged multi-model frames/sec on 1 GPU; conv TFLOP/s as % of "
+          "bf16 MFMA peak")
+PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense
+PEAK_FP32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+DESCRIPTIONS = {
+    "tiny2": "2 tiny CNNs sharing 2 convs, fp32, 1 frame each, 3x32x32",
+    "resnet18x2": "2x ResNet-18, all convs merged, 4 frames each, 3x224x224",
+    "r50x2_vgg16x2": "2x ResNet-50 (stem+layer1-3 merged) + 2x VGG-16 "
+                     "(13 convs merged), 8 frames each, 3x224x224",
+    "yolov3x3": "3x YOLOv3 sharing the Darknet-53 backbone, 4 frames each, "
+                "3x416x416",
+    "mix8_budget40": "ResNet-152x2 + ResNet-50x3 + VGG-19x3, partial "
+                     "merging, 8 frames each, 3x224x224, weights capped at "
+                     "40% of the unmerged bytes (rest streamed per round)",
+}
+
+
+def log(msg):
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr,
+          flush=True)
+
+
+def cpu_baseline(wl, params, frames, seconds):
+    """The oracle (test infrastructure) on the host cores, on a bounded
+    sample: frame j of every model, j = 0, 1, ... until `seconds` pass."""
+    import oracle
+    from oracle import model as om
+    eff = om.effective_params(params, wl.groups)
+    done, t0, j = 0, time.perf_counter(), 0
+    max_n = max(m.n_frames for m in wl.models)
+    while j < max_n:
+        for i, m in enumerate(wl.models):
+            if j < m.n_frames:
+                om.run_model(m.layers, eff[i], frames[i][j:j + 1])
+                done += 1
+        j += 1
+        if time.perf_counter() - t0 >= seconds:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": done / dt, "unit": "frames/s",
+            "cores": oracle.threads(), "kind": "oracle",
+            "sample": f"{done} frames ({j} per model) of the same workload, "
+                      f"{dt:.1f} s, fp32 with fp64 accumulation"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="r50x2_vgg16x2",
+                    choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--profile-steps", type=int, default=20)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): "
+              "merged inference keeps each merged group's weights on one "
+              "device and needs no collectives", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2201_07705_amd as P
+    from paper_2201_07705_amd import gemel as G
+    from workloads import configs
+
+    wl = configs.get(args.config)
+    log(f"workload {wl.name}: generating seeded inputs")
+    params = [wl.params(i) for i in range(len(wl.models))]
+    frames = [wl.frames(i) for i in range(len(wl.models))]
+    ctx = P.Context(0, wl.dtype)
+    ids = [ctx.register_model(m.layers, params[i], m.in_chw)
+           for i, m in enumerate(wl.models)]
+    ctx.merge([[(ids[a], b) for a, b in g] for g in wl.groups])
+    budget = 0
+    if wl.budget_frac:
+        budget = int(wl.budget_frac * ctx.query(G.Q_UNMERGED_BYTES))
+        ctx.set_option(G.OPT_WEIGHT_BUDGET, budget)
+    dev = [torch.from_numpy(f).cuda() for f in frames]
+    stream = torch.cuda.Stream()
+    outs = ctx.alloc_outputs(ids, [m.n_frames for m in wl.models])
+    log(f"warmup {args.warmup}")
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            ctx.infer(ids, dev, stream=stream, outputs=outs)
+    torch.cuda.synchronize()
+    log(f"timed {args.steps} steps")
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), \
+        torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    with torch.cuda.stream(stream):
+        ev0.record(stream)
+        for _ in range(args.steps):
+            ctx.infer(ids, dev, stream=stream, outputs=outs)
+        ev1.record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    wall_s = t1 - t0
+    ev_ms = ev0.elapsed_time(ev1)
+    step_ms = wall_s * 1e3 / args.steps
+    total_frames = wl.total_frames()
+    fps = total_frames * args.steps / wall_s
+    flops = wl.flops()
+
+    # per-kernel-family HIP-event timings (separate, untimed pass)
+    log(f"profiled pass {args.profile_steps} steps")
+    ctx.set_option(G.OPT_PROFILE, 1)
+    with torch.cuda.stream(stream):
+        for _ in range(args.profile_steps):
+            ctx.infer(ids, dev, stream=stream, outputs=outs)
+    torch.cuda.synchronize()
+    prof, rounds = ctx.profile()
+    ctx.set_option(G.OPT_PROFILE, 0)
+    fam = max(prof, key=lambda k: prof[k]["ms"])
+    st = prof[fam]
+    kern = {}
+    for k, v in prof.items():
+        if v["launches"]:
+            kern[k] = {"launches": v["launches"], "ms": round(v["ms"], 4),
+                       "tflops": round(v["flops"] / v["ms"] / 1e9, 2)
+                       if v["ms"] and v["flops"] else None,
+                       "gbs": round(v["bytes"] / v["ms"] / 1e6, 1)
+                       if v["ms"] else None}
+    if fam in ("conv_mfma", "conv_f32") or (fam == "fc" and
+                                            st["flops"] / st["bytes"] > 315):
+        peak = PEAK_BF16_TFLOPS if wl.bf16 else PEAK_FP32_TFLOPS
+        ach = st["flops"] / (st["ms"] * 1e-3) / 1e12
+        roof = {"bound": "mfma" if wl.bf16 else "alu", "achieved": ach,
+                "peak": peak, "unit": "TFLOP/s", "frac": ach / peak,
+                "traffic": None}
+    else:
+        ach = st["bytes"] / (st["ms"] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": ach / PEAK_HBM_GBS, "traffic": None}
+    roof.update({"kernel": fam, "launches_per_step": st["launches"],
+                 "avg_launch_us": st["ms"] * 1e3 / max(st["launches"], 1),
+                 "algorithmic_per_launch":
+                     (st["flops"] if roof["unit"] == "TFLOP/s" else
+                      st["bytes"]) / max(st["launches"], 1)})
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle on host cores)")
+        cpu = cpu_baseline(wl, params, frames, args.cpu_seconds)
+
+    line = {
+        "metric": METRIC, "value": fps, "unit": "frames/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": step_ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if wl.bf16 else "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "description": DESCRIPTIONS[wl.name],
+                   "frames_per_step": total_frames,
+                   "gflop_per_step": round(flops / 1e9, 2),
+                   "merged_groups": len(wl.groups),
+                   "weight_budget_bytes": budget},
+        "tflops_per_step": flops / (step_ms * 1e-3) / 1e12,
+        "event_ms_per_step": ev_ms / args.steps,
+        "roofline": roof, "kernels": kern, "cpu_baseline": cpu,
+        "streamed_bytes_per_step": ctx.query(G.Q_STREAMED_BYTES),
+        "launches_per_step": ctx.query(G.Q_LAUNCHES),
+    }
+    ctx.close()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -244,12 +244,50 @@ enum {
     GEMEL_OPT_SPLIT_MERGED = 4,  /* 1: run merged layers per model (one
                                     launch per member, same single weight
                                     copy); 0 (default): one launch         */
-    GEMEL_OPT_WEIGHT_BUDGET = 5  /* replace the hbm_weight_budget given to
+    GEMEL_OPT_WEIGHT_BUDGET = 5, /* replace the hbm_weight_budget given to
                                     gemel_create (bytes, 0 = unlimited)    */
+    GEMEL_OPT_PROFILE = 6        /* 1: time every kernel launch with HIP
+                                    events on the launch stream (disables
+                                    graph replay); 0 (default): off. Setting
+                                    it clears the collected statistics.    */
 };
 
 /* Set an option; takes effect at the next gemel_infer. Errors: EINVAL. */
 gemel_status gemel_set_option(gemel_ctx *ctx, int32_t key, int64_t value);
+
+/* Kernel families reported by gemel_profile. */
+enum {
+    GEMEL_K_CONV_MFMA = 0,   /* bf16 implicit-GEMM convolution (MFMA)       */
+    GEMEL_K_CONV_F32 = 1,    /* fp32 direct convolution                     */
+    GEMEL_K_SPLITK_REDUCE = 2, /* split-K reduction + epilogue (conv, FC)   */
+    GEMEL_K_FC = 3,          /* weight-streaming fully connected            */
+    GEMEL_K_PACK = 4,        /* NCHW f32 frames -> NHWC                     */
+    GEMEL_K_POOL = 5,        /* max and global average pooling              */
+    GEMEL_K_ROUTE = 6,       /* upsample and concat                         */
+    GEMEL_K_EXPORT = 7,      /* internal tensor -> NCHW f32 output          */
+    GEMEL_K_COUNT = 8
+};
+
+/* Per-round statistics of one kernel family, averaged over the rounds run
+ * with GEMEL_OPT_PROFILE on. flops and bytes are algorithmic: 2 x MAC of
+ * the logical (unpadded) layer shapes, and every weight, input, residual
+ * and output byte counted once. */
+typedef struct gemel_kernel_stat {
+    int32_t kind;        /* GEMEL_K_*                                       */
+    int32_t launches;    /* launches per round                              */
+    double flops;        /* algorithmic FLOPs per round                     */
+    double bytes;        /* algorithmic bytes per round                     */
+    double ms;           /* summed kernel time per round (HIP events)       */
+} gemel_kernel_stat;
+
+/*
+ * Read the profile: stats must hold GEMEL_K_COUNT entries (one per family,
+ * in GEMEL_K_* order); *rounds receives the number of profiled rounds the
+ * averages cover. Waits for the profiled rounds to finish on the device.
+ * Errors: EINVAL (null pointers), ESTATE (profiling never enabled), EDEVICE.
+ */
+gemel_status gemel_profile(gemel_ctx *ctx, gemel_kernel_stat *stats,
+                           int32_t *rounds);
 
 /* Description of the last error (see general conventions). */
 const char *gemel_last_error(const gemel_ctx *ctx);

@@ -75,6 +75,9 @@ struct Launch {
     LaunchType type;
     int tile = 0;
     bool bf16 = true;
+    // kernel family (GEMEL_K_*) and algorithmic work of this launch
+    int kind = 0;
+    double flops = 0, bytes = 0;
     ConvArgs conv{};
     ReduceArgs red{};
     FcArgs fc{};
@@ -108,7 +111,22 @@ struct Plan {
     hipStream_t graph_stream = nullptr;
 };
 
+// Per-launch timing with HIP events (GEMEL_OPT_PROFILE).
+struct Profile {
+    struct Rec {
+        hipEvent_t a, b;
+        int kind;
+    };
+    std::vector<hipEvent_t> pool;    // free events
+    std::vector<Rec> pending;        // recorded, not yet read
+    double ms[GEMEL_K_COUNT] = {}, flops[GEMEL_K_COUNT] = {}, bytes[GEMEL_K_COUNT] = {};
+    int64_t launches[GEMEL_K_COUNT] = {};
+    int rounds = 0;
+    bool used = false;
+};
+
 struct Options {
+    int profile = 0;
     int use_graph = 1;
     int64_t slot_bytes = 32ll << 20;
     int slots = 3;
@@ -142,6 +160,7 @@ struct gemel_ctx {
     int64_t graph_replays = 0;
     std::map<std::vector<int>, std::unique_ptr<gemel::Plan>> plans;
     gemel::Plan *last_plan = nullptr;
+    gemel::Profile prof;
 };
 
 namespace gemel {
@@ -153,5 +172,7 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models,
                  const void *const *frames, const int32_t *n_frames, void *const *outputs,
                  hipStream_t stream);
 size_t unmerged_bytes(const gemel_ctx *ctx);
+void profile_reset(gemel_ctx *ctx);
+gemel_status profile_read(gemel_ctx *ctx, gemel_kernel_stat *stats, int32_t *rounds);
 size_t merged_bytes(const gemel_ctx *ctx);
 }  // namespace gemel

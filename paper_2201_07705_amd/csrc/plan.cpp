@@ -446,6 +446,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
             for (size_t b = 0; b < kv.second.size(); b += GEMEL_MAX_SEG) {
                 Launch L;
                 L.type = L_PACK;
+                L.kind = GEMEL_K_PACK;
                 L.bf16 = bf16;
                 EwArgs &a = L.ew;
                 a.H = kv.first[1]; a.W = kv.first[2]; a.Co = kv.first[3]; a.c_logical = kv.first[0];
@@ -459,6 +460,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     sg.frames = nfr[(size_t)s];
                     a.max_frames = std::max(a.max_frames, sg.frames);
                     L.patches.push_back({Patch::FRAMES, s, 0, a.nseg});
+                    L.bytes += (double)sg.frames * a.H * a.W * a.c_logical * (4.0 + esz);
                     a.nseg++;
                 }
                 P.launches.push_back(L);
@@ -489,9 +491,17 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     return fail(ctx, GEMEL_EBUDGET, "an output layer's weights exceed one staging slot");
                 for (int64_t r0 = 0; r0 < blob->rows; r0 += per) rows.push_back({r0, std::min(per, blob->rows - r0)});
             }
+            int64_t frames_in = 0;
+            for (auto [s, l] : nd.mem) frames_in += nfr[(size_t)s];
+            const double in_elems = (double)frames_in * L0.in_h * L0.in_w * L0.in_c;
+            const double kdepth = L0.op == GEMEL_OP_CONV ? (double)L0.kh * L0.kw * L0.cin : (double)L0.cin;
             for (auto [row0, nrows] : rows) {
                 Launch Lc;
                 Lc.bf16 = bf16;
+                const double co = (double)std::max<int64_t>(0, std::min<int64_t>(nrows, L0.out_c - row0));
+                Lc.flops = 2.0 * (double)M * co * kdepth;
+                Lc.bytes = co * kdepth * esz + in_elems * esz + (double)M * co * (direct ? 4.0 : esz) +
+                           (L0.res >= 0 ? (double)M * co * esz : 0.0);
                 if (!blob->w_dev) {
                     Lc.chunk = (int)P.chunks.size();
                     P.chunks.push_back(Chunk{blob, row0, nrows});
@@ -519,6 +529,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                         f += nfr[(size_t)s];
                         a.nseg++;
                     }
+                    Lc.kind = GEMEL_K_FC;
                     if (fc_f32) {
                         a.k_splits = 1;
                         a.k_per_split = a.K;
@@ -533,6 +544,9 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     if (Lc.type == L_FC_BF16 && a.k_splits > 1) {
                         Launch R = Lc;
                         R.type = L_FC_REDUCE;
+                        R.kind = GEMEL_K_SPLITK_REDUCE;
+                        R.flops = 0;
+                        R.bytes = (double)a.k_splits * a.M * a.N * 4.0;
                         R.chunk = -1;
                         P.launches.push_back(R);
                     }
@@ -576,16 +590,20 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 if (bf16) {
                     pick_conv_config(a.M, a.N, a.K, Lc.tile, a.k_splits, a.k_per_split);
                     Lc.type = L_CONV_BF16;
+                    Lc.kind = L0.op == GEMEL_OP_CONV ? GEMEL_K_CONV_MFMA : GEMEL_K_FC;
                 } else {
                     a.k_splits = 1;
                     a.k_per_split = a.K;
                     Lc.type = L_CONV_F32;
+                    Lc.kind = L0.op == GEMEL_OP_CONV ? GEMEL_K_CONV_F32 : GEMEL_K_FC;
                 }
                 P.launches.push_back(Lc);
                 if (a.k_splits > 1) {
                     partial_need = std::max(partial_need, (size_t)a.k_splits * a.M * a.N * 4);
                     Launch R;
                     R.type = L_CONV_REDUCE;
+                    R.kind = GEMEL_K_SPLITK_REDUCE;
+                    R.bytes = (double)a.k_splits * a.M * a.N * 4.0;
                     R.bf16 = bf16;
                     R.patches = Lc.patches;
                     ReduceArgs &r = R.red;
@@ -620,11 +638,14 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
         }
         if (!a.nseg) continue;
         switch (L0.op) {
-        case GEMEL_OP_MAXPOOL: Le.type = L_MAXPOOL; break;
-        case GEMEL_OP_AVGPOOL: Le.type = L_AVGPOOL; break;
-        case GEMEL_OP_UPSAMPLE2X: Le.type = L_UPSAMPLE; break;
-        default: Le.type = L_CONCAT; break;
+        case GEMEL_OP_MAXPOOL: Le.type = L_MAXPOOL; Le.kind = GEMEL_K_POOL; break;
+        case GEMEL_OP_AVGPOOL: Le.type = L_AVGPOOL; Le.kind = GEMEL_K_POOL; break;
+        case GEMEL_OP_UPSAMPLE2X: Le.type = L_UPSAMPLE; Le.kind = GEMEL_K_ROUTE; break;
+        default: Le.type = L_CONCAT; Le.kind = GEMEL_K_ROUTE; break;
         }
+        for (int i = 0; i < a.nseg; ++i)
+            Le.bytes += (double)a.seg[i].frames * esz *
+                        ((double)L0.in_h * L0.in_w * L0.in_c + (double)L0.out_h * L0.out_w * L0.out_c);
         P.launches.push_back(Le);
     }
     // outputs that are also read internally (or not conv/fc): export to NCHW f32
@@ -635,6 +656,8 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
             if (direct_output(L)) continue;
             Launch Le;
             Le.type = L_EXPORT;
+            Le.kind = GEMEL_K_EXPORT;
+            Le.bytes = (double)nfr[(size_t)s] * L.out_h * L.out_w * L.out_c * (esz + 4.0);
             Le.bf16 = bf16;
             EwArgs &a = Le.ew;
             a.H = L.out_h; a.W = L.out_w; a.C = L.out_cp; a.c_logical = L.out_c;
@@ -748,8 +771,28 @@ static gemel_status enqueue(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStre
             HIPCHK(hipStreamWaitEvent(st, ctx->ev_copied[(size_t)(L.chunk % nslots)], 0), "hipStreamWaitEvent");
             wptr = slot_ptr(L.chunk);
         }
+        Profile::Rec rec{nullptr, nullptr, L.kind};
+        if (ctx->opt.profile) {
+            for (hipEvent_t *ev : {&rec.a, &rec.b}) {
+                if (ctx->prof.pool.empty()) {
+                    hipEvent_t e2;
+                    HIPCHK(hipEventCreate(&e2), "hipEventCreate");
+                    ctx->prof.pool.push_back(e2);
+                }
+                *ev = ctx->prof.pool.back();
+                ctx->prof.pool.pop_back();
+            }
+            ctx->prof.pending.push_back(rec);
+            HIPCHK(hipEventRecord(rec.a, st), "hipEventRecord");
+        }
         hipError_t e = launch_one(L, cp, P, wptr, st);
         if (e != hipSuccess) return fail(ctx, GEMEL_EDEVICE, std::string("kernel launch: ") + hipGetErrorString(e));
+        if (ctx->opt.profile) {
+            HIPCHK(hipEventRecord(rec.b, st), "hipEventRecord");
+            ctx->prof.flops[L.kind] += L.flops;
+            ctx->prof.bytes[L.kind] += L.bytes;
+            ctx->prof.launches[L.kind] += 1;
+        }
         if (L.chunk >= 0) HIPCHK(hipEventRecord(ctx->ev_free[(size_t)(L.chunk % nslots)], st), "hipEventRecord");
     }
     return GEMEL_OK;
@@ -796,8 +839,12 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         const int no = (int)ctx->models[(size_t)id]->outputs.size();
         for (int o = 0; o < no; ++o) cp.outputs.push_back(outputs[caller_out_base[(size_t)ci] + o]);
     }
-    const bool graphable = ctx->opt.use_graph && P.chunks.empty() && stream != nullptr;
-    if (!graphable) return enqueue(ctx, P, cp, stream);
+    const bool graphable = ctx->opt.use_graph && !ctx->opt.profile && P.chunks.empty() && stream != nullptr;
+    if (!graphable) {
+        st = enqueue(ctx, P, cp, stream);
+        if (!st && ctx->opt.profile) ctx->prof.rounds++;
+        return st;
+    }
     if (P.graph && P.graph_stream == stream && P.graph_frames == cp.frames && P.graph_outputs == cp.outputs) {
         HIPCHK(hipGraphLaunch(P.graph, stream), "hipGraphLaunch");
         ctx->graph_replays++;
@@ -825,6 +872,44 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
     P.graph_frames = cp.frames;
     P.graph_outputs = cp.outputs;
     HIPCHK(hipGraphLaunch(P.graph, stream), "hipGraphLaunch");
+    return GEMEL_OK;
+}
+
+void profile_reset(gemel_ctx *ctx) {
+    Profile &p = ctx->prof;
+    if (!p.pending.empty() || !p.pool.empty()) {
+        for (auto &r : p.pending) {
+            (void)hipEventSynchronize(r.b);
+            (void)hipEventDestroy(r.a);
+            (void)hipEventDestroy(r.b);
+        }
+        for (auto e : p.pool) (void)hipEventDestroy(e);
+    }
+    const bool used = p.used;
+    p = Profile();
+    p.used = used;
+}
+
+gemel_status profile_read(gemel_ctx *ctx, gemel_kernel_stat *stats, int32_t *rounds) {
+    Profile &p = ctx->prof;
+    for (auto &r : p.pending) {
+        float ms = 0.f;
+        HIPCHK(hipEventSynchronize(r.b), "hipEventSynchronize");
+        HIPCHK(hipEventElapsedTime(&ms, r.a, r.b), "hipEventElapsedTime");
+        p.ms[r.kind] += ms;
+        p.pool.push_back(r.a);
+        p.pool.push_back(r.b);
+    }
+    p.pending.clear();
+    const double n = p.rounds ? (double)p.rounds : 1.0;
+    for (int k = 0; k < GEMEL_K_COUNT; ++k) {
+        stats[k].kind = k;
+        stats[k].launches = (int32_t)((double)p.launches[k] / n + 0.5);
+        stats[k].flops = p.flops[k] / n;
+        stats[k].bytes = p.bytes[k] / n;
+        stats[k].ms = p.ms[k] / n;
+    }
+    *rounds = p.rounds;
     return GEMEL_OK;
 }
 

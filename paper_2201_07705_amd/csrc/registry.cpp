@@ -416,6 +416,12 @@ gemel_status gemel_set_option(gemel_ctx *ctx, int32_t key, int64_t value) {
         ctx->opt.split_merged = (int)value;
         drop_plans(ctx);
         break;
+    case GEMEL_OPT_PROFILE:
+        if (value != 0 && value != 1) return fail(ctx, GEMEL_EINVAL, "profile is 0 or 1");
+        profile_reset(ctx);
+        ctx->opt.profile = (int)value;
+        if (value) ctx->prof.used = true;
+        break;
     case GEMEL_OPT_WEIGHT_BUDGET:
         if (value < 0) return fail(ctx, GEMEL_EINVAL, "budget must be >= 0");
         ctx->budget = (uint64_t)value;
@@ -427,6 +433,13 @@ gemel_status gemel_set_option(gemel_ctx *ctx, int32_t key, int64_t value) {
     return GEMEL_OK;
 }
 
+gemel_status gemel_profile(gemel_ctx *ctx, gemel_kernel_stat *stats, int32_t *rounds) {
+    if (!ctx) return GEMEL_EINVAL;
+    if (!stats || !rounds) return fail(ctx, GEMEL_EINVAL, "null stats or rounds");
+    if (!ctx->prof.used) return fail(ctx, GEMEL_ESTATE, "profiling was never enabled");
+    return profile_read(ctx, stats, rounds);
+}
+
 const char *gemel_last_error(const gemel_ctx *ctx) {
     return ctx ? ctx->err.c_str() : g_create_err.c_str();
 }
@@ -434,6 +447,7 @@ const char *gemel_last_error(const gemel_ctx *ctx) {
 gemel_status gemel_destroy(gemel_ctx *ctx) {
     if (!ctx) return GEMEL_OK;
     gemel_status st = GEMEL_OK;
+    profile_reset(ctx);
     if (ctx->dev_ready) {
         int prev = 0;
         (void)hipGetDevice(&prev);

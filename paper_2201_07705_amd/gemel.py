@@ -37,12 +37,14 @@ Q_UNMERGED_BYTES, Q_MERGED_BYTES, Q_RESIDENT_BYTES, Q_PEAK_BYTES, \
     Q_STREAMED_BYTES, Q_ACTIVATION_BYTES, Q_LAUNCHES, Q_N_MODELS, \
     Q_GRAPH_REPLAYS = range(9)
 OPT_USE_GRAPH, OPT_SWAP_SLOT_BYTES, OPT_SWAP_SLOTS, OPT_FAIL_COPY_AT, \
-    OPT_SPLIT_MERGED, OPT_WEIGHT_BUDGET = range(6)
+    OPT_SPLIT_MERGED, OPT_WEIGHT_BUDGET, OPT_PROFILE = range(7)
+KERNEL_FAMILIES = ("conv_mfma", "conv_f32", "splitk_reduce", "fc", "pack",
+                   "pool", "route", "export")
 
 EXPORTED = ("gemel_create", "gemel_register_model", "gemel_merge",
             "gemel_infer", "gemel_model_outputs", "gemel_output_shape",
-            "gemel_query", "gemel_set_option", "gemel_last_error",
-            "gemel_destroy")
+            "gemel_query", "gemel_set_option", "gemel_profile",
+            "gemel_last_error", "gemel_destroy")
 
 _fp = ctypes.POINTER(ctypes.c_float)
 
@@ -67,6 +69,12 @@ class Member(ctypes.Structure):
 class Group(ctypes.Structure):
     _fields_ = [("n_members", ctypes.c_int32),
                 ("members", ctypes.POINTER(Member))]
+
+
+class KernelStat(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("launches", ctypes.c_int32),
+                ("flops", ctypes.c_double), ("bytes", ctypes.c_double),
+                ("ms", ctypes.c_double)]
 
 
 class GemelError(RuntimeError):
@@ -126,6 +134,8 @@ def lib():
                                          ctypes.POINTER(i64)]
         L.gemel_query.argtypes = [vp, i32, ctypes.POINTER(i64)]
         L.gemel_set_option.argtypes = [vp, i32, i64]
+        L.gemel_profile.argtypes = [vp, ctypes.POINTER(KernelStat),
+                                    ctypes.POINTER(i32)]
         L.gemel_last_error.argtypes = [vp]
         L.gemel_last_error.restype = ctypes.c_char_p
         L.gemel_destroy.argtypes = [vp]
@@ -240,6 +250,16 @@ class Context:
 
     def set_option(self, key, value):
         self._check(lib().gemel_set_option(self._h, key, value))
+
+    def profile(self):
+        """Per-round kernel statistics by family: {name: dict(launches,
+        flops, bytes, ms)} and the number of profiled rounds."""
+        st = (KernelStat * len(KERNEL_FAMILIES))()
+        rounds = ctypes.c_int32()
+        self._check(lib().gemel_profile(self._h, st, ctypes.byref(rounds)))
+        return {name: dict(launches=s.launches, flops=s.flops, bytes=s.bytes,
+                           ms=s.ms)
+                for name, s in zip(KERNEL_FAMILIES, st)}, rounds.value
 
     def infer_raw(self, model_ids, frame_ptrs, n_frames, out_ptrs, stream):
         n = len(model_ids)
