@@ -246,10 +246,18 @@ enum {
                                     copy); 0 (default): one launch         */
     GEMEL_OPT_WEIGHT_BUDGET = 5, /* replace the hbm_weight_budget given to
                                     gemel_create (bytes, 0 = unlimited)    */
-    GEMEL_OPT_PROFILE = 6        /* 1: time every kernel launch with HIP
+    GEMEL_OPT_PROFILE = 6,       /* 1: time every kernel launch with HIP
                                     events on the launch stream (disables
                                     graph replay); 0 (default): off. Setting
                                     it clears the collected statistics.    */
+    GEMEL_OPT_CONV_TILE = 7      /* -1 (default): pick each conv's tile
+                                    shape and split-K by the cost model;
+                                    0..5: force one tile shape (128x128,
+                                    128x64, 64x64, 256x256, 256x128,
+                                    256x64) with split-K still chosen      */
+    GEMEL_OPT_CONV_SPLITS = 8    /* 0 (default): split-K chosen per conv;
+                                    n >= 1: force n depth splits (capped
+                                    so that every split has work)          */
 };
 
 /* Set an option; takes effect at the next gemel_infer. Errors: EINVAL. */

@@ -127,6 +127,8 @@ struct Profile {
 
 struct Options {
     int profile = 0;
+    int conv_tile = -1;
+    int conv_splits = 0;
     int use_graph = 1;
     int64_t slot_bytes = 32ll << 20;
     int slots = 3;
@@ -150,6 +152,7 @@ struct gemel_ctx {
     hipStream_t side = nullptr;      // weight-copy stream
     std::vector<hipEvent_t> ev_copied, ev_free;
     void *wpool = nullptr;           // resident weights + all scale/shift
+    void *zero_page = nullptr;       // 256 zero bytes inside wpool
     size_t wpool_bytes = 0;
     void *staging = nullptr;         // slots x slot_bytes
     int staging_slots = 0;

@@ -29,6 +29,7 @@ namespace gemel {
 typedef unsigned short u16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf2f(u16 h) {
     return __uint_as_float((uint32_t)h << 16);
@@ -125,97 +126,130 @@ __device__ __forceinline__ void store1_nchw_f32(const ConvSeg &sg, const Epi &e,
         epi(z, r, e.has_res, e.res_mode, e.act, e.slope);
 }
 
-template <int BM, int BN>
-__global__ __launch_bounds__(256, 2) void conv_bf16_kernel(const ConvArgs a) {
+// Implicit-GEMM tile kernel. BM x BN output tile, WM x WN waves (each a
+// (BM/WM) x (BN/WN) wave tile of 16x16 MFMA blocks), depth 64 per step.
+// Global loads run DEPTH steps ahead of the MFMAs (DEPTH register sets, the
+// loop unrolled by two) and land in a double-buffered LDS tile whose rows
+// are padded by 16 bytes so that the 16-byte fragment reads of 16
+// consecutive rows hit distinct banks. Masked-off loads read a zero page
+// instead of branching. CIN64: Cin is a multiple of 64, so one depth step
+// covers a single filter tap (r, s) and the gather offsets are uniform.
+template <int BM, int BN, int WM, int WN, int DEPTH, bool CIN64>
+__global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a) {
+    static_assert(DEPTH == 1 || DEPTH == 2, "prefetch depth");
+    constexpr int NT = 64 * WM * WN;
     constexpr int BK = CONV_BK;
-    constexpr int LDA = BK + 8;            // +16 B per row: conflict-free b128
-    constexpr int WM = BM / 2, WN = BN / 2;
-    constexpr int FM = WM / 16, FN = WN / 16;
-    constexpr int AP = BM / 32, BP = BN / 32;  // 16-byte loads per thread
+    constexpr int LDA = BK + 8;
+    constexpr int TM = BM / WM, TN = BN / WN;
+    constexpr int FM = TM / 16, FN = TN / 16;
+    constexpr int RPP = NT / 8;                 // rows per load pass
+    constexpr int AP = BM / RPP, BP = BN / RPP; // 16-byte loads per thread
+    static_assert(AP * RPP == BM && BP * RPP == BN && AP >= 1 && BP >= 1, "tile/threads");
+    constexpr int STAGE = (BM + BN) * LDA;      // bf16 elements per stage
+    constexpr int SMEM_AB = 2 * STAGE * 2;
     constexpr int LDC = BN + 4;
-    constexpr int SMEM_AB = 2 * (BM + BN) * LDA * 2;
-    constexpr int SMEM_C = BM * LDC * 4;
+    constexpr int FIT = SMEM_AB / (LDC * 4);
+    constexpr int WPP = (FIT / TM) < WM ? (FIT / TM) : WM;   // wave rows per epilogue pass
+    static_assert(WPP >= 1, "epilogue staging does not fit");
+    constexpr int EPI_ROWS = WPP * TM;
+    constexpr int SMEM_C = EPI_ROWS * LDC * 4;
     constexpr int SMEM = SMEM_AB > SMEM_C ? SMEM_AB : SMEM_C;
+    constexpr int CH = BN / 8;                  // 8-channel chunks per row
+    static_assert(NT % CH == 0, "epilogue chunk per thread");
     __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM];
     u16 *const sAB = (u16 *)smem;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WN, wn = wave - (wave / WN) * WN;
     const int tiles_n = (a.N + BN - 1) / BN;
-    const int tm = blockIdx.x / tiles_n, tn = blockIdx.x - tm * tiles_n;
+    const int tiles = ((a.M + BM - 1) / BM) * tiles_n;
+    // XCD-aware order: consecutive tiles (same rows, all column tiles) run
+    // on one XCD and share its L2.
+    const int G = gridDim.x;
+    const int t = (G & 7) == 0 ? (int)(blockIdx.x & 7) * (G >> 3) + (int)(blockIdx.x >> 3) : (int)blockIdx.x;
+    if (t >= tiles) return;
+    const int tm = t / tiles_n, tn = t - (t / tiles_n) * tiles_n;
     const int k_begin = blockIdx.y * a.k_per_split;
     const int k_end = min(a.K, k_begin + a.k_per_split);
     const int HWo = a.Ho * a.Wo;
     const size_t frame_elems = (size_t)a.H * a.W * a.in_cs;
+    const u16 *const zp = (const u16 *)a.zero;
+    const int H = a.H, W = a.W, in_cs = a.in_cs, N = a.N, K = a.K, Cin = a.Cin, kw = a.kw;
 
-    // ---- loader set-up: thread owns K chunk q of rows r0 + 32 j ----
+    // ---- loader set-up: thread owns K chunk q of rows r0 + RPP j ----
     const int q = tid & 7, r0 = tid >> 3;
     const u16 *abase[AP];
     int ahi[AP], awi[AP];
 #pragma unroll
     for (int j = 0; j < AP; ++j) {
-        const int gm = tm * BM + r0 + 32 * j;
-        abase[j] = (const u16 *)a.seg[0].in;
+        const int gm = tm * BM + r0 + RPP * j;
+        abase[j] = zp;
         ahi[j] = -(1 << 28);
         awi[j] = 0;
         if (gm < a.M) {
-            const int s = seg_of_row(a, gm);
+            const int sg = seg_of_row(a, gm);
             const int fr = gm / HWo;
             const int pix = gm - fr * HWo;
             const int ho = pix / a.Wo, wo = pix - (pix / a.Wo) * a.Wo;
-            abase[j] = (const u16 *)a.seg[s].in + (size_t)(fr - a.seg[s].f_start) * frame_elems;
+            abase[j] = (const u16 *)a.seg[sg].in + (size_t)(fr - a.seg[sg].f_start) * frame_elems;
             ahi[j] = ho * a.stride - a.pad;
             awi[j] = wo * a.stride - a.pad;
         }
     }
-    const u16 *bbase[BP];
-    bool bok[BP];
-#pragma unroll
-    for (int j = 0; j < BP; ++j) {
-        const int gn = tn * BN + r0 + 32 * j;
-        bok[j] = gn < a.N;
-        bbase[j] = (const u16 *)a.w + (size_t)(bok[j] ? gn : 0) * a.K;
-    }
-    // (r, s, c) of this thread's chunk at depth k
-    int k = k_begin + q * 8;
-    int c, r, s;
+    const int gn0 = tn * BN + r0;
+    const u16 *const bbase = (const u16 *)a.w + (size_t)(gn0 < a.N ? gn0 : 0) * a.K + q * 8;
+
+    // loader position: the next depth step to fetch
+    int kb = k_begin;      // step base
+    int lc, lr, ls;        // CIN64: tap (lr, ls), channel base lc; else this thread's chunk
     {
-        const int rs = k / a.Cin;
-        c = k - rs * a.Cin;
-        r = rs / a.kw;
-        s = rs - r * a.kw;
+        const int k0 = CIN64 ? k_begin : k_begin + q * 8;
+        const int rs = k0 / Cin;
+        lc = k0 - rs * Cin;
+        lr = rs / kw;
+        ls = rs - lr * kw;
     }
 
-    uint4 ra[AP], rb[BP];
-    auto gload = [&]() {
-        const bool kok = k < k_end;
+    auto gload = [&](u32x4 (&ra)[AP], u32x4 (&rb)[BP]) __attribute__((always_inline)) {
+        const int kq = kb + q * 8;
+        const bool kok = CIN64 ? true : kq < k_end;
+        const int c = CIN64 ? lc + q * 8 : lc;
 #pragma unroll
         for (int j = 0; j < AP; ++j) {
-            const int hi = ahi[j] + r, wi = awi[j] + s;
-            if (kok && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W)
-                ra[j] = *(const uint4 *)(abase[j] + ((size_t)(hi * a.W + wi) * a.in_cs + c));
-            else
-                ra[j] = make_uint4(0, 0, 0, 0);
+            const int hi = ahi[j] + lr, wi = awi[j] + ls;
+            const bool ok = kok && (unsigned)hi < (unsigned)H && (unsigned)wi < (unsigned)W;
+            const u16 *p = ok ? abase[j] + ((size_t)(hi * W + wi) * in_cs + c) : zp;
+            ra[j] = *(const u32x4 *)p;
         }
 #pragma unroll
-        for (int j = 0; j < BP; ++j)
-            rb[j] = (kok && bok[j]) ? *(const uint4 *)(bbase[j] + k) : make_uint4(0, 0, 0, 0);
-    };
-    auto advance = [&]() {
-        k += BK;
-        c += BK;
-        while (c >= a.Cin) {
-            c -= a.Cin;
-            if (++s == a.kw) { s = 0; ++r; }
+        for (int j = 0; j < BP; ++j) {
+            const bool ok = kok && gn0 + RPP * j < N;
+            const u16 *p = ok ? bbase + (size_t)RPP * j * K + kb : zp;
+            rb[j] = *(const u32x4 *)p;
+        }
+        // advance the loader by one step
+        kb += BK;
+        if (CIN64) {
+            lc += BK;
+            if (lc == Cin) {
+                lc = 0;
+                if (++ls == kw) { ls = 0; ++lr; }
+            }
+        } else {
+            lc += BK;
+            while (lc >= Cin) {
+                lc -= Cin;
+                if (++ls == kw) { ls = 0; ++lr; }
+            }
         }
     };
-    auto sstore = [&](int stage) {
-        u16 *As = sAB + stage * (BM + BN) * LDA;
+    auto sstore = [&](int stage, const u32x4 (&ra)[AP], const u32x4 (&rb)[BP]) __attribute__((always_inline)) {
+        u16 *As = sAB + stage * STAGE;
         u16 *Bs = As + BM * LDA;
 #pragma unroll
-        for (int j = 0; j < AP; ++j) *(uint4 *)(As + (r0 + 32 * j) * LDA + q * 8) = ra[j];
+        for (int j = 0; j < AP; ++j) *(u32x4 *)(As + (r0 + RPP * j) * LDA + q * 8) = ra[j];
 #pragma unroll
-        for (int j = 0; j < BP; ++j) *(uint4 *)(Bs + (r0 + 32 * j) * LDA + q * 8) = rb[j];
+        for (int j = 0; j < BP; ++j) *(u32x4 *)(Bs + (r0 + RPP * j) * LDA + q * 8) = rb[j];
     };
 
     f32x4 acc[FM][FN];
@@ -224,83 +258,132 @@ __global__ __launch_bounds__(256, 2) void conv_bf16_kernel(const ConvArgs a) {
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int nk = (k_end - k_begin + BK - 1) / BK;
-    gload();
-    sstore(0);
-    __syncthreads();
-    for (int it = 0; it < nk; ++it) {
-        const bool more = it + 1 < nk;
-        if (more) {
-            advance();
-            gload();
-        }
-        const u16 *As = sAB + (it & 1) * (BM + BN) * LDA;
+    auto compute = [&](int stage) __attribute__((always_inline)) {
+        const u16 *As = sAB + stage * STAGE;
         const u16 *Bs = As + BM * LDA;
 #pragma unroll
         for (int kk = 0; kk < BK / 32; ++kk) {
-            bf16x8 af[FM], bfr[FN];
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
-                af[i] = *(const bf16x8 *)(As + (wm * WM + i * 16 + (lane & 15)) * LDA + kk * 32 + (lane >> 4) * 8);
+            bf16x8 bfr[FN];
 #pragma unroll
             for (int j = 0; j < FN; ++j)
-                bfr[j] = *(const bf16x8 *)(Bs + (wn * WN + j * 16 + (lane & 15)) * LDA + kk * 32 + (lane >> 4) * 8);
+                bfr[j] = *(const bf16x8 *)(Bs + (wn * TN + j * 16 + (lane & 15)) * LDA + kk * 32 + (lane >> 4) * 8);
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const bf16x8 af = *(const bf16x8 *)(As + (wm * TM + i * 16 + (lane & 15)) * LDA + kk * 32 + (lane >> 4) * 8);
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bfr[j], acc[i][j], 0, 0, 0);
+            }
+        }
+    };
+
+    const int nk = (k_end - k_begin + BK - 1) / BK;
+    if (DEPTH == 2) {
+        u32x4 ra0[AP], rb0[BP], ra1[AP], rb1[BP];
+        gload(ra0, rb0);
+        if (nk > 1) gload(ra1, rb1);
+        sstore(0, ra0, rb0);
+        __syncthreads();
+        for (int it = 0; it < nk; it += 2) {
+            if (it + 2 < nk) gload(ra0, rb0);
+            compute(0);
+            if (it + 1 < nk) sstore(1, ra1, rb1);
+            __syncthreads();
+            if (it + 1 >= nk) break;
+            if (it + 3 < nk) gload(ra1, rb1);
+            compute(1);
+            if (it + 2 < nk) sstore(0, ra0, rb0);
+            __syncthreads();
+        }
+    } else {
+        u32x4 ra0[AP], rb0[BP];
+        gload(ra0, rb0);
+        sstore(0, ra0, rb0);
+        __syncthreads();
+        for (int it = 0; it < nk; ++it) {
+            const bool more = it + 1 < nk;
+            if (more) gload(ra0, rb0);
+            compute(it & 1);
+            if (more) sstore((it + 1) & 1, ra0, rb0);
+            __syncthreads();
+        }
+    }
+
+    // ---- epilogue: fp32 tile staged through LDS, WPP wave rows per pass ----
+    float *Cs = (float *)smem;
+    const Epi e = epi_of(a, HWo);
+    const int my_ch = tid % CH;
+    const int my_gn = tn * BN + my_ch * 8;
+    float sc[8], sh[8];
+    const bool pre = a.uni_affine && a.k_splits <= 1 && a.out_mode == OUT_NHWC && my_gn < a.N;
+    if (pre) {
+        const float4 s0 = *(const float4 *)(a.seg[0].scale + my_gn), s1 = *(const float4 *)(a.seg[0].scale + my_gn + 4);
+        const float4 h0 = *(const float4 *)(a.seg[0].shift + my_gn), h1 = *(const float4 *)(a.seg[0].shift + my_gn + 4);
+        sc[0] = s0.x; sc[1] = s0.y; sc[2] = s0.z; sc[3] = s0.w; sc[4] = s1.x; sc[5] = s1.y; sc[6] = s1.z; sc[7] = s1.w;
+        sh[0] = h0.x; sh[1] = h0.y; sh[2] = h0.z; sh[3] = h0.w; sh[4] = h1.x; sh[5] = h1.y; sh[6] = h1.z; sh[7] = h1.w;
+    }
+    for (int pass = 0; pass < WM; pass += WPP) {
+        if (wm >= pass && wm < pass + WPP) {
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
                 for (int j = 0; j < FN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        Cs[((wm - pass) * TM + i * 16 + (lane >> 4) * 4 + v) * LDC + wn * TN + j * 16 + (lane & 15)] =
+                            acc[i][j][v];
         }
-        if (more) sstore((it + 1) & 1);
         __syncthreads();
-    }
-
-    // ---- epilogue: fp32 tile through LDS ----
-    float *Cs = (float *)smem;
+        const int row0 = pass * TM;
+        const int nrows = min(EPI_ROWS, BM - row0);
+        if (a.k_splits > 1) {
+            float *P = a.partial + (size_t)blockIdx.y * a.M * a.N;
+            for (int item = tid; item < nrows * CH; item += NT) {
+                const int rl = item / CH, ch = item - (item / CH) * CH;
+                const int gm = tm * BM + row0 + rl, gn = tn * BN + ch * 8;
+                if (gm >= a.M || gn >= a.N) continue;
+                const float *src = Cs + rl * LDC + ch * 8;
+                float4 *dst = (float4 *)(P + (size_t)gm * a.N + gn);
+                dst[0] = *(const float4 *)src;
+                dst[1] = *(const float4 *)(src + 4);
+            }
+        } else if (a.out_mode == OUT_NHWC) {
+            for (int item = tid; item < nrows * CH; item += NT) {
+                const int rl = item / CH, ch = item - (item / CH) * CH;
+                const int gm = tm * BM + row0 + rl, gn = tn * BN + ch * 8;
+                if (gm >= a.M || gn >= a.N) continue;
+                const float4 v0 = *(const float4 *)(Cs + rl * LDC + ch * 8);
+                const float4 v1 = *(const float4 *)(Cs + rl * LDC + ch * 8 + 4);
+                float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+                const ConvSeg &sg = a.seg[seg_of_row(a, gm)];
+                if (pre) {
+                    const size_t off = (size_t)(gm - sg.m_start) * e.out_cs + gn;
+                    u16 rv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                    if (e.has_res) {
+                        const uint4 r4 = *(const uint4 *)((const u16 *)sg.res + off);
+                        const u16 *rp = (const u16 *)&r4;
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+                        for (int jj = 0; jj < 8; ++jj) rv[jj] = rp[jj];
+                    }
+                    uint4 o;
+                    u16 *op = (u16 *)&o;
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int v = 0; v < 4; ++v)
-                Cs[(wm * WM + i * 16 + (lane >> 4) * 4 + v) * LDC + wn * WN + j * 16 + (lane & 15)] = acc[i][j][v];
-    __syncthreads();
-
-    constexpr int CH = BN / 8;            // 8-channel chunks per row
-    if (a.k_splits > 1) {
-        float *P = a.partial + (size_t)blockIdx.y * a.M * a.N;
-        for (int item = tid; item < BM * CH; item += 256) {
-            const int row = item / CH, ch = item - (item / CH) * CH;
-            const int gm = tm * BM + row, gn = tn * BN + ch * 8;
-            if (gm >= a.M || gn >= a.N) continue;
-            const float *src = Cs + row * LDC + ch * 8;
-            float4 *dst = (float4 *)(P + (size_t)gm * a.N + gn);
-            dst[0] = *(const float4 *)src;
-            dst[1] = *(const float4 *)(src + 4);
+                    for (int jj = 0; jj < 8; ++jj)
+                        op[jj] = f2bf(epi(v[jj] * sc[jj] + sh[jj], bf2f(rv[jj]), e.has_res, e.res_mode, e.act, e.slope));
+                    *(uint4 *)((u16 *)sg.out + off) = o;
+                } else {
+                    store8_nhwc_bf16(sg, e, gm, gn, v);
+                }
+            }
+        } else {
+            for (int item = tid; item < nrows * BN; item += NT) {
+                const int col = item / nrows, rl = item - (item / nrows) * nrows;
+                const int gm = tm * BM + row0 + rl, gn = tn * BN + col;
+                if (gm >= a.M || gn >= a.N) continue;
+                store1_nchw_f32<true>(a.seg[seg_of_row(a, gm)], e, gm, gn, Cs[rl * LDC + col]);
+            }
         }
-        return;
-    }
-    const Epi e = epi_of(a, HWo);
-    if (a.out_mode == OUT_NHWC) {
-        for (int item = tid; item < BM * CH; item += 256) {
-            const int row = item / CH, ch = item - (item / CH) * CH;
-            const int gm = tm * BM + row, gn = tn * BN + ch * 8;
-            if (gm >= a.M || gn >= a.N) continue;
-            float v[8];
-            const float4 v0 = *(const float4 *)(Cs + row * LDC + ch * 8);
-            const float4 v1 = *(const float4 *)(Cs + row * LDC + ch * 8 + 4);
-            v[0] = v0.x; v[1] = v0.y; v[2] = v0.z; v[3] = v0.w;
-            v[4] = v1.x; v[5] = v1.y; v[6] = v1.z; v[7] = v1.w;
-            store8_nhwc_bf16(a.seg[seg_of_row(a, gm)], e, gm, gn, v);
-        }
-    } else {
-        // fp32 NCHW: consecutive threads take consecutive rows of a column
-        for (int item = tid; item < BM * BN; item += 256) {
-            const int col = item / BM, row = item - (item / BM) * BM;
-            const int gm = tm * BM + row, gn = tn * BN + col;
-            if (gm >= a.M || gn >= a.N) continue;
-            store1_nchw_f32<true>(a.seg[seg_of_row(a, gm)], e, gm, gn, Cs[row * LDC + col]);
-        }
+        __syncthreads();
     }
 }
 
@@ -365,24 +448,15 @@ __global__ __launch_bounds__(256) void conv_f32_kernel(const ConvArgs a) {
     }
 }
 
-int conv_tile_bm(int tile) {
-    switch (tile) {
-    case TILE_128x128: return 128;
-    case TILE_128x64: return 128;
-    case TILE_64x64: return 64;
-    case TILE_256x128: return 256;
-    }
-    return 0;
-}
-int conv_tile_bn(int tile) {
-    switch (tile) {
-    case TILE_128x128: return 128;
-    case TILE_128x64: return 64;
-    case TILE_64x64: return 64;
-    case TILE_256x128: return 128;
-    }
-    return 0;
-}
+struct TileShape {
+    int bm, bn, threads;
+};
+static const TileShape kTiles[TILE_COUNT] = {
+    {128, 128, 256}, {128, 64, 256}, {64, 64, 256}, {256, 256, 512}, {256, 128, 512}, {256, 64, 256}};
+
+int conv_tile_bm(int tile) { return tile >= 0 && tile < TILE_COUNT ? kTiles[tile].bm : 0; }
+int conv_tile_bn(int tile) { return tile >= 0 && tile < TILE_COUNT ? kTiles[tile].bn : 0; }
+int conv_tile_threads(int tile) { return tile >= 0 && tile < TILE_COUNT ? kTiles[tile].threads : 0; }
 
 static bool conv_args_ok(const ConvArgs &a) {
     if (a.M <= 0 || a.N <= 0 || a.K <= 0 || a.nseg < 1 || a.nseg > GEMEL_MAX_SEG) return false;
@@ -403,19 +477,31 @@ static bool conv_args_ok(const ConvArgs &a) {
     return true;
 }
 
+template <bool C64>
+static void launch_tile(int tile, dim3 grid, hipStream_t st, const ConvArgs &a) {
+    switch (tile) {
+    case TILE_128x128: hipLaunchKernelGGL((conv_bf16_kernel<128, 128, 2, 2, 1, C64>), grid, dim3(256), 0, st, a); break;
+    case TILE_128x64: hipLaunchKernelGGL((conv_bf16_kernel<128, 64, 2, 2, 1, C64>), grid, dim3(256), 0, st, a); break;
+    case TILE_64x64: hipLaunchKernelGGL((conv_bf16_kernel<64, 64, 2, 2, 1, C64>), grid, dim3(256), 0, st, a); break;
+    case TILE_256x256: hipLaunchKernelGGL((conv_bf16_kernel<256, 256, 2, 4, 1, C64>), grid, dim3(512), 0, st, a); break;
+    case TILE_256x128: hipLaunchKernelGGL((conv_bf16_kernel<256, 128, 4, 2, 1, C64>), grid, dim3(512), 0, st, a); break;
+    case TILE_256x64: hipLaunchKernelGGL((conv_bf16_kernel<256, 64, 4, 1, 1, C64>), grid, dim3(256), 0, st, a); break;
+    }
+}
+
 hipError_t launch_conv_bf16(const ConvArgs &a, int tile, hipStream_t st) {
-    if (!conv_args_ok(a)) return hipErrorInvalidValue;
+    if (!conv_args_ok(a) || !a.zero) return hipErrorInvalidValue;
     const int bm = conv_tile_bm(tile), bn = conv_tile_bn(tile);
     if (!bm) return hipErrorInvalidValue;
     const long tiles = (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn);
-    if (tiles > 0x7fffffffL) return hipErrorInvalidValue;
-    dim3 grid((unsigned)tiles, (unsigned)a.k_splits), block(256);
-    switch (tile) {
-    case TILE_128x128: hipLaunchKernelGGL((conv_bf16_kernel<128, 128>), grid, block, 0, st, a); break;
-    case TILE_128x64: hipLaunchKernelGGL((conv_bf16_kernel<128, 64>), grid, block, 0, st, a); break;
-    case TILE_64x64: hipLaunchKernelGGL((conv_bf16_kernel<64, 64>), grid, block, 0, st, a); break;
-    case TILE_256x128: hipLaunchKernelGGL((conv_bf16_kernel<256, 128>), grid, block, 0, st, a); break;
-    }
+    const long blocks = tiles >= 8 ? (tiles + 7) / 8 * 8 : tiles;
+    if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
+    dim3 grid((unsigned)blocks, (unsigned)a.k_splits);
+    const bool c64 = a.Cin % 64 == 0 && a.k_per_split % CONV_BK == 0 && a.in_cs % 8 == 0;
+    if (c64)
+        launch_tile<true>(tile, grid, st, a);
+    else
+        launch_tile<false>(tile, grid, st, a);
     return hipGetLastError();
 }
 

@@ -25,6 +25,7 @@ struct ConvSeg {
 
 struct ConvArgs {
     const void *w;        // [N][K], k = (r * kw + s) * Cin + c
+    const void *zero;     // >= 16 zero bytes (target of masked-off loads)
     int32_t M, N, K;      // rows = frames*Ho*Wo, cols = out channels, depth
     int32_t H, W, Cin;    // input spatial size, physical input channels
     int32_t in_cs;        // input pixel stride in elements (>= Cin)
@@ -38,6 +39,7 @@ struct ConvArgs {
     int32_t has_res;
     int32_t out_mode;     // OUT_NHWC or OUT_NCHW_F32
     int32_t nseg;
+    int32_t uni_affine;   // every segment uses the same scale/shift arrays
     int32_t k_splits;     // >1: write fp32 partials to `partial`
     int32_t k_per_split;  // depth handled by one split (multiple of BK)
     float *partial;       // [k_splits][M][N] when k_splits > 1

@@ -9,7 +9,16 @@
 namespace gemel {
 
 // Tile configurations of the bf16 implicit-GEMM convolution.
-enum ConvTile { TILE_128x128 = 0, TILE_128x64 = 1, TILE_64x64 = 2, TILE_256x128 = 3 };
+enum ConvTile {
+    TILE_128x128 = 0,  // 4 waves, 64x64 per wave
+    TILE_128x64 = 1,   // 4 waves, 64x32 per wave
+    TILE_64x64 = 2,    // 4 waves, 32x32 per wave
+    TILE_256x256 = 3,  // 8 waves, 128x64 per wave
+    TILE_256x128 = 4,  // 8 waves, 64x64 per wave
+    TILE_256x64 = 5,   // 4 waves, 64x64 per wave
+    TILE_COUNT = 6
+};
+int conv_tile_threads(int tile);
 int conv_tile_bm(int tile);
 int conv_tile_bn(int tile);
 constexpr int CONV_BK = 64;

@@ -21,6 +21,9 @@
 // side stream: copy i waits for the consumer of the chunk that last used
 // its slot, and consumer i waits for copy i.
 #include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <numeric>
 #include <queue>
@@ -76,6 +79,7 @@ void free_placement(gemel_ctx *ctx) {
     if (ctx->wpool) (void)hipFree(ctx->wpool);
     if (ctx->staging) (void)hipFree(ctx->staging);
     ctx->wpool = ctx->staging = nullptr;
+    ctx->zero_page = nullptr;
     ctx->wpool_bytes = 0;
     for (auto e : ctx->ev_copied) (void)hipEventDestroy(e);
     for (auto e : ctx->ev_free) (void)hipEventDestroy(e);
@@ -167,7 +171,7 @@ gemel_status materialise(gemel_ctx *ctx) {
                 return fail(ctx, GEMEL_EBUDGET, "a weight row block does not fit one staging slot");
     }
 
-    size_t pool = aff_total;
+    size_t pool = aff_total + 256;  // + zero page
     for (size_t i = 0; i < blobs.size(); ++i)
         if (resident[i]) pool += (size_t)round_up((int64_t)blobs[i]->w_bytes(), 256);
     if (hipMalloc(&ctx->wpool, pool) != hipSuccess) {
@@ -176,7 +180,15 @@ gemel_status materialise(gemel_ctx *ctx) {
         return fail(ctx, GEMEL_ENOMEM, "device allocation of the weight pool failed");
     }
     ctx->wpool_bytes = pool;
-    size_t off = 0;
+    {
+        static const uint8_t zeros[256] = {};
+        ctx->zero_page = ctx->wpool;
+        if (hipMemcpy(ctx->zero_page, zeros, sizeof(zeros), hipMemcpyHostToDevice) != hipSuccess) {
+            free_placement(ctx);
+            return fail(ctx, GEMEL_EDEVICE, "zero page upload failed");
+        }
+    }
+    size_t off = 256;
     for (size_t i = 0; i < blobs.size(); ++i) {
         Blob &b = *blobs[i];
         ctx->placed.push_back(blobs[i]);
@@ -252,17 +264,48 @@ bool direct_output(const Layer &l) {
     return l.is_output && l.consumers == 0 && (l.op == GEMEL_OP_CONV || l.op == GEMEL_OP_FC);
 }
 
-// Launch configuration of a bf16 implicit-GEMM conv of size M x N x K.
-void pick_conv_config(int64_t M, int64_t N, int64_t K, int &tile, int &splits, int &kps) {
-    tile = N <= 64 ? TILE_128x64 : TILE_128x128;
-    const int64_t bm = conv_tile_bm(tile), bn = conv_tile_bn(tile);
-    const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+// Launch configuration of a bf16 implicit-GEMM conv of size M x N x K:
+// the tile shape and split-K factor with the smallest estimated time.
+// Model: a tile costs 2*bm*bn*depth FLOPs at a per-CU rate scaled by a
+// measured relative efficiency of its shape; tiles run in waves of
+// (256 CUs x resident tiles per CU); split-K adds the partial-sum round
+// trip through memory and a reduction launch.
+struct TileCost {
+    int tile;
+    double eff;   // relative MFMA efficiency of the tile shape
+    int occ;      // tiles resident per CU
+};
+static const TileCost kTileCost[] = {
+    {TILE_256x256, 1.00, 1}, {TILE_256x128, 0.90, 1}, {TILE_128x128, 0.80, 1},
+    {TILE_256x64, 0.75, 1},  {TILE_128x64, 0.65, 2},  {TILE_64x64, 0.45, 3}};
+
+void pick_conv_config(int64_t M, int64_t N, int64_t K, int force, int force_splits, int &tile, int &splits,
+                      int &kps) {
+    const double cu_flops = 4096.0 * 2.4e9;   // per CU, dense bf16
+    double best = 1e300;
+    tile = force >= 0 ? force : TILE_64x64;
     splits = 1;
-    if (tiles < 512) {
-        const int64_t want = (512 + tiles - 1) / tiles;
-        const int64_t maxs = std::max<int64_t>(1, K / (4 * CONV_BK));
-        splits = (int)std::min(want, maxs);
+    for (const TileCost &tc : kTileCost) {
+        if (force >= 0 && tc.tile != force) continue;
+        const int64_t bm = conv_tile_bm(tc.tile), bn = conv_tile_bn(tc.tile);
+        if (force < 0 && bn > 64 && N <= bn / 2) continue;   // mostly padding columns
+        const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+        for (int s = 1; s <= 16; s *= 2) {
+            if (s > 1 && K / s < 4 * CONV_BK) break;
+            const int64_t k_s = round_up((K + s - 1) / s, CONV_BK);
+            const int64_t s_eff = (K + k_s - 1) / k_s;
+            const double waves = std::ceil((double)(tiles * s_eff) / (256.0 * tc.occ));
+            double t = waves * tc.occ * (2.0 * bm * bn * k_s) / (cu_flops * tc.eff);
+            t += 3e-6;                                  // launch + tail
+            if (s_eff > 1) t += (double)s_eff * M * N * 4.0 * 2.0 / 4e12 + 4e-6;
+            if (t < best) {
+                best = t;
+                tile = tc.tile;
+                splits = (int)s_eff;
+            }
+        }
     }
+    if (force_splits > 0) splits = (int)std::min<int64_t>(force_splits, (K + CONV_BK - 1) / CONV_BK);
     kps = (int)round_up((K + splits - 1) / splits, CONV_BK);
     splits = (int)((K + kps - 1) / kps);
 }
@@ -554,6 +597,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 }
                 ConvArgs &a = Lc.conv;
                 a.w = wptr;
+                a.zero = ctx->zero_page;
                 a.M = (int)M; a.N = (int)nrows; a.K = (int)blob->k;
                 if (L0.op == GEMEL_OP_CONV) {
                     a.H = L0.in_h; a.W = L0.in_w; a.Cin = L0.in_cp; a.in_cs = L0.in_cp;
@@ -587,8 +631,12 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     a.nseg++;
                 }
                 if (!a.nseg) continue;
+                a.uni_affine = 1;
+                for (int i = 1; i < a.nseg; ++i)
+                    if (a.seg[i].scale != a.seg[0].scale || a.seg[i].shift != a.seg[0].shift) a.uni_affine = 0;
                 if (bf16) {
-                    pick_conv_config(a.M, a.N, a.K, Lc.tile, a.k_splits, a.k_per_split);
+                    pick_conv_config(a.M, a.N, a.K, ctx->opt.conv_tile, ctx->opt.conv_splits, Lc.tile, a.k_splits,
+                                     a.k_per_split);
                     Lc.type = L_CONV_BF16;
                     Lc.kind = L0.op == GEMEL_OP_CONV ? GEMEL_K_CONV_MFMA : GEMEL_K_FC;
                 } else {
@@ -669,6 +717,20 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
             a.max_frames = a.seg[0].frames;
             Le.patches.push_back({Patch::OUTPUT, s, L.out_index, 0});
             P.launches.push_back(Le);
+        }
+    }
+    if (const char *tr = std::getenv("GEMEL_TRACE_PLAN"); tr && tr[0] == '1') {
+        static const char *names[] = {"pack", "conv_bf16", "conv_f32", "conv_reduce", "fc_bf16", "fc_f32",
+                                      "fc_reduce", "maxpool", "avgpool", "upsample", "concat", "export"};
+        for (size_t i = 0; i < P.launches.size(); ++i) {
+            const Launch &L = P.launches[i];
+            const bool cv = L.type == L_CONV_BF16 || L.type == L_CONV_F32;
+            const bool fcl = L.type == L_FC_BF16 || L.type == L_FC_F32;
+            std::fprintf(stderr, "plan %zu %s M=%d N=%d K=%d tile=%d splits=%d segs=%d gflop=%.3f mb=%.2f\n", i,
+                         names[L.type], cv ? L.conv.M : fcl ? L.fc.M : 0, cv ? L.conv.N : fcl ? L.fc.N : 0,
+                         cv ? L.conv.K : fcl ? L.fc.K : 0, L.tile,
+                         cv ? L.conv.k_splits : fcl ? L.fc.k_splits : 0,
+                         cv ? L.conv.nseg : fcl ? L.fc.nseg : L.ew.nseg, L.flops / 1e9, L.bytes / 1e6);
         }
     }
     if (partial_need) {

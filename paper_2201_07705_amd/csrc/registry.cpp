@@ -416,6 +416,16 @@ gemel_status gemel_set_option(gemel_ctx *ctx, int32_t key, int64_t value) {
         ctx->opt.split_merged = (int)value;
         drop_plans(ctx);
         break;
+    case GEMEL_OPT_CONV_TILE:
+        if (value < -1 || value >= TILE_COUNT) return fail(ctx, GEMEL_EINVAL, "conv tile is -1..5");
+        ctx->opt.conv_tile = (int)value;
+        drop_plans(ctx);
+        break;
+    case GEMEL_OPT_CONV_SPLITS:
+        if (value < 0 || value > 64) return fail(ctx, GEMEL_EINVAL, "conv splits is 0..64");
+        ctx->opt.conv_splits = (int)value;
+        drop_plans(ctx);
+        break;
     case GEMEL_OPT_PROFILE:
         if (value != 0 && value != 1) return fail(ctx, GEMEL_EINVAL, "profile is 0 or 1");
         profile_reset(ctx);

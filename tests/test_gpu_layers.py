@@ -30,7 +30,7 @@ def conv(name, src, cin, cout, k, s=1, p=0, **kw):
 
 
 def run_case(layers_per_model, in_chw, frames, dtype, groups=(), seed=7,
-             tol=None, dist="normal"):
+             tol=None, dist="normal", tile=-1):
     models = [ModelSpec(f"m{i}", "custom", lay, n, in_chw)
               for i, (lay, n) in enumerate(zip(layers_per_model, frames))]
     wl = Workload(f"case{seed}", seed, dtype, models, list(groups), dist)
@@ -38,6 +38,9 @@ def run_case(layers_per_model, in_chw, frames, dtype, groups=(), seed=7,
     fr = [wl.frames(i) for i in range(len(models))]
     g = GpuWorkload(wl, params)
     try:
+        if tile >= 0:
+            from paper_2201_07705_amd import gemel as G
+            g.ctx.set_option(G.OPT_CONV_TILE, tile)
         got = g.run(fr)
     finally:
         g.close()
@@ -67,6 +70,22 @@ def test_conv_layer_output_store(dtype, case):
     log(f"conv {case} {dtype}")
     lay = [conv("c", -1, cin, cout, k, s, p, bias=True, act="relu", out=True)]
     run_case([lay], (cin, hw, hw), [n], dtype)
+
+
+TILES = ["128x128", "128x64", "64x64", "256x256", "256x128", "256x64"]
+
+
+@pytest.mark.parametrize("tile", range(len(TILES)), ids=lambda t: TILES[t])
+@pytest.mark.parametrize("case", CONV_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_conv_every_tile_shape(tile, case):
+    """Every tile shape (forced) on every conv case, internal bf16 store
+    with a residual and the fp32 output store."""
+    cin, cout, k, s, p, hw, n = case
+    log(f"tile {TILES[tile]} conv {case}")
+    lay = [conv("c", -1, cin, cout, k, s, p, bn=True, act="leaky"),
+           conv("d", 0, cout, cout, 1, 1, 0, bn=True, act="relu", res=0),
+           conv("o", 1, cout, 24, 3, 1, 1, bias=True, out=True)]
+    run_case([lay], (cin, hw, hw), [n], "bf16", tile=tile)
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
