@@ -250,7 +250,7 @@ enum {
                                     events on the launch stream (disables
                                     graph replay); 0 (default): off. Setting
                                     it clears the collected statistics.    */
-    GEMEL_OPT_CONV_TILE = 7      /* -1 (default): pick each conv's tile
+    GEMEL_OPT_CONV_TILE = 7,     /* -1 (default): pick each conv's tile
                                     shape and split-K by the cost model;
                                     0..5: force one tile shape (128x128,
                                     128x64, 64x64, 256x256, 256x128,

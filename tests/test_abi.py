@@ -29,6 +29,24 @@ def test_library_exports_every_declared_function():
         assert hasattr(lib, name), name
 
 
+def test_header_compiles_as_c_and_cxx():
+    import subprocess
+    h = os.path.join(ROOT, "include", "gemel.h")
+    for lang in ("c", "c++"):
+        r = subprocess.run(["gcc", "-fsyntax-only", "-Wall", "-Werror", "-x",
+                            lang, h], capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
+
+
+def test_library_is_newer_than_its_sources():
+    import glob
+    lib = os.path.join(ROOT, "paper_2201_07705_amd", "libgemel.so")
+    srcs = glob.glob(os.path.join(ROOT, "paper_2201_07705_amd", "csrc", "*")) \
+        + [os.path.join(ROOT, "include", "gemel.h")]
+    newest = max(os.path.getmtime(p) for p in srcs)
+    assert os.path.getmtime(lib) >= newest, "libgemel.so is stale: rebuild"
+
+
 def test_header_enums_match_binding():
     txt = open(os.path.join(ROOT, "include", "gemel.h")).read()
     for name, val in [("GEMEL_EBUDGET", G.EBUDGET), ("GEMEL_OP_CONCAT", 5),
