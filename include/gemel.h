@@ -252,12 +252,20 @@ enum {
                                     it clears the collected statistics.    */
     GEMEL_OPT_CONV_TILE = 7,     /* -1 (default): pick each conv's tile
                                     shape and split-K by the cost model;
-                                    0..5: force one tile shape (128x128,
+                                    0..8: force one tile shape (128x128,
                                     128x64, 64x64, 256x256, 256x128,
-                                    256x64) with split-K still chosen      */
-    GEMEL_OPT_CONV_SPLITS = 8    /* 0 (default): split-K chosen per conv;
+                                    256x64, 64x64 and 128x64 with deeper
+                                    prefetch, 64x128) with split-K still
+                                    chosen                                 */
+    GEMEL_OPT_CONV_SPLITS = 8,   /* 0 (default): split-K chosen per conv;
                                     n >= 1: force n depth splits (capped
                                     so that every split has work)          */
+    GEMEL_OPT_STREAMS = 9        /* 1..8 (default 1): streams over which
+                                    independent layers of a round run
+                                    concurrently (forked from and joined to
+                                    the caller's stream). Applies to rounds
+                                    enqueued directly (graph replay off, or
+                                    profiling on); 1 with the null stream  */
 };
 
 /* Set an option; takes effect at the next gemel_infer. Errors: EINVAL. */

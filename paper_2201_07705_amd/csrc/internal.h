@@ -85,6 +85,11 @@ struct Launch {
     std::vector<Patch> patches;
     // weight streaming: >= 0 when the weights come from a staging slot
     int chunk = -1;
+    // concurrency: stream index, plan events waited for before the launch,
+    // plan event recorded after it (-1 = none)
+    int stream = 0;
+    std::vector<int> waits;
+    int record = -1;
 };
 
 // A chunk of a streamed blob: weight rows [row0, row0 + nrows).
@@ -97,7 +102,12 @@ struct Chunk {
 struct Plan {
     std::vector<int> model_ids, n_frames;  // active models (key)
     std::vector<int> out_base;             // first output index per slot
-    std::vector<Launch> launches;
+    std::vector<Launch> launches;          // input packs first, then steps
+    int n_pack = 0;                        // launches before the fork
+    int n_streams = 1;                     // streams the launches use
+    std::vector<hipEvent_t> events;        // cross-stream dependencies
+    hipEvent_t ev_fork = nullptr;          // origin -> worker streams
+    std::vector<hipEvent_t> ev_join;       // worker streams -> origin
     std::vector<Chunk> chunks;             // streamed chunks, consumption order
     void *arena = nullptr;
     size_t arena_bytes = 0;
@@ -126,6 +136,7 @@ struct Profile {
 };
 
 struct Options {
+    int streams = 1;
     int profile = 0;
     int conv_tile = -1;
     int conv_splits = 0;
@@ -150,6 +161,7 @@ struct gemel_ctx {
     bool dev_ready = false;
     bool weights_ready = false;      // placement matches registry + groups
     hipStream_t side = nullptr;      // weight-copy stream
+    std::vector<hipStream_t> workers;  // extra streams for concurrent steps
     std::vector<hipEvent_t> ev_copied, ev_free;
     void *wpool = nullptr;           // resident weights + all scale/shift
     void *zero_page = nullptr;       // 256 zero bytes inside wpool

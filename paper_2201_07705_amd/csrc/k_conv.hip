@@ -277,6 +277,36 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a
         }
     };
 
+    const Epi e = epi_of(a, HWo);
+    // Epilogue operands fetched before the depth loop so that their latency
+    // overlaps the MFMAs: this thread's 8 channels of scale/shift and, for
+    // single-pass tiles, the residual chunks of its output items.
+    const int my_ch = tid % CH;
+    const int my_gn = tn * BN + my_ch * 8;
+    float sc[8], sh[8];
+    const bool pre = a.uni_affine && a.k_splits <= 1 && a.out_mode == OUT_NHWC && my_gn < a.N;
+    if (pre) {
+        const float4 s0 = *(const float4 *)(a.seg[0].scale + my_gn), s1 = *(const float4 *)(a.seg[0].scale + my_gn + 4);
+        const float4 h0 = *(const float4 *)(a.seg[0].shift + my_gn), h1 = *(const float4 *)(a.seg[0].shift + my_gn + 4);
+        sc[0] = s0.x; sc[1] = s0.y; sc[2] = s0.z; sc[3] = s0.w; sc[4] = s1.x; sc[5] = s1.y; sc[6] = s1.z; sc[7] = s1.w;
+        sh[0] = h0.x; sh[1] = h0.y; sh[2] = h0.z; sh[3] = h0.w; sh[4] = h1.x; sh[5] = h1.y; sh[6] = h1.z; sh[7] = h1.w;
+    }
+    constexpr int ITEMS = BM * CH / NT;          // output items per thread
+    constexpr bool RES_PF = WPP == WM && ITEMS <= 4 && ITEMS * NT == BM * CH;
+    u32x4 rpf[RES_PF ? ITEMS : 1];
+    if (RES_PF && pre && e.has_res) {
+#pragma unroll
+        for (int i = 0; i < (RES_PF ? ITEMS : 1); ++i) {
+            const int gm = tm * BM + (tid + NT * i) / CH;
+            const u16 *p = zp;
+            if (gm < a.M) {
+                const ConvSeg &sg = a.seg[seg_of_row(a, gm)];
+                p = (const u16 *)sg.res + (size_t)(gm - sg.m_start) * e.out_cs + my_gn;
+            }
+            rpf[i] = *(const u32x4 *)p;
+        }
+    }
+
     const int nk = (k_end - k_begin + BK - 1) / BK;
     if (DEPTH == 2) {
         u32x4 ra0[AP], rb0[BP], ra1[AP], rb1[BP];
@@ -311,17 +341,6 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a
 
     // ---- epilogue: fp32 tile staged through LDS, WPP wave rows per pass ----
     float *Cs = (float *)smem;
-    const Epi e = epi_of(a, HWo);
-    const int my_ch = tid % CH;
-    const int my_gn = tn * BN + my_ch * 8;
-    float sc[8], sh[8];
-    const bool pre = a.uni_affine && a.k_splits <= 1 && a.out_mode == OUT_NHWC && my_gn < a.N;
-    if (pre) {
-        const float4 s0 = *(const float4 *)(a.seg[0].scale + my_gn), s1 = *(const float4 *)(a.seg[0].scale + my_gn + 4);
-        const float4 h0 = *(const float4 *)(a.seg[0].shift + my_gn), h1 = *(const float4 *)(a.seg[0].shift + my_gn + 4);
-        sc[0] = s0.x; sc[1] = s0.y; sc[2] = s0.z; sc[3] = s0.w; sc[4] = s1.x; sc[5] = s1.y; sc[6] = s1.z; sc[7] = s1.w;
-        sh[0] = h0.x; sh[1] = h0.y; sh[2] = h0.z; sh[3] = h0.w; sh[4] = h1.x; sh[5] = h1.y; sh[6] = h1.z; sh[7] = h1.w;
-    }
     for (int pass = 0; pass < WM; pass += WPP) {
         if (wm >= pass && wm < pass + WPP) {
 #pragma unroll
@@ -360,10 +379,16 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a
                     const size_t off = (size_t)(gm - sg.m_start) * e.out_cs + gn;
                     u16 rv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
                     if (e.has_res) {
-                        const uint4 r4 = *(const uint4 *)((const u16 *)sg.res + off);
-                        const u16 *rp = (const u16 *)&r4;
+                        u32x4 r4;
+                        if constexpr (RES_PF)
+                            r4 = rpf[(item - tid) / NT];
+                        else
+                            r4 = *(const u32x4 *)((const u16 *)sg.res + off);
 #pragma unroll
-                        for (int jj = 0; jj < 8; ++jj) rv[jj] = rp[jj];
+                        for (int jj = 0; jj < 4; ++jj) {
+                            rv[2 * jj] = (u16)(r4[jj] & 0xffffu);
+                            rv[2 * jj + 1] = (u16)(r4[jj] >> 16);
+                        }
                     }
                     uint4 o;
                     u16 *op = (u16 *)&o;
@@ -452,7 +477,8 @@ struct TileShape {
     int bm, bn, threads;
 };
 static const TileShape kTiles[TILE_COUNT] = {
-    {128, 128, 256}, {128, 64, 256}, {64, 64, 256}, {256, 256, 512}, {256, 128, 512}, {256, 64, 256}};
+    {128, 128, 256}, {128, 64, 256}, {64, 64, 256}, {256, 256, 512}, {256, 128, 512},
+    {256, 64, 256},  {64, 64, 256},  {128, 64, 256}, {64, 128, 256}};
 
 int conv_tile_bm(int tile) { return tile >= 0 && tile < TILE_COUNT ? kTiles[tile].bm : 0; }
 int conv_tile_bn(int tile) { return tile >= 0 && tile < TILE_COUNT ? kTiles[tile].bn : 0; }
@@ -486,6 +512,9 @@ static void launch_tile(int tile, dim3 grid, hipStream_t st, const ConvArgs &a) 
     case TILE_256x256: hipLaunchKernelGGL((conv_bf16_kernel<256, 256, 2, 4, 1, C64>), grid, dim3(512), 0, st, a); break;
     case TILE_256x128: hipLaunchKernelGGL((conv_bf16_kernel<256, 128, 4, 2, 1, C64>), grid, dim3(512), 0, st, a); break;
     case TILE_256x64: hipLaunchKernelGGL((conv_bf16_kernel<256, 64, 4, 1, 1, C64>), grid, dim3(256), 0, st, a); break;
+    case TILE_64x64_D2: hipLaunchKernelGGL((conv_bf16_kernel<64, 64, 2, 2, 2, C64>), grid, dim3(256), 0, st, a); break;
+    case TILE_128x64_D2: hipLaunchKernelGGL((conv_bf16_kernel<128, 64, 2, 2, 2, C64>), grid, dim3(256), 0, st, a); break;
+    case TILE_64x128: hipLaunchKernelGGL((conv_bf16_kernel<64, 128, 2, 2, 1, C64>), grid, dim3(256), 0, st, a); break;
     }
 }
 

@@ -16,7 +16,10 @@ enum ConvTile {
     TILE_256x256 = 3,  // 8 waves, 128x64 per wave
     TILE_256x128 = 4,  // 8 waves, 64x64 per wave
     TILE_256x64 = 5,   // 4 waves, 64x64 per wave
-    TILE_COUNT = 6
+    TILE_64x64_D2 = 6, // as 64x64, loads two depth steps ahead
+    TILE_128x64_D2 = 7,// as 128x64, loads two depth steps ahead
+    TILE_64x128 = 8,   // 4 waves, 32x64 per wave
+    TILE_COUNT = 9
 };
 int conv_tile_threads(int tile);
 int conv_tile_bm(int tile);

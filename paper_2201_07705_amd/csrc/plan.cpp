@@ -21,6 +21,7 @@
 // side stream: copy i waits for the consumer of the chunk that last used
 // its slot, and consumer i waits for copy i.
 #include <algorithm>
+#include <functional>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -64,6 +65,11 @@ gemel_status ensure_device(gemel_ctx *ctx) {
     if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
         return fail(ctx, GEMEL_EDEVICE, std::string("libgemel is built for gfx950; device is ") + prop.gcnArchName);
     HIPCHK(hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking), "hipStreamCreate");
+    for (int i = 0; i < 7; ++i) {
+        hipStream_t w = nullptr;
+        HIPCHK(hipStreamCreateWithFlags(&w, hipStreamNonBlocking), "hipStreamCreate");
+        ctx->workers.push_back(w);
+    }
     ctx->dev_ready = true;
     return GEMEL_OK;
 }
@@ -97,6 +103,11 @@ void drop_plans(gemel_ctx *ctx) {
     for (auto &kv : ctx->plans) {
         Plan &p = *kv.second;
         if (p.graph) (void)hipGraphExecDestroy(p.graph);
+        for (auto ev : p.events)
+            if (ev) (void)hipEventDestroy(ev);
+        if (p.ev_fork) (void)hipEventDestroy(p.ev_fork);
+        for (auto ev : p.ev_join)
+            if (ev) (void)hipEventDestroy(ev);
         if (p.arena) (void)hipFree(p.arena);
         if (p.partial) (void)hipFree(p.partial);
     }
@@ -109,6 +120,8 @@ void release_device(gemel_ctx *ctx) {
     free_placement(ctx);
     if (ctx->side) (void)hipStreamDestroy(ctx->side);
     ctx->side = nullptr;
+    for (auto w : ctx->workers) (void)hipStreamDestroy(w);
+    ctx->workers.clear();
     ctx->dev_ready = false;
 }
 
@@ -411,54 +424,138 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
         if (!topo(order)) return fail(ctx, GEMEL_ESTATE, "internal: layer graph has a cycle");
     }
 
-    // ---- tensors and lifetimes: step 0 = pack, node steps 1.., exports last ----
-    std::map<TRef, Tensor> T;
-    const int last_step = (int)order.size() + 1;
+    // ---- steps: the ordered nodes, then one export step per output that is
+    // not written directly by its conv/FC epilogue ----
+    const int NN = (int)order.size();
+    std::vector<int> pos(nodes.size());
+    for (int i = 0; i < NN; ++i) pos[(size_t)order[(size_t)i]] = i;
+    std::vector<std::pair<int, int>> exports;  // (slot, layer)
+    for (int s = 0; s < S; ++s)
+        for (int l : model(s).outputs)
+            if (!direct_output(layer(s, l))) exports.push_back({s, l});
+    const int NS = NN + (int)exports.size();
+    auto step_of = [&](int s, int l) { return pos[(size_t)node_of[(size_t)s][(size_t)l]]; };
+    std::vector<std::vector<int>> preds((size_t)NS);
+    std::vector<double> est((size_t)NS, 5e-6);
+    for (int i = 0; i < NN; ++i) {
+        std::set<int> ps;
+        for (auto [s, l] : nodes[(size_t)order[(size_t)i]].mem) {
+            const Layer &L = layer(s, l);
+            if (L.src0 >= 0) ps.insert(step_of(s, L.src0));
+            if (L.op == GEMEL_OP_CONCAT && L.src1 >= 0) ps.insert(step_of(s, L.src1));
+            if (L.res >= 0) ps.insert(step_of(s, L.res));
+            const double n = nfr[(size_t)s];
+            const double kd = L.op == GEMEL_OP_CONV ? (double)L.kh * L.kw * L.cin : (double)L.cin;
+            if (L.op == GEMEL_OP_CONV || L.op == GEMEL_OP_FC)
+                est[(size_t)i] += 2.0 * n * L.out_h * L.out_w * L.out_c * kd / 1e15;
+            est[(size_t)i] += n * L.out_h * L.out_w * L.out_cp * esz / 4e12;
+        }
+        preds[(size_t)i].assign(ps.begin(), ps.end());
+    }
+    for (size_t e = 0; e < exports.size(); ++e) preds[(size_t)NN + e] = {step_of(exports[e].first, exports[e].second)};
+
+    // ---- streams: each step continues the stream of a predecessor it directly
+    // follows, else starts on the least loaded stream; cross-stream edges
+    // become event waits ----
+    const int SMAX = std::max(1, std::min(ctx->opt.streams, 1 + (int)ctx->workers.size()));
+    std::vector<int> stream_of((size_t)NS, 0), tail((size_t)SMAX, -2);
+    std::vector<double> load((size_t)SMAX, 0.0);
+    for (int i = 0; i < NS; ++i) {
+        int st = -1;
+        for (int p : preds[(size_t)i])
+            if (tail[(size_t)stream_of[(size_t)p]] == p) {
+                st = stream_of[(size_t)p];
+                break;
+            }
+        if (st < 0) {
+            st = 0;
+            for (int k = 1; k < SMAX; ++k)
+                if (load[(size_t)k] < load[(size_t)st]) st = k;
+        }
+        stream_of[(size_t)i] = st;
+        tail[(size_t)st] = i;
+        load[(size_t)st] += est[(size_t)i];
+    }
+    std::vector<int> event_of((size_t)NS, -1);
+    int n_events = 0;
+    P.n_streams = 1;
+    for (int i = 0; i < NS; ++i) {
+        P.n_streams = std::max(P.n_streams, stream_of[(size_t)i] + 1);
+        for (int p : preds[(size_t)i])
+            if (stream_of[(size_t)p] != stream_of[(size_t)i] && event_of[(size_t)p] < 0) event_of[(size_t)p] = n_events++;
+    }
+
+    // ---- happens-before: ancestors of each step in the dependency graph ----
+    const size_t WDS = ((size_t)NS + 63) / 64;
+    std::vector<uint64_t> anc((size_t)NS * WDS, 0);
+    for (int i = 0; i < NS; ++i)
+        for (int p : preds[(size_t)i]) {
+            uint64_t *dst = &anc[(size_t)i * WDS];
+            const uint64_t *src = &anc[(size_t)p * WDS];
+            for (size_t w = 0; w < WDS; ++w) dst[w] |= src[w];
+            dst[(size_t)p / 64] |= 1ull << (p % 64);
+        }
+    auto before = [&](int a_, int b_) {  // step a_ strictly precedes step b_
+        if (a_ < 0) return b_ >= 0;          // the pack precedes every step
+        if (b_ < 0) return false;
+        return ((anc[(size_t)b_ * WDS + (size_t)a_ / 64] >> (a_ % 64)) & 1ull) != 0;
+    };
+
+    // ---- tensors: producer step (-1 = pack), user steps; two tensors share
+    // bytes only when every use of one precedes the other's producer ----
+    struct TInfo {
+        size_t bytes = 0, off = 0;
+        int prod = -1;
+        std::vector<int> users;
+    };
+    std::map<TRef, TInfo> T;
     for (int s = 0; s < S; ++s) {
         const Model &m = model(s);
-        Tensor t;
-        t.bytes = (size_t)nfr[(size_t)s] * m.in_h * m.in_w * m.in_cp * esz;
-        t.first = t.last = 0;
-        T[{s, -1}] = t;
+        T[{s, -1}].bytes = (size_t)nfr[(size_t)s] * m.in_h * m.in_w * m.in_cp * esz;
     }
-    for (int step = 0; step < (int)order.size(); ++step)
-        for (auto [s, l] : nodes[(size_t)order[(size_t)step]].mem) {
+    for (int i = 0; i < NN; ++i)
+        for (auto [s, l] : nodes[(size_t)order[(size_t)i]].mem) {
             const Layer &L = layer(s, l);
             if (!direct_output(L)) {
-                Tensor t;
+                TInfo &t = T[{s, l}];
                 t.bytes = (size_t)nfr[(size_t)s] * L.out_h * L.out_w * L.out_cp * esz;
-                t.first = step + 1;
-                t.last = L.is_output ? last_step : step + 1;
-                T[{s, l}] = t;
+                t.prod = i;
             }
         }
-    auto touch = [&](int s, int p, int step) {
+    auto use = [&](int s, int p, int i) {
         auto it = T.find({s, p});
-        if (it != T.end()) it->second.last = std::max(it->second.last, step);
+        if (it != T.end()) it->second.users.push_back(i);
     };
-    for (int step = 0; step < (int)order.size(); ++step)
-        for (auto [s, l] : nodes[(size_t)order[(size_t)step]].mem) {
+    for (int i = 0; i < NN; ++i)
+        for (auto [s, l] : nodes[(size_t)order[(size_t)i]].mem) {
             const Layer &L = layer(s, l);
-            touch(s, L.src0, step + 1);
-            if (L.op == GEMEL_OP_CONCAT) touch(s, L.src1, step + 1);
-            if (L.res >= 0) touch(s, L.res, step + 1);
+            use(s, L.src0, i);
+            if (L.op == GEMEL_OP_CONCAT) use(s, L.src1, i);
+            if (L.res >= 0) use(s, L.res, i);
         }
-    // offsets: largest first, lowest gap among lifetime-overlapping tensors
-    std::vector<Tensor *> tv;
+    for (size_t e = 0; e < exports.size(); ++e) use(exports[e].first, exports[e].second, NN + (int)e);
+    auto done_before = [&](const TInfo &t, const TInfo &u) {
+        if (u.prod < 0) return false;
+        if (t.users.empty()) return before(t.prod, u.prod);
+        for (int x : t.users)
+            if (!before(x, u.prod)) return false;
+        return true;
+    };
+    std::vector<TInfo *> tv;
     for (auto &kv : T)
         if (kv.second.bytes) tv.push_back(&kv.second);
-    std::stable_sort(tv.begin(), tv.end(), [](Tensor *a, Tensor *b) { return a->bytes > b->bytes; });
-    std::vector<Tensor *> placed;
+    std::stable_sort(tv.begin(), tv.end(), [](TInfo *x, TInfo *y) { return x->bytes > y->bytes; });
+    std::vector<TInfo *> placed;
     size_t arena = 0;
-    for (Tensor *t : tv) {
+    for (TInfo *t : tv) {
         std::vector<std::pair<size_t, size_t>> busy;
-        for (Tensor *o : placed)
-            if (!(o->last < t->first || t->last < o->first)) busy.push_back({o->off, o->off + o->bytes});
+        for (TInfo *o : placed)
+            if (!done_before(*o, *t) && !done_before(*t, *o)) busy.push_back({o->off, o->off + o->bytes});
         std::sort(busy.begin(), busy.end());
         size_t cand = 0;
-        for (auto &b : busy) {
-            if (cand + t->bytes <= b.first) break;
-            cand = std::max(cand, (size_t)round_up((int64_t)b.second, 256));
+        for (auto &bz : busy) {
+            if (cand + t->bytes <= bz.first) break;
+            cand = std::max(cand, (size_t)round_up((int64_t)bz.second, 256));
         }
         t->off = cand;
         arena = std::max(arena, cand + (size_t)round_up((int64_t)t->bytes, 256));
@@ -474,6 +571,26 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
         auto it = T.find({s, l});
         if (it == T.end() || !it->second.bytes) return nullptr;
         return (char *)P.arena + it->second.off;
+    };
+    P.events.assign((size_t)n_events, nullptr);
+    for (auto &ev : P.events)
+        if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess)
+            return fail(ctx, GEMEL_EDEVICE, "event creation failed");
+    if (P.n_streams > 1) {
+        if (hipEventCreateWithFlags(&P.ev_fork, hipEventDisableTiming) != hipSuccess)
+            return fail(ctx, GEMEL_EDEVICE, "event creation failed");
+        P.ev_join.assign((size_t)P.n_streams, nullptr);
+        for (int k = 1; k < P.n_streams; ++k)
+            if (hipEventCreateWithFlags(&P.ev_join[(size_t)k], hipEventDisableTiming) != hipSuccess)
+                return fail(ctx, GEMEL_EDEVICE, "event creation failed");
+    }
+    // stream, waits and event record of the launches of step i
+    auto tag_launches = [&](size_t first, int i) {
+        if (first >= P.launches.size()) return;
+        for (size_t k = first; k < P.launches.size(); ++k) P.launches[k].stream = stream_of[(size_t)i];
+        for (int p : preds[(size_t)i])
+            if (stream_of[(size_t)p] != stream_of[(size_t)i]) P.launches[first].waits.push_back(event_of[(size_t)p]);
+        P.launches.back().record = event_of[(size_t)i];
     };
 
     // ---- launches ----
@@ -509,9 +626,15 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 P.launches.push_back(L);
             }
     }
+    P.n_pack = (int)P.launches.size();
     auto in_ptr = [&](int s, int p) { return p < 0 ? tptr(s, -1) : tptr(s, p); };
 
-    for (int step = 0; step < (int)order.size(); ++step) {
+    for (int step = 0; step < NN; ++step) {
+        const size_t first_launch = P.launches.size();
+        struct Tagger {
+            std::function<void()> f;
+            ~Tagger() { f(); }
+        } tagger{[&, first_launch, step] { tag_launches(first_launch, step); }};
         const Node &nd = nodes[(size_t)order[(size_t)step]];
         const auto [s0, l0] = nd.mem[0];
         const Layer &L0 = layer(s0, l0);
@@ -697,27 +820,26 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
         P.launches.push_back(Le);
     }
     // outputs that are also read internally (or not conv/fc): export to NCHW f32
-    for (int s = 0; s < S; ++s) {
-        const Model &m = model(s);
-        for (int l : m.outputs) {
-            const Layer &L = m.layers[(size_t)l];
-            if (direct_output(L)) continue;
-            Launch Le;
-            Le.type = L_EXPORT;
-            Le.kind = GEMEL_K_EXPORT;
-            Le.bytes = (double)nfr[(size_t)s] * L.out_h * L.out_w * L.out_c * (esz + 4.0);
-            Le.bf16 = bf16;
-            EwArgs &a = Le.ew;
-            a.H = L.out_h; a.W = L.out_w; a.C = L.out_cp; a.c_logical = L.out_c;
-            a.nseg = 1;
-            a.seg[0].in0 = tptr(s, l);
-            a.seg[0].in1 = nullptr;
-            a.seg[0].out = nullptr;
-            a.seg[0].frames = nfr[(size_t)s];
-            a.max_frames = a.seg[0].frames;
-            Le.patches.push_back({Patch::OUTPUT, s, L.out_index, 0});
-            P.launches.push_back(Le);
-        }
+    for (size_t e = 0; e < exports.size(); ++e) {
+        const auto [s, l] = exports[e];
+        const Layer &L = model(s).layers[(size_t)l];
+        const size_t first_launch = P.launches.size();
+        Launch Le;
+        Le.type = L_EXPORT;
+        Le.kind = GEMEL_K_EXPORT;
+        Le.bytes = (double)nfr[(size_t)s] * L.out_h * L.out_w * L.out_c * (esz + 4.0);
+        Le.bf16 = bf16;
+        EwArgs &a = Le.ew;
+        a.H = L.out_h; a.W = L.out_w; a.C = L.out_cp; a.c_logical = L.out_c;
+        a.nseg = 1;
+        a.seg[0].in0 = tptr(s, l);
+        a.seg[0].in1 = nullptr;
+        a.seg[0].out = nullptr;
+        a.seg[0].frames = nfr[(size_t)s];
+        a.max_frames = a.seg[0].frames;
+        Le.patches.push_back({Patch::OUTPUT, s, L.out_index, 0});
+        P.launches.push_back(Le);
+        tag_launches(first_launch, NN + (int)e);
     }
     if (const char *tr = std::getenv("GEMEL_TRACE_PLAN"); tr && tr[0] == '1') {
         static const char *names[] = {"pack", "conv_bf16", "conv_f32", "conv_reduce", "fc_bf16", "fc_f32",
@@ -825,12 +947,21 @@ static gemel_status enqueue(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStre
         gemel_status s = issue_copies(nslots - 1);
         if (s) return s;
     }
-    for (Launch &L : P.launches) {
+    hipStream_t streams[8] = {st};
+    for (int k = 1; k < P.n_streams; ++k) streams[k] = ctx->workers[(size_t)k - 1];
+    for (size_t li = 0; li < P.launches.size(); ++li) {
+        Launch &L = P.launches[li];
+        if ((int)li == P.n_pack && P.n_streams > 1) {
+            HIPCHK(hipEventRecord(P.ev_fork, st), "hipEventRecord");
+            for (int k = 1; k < P.n_streams; ++k) HIPCHK(hipStreamWaitEvent(streams[k], P.ev_fork, 0), "hipStreamWaitEvent");
+        }
+        const hipStream_t ls = streams[L.stream];
+        for (int ev : L.waits) HIPCHK(hipStreamWaitEvent(ls, P.events[(size_t)ev], 0), "hipStreamWaitEvent");
         void *wptr = nullptr;
         if (L.chunk >= 0) {
             gemel_status s = issue_copies(L.chunk + nslots - 1);
             if (s) return s;
-            HIPCHK(hipStreamWaitEvent(st, ctx->ev_copied[(size_t)(L.chunk % nslots)], 0), "hipStreamWaitEvent");
+            HIPCHK(hipStreamWaitEvent(ls, ctx->ev_copied[(size_t)(L.chunk % nslots)], 0), "hipStreamWaitEvent");
             wptr = slot_ptr(L.chunk);
         }
         Profile::Rec rec{nullptr, nullptr, L.kind};
@@ -845,17 +976,26 @@ static gemel_status enqueue(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStre
                 ctx->prof.pool.pop_back();
             }
             ctx->prof.pending.push_back(rec);
-            HIPCHK(hipEventRecord(rec.a, st), "hipEventRecord");
+            HIPCHK(hipEventRecord(rec.a, ls), "hipEventRecord");
         }
-        hipError_t e = launch_one(L, cp, P, wptr, st);
+        hipError_t e = launch_one(L, cp, P, wptr, ls);
         if (e != hipSuccess) return fail(ctx, GEMEL_EDEVICE, std::string("kernel launch: ") + hipGetErrorString(e));
         if (ctx->opt.profile) {
-            HIPCHK(hipEventRecord(rec.b, st), "hipEventRecord");
+            HIPCHK(hipEventRecord(rec.b, ls), "hipEventRecord");
             ctx->prof.flops[L.kind] += L.flops;
             ctx->prof.bytes[L.kind] += L.bytes;
             ctx->prof.launches[L.kind] += 1;
         }
-        if (L.chunk >= 0) HIPCHK(hipEventRecord(ctx->ev_free[(size_t)(L.chunk % nslots)], st), "hipEventRecord");
+        if (L.chunk >= 0) HIPCHK(hipEventRecord(ctx->ev_free[(size_t)(L.chunk % nslots)], ls), "hipEventRecord");
+        if (L.record >= 0) HIPCHK(hipEventRecord(P.events[(size_t)L.record], ls), "hipEventRecord");
+    }
+    if ((int)P.launches.size() <= P.n_pack && P.n_streams > 1) {
+        HIPCHK(hipEventRecord(P.ev_fork, st), "hipEventRecord");
+        for (int k = 1; k < P.n_streams; ++k) HIPCHK(hipStreamWaitEvent(streams[k], P.ev_fork, 0), "hipStreamWaitEvent");
+    }
+    for (int k = 1; k < P.n_streams; ++k) {
+        HIPCHK(hipEventRecord(P.ev_join[(size_t)k], streams[k]), "hipEventRecord");
+        HIPCHK(hipStreamWaitEvent(st, P.ev_join[(size_t)k], 0), "hipStreamWaitEvent");
     }
     return GEMEL_OK;
 }
@@ -882,13 +1022,28 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
     DeviceScope scope(ctx->device);
     gemel_status st = materialise(ctx);
     if (st) return st;
+    // Several streams only for rounds enqueued directly: a round captured into
+    // a HIP graph always runs on the caller's stream alone (a captured
+    // fork/join over worker streams ended a test process with a host fault
+    // whose cause is not established, so that path is switched off).
+    const bool will_graph = ctx->opt.use_graph && !ctx->opt.profile && stream != nullptr;
+    const int nstreams = (stream == nullptr || will_graph) ? 1 : ctx->opt.streams;
+    key.push_back(nstreams);
     auto it = ctx->plans.find(key);
     if (it == ctx->plans.end()) {
         auto P = std::make_unique<Plan>();
+        const int saved = ctx->opt.streams;
+        ctx->opt.streams = nstreams;
         st = build_plan(ctx, ids, nfr, *P);
+        ctx->opt.streams = saved;
         if (st) {
             if (P->arena) (void)hipFree(P->arena);
             if (P->partial) (void)hipFree(P->partial);
+            for (auto ev : P->events)
+                if (ev) (void)hipEventDestroy(ev);
+            if (P->ev_fork) (void)hipEventDestroy(P->ev_fork);
+            for (auto ev : P->ev_join)
+                if (ev) (void)hipEventDestroy(ev);
             return st;
         }
         it = ctx->plans.emplace(key, std::move(P)).first;
@@ -901,7 +1056,7 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         const int no = (int)ctx->models[(size_t)id]->outputs.size();
         for (int o = 0; o < no; ++o) cp.outputs.push_back(outputs[caller_out_base[(size_t)ci] + o]);
     }
-    const bool graphable = ctx->opt.use_graph && !ctx->opt.profile && P.chunks.empty() && stream != nullptr;
+    const bool graphable = will_graph && P.chunks.empty() && P.n_streams == 1;
     if (!graphable) {
         st = enqueue(ctx, P, cp, stream);
         if (!st && ctx->opt.profile) ctx->prof.rounds++;

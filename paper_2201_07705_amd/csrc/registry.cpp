@@ -417,13 +417,18 @@ gemel_status gemel_set_option(gemel_ctx *ctx, int32_t key, int64_t value) {
         drop_plans(ctx);
         break;
     case GEMEL_OPT_CONV_TILE:
-        if (value < -1 || value >= TILE_COUNT) return fail(ctx, GEMEL_EINVAL, "conv tile is -1..5");
+        if (value < -1 || value >= TILE_COUNT) return fail(ctx, GEMEL_EINVAL, "conv tile is -1..8");
         ctx->opt.conv_tile = (int)value;
         drop_plans(ctx);
         break;
     case GEMEL_OPT_CONV_SPLITS:
         if (value < 0 || value > 64) return fail(ctx, GEMEL_EINVAL, "conv splits is 0..64");
         ctx->opt.conv_splits = (int)value;
+        drop_plans(ctx);
+        break;
+    case GEMEL_OPT_STREAMS:
+        if (value < 1 || value > 8) return fail(ctx, GEMEL_EINVAL, "streams is 1..8");
+        ctx->opt.streams = (int)value;
         drop_plans(ctx);
         break;
     case GEMEL_OPT_PROFILE:

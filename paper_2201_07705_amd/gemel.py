@@ -38,7 +38,7 @@ Q_UNMERGED_BYTES, Q_MERGED_BYTES, Q_RESIDENT_BYTES, Q_PEAK_BYTES, \
     Q_GRAPH_REPLAYS = range(9)
 OPT_USE_GRAPH, OPT_SWAP_SLOT_BYTES, OPT_SWAP_SLOTS, OPT_FAIL_COPY_AT, \
     OPT_SPLIT_MERGED, OPT_WEIGHT_BUDGET, OPT_PROFILE, OPT_CONV_TILE, \
-    OPT_CONV_SPLITS = range(9)
+    OPT_CONV_SPLITS, OPT_STREAMS = range(10)
 KERNEL_FAMILIES = ("conv_mfma", "conv_f32", "splitk_reduce", "fc", "pack",
                    "pool", "route", "export")
 
@@ -100,6 +100,40 @@ def _hip_runtimes():
     return paths
 
 
+def load(path):
+    """Load another build of the same ABI (e.g. a CPU build of the host
+    code used by the tests) with its C signatures declared."""
+    return _configure(ctypes.CDLL(path))
+
+
+def _configure(L):
+    """Declare the C signatures of the ABI on a loaded library."""
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    L.gemel_create.argtypes = [ctypes.POINTER(vp), i32, i32,
+                               ctypes.c_uint64]
+    L.gemel_register_model.argtypes = [vp, ctypes.POINTER(LayerDesc), i32,
+                                       i32, i32, i32,
+                                       ctypes.POINTER(i32)]
+    L.gemel_merge.argtypes = [vp, ctypes.POINTER(Group), i32]
+    L.gemel_infer.argtypes = [vp, ctypes.POINTER(i32), i32,
+                              ctypes.POINTER(vp), ctypes.POINTER(i32),
+                              ctypes.POINTER(vp), vp]
+    L.gemel_model_outputs.argtypes = [vp, i32, ctypes.POINTER(i32)]
+    L.gemel_output_shape.argtypes = [vp, i32, i32, i32,
+                                     ctypes.POINTER(i64)]
+    L.gemel_query.argtypes = [vp, i32, ctypes.POINTER(i64)]
+    L.gemel_set_option.argtypes = [vp, i32, i64]
+    L.gemel_profile.argtypes = [vp, ctypes.POINTER(KernelStat),
+                                ctypes.POINTER(i32)]
+    L.gemel_last_error.argtypes = [vp]
+    L.gemel_last_error.restype = ctypes.c_char_p
+    L.gemel_destroy.argtypes = [vp]
+    for name in EXPORTED:
+        if name != "gemel_last_error":
+            getattr(L, name).restype = ctypes.c_int32
+    return L
+
+
 def lib():
     """Load libgemel.so (raises if it has not been built).
 
@@ -120,29 +154,7 @@ def lib():
         rts = _hip_runtimes()
         if len(rts) > 1:
             raise RuntimeError(f"two HIP runtimes are loaded: {sorted(rts)}")
-        vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
-        L.gemel_create.argtypes = [ctypes.POINTER(vp), i32, i32,
-                                   ctypes.c_uint64]
-        L.gemel_register_model.argtypes = [vp, ctypes.POINTER(LayerDesc), i32,
-                                           i32, i32, i32,
-                                           ctypes.POINTER(i32)]
-        L.gemel_merge.argtypes = [vp, ctypes.POINTER(Group), i32]
-        L.gemel_infer.argtypes = [vp, ctypes.POINTER(i32), i32,
-                                  ctypes.POINTER(vp), ctypes.POINTER(i32),
-                                  ctypes.POINTER(vp), vp]
-        L.gemel_model_outputs.argtypes = [vp, i32, ctypes.POINTER(i32)]
-        L.gemel_output_shape.argtypes = [vp, i32, i32, i32,
-                                         ctypes.POINTER(i64)]
-        L.gemel_query.argtypes = [vp, i32, ctypes.POINTER(i64)]
-        L.gemel_set_option.argtypes = [vp, i32, i64]
-        L.gemel_profile.argtypes = [vp, ctypes.POINTER(KernelStat),
-                                    ctypes.POINTER(i32)]
-        L.gemel_last_error.argtypes = [vp]
-        L.gemel_last_error.restype = ctypes.c_char_p
-        L.gemel_destroy.argtypes = [vp]
-        for name in EXPORTED:
-            if name != "gemel_last_error":
-                getattr(L, name).restype = ctypes.c_int32
+        _configure(L)
         _lib = L
     return _lib
 
@@ -190,12 +202,13 @@ def layer_descs(layers, params):
 class Context:
     """One libgemel context on one device."""
 
-    def __init__(self, device=0, dtype="bf16", budget=0):
+    def __init__(self, device=0, dtype="bf16", budget=0, library=None):
+        self._lib = library or lib()
         self._h = ctypes.c_void_p()
-        st = lib().gemel_create(ctypes.byref(self._h), device,
+        st = self._lib.gemel_create(ctypes.byref(self._h), device,
                                 BF16 if dtype == "bf16" else F32, budget)
         if st != OK:
-            raise GemelError(st, lib().gemel_last_error(None).decode())
+            raise GemelError(st, self._lib.gemel_last_error(None).decode())
         self.dtype = dtype
         self.device = device
         self._in_shape = {}
@@ -204,13 +217,13 @@ class Context:
     # -- raw calls (status returned, message on failure) --
     def _check(self, st):
         if st != OK:
-            raise GemelError(st, lib().gemel_last_error(self._h).decode())
+            raise GemelError(st, self._lib.gemel_last_error(self._h).decode())
         return st
 
     def register_model(self, layers, params, in_chw):
         arr, keep = layer_descs(layers, params)
         mid = ctypes.c_int32(-1)
-        self._check(lib().gemel_register_model(
+        self._check(self._lib.gemel_register_model(
             self._h, arr, len(layers), in_chw[0], in_chw[1], in_chw[2],
             ctypes.byref(mid)))
         del keep
@@ -228,17 +241,17 @@ class Context:
             keep.append(m)
             garr[i].n_members = len(g)
             garr[i].members = ctypes.cast(m, ctypes.POINTER(Member))
-        self._check(lib().gemel_merge(self._h, garr, n))
+        self._check(self._lib.gemel_merge(self._h, garr, n))
 
     def n_outputs(self, model_id):
         n = ctypes.c_int32()
-        self._check(lib().gemel_model_outputs(self._h, model_id,
+        self._check(self._lib.gemel_model_outputs(self._h, model_id,
                                               ctypes.byref(n)))
         return n.value
 
     def output_shape(self, model_id, idx, n_frames):
         dims = (ctypes.c_int64 * 4)()
-        self._check(lib().gemel_output_shape(self._h, model_id, idx,
+        self._check(self._lib.gemel_output_shape(self._h, model_id, idx,
                                              n_frames, dims))
         if self._out_ops.get(model_id, [None] * (idx + 1))[idx] == "fc":
             return (n_frames, dims[1])
@@ -246,18 +259,18 @@ class Context:
 
     def query(self, key):
         v = ctypes.c_int64()
-        self._check(lib().gemel_query(self._h, key, ctypes.byref(v)))
+        self._check(self._lib.gemel_query(self._h, key, ctypes.byref(v)))
         return v.value
 
     def set_option(self, key, value):
-        self._check(lib().gemel_set_option(self._h, key, value))
+        self._check(self._lib.gemel_set_option(self._h, key, value))
 
     def profile(self):
         """Per-round kernel statistics by family: {name: dict(launches,
         flops, bytes, ms)} and the number of profiled rounds."""
         st = (KernelStat * len(KERNEL_FAMILIES))()
         rounds = ctypes.c_int32()
-        self._check(lib().gemel_profile(self._h, st, ctypes.byref(rounds)))
+        self._check(self._lib.gemel_profile(self._h, st, ctypes.byref(rounds)))
         return {name: dict(launches=s.launches, flops=s.flops, bytes=s.bytes,
                            ms=s.ms)
                 for name, s in zip(KERNEL_FAMILIES, st)}, rounds.value
@@ -268,12 +281,12 @@ class Context:
         fp = (ctypes.c_void_p * n)(*frame_ptrs)
         nf = (ctypes.c_int32 * n)(*n_frames)
         op = (ctypes.c_void_p * max(len(out_ptrs), 1))(*out_ptrs)
-        return lib().gemel_infer(self._h, ids, n, fp, nf, op,
+        return self._lib.gemel_infer(self._h, ids, n, fp, nf, op,
                                  ctypes.c_void_p(stream))
 
     def close(self):
         if self._h:
-            st = lib().gemel_destroy(self._h)
+            st = self._lib.gemel_destroy(self._h)
             self._h = ctypes.c_void_p()
             if st != OK:
                 raise GemelError(st, "destroy found a device fault")
@@ -281,7 +294,7 @@ class Context:
     def __del__(self):
         try:
             if self._h:
-                lib().gemel_destroy(self._h)
+                self._lib.gemel_destroy(self._h)
         except Exception:
             pass
 
