@@ -252,11 +252,13 @@ enum {
                                     it clears the collected statistics.    */
     GEMEL_OPT_CONV_TILE = 7,     /* -1 (default): pick each conv's tile
                                     shape and split-K by the cost model;
-                                    0..8: force one tile shape (128x128,
+                                    0..12: force one tile shape (128x128,
                                     128x64, 64x64, 256x256, 256x128,
                                     256x64, 64x64 and 128x64 with deeper
-                                    prefetch, 64x128) with split-K still
-                                    chosen                                 */
+                                    prefetch, 64x128; then the LDS-DMA
+                                    pipeline's 256x256, 256x128, 128x128,
+                                    128x64, used where Cin % 32 == 0) with
+                                    split-K still chosen                   */
     GEMEL_OPT_CONV_SPLITS = 8,   /* 0 (default): split-K chosen per conv;
                                     n >= 1: force n depth splits (capped
                                     so that every split has work)          */

@@ -478,7 +478,8 @@ struct TileShape {
 };
 static const TileShape kTiles[TILE_COUNT] = {
     {128, 128, 256}, {128, 64, 256}, {64, 64, 256}, {256, 256, 512}, {256, 128, 512},
-    {256, 64, 256},  {64, 64, 256},  {128, 64, 256}, {64, 128, 256}};
+    {256, 64, 256},  {64, 64, 256},  {128, 64, 256}, {64, 128, 256},
+    {256, 256, 512}, {256, 128, 256}, {128, 128, 256}, {128, 64, 128}};
 
 int conv_tile_bm(int tile) { return tile >= 0 && tile < TILE_COUNT ? kTiles[tile].bm : 0; }
 int conv_tile_bn(int tile) { return tile >= 0 && tile < TILE_COUNT ? kTiles[tile].bn : 0; }
@@ -519,6 +520,7 @@ static void launch_tile(int tile, dim3 grid, hipStream_t st, const ConvArgs &a) 
 }
 
 hipError_t launch_conv_bf16(const ConvArgs &a, int tile, hipStream_t st) {
+    if (tile_is_dma(tile)) return launch_conv_dma(a, tile, st);
     if (!conv_args_ok(a) || !a.zero) return hipErrorInvalidValue;
     const int bm = conv_tile_bm(tile), bn = conv_tile_bn(tile);
     if (!bm) return hipErrorInvalidValue;

@@ -1,0 +1,336 @@
+// Implicit-GEMM convolution with an LDS-DMA pipeline (gfx950).
+//
+// Same GEMM as conv_bf16 (C[M][N] = A[M][K] * B[N][K]^T over the merged
+// frames of several models, bf16 MFMA, fp32 accumulation, fused epilogue),
+// organised for latency tolerance: each depth step of 32 is fetched by
+// global_load_lds_dwordx4 straight into one of STAGES LDS buffers, so
+// STAGES-1 steps are in flight while the MFMAs consume the oldest one and
+// no registers hold staged data. Each stage lives in its own __shared__
+// array (the compiler then tracks which buffer an outstanding LDS-DMA
+// writes and waits only where a read could alias it); the waits on the
+// loads are explicit vmcnt counts, and workgroup syncs are bare s_barrier
+// (a fenced barrier would drain every outstanding load).
+//
+// An LDS-DMA instruction writes 64 consecutive 16-byte slots per wave, so
+// the layout is chosen through the addresses: slot p of a stage holds row
+// p/4, 16-byte chunk (p%4) ^ ((row/2)%4) of that row. The swizzle puts the
+// 16-byte fragment reads of 8 consecutive rows at the same chunk onto
+// distinct banks.
+//
+// Requirements: Cin a multiple of 32 (a step is one filter tap and 32
+// channels), input pixel stride a multiple of 8, depth per split a
+// multiple of 32.
+#include <hip/hip_runtime.h>
+
+#include <type_traits>
+
+#include "kargs.h"
+#include "kernels.h"
+
+namespace gemel {
+
+namespace {
+
+typedef unsigned short u16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) unsigned char lds_u8;
+
+__device__ __forceinline__ float d_bf2f(u16 h) { return __uint_as_float((uint32_t)h << 16); }
+__device__ __forceinline__ u16 d_f2bf(float f) { return __builtin_bit_cast(u16, (__bf16)f); }
+__device__ __forceinline__ float d_act(float y, int act, float slope) {
+    if (act == 1) return fmaxf(y, 0.f);
+    if (act == 2) return y > 0.f ? y : y * slope;
+    return y;
+}
+__device__ __forceinline__ float d_epi(float z, float r, int has_res, int res_mode, int act, float slope) {
+    if (!has_res) return d_act(z, act, slope);
+    if (res_mode == 0) return d_act(z + r, act, slope);
+    return d_act(z, act, slope) + r;
+}
+__device__ __forceinline__ int d_seg(const ConvArgs &a, int gm) {
+    int s = 0;
+    for (int i = 1; i < a.nseg; ++i) s += (gm >= a.seg[i].m_start) ? 1 : 0;
+    return s;
+}
+
+// Calls f(std::integral_constant<int, i>) for i = 0 .. I-1 with a
+// compile-time i, so that register arrays are indexed statically.
+template <int I>
+struct StaticFor {
+    template <typename F>
+    __device__ __forceinline__ static void run(F &&f) {
+        StaticFor<I - 1>::run(f);
+        f(std::integral_constant<int, I - 1>{});
+    }
+};
+template <>
+struct StaticFor<0> {
+    template <typename F>
+    __device__ __forceinline__ static void run(F &&) {}
+};
+
+// vmcnt-only wait: expcnt and lgkmcnt left at their maxima (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+}  // namespace
+
+template <int BM, int BN, int WM, int WN, int STAGES>
+__global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a) {
+    constexpr int NW = WM * WN, NT = 64 * NW;
+    constexpr int BK = 32;
+    constexpr int TM = BM / WM, TN = BN / WN;
+    constexpr int FM = TM / 16, FN = TN / 16;
+    constexpr int A_SLOTS = BM * 4, B_SLOTS = BN * 4;          // 16-byte slots per stage
+    constexpr int AI = A_SLOTS / NT, BI = B_SLOTS / NT;        // DMA instructions per thread
+    static_assert(AI * NT == A_SLOTS && BI * NT == B_SLOTS && AI >= 1 && BI >= 1, "tile/threads");
+    constexpr int STAGE_BYTES = (A_SLOTS + B_SLOTS) * 16;
+    constexpr int EPI_LD = TN + 4;                              // fp32 row pitch of a wave's staging
+    constexpr int HALF = (NW + 1) / 2;                          // waves staging in each of st0, st1
+    static_assert(HALF * 16 * EPI_LD * 4 <= STAGE_BYTES, "epilogue staging must fit two stages");
+    static_assert(STAGES >= 2 && STAGES <= 4, "stages");
+    static_assert(TN == 64, "a lane owns one 8-channel chunk of its wave's 64 columns");
+    constexpr int PER_STEP = AI + BI;                           // vm ops per thread per step
+    __shared__ __attribute__((aligned(1024))) unsigned char st0[STAGE_BYTES];
+    __shared__ __attribute__((aligned(1024))) unsigned char st1[STAGE_BYTES];
+    __shared__ __attribute__((aligned(1024))) unsigned char st2[STAGES > 2 ? STAGE_BYTES : 16];
+    __shared__ __attribute__((aligned(1024))) unsigned char st3[STAGES > 3 ? STAGE_BYTES : 16];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave / WN, wn = wave - (wave / WN) * WN;
+    const int tiles_n = (a.N + BN - 1) / BN;
+    const int tiles = ((a.M + BM - 1) / BM) * tiles_n;
+    const int G = gridDim.x;
+    const int t = (G & 7) == 0 ? (int)(blockIdx.x & 7) * (G >> 3) + (int)(blockIdx.x >> 3) : (int)blockIdx.x;
+    if (t >= tiles) return;
+    const int tm = t / tiles_n, tn = t - (t / tiles_n) * tiles_n;
+    const int k_begin = blockIdx.y * a.k_per_split;
+    const int k_end = min(a.K, k_begin + a.k_per_split);
+    const int HWo = a.Ho * a.Wo;
+    const int H = a.H, W = a.W, in_cs = a.in_cs, N = a.N, K = a.K, Cin = a.Cin, kw = a.kw;
+    const size_t frame_elems = (size_t)H * W * in_cs;
+    const u16 *const zp = (const u16 *)a.zero;
+
+    // ---- DMA assignment: instruction i of this thread fills slot
+    // (i*NW + wave)*64 + lane: row ((i*NW + wave)*16 + lane/4), chunk cq ----
+    const int cq = (lane & 3) ^ ((lane >> 3) & 3);
+    const u16 *abase[AI];
+    int ahi[AI], awi[AI];
+#pragma unroll
+    for (int i = 0; i < AI; ++i) {
+        const int gm = tm * BM + (i * NW + wave) * 16 + (lane >> 2);
+        abase[i] = zp;
+        ahi[i] = -(1 << 28);
+        awi[i] = 0;
+        if (gm < a.M) {
+            const int sg = d_seg(a, gm);
+            const int fr = gm / HWo;
+            const int pix = gm - fr * HWo;
+            const int ho = pix / a.Wo, wo = pix - (pix / a.Wo) * a.Wo;
+            abase[i] = (const u16 *)a.seg[sg].in + (size_t)(fr - a.seg[sg].f_start) * frame_elems;
+            ahi[i] = ho * a.stride - a.pad;
+            awi[i] = wo * a.stride - a.pad;
+        }
+    }
+    const u16 *bbase[BI];
+#pragma unroll
+    for (int i = 0; i < BI; ++i) {
+        const int gn = tn * BN + (i * NW + wave) * 16 + (lane >> 2);
+        bbase[i] = gn < N ? (const u16 *)a.w + (size_t)gn * K + cq * 8 : nullptr;
+    }
+    // loader position (uniform): next step's tap (lr, ls) and channel base lc
+    int kb = k_begin, lc, lr, ls;
+    {
+        const int rs = k_begin / Cin;
+        lc = k_begin - rs * Cin;
+        lr = rs / kw;
+        ls = rs - lr * kw;
+    }
+    auto issue = [&](unsigned char *stage) __attribute__((always_inline)) {
+        const int c = lc + cq * 8;
+#pragma unroll
+        for (int i = 0; i < AI; ++i) {
+            const int hi = ahi[i] + lr, wi = awi[i] + ls;
+            const bool ok = (unsigned)hi < (unsigned)H && (unsigned)wi < (unsigned)W;
+            const u16 *p = ok ? abase[i] + ((size_t)(hi * W + wi) * in_cs + c) : zp;
+            __builtin_amdgcn_global_load_lds((const void *)p, (lds_u8 *)(stage + (i * NW + wave) * 1024), 16, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < BI; ++i) {
+            const u16 *p = bbase[i] ? bbase[i] + kb : zp;
+            __builtin_amdgcn_global_load_lds((const void *)p,
+                                             (lds_u8 *)(stage + A_SLOTS * 16 + (i * NW + wave) * 1024), 16, 0, 0);
+        }
+        kb += BK;
+        lc += BK;
+        if (lc == Cin) {
+            lc = 0;
+            if (++ls == kw) { ls = 0; ++lr; }
+        }
+    };
+
+    f32x4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // fragment read offsets inside a stage (swizzled slots)
+    const int g = lane >> 4;
+    auto frag_off = [&](int row) __attribute__((always_inline)) { return (row * 4 + (g ^ ((row >> 1) & 3))) * 16; };
+    int aoff[FM], boff[FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) aoff[i] = frag_off(wm * TM + i * 16 + (lane & 15));
+#pragma unroll
+    for (int j = 0; j < FN; ++j) boff[j] = A_SLOTS * 16 + frag_off(wn * TN + j * 16 + (lane & 15));
+    auto compute = [&](const unsigned char *stage) __attribute__((always_inline)) {
+        bf16x8 bfr[FN];
+#pragma unroll
+        for (int j = 0; j < FN; ++j) bfr[j] = *(const bf16x8 *)(stage + boff[j]);
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            const bf16x8 af = *(const bf16x8 *)(stage + aoff[i]);
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bfr[j], acc[i][j], 0, 0, 0);
+        }
+    };
+
+    // epilogue constants of this lane's 8 channels (every segment shares
+    // one scale/shift pair), fetched ahead of the depth loop
+    const int my_gn = tn * BN + wn * TN + (lane & 7) * 8;
+    f32x4 sc0 = {1.f, 1.f, 1.f, 1.f}, sc1 = sc0, sh0 = {0.f, 0.f, 0.f, 0.f}, sh1 = sh0;
+    if (a.k_splits <= 1 && my_gn < N) {
+        const float *scl = a.seg[0].scale + my_gn, *shl = a.seg[0].shift + my_gn;
+        sc0 = *(const f32x4 *)scl;
+        sc1 = *(const f32x4 *)(scl + 4);
+        sh0 = *(const f32x4 *)shl;
+        sh1 = *(const f32x4 *)(shl + 4);
+    }
+
+    const int nk = (k_end - k_begin) / BK;
+    unsigned char *const stg[4] = {st0, st1, st2, st3};
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s)
+        if (s < nk) issue(stg[s]);
+
+    // main loop, unrolled by STAGES so that every buffer index is static
+    for (int base = 0; base < nk; base += STAGES) {
+#pragma unroll
+        for (int s = 0; s < STAGES; ++s) {
+            const int it = base + s;
+            if (it < nk) {
+                // step it must have landed; the newer steps may still fly
+                if (it + STAGES - 2 < nk) wait_vm<(STAGES - 2) * PER_STEP>();
+                else wait_vm<0>();
+                __builtin_amdgcn_s_barrier();
+                if (it + STAGES - 1 < nk) issue(stg[(s + STAGES - 1) % STAGES]);
+                compute(stg[s]);
+            }
+        }
+    }
+
+    // ---- epilogue: each wave stages 16 rows of its tile at a time ----
+    wait_vm<0>();
+    __builtin_amdgcn_s_barrier();
+    float *ew = (float *)((wave < HALF ? st0 : st1) + (wave < HALF ? wave : wave - HALF) * 16 * EPI_LD * 4);
+    const int out_cs = a.out_cs;
+    StaticFor<FM>::run([&](auto ic) __attribute__((always_inline)) {
+        constexpr int i = decltype(ic)::value;
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) ew[((lane >> 4) * 4 + v) * EPI_LD + j * 16 + (lane & 15)] = acc[i][j][v];
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        for (int item = lane; item < 16 * (TN / 8); item += 64) {
+            const int rl = item / (TN / 8), ch = item - (item / (TN / 8)) * (TN / 8);
+            const int gm = tm * BM + wm * TM + i * 16 + rl;
+            const int gn = tn * BN + wn * TN + ch * 8;
+            if (gm >= a.M || gn >= N) continue;
+            const float *src = ew + rl * EPI_LD + ch * 8;
+            const float4 v0 = *(const float4 *)src, v1 = *(const float4 *)(src + 4);
+            float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+            const ConvSeg &sg = a.seg[d_seg(a, gm)];
+            const int lr_ = gm - sg.m_start;
+            if (a.k_splits > 1) {
+                float4 *dst = (float4 *)(a.partial + ((size_t)blockIdx.y * a.M + gm) * N + gn);
+                dst[0] = v0;
+                dst[1] = v1;
+                continue;
+            }
+            const float s8[8] = {sc0[0], sc0[1], sc0[2], sc0[3], sc1[0], sc1[1], sc1[2], sc1[3]};
+            const float h8[8] = {sh0[0], sh0[1], sh0[2], sh0[3], sh1[0], sh1[1], sh1[2], sh1[3]};
+            if (a.out_mode == OUT_NHWC) {
+                const size_t off = (size_t)lr_ * out_cs + gn;
+                u32x4 r4 = {0u, 0u, 0u, 0u};
+                if (a.has_res) r4 = *(const u32x4 *)((const u16 *)sg.res + off);
+                u32x4 o;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const float r0 = d_bf2f((u16)(r4[q] & 0xffffu)), r1 = d_bf2f((u16)(r4[q] >> 16));
+                    const u16 y0 = d_f2bf(d_epi(v[2 * q] * s8[2 * q] + h8[2 * q], r0, a.has_res, a.res_mode, a.act, a.slope));
+                    const u16 y1 = d_f2bf(d_epi(v[2 * q + 1] * s8[2 * q + 1] + h8[2 * q + 1], r1, a.has_res, a.res_mode,
+                                                a.act, a.slope));
+                    o[q] = (uint32_t)y0 | ((uint32_t)y1 << 16);
+                }
+                *(u32x4 *)((u16 *)sg.out + off) = o;
+            } else {
+                const int f = lr_ / HWo, pix = lr_ - (lr_ / HWo) * HWo;
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const int c = gn + q;
+                    if (c >= a.cout) break;
+                    const float r = a.has_res ? d_bf2f(((const u16 *)sg.res)[(size_t)lr_ * out_cs + c]) : 0.f;
+                    ((float *)sg.out)[((size_t)f * a.cout + c) * HWo + pix] =
+                        d_epi(v[q] * s8[q] + h8[q], r, a.has_res, a.res_mode, a.act, a.slope);
+                }
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    });
+}
+
+bool conv_dma_supported(const ConvArgs &a) {
+    return a.Cin % 32 == 0 && a.in_cs % 8 == 0 && a.K % 32 == 0 && a.k_per_split % 32 == 0 && a.zero &&
+           a.uni_affine;
+}
+
+hipError_t launch_conv_dma(const ConvArgs &a, int tile, hipStream_t st) {
+    if (!conv_dma_supported(a) || a.M <= 0 || a.N <= 0 || a.N % 8 || a.nseg < 1 || a.nseg > GEMEL_MAX_SEG)
+        return hipErrorInvalidValue;
+    if (a.K != a.kh * a.kw * a.Cin || a.out_cs < a.N || a.seg[0].m_start != 0) return hipErrorInvalidValue;
+    if (a.k_splits > 1 && !a.partial) return hipErrorInvalidValue;
+    if ((long)a.k_per_split * a.k_splits < a.K) return hipErrorInvalidValue;
+    for (int i = 0; i < a.nseg; ++i) {
+        if (!a.seg[i].in || !a.seg[i].scale || !a.seg[i].shift) return hipErrorInvalidValue;
+        if (a.k_splits <= 1 && !a.seg[i].out) return hipErrorInvalidValue;
+        if (a.has_res && !a.seg[i].res) return hipErrorInvalidValue;
+        if (a.seg[i].m_start != a.seg[i].f_start * a.Ho * a.Wo) return hipErrorInvalidValue;
+    }
+    const int bm = conv_tile_bm(tile), bn = conv_tile_bn(tile);
+    if (!bm) return hipErrorInvalidValue;
+    const long tiles = (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn);
+    const long blocks = tiles >= 8 ? (tiles + 7) / 8 * 8 : tiles;
+    if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
+    dim3 grid((unsigned)blocks, (unsigned)a.k_splits);
+    switch (tile) {
+    case TILE_DMA_256x256: hipLaunchKernelGGL((conv_dma_kernel<256, 256, 2, 4, 4>), grid, dim3(512), 0, st, a); break;
+    case TILE_DMA_256x128: hipLaunchKernelGGL((conv_dma_kernel<256, 128, 2, 2, 4>), grid, dim3(256), 0, st, a); break;
+    case TILE_DMA_128x128: hipLaunchKernelGGL((conv_dma_kernel<128, 128, 2, 2, 4>), grid, dim3(256), 0, st, a); break;
+    case TILE_DMA_128x64: hipLaunchKernelGGL((conv_dma_kernel<128, 64, 2, 1, 4>), grid, dim3(128), 0, st, a); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace gemel

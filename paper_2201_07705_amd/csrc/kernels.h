@@ -19,7 +19,12 @@ enum ConvTile {
     TILE_64x64_D2 = 6, // as 64x64, loads two depth steps ahead
     TILE_128x64_D2 = 7,// as 128x64, loads two depth steps ahead
     TILE_64x128 = 8,   // 4 waves, 32x64 per wave
-    TILE_COUNT = 9
+    // LDS-DMA pipeline (k_conv_dma.hip), Cin a multiple of 32
+    TILE_DMA_256x256 = 9,  // 8 waves, 128x64 per wave, 4 stages of depth 32
+    TILE_DMA_256x128 = 10, // 4 waves, 128x64 per wave
+    TILE_DMA_128x128 = 11, // 4 waves, 64x64 per wave
+    TILE_DMA_128x64 = 12,  // 2 waves, 64x64 per wave
+    TILE_COUNT = 13
 };
 int conv_tile_threads(int tile);
 int conv_tile_bm(int tile);
@@ -27,6 +32,9 @@ int conv_tile_bn(int tile);
 constexpr int CONV_BK = 64;
 
 hipError_t launch_conv_bf16(const ConvArgs &a, int tile, hipStream_t st);
+bool conv_dma_supported(const ConvArgs &a);
+hipError_t launch_conv_dma(const ConvArgs &a, int tile, hipStream_t st);
+inline bool tile_is_dma(int tile) { return tile >= TILE_DMA_256x256 && tile < TILE_COUNT; }
 hipError_t launch_conv_f32(const ConvArgs &a, hipStream_t st);
 // Split-K reduction + fused epilogue (bf16 or f32 internal activations).
 hipError_t launch_conv_reduce(const ReduceArgs &a, bool bf16, hipStream_t st);

@@ -279,38 +279,51 @@ bool direct_output(const Layer &l) {
 
 // Launch configuration of a bf16 implicit-GEMM conv of size M x N x K:
 // the tile shape and split-K factor with the smallest estimated time.
-// Model: a tile costs 2*bm*bn*depth FLOPs at a per-CU rate scaled by a
-// measured relative efficiency of its shape; tiles run in waves of
-// (256 CUs x resident tiles per CU); split-K adds the partial-sum round
-// trip through memory and a reduction launch.
+// Model (fitted to measured times of every tile shape on the conv shapes of
+// the ResNet, VGG and Darknet workloads): tiles run in waves of (256 CUs x
+// resident tiles per CU); a wave costs its tiles' FLOPs at the tile shape's
+// MFMA efficiency plus a per-wave latency; split-K adds the partial-sum
+// round trip through memory.
 struct TileCost {
     int tile;
-    double eff;   // relative MFMA efficiency of the tile shape
+    double eff;   // MFMA efficiency of the tile shape
     int occ;      // tiles resident per CU
+    double lat;   // seconds of latency per wave of tiles
 };
 static const TileCost kTileCost[] = {
-    {TILE_256x256, 1.00, 1}, {TILE_256x128, 0.90, 1}, {TILE_128x128, 0.80, 1},
-    {TILE_256x64, 0.75, 1},  {TILE_128x64, 0.65, 2},  {TILE_64x64, 0.45, 3}};
+    {TILE_128x128, 0.441, 2, 5.61e-6},
+    {TILE_128x64, 0.311, 2, 3.88e-6},
+    {TILE_64x64, 0.375, 4, 2.79e-6},
+    {TILE_256x256, 0.469, 1, 11.42e-6},
+    {TILE_256x128, 0.351, 1, 6.62e-6},
+    {TILE_256x64, 0.217, 1, 5.53e-6},
+    {TILE_64x64_D2, 0.301, 3, 2.48e-6},
+    {TILE_128x64_D2, 0.313, 2, 4.03e-6},
+    {TILE_64x128, 0.332, 2, 3.60e-6},
+    {TILE_DMA_256x256, 0.529, 1, 7.94e-6},
+    {TILE_DMA_256x128, 0.330, 1, 7.72e-6},
+    {TILE_DMA_128x128, 0.526, 2, 4.83e-6},
+    {TILE_DMA_128x64, 0.379, 3, 5.06e-6},
+};
 
-void pick_conv_config(int64_t M, int64_t N, int64_t K, int force, int force_splits, int &tile, int &splits,
-                      int &kps) {
+void pick_conv_config(int64_t M, int64_t N, int64_t K, bool dma_ok, int force, int force_splits, int &tile,
+                      int &splits, int &kps) {
     const double cu_flops = 4096.0 * 2.4e9;   // per CU, dense bf16
     double best = 1e300;
     tile = force >= 0 ? force : TILE_64x64;
     splits = 1;
     for (const TileCost &tc : kTileCost) {
         if (force >= 0 && tc.tile != force) continue;
+        if (force < 0 && tile_is_dma(tc.tile) && !dma_ok) continue;
         const int64_t bm = conv_tile_bm(tc.tile), bn = conv_tile_bn(tc.tile);
-        if (force < 0 && bn > 64 && N <= bn / 2) continue;   // mostly padding columns
         const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
         for (int s = 1; s <= 16; s *= 2) {
             if (s > 1 && K / s < 4 * CONV_BK) break;
             const int64_t k_s = round_up((K + s - 1) / s, CONV_BK);
             const int64_t s_eff = (K + k_s - 1) / k_s;
             const double waves = std::ceil((double)(tiles * s_eff) / (256.0 * tc.occ));
-            double t = waves * tc.occ * (2.0 * bm * bn * k_s) / (cu_flops * tc.eff);
-            t += 3e-6;                                  // launch + tail
-            if (s_eff > 1) t += (double)s_eff * M * N * 4.0 * 2.0 / 4e12 + 4e-6;
+            double t = waves * (tc.occ * (2.0 * bm * bn * k_s) / (cu_flops * tc.eff) + tc.lat);
+            if (s_eff > 1) t += (double)s_eff * M * N * 4.0 * 2.0 / 4e12 + 2e-6;
             if (t < best) {
                 best = t;
                 tile = tc.tile;
@@ -758,8 +771,10 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 for (int i = 1; i < a.nseg; ++i)
                     if (a.seg[i].scale != a.seg[0].scale || a.seg[i].shift != a.seg[0].shift) a.uni_affine = 0;
                 if (bf16) {
-                    pick_conv_config(a.M, a.N, a.K, ctx->opt.conv_tile, ctx->opt.conv_splits, Lc.tile, a.k_splits,
-                                     a.k_per_split);
+                    const bool dma_ok = a.Cin % 32 == 0 && a.in_cs % 8 == 0 && a.uni_affine;
+                    pick_conv_config(a.M, a.N, a.K, dma_ok, ctx->opt.conv_tile, ctx->opt.conv_splits, Lc.tile,
+                                     a.k_splits, a.k_per_split);
+                    if (tile_is_dma(Lc.tile) && !conv_dma_supported(a)) Lc.tile = TILE_64x64;
                     Lc.type = L_CONV_BF16;
                     Lc.kind = L0.op == GEMEL_OP_CONV ? GEMEL_K_CONV_MFMA : GEMEL_K_FC;
                 } else {

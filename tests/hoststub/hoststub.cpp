@@ -125,8 +125,8 @@ hipError_t hipGraphLaunch(hipGraphExec_t, hipStream_t) { return hipSuccess; }
 
 namespace gemel {
 
-static const int kBm[TILE_COUNT] = {128, 128, 64, 256, 256, 256, 64, 128, 64};
-static const int kBn[TILE_COUNT] = {128, 64, 64, 256, 128, 64, 64, 64, 128};
+static const int kBm[TILE_COUNT] = {128, 128, 64, 256, 256, 256, 64, 128, 64, 256, 256, 128, 128};
+static const int kBn[TILE_COUNT] = {128, 64, 64, 256, 128, 64, 64, 64, 128, 256, 128, 128, 64};
 int conv_tile_bm(int t) { return t >= 0 && t < TILE_COUNT ? kBm[t] : 0; }
 int conv_tile_bn(int t) { return t >= 0 && t < TILE_COUNT ? kBn[t] : 0; }
 int conv_tile_threads(int t) { return (t == TILE_256x256 || t == TILE_256x128) ? 512 : 256; }
@@ -171,8 +171,18 @@ static hipError_t conv_common(const ConvArgs &a, int esz, const char *kern, bool
     return verdict(ok);
 }
 
+bool conv_dma_supported(const ConvArgs &a) {
+    return a.Cin % 32 == 0 && a.in_cs % 8 == 0 && a.K % 32 == 0 && a.k_per_split % 32 == 0 && a.zero &&
+           a.uni_affine;
+}
+hipError_t launch_conv_dma(const ConvArgs &a, int tile, hipStream_t s) { return launch_conv_bf16(a, tile, s); }
 hipError_t launch_conv_bf16(const ConvArgs &a, int tile, hipStream_t) {
     if (tile < 0 || tile >= TILE_COUNT) return hipErrorInvalidValue;
+    if (tile_is_dma(tile) && !conv_dma_supported(a)) {
+        ++violations;
+        last = "dma tile on an unsupported conv";
+        return hipErrorInvalidValue;
+    }
     return conv_common(a, 2, "conv_bf16", true);
 }
 hipError_t launch_conv_f32(const ConvArgs &a, hipStream_t) { return conv_common(a, 4, "conv_f32", false); }
