@@ -235,8 +235,12 @@ gemel_status gemel_query(gemel_ctx *ctx, int32_t key, int64_t *val);
 
 /* Tunables and test hooks of gemel_set_option. */
 enum {
-    GEMEL_OPT_USE_GRAPH = 0,     /* 1 (default): replay a captured HIP graph
-                                    when frames/outputs pointers repeat    */
+    GEMEL_OPT_USE_GRAPH = 0,     /* 1 (default): a round without streamed
+                                    weights is replayed as a HIP graph
+                                    (built once per frames/outputs pointer
+                                    set and stream, edges as set by
+                                    GEMEL_OPT_GRAPH_DAG); 0: rounds are
+                                    enqueued directly                      */
     GEMEL_OPT_SWAP_SLOT_BYTES = 1, /* staging slot size (default 32 MiB)   */
     GEMEL_OPT_SWAP_SLOTS = 2,    /* number of staging slots (default 3)    */
     GEMEL_OPT_FAIL_COPY_AT = 3,  /* test hook: the n-th (1-based) swap copy
@@ -262,12 +266,25 @@ enum {
     GEMEL_OPT_CONV_SPLITS = 8,   /* 0 (default): split-K chosen per conv;
                                     n >= 1: force n depth splits (capped
                                     so that every split has work)          */
-    GEMEL_OPT_STREAMS = 9        /* 1..8 (default 1): streams over which
-                                    independent layers of a round run
-                                    concurrently (forked from and joined to
-                                    the caller's stream). Applies to rounds
-                                    enqueued directly (graph replay off, or
-                                    profiling on); 1 with the null stream  */
+    GEMEL_OPT_STREAMS = 9,       /* 1..8 (default 3): at most this many
+                                    streams carry a round (forked from and
+                                    joined to the caller's stream; 1 with
+                                    the null stream). A branch of the
+                                    layer graph gets a stream of its own
+                                    when the work only it leads to is worth
+                                    the fork; cross-stream dependencies are
+                                    event waits                            */
+    GEMEL_OPT_GRAPH_DAG = 10,    /* graph edges: 0 (default): a node
+                                    follows the launches whose results it
+                                    reads and the previous launch of its
+                                    stream; 1: only the launches whose
+                                    results it reads (activation bytes are
+                                    reused only along such dependencies)   */
+    GEMEL_OPT_FORK_US = 11       /* a branch gets a stream of its own when
+                                    the work only it leads to is estimated
+                                    at this many microseconds or more
+                                    (default 30), or spans 3 or more
+                                    launch steps                           */
 };
 
 /* Set an option; takes effect at the next gemel_infer. Errors: EINVAL. */

@@ -90,6 +90,12 @@ struct Launch {
     int stream = 0;
     std::vector<int> waits;
     int record = -1;
+    // plan step (layer node or export) the launch belongs to, and the
+    // launches it must follow: the last launch of each producer step (the
+    // input packs for a step reading a model input), or the previous launch
+    // of its own step
+    int step = -1;
+    std::vector<int> deps;
 };
 
 // A chunk of a streamed blob: weight rows [row0, row0 + nrows).
@@ -111,11 +117,15 @@ struct Plan {
     std::vector<Chunk> chunks;             // streamed chunks, consumption order
     void *arena = nullptr;
     size_t arena_bytes = 0;
+    // split-K partial sums: one region per split-K step; steps that may run
+    // concurrently get disjoint regions
     float *partial = nullptr;
     size_t partial_bytes = 0;
     size_t streamed_bytes = 0;
-    // HIP graph of the launch sequence for one set of caller pointers
+    // HIP graph of the round for one set of caller pointers (edges: the
+    // launches' data dependencies, plus stream order unless graph_dag is 1)
     hipGraphExec_t graph = nullptr;
+    int graph_dag = -1;
     std::vector<const void *> graph_frames;
     std::vector<void *> graph_outputs;
     hipStream_t graph_stream = nullptr;
@@ -136,11 +146,13 @@ struct Profile {
 };
 
 struct Options {
-    int streams = 1;
+    int streams = 3;
     int profile = 0;
     int conv_tile = -1;
     int conv_splits = 0;
     int use_graph = 1;
+    int graph_dag = 0;
+    int fork_us = 30;
     int64_t slot_bytes = 32ll << 20;
     int slots = 3;
     int64_t fail_copy_at = 0;

@@ -505,22 +505,24 @@ static bool conv_args_ok(const ConvArgs &a) {
 }
 
 template <bool C64>
-static void launch_tile(int tile, dim3 grid, hipStream_t st, const ConvArgs &a) {
+static hipError_t launch_tile(int tile, dim3 grid, const Sink &sk, const ConvArgs &a) {
+    hipError_t e = hipErrorInvalidValue;
     switch (tile) {
-    case TILE_128x128: hipLaunchKernelGGL((conv_bf16_kernel<128, 128, 2, 2, 1, C64>), grid, dim3(256), 0, st, a); break;
-    case TILE_128x64: hipLaunchKernelGGL((conv_bf16_kernel<128, 64, 2, 2, 1, C64>), grid, dim3(256), 0, st, a); break;
-    case TILE_64x64: hipLaunchKernelGGL((conv_bf16_kernel<64, 64, 2, 2, 1, C64>), grid, dim3(256), 0, st, a); break;
-    case TILE_256x256: hipLaunchKernelGGL((conv_bf16_kernel<256, 256, 2, 4, 1, C64>), grid, dim3(512), 0, st, a); break;
-    case TILE_256x128: hipLaunchKernelGGL((conv_bf16_kernel<256, 128, 4, 2, 1, C64>), grid, dim3(512), 0, st, a); break;
-    case TILE_256x64: hipLaunchKernelGGL((conv_bf16_kernel<256, 64, 4, 1, 1, C64>), grid, dim3(256), 0, st, a); break;
-    case TILE_64x64_D2: hipLaunchKernelGGL((conv_bf16_kernel<64, 64, 2, 2, 2, C64>), grid, dim3(256), 0, st, a); break;
-    case TILE_128x64_D2: hipLaunchKernelGGL((conv_bf16_kernel<128, 64, 2, 2, 2, C64>), grid, dim3(256), 0, st, a); break;
-    case TILE_64x128: hipLaunchKernelGGL((conv_bf16_kernel<64, 128, 2, 2, 1, C64>), grid, dim3(256), 0, st, a); break;
+    case TILE_128x128: e = submit(sk, reinterpret_cast<const void *>(&conv_bf16_kernel<128, 128, 2, 2, 1, C64>), grid, dim3(256), a); break;
+    case TILE_128x64: e = submit(sk, reinterpret_cast<const void *>(&conv_bf16_kernel<128, 64, 2, 2, 1, C64>), grid, dim3(256), a); break;
+    case TILE_64x64: e = submit(sk, reinterpret_cast<const void *>(&conv_bf16_kernel<64, 64, 2, 2, 1, C64>), grid, dim3(256), a); break;
+    case TILE_256x256: e = submit(sk, reinterpret_cast<const void *>(&conv_bf16_kernel<256, 256, 2, 4, 1, C64>), grid, dim3(512), a); break;
+    case TILE_256x128: e = submit(sk, reinterpret_cast<const void *>(&conv_bf16_kernel<256, 128, 4, 2, 1, C64>), grid, dim3(512), a); break;
+    case TILE_256x64: e = submit(sk, reinterpret_cast<const void *>(&conv_bf16_kernel<256, 64, 4, 1, 1, C64>), grid, dim3(256), a); break;
+    case TILE_64x64_D2: e = submit(sk, reinterpret_cast<const void *>(&conv_bf16_kernel<64, 64, 2, 2, 2, C64>), grid, dim3(256), a); break;
+    case TILE_128x64_D2: e = submit(sk, reinterpret_cast<const void *>(&conv_bf16_kernel<128, 64, 2, 2, 2, C64>), grid, dim3(256), a); break;
+    case TILE_64x128: e = submit(sk, reinterpret_cast<const void *>(&conv_bf16_kernel<64, 128, 2, 2, 1, C64>), grid, dim3(256), a); break;
     }
+    return e;
 }
 
-hipError_t launch_conv_bf16(const ConvArgs &a, int tile, hipStream_t st) {
-    if (tile_is_dma(tile)) return launch_conv_dma(a, tile, st);
+hipError_t launch_conv_bf16(const ConvArgs &a, int tile, const Sink &sk) {
+    if (tile_is_dma(tile)) return launch_conv_dma(a, tile, sk);
     if (!conv_args_ok(a) || !a.zero) return hipErrorInvalidValue;
     const int bm = conv_tile_bm(tile), bn = conv_tile_bn(tile);
     if (!bm) return hipErrorInvalidValue;
@@ -529,22 +531,17 @@ hipError_t launch_conv_bf16(const ConvArgs &a, int tile, hipStream_t st) {
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
     dim3 grid((unsigned)blocks, (unsigned)a.k_splits);
     const bool c64 = a.Cin % 64 == 0 && a.k_per_split % CONV_BK == 0 && a.in_cs % 8 == 0;
-    if (c64)
-        launch_tile<true>(tile, grid, st, a);
-    else
-        launch_tile<false>(tile, grid, st, a);
-    return hipGetLastError();
+    return c64 ? launch_tile<true>(tile, grid, sk, a) : launch_tile<false>(tile, grid, sk, a);
 }
 
-hipError_t launch_conv_f32(const ConvArgs &a, hipStream_t st) {
+hipError_t launch_conv_f32(const ConvArgs &a, const Sink &sk) {
     if (!conv_args_ok(a) || a.k_splits != 1) return hipErrorInvalidValue;
     const long n = (long)a.M * a.N;
     dim3 grid((unsigned)((n + 255) / 256)), block(256);
-    hipLaunchKernelGGL(conv_f32_kernel, grid, block, 0, st, a);
-    return hipGetLastError();
+    return submit(sk, reinterpret_cast<const void *>(&conv_f32_kernel), grid, block, a);
 }
 
-hipError_t launch_conv_reduce(const ReduceArgs &a, bool bf16, hipStream_t st) {
+hipError_t launch_conv_reduce(const ReduceArgs &a, bool bf16, const Sink &sk) {
     if (a.M <= 0 || a.N <= 0 || a.N % 8 || a.splits < 1 || !a.partial || a.nseg < 1 || a.nseg > GEMEL_MAX_SEG)
         return hipErrorInvalidValue;
     for (int i = 0; i < a.nseg; ++i)
@@ -552,11 +549,8 @@ hipError_t launch_conv_reduce(const ReduceArgs &a, bool bf16, hipStream_t st) {
             return hipErrorInvalidValue;
     const long n = (long)a.M * (a.N / 8);
     dim3 grid((unsigned)((n + 255) / 256)), block(256);
-    if (bf16)
-        hipLaunchKernelGGL(conv_reduce_kernel<true>, grid, block, 0, st, a);
-    else
-        hipLaunchKernelGGL(conv_reduce_kernel<false>, grid, block, 0, st, a);
-    return hipGetLastError();
+    return bf16 ? submit(sk, reinterpret_cast<const void *>(&conv_reduce_kernel<true>), grid, block, a)
+                : submit(sk, reinterpret_cast<const void *>(&conv_reduce_kernel<false>), grid, block, a);
 }
 
 }  // namespace gemel

@@ -305,7 +305,7 @@ bool conv_dma_supported(const ConvArgs &a) {
            a.uni_affine;
 }
 
-hipError_t launch_conv_dma(const ConvArgs &a, int tile, hipStream_t st) {
+hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) {
     if (!conv_dma_supported(a) || a.M <= 0 || a.N <= 0 || a.N % 8 || a.nseg < 1 || a.nseg > GEMEL_MAX_SEG)
         return hipErrorInvalidValue;
     if (a.K != a.kh * a.kw * a.Cin || a.out_cs < a.N || a.seg[0].m_start != 0) return hipErrorInvalidValue;
@@ -323,14 +323,15 @@ hipError_t launch_conv_dma(const ConvArgs &a, int tile, hipStream_t st) {
     const long blocks = tiles >= 8 ? (tiles + 7) / 8 * 8 : tiles;
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
     dim3 grid((unsigned)blocks, (unsigned)a.k_splits);
+    hipError_t e = hipErrorInvalidValue;
     switch (tile) {
-    case TILE_DMA_256x256: hipLaunchKernelGGL((conv_dma_kernel<256, 256, 2, 4, 4>), grid, dim3(512), 0, st, a); break;
-    case TILE_DMA_256x128: hipLaunchKernelGGL((conv_dma_kernel<256, 128, 2, 2, 4>), grid, dim3(256), 0, st, a); break;
-    case TILE_DMA_128x128: hipLaunchKernelGGL((conv_dma_kernel<128, 128, 2, 2, 4>), grid, dim3(256), 0, st, a); break;
-    case TILE_DMA_128x64: hipLaunchKernelGGL((conv_dma_kernel<128, 64, 2, 1, 4>), grid, dim3(128), 0, st, a); break;
-    default: return hipErrorInvalidValue;
+    case TILE_DMA_256x256: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<256, 256, 2, 4, 4>), grid, dim3(512), a); break;
+    case TILE_DMA_256x128: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<256, 128, 2, 2, 4>), grid, dim3(256), a); break;
+    case TILE_DMA_128x128: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<128, 128, 2, 2, 4>), grid, dim3(256), a); break;
+    case TILE_DMA_128x64: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<128, 64, 2, 1, 4>), grid, dim3(128), a); break;
+    default: break;
     }
-    return hipGetLastError();
+    return e;
 }
 
 }  // namespace gemel

@@ -152,35 +152,32 @@ static bool fc_args_ok(const FcArgs &a) {
     return true;
 }
 
-hipError_t launch_fc_bf16(const FcArgs &a, hipStream_t st) {
+hipError_t launch_fc_bf16(const FcArgs &a, const Sink &sk) {
     if (!fc_args_ok(a) || a.M > 64 || (a.k_splits > 1 && a.k_per_split % 128)) return hipErrorInvalidValue;
     dim3 grid((unsigned)((a.N + 63) / 64), (unsigned)a.k_splits), block(256);
     const int mb = (a.M + 15) / 16;
+    hipError_t e;
     switch (mb) {
-    case 1: hipLaunchKernelGGL(fc_bf16_kernel<1>, grid, block, 0, st, a); break;
-    case 2: hipLaunchKernelGGL(fc_bf16_kernel<2>, grid, block, 0, st, a); break;
-    case 3: hipLaunchKernelGGL(fc_bf16_kernel<3>, grid, block, 0, st, a); break;
-    default: hipLaunchKernelGGL(fc_bf16_kernel<4>, grid, block, 0, st, a); break;
+    case 1: e = submit(sk, reinterpret_cast<const void *>(&fc_bf16_kernel<1>), grid, block, a); break;
+    case 2: e = submit(sk, reinterpret_cast<const void *>(&fc_bf16_kernel<2>), grid, block, a); break;
+    case 3: e = submit(sk, reinterpret_cast<const void *>(&fc_bf16_kernel<3>), grid, block, a); break;
+    default: e = submit(sk, reinterpret_cast<const void *>(&fc_bf16_kernel<4>), grid, block, a); break;
     }
-    return hipGetLastError();
+    return e;
 }
 
-hipError_t launch_fc_f32(const FcArgs &a, hipStream_t st) {
+hipError_t launch_fc_f32(const FcArgs &a, const Sink &sk) {
     if (!fc_args_ok(a) || a.k_splits != 1) return hipErrorInvalidValue;
     const long n = (long)a.M * a.N;
-    hipLaunchKernelGGL(fc_f32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a);
-    return hipGetLastError();
+    return submit(sk, reinterpret_cast<const void *>(&fc_f32_kernel), dim3((unsigned)((n + 255) / 256)), dim3(256), a);
 }
 
-hipError_t launch_fc_reduce(const FcArgs &a, bool bf16, hipStream_t st) {
+hipError_t launch_fc_reduce(const FcArgs &a, bool bf16, const Sink &sk) {
     if (!fc_args_ok(a) || a.k_splits < 2) return hipErrorInvalidValue;
     const long n = (long)a.M * a.N;
     dim3 grid((unsigned)((n + 255) / 256)), block(256);
-    if (bf16)
-        hipLaunchKernelGGL(fc_reduce_kernel<true>, grid, block, 0, st, a);
-    else
-        hipLaunchKernelGGL(fc_reduce_kernel<false>, grid, block, 0, st, a);
-    return hipGetLastError();
+    return bf16 ? submit(sk, reinterpret_cast<const void *>(&fc_reduce_kernel<true>), grid, block, a)
+                : submit(sk, reinterpret_cast<const void *>(&fc_reduce_kernel<false>), grid, block, a);
 }
 
 }  // namespace gemel

@@ -177,52 +177,50 @@ static bool ew_ok(const EwArgs &a, bool need_in1) {
     return true;
 }
 
-template <typename K>
-static hipError_t ew_launch(K kern, long items_per_frame, const EwArgs &a, hipStream_t st) {
+static hipError_t ew_launch(const void *kern, long items_per_frame, const EwArgs &a, const Sink &sk) {
     const long items = items_per_frame * a.max_frames;
     if (items <= 0) return hipSuccess;
     const long blocks = (items + 255) / 256;
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(kern, dim3((unsigned)blocks, (unsigned)a.nseg), dim3(256), 0, st, a);
-    return hipGetLastError();
+    return submit(sk, kern, dim3((unsigned)blocks, (unsigned)a.nseg), dim3(256), a);
 }
 
-hipError_t launch_pack(const EwArgs &a, bool bf16, hipStream_t st) {
+hipError_t launch_pack(const EwArgs &a, bool bf16, const Sink &sk) {
     if (!ew_ok(a, false) || a.Co % 8 || a.c_logical > a.Co || a.c_logical <= 0) return hipErrorInvalidValue;
     const long per = (long)a.H * a.W;
-    return bf16 ? ew_launch(pack_kernel<u16>, per, a, st) : ew_launch(pack_kernel<float>, per, a, st);
+    return bf16 ? ew_launch(reinterpret_cast<const void *>(&pack_kernel<u16>), per, a, sk) : ew_launch(reinterpret_cast<const void *>(&pack_kernel<float>), per, a, sk);
 }
 
-hipError_t launch_maxpool(const EwArgs &a, bool bf16, hipStream_t st) {
+hipError_t launch_maxpool(const EwArgs &a, bool bf16, const Sink &sk) {
     if (!ew_ok(a, false) || a.C % 8 || a.k <= 0 || a.stride <= 0 || a.pad >= a.k) return hipErrorInvalidValue;
     if (a.Ho != (a.H + 2 * a.pad - a.k) / a.stride + 1 || a.Wo != (a.W + 2 * a.pad - a.k) / a.stride + 1)
         return hipErrorInvalidValue;
     const long per = (long)a.Ho * a.Wo * (a.C / 8);
-    return bf16 ? ew_launch(maxpool_kernel<u16>, per, a, st) : ew_launch(maxpool_kernel<float>, per, a, st);
+    return bf16 ? ew_launch(reinterpret_cast<const void *>(&maxpool_kernel<u16>), per, a, sk) : ew_launch(reinterpret_cast<const void *>(&maxpool_kernel<float>), per, a, sk);
 }
 
-hipError_t launch_avgpool(const EwArgs &a, bool bf16, hipStream_t st) {
+hipError_t launch_avgpool(const EwArgs &a, bool bf16, const Sink &sk) {
     if (!ew_ok(a, false) || a.C % 8 || a.H <= 0 || a.W <= 0) return hipErrorInvalidValue;
     const long per = a.C / 8;
-    return bf16 ? ew_launch(avgpool_kernel<u16>, per, a, st) : ew_launch(avgpool_kernel<float>, per, a, st);
+    return bf16 ? ew_launch(reinterpret_cast<const void *>(&avgpool_kernel<u16>), per, a, sk) : ew_launch(reinterpret_cast<const void *>(&avgpool_kernel<float>), per, a, sk);
 }
 
-hipError_t launch_upsample2x(const EwArgs &a, bool bf16, hipStream_t st) {
+hipError_t launch_upsample2x(const EwArgs &a, bool bf16, const Sink &sk) {
     if (!ew_ok(a, false) || a.C % 8 || a.Ho != 2 * a.H || a.Wo != 2 * a.W) return hipErrorInvalidValue;
     const long per = (long)a.Ho * a.Wo * (a.C / 8);
-    return bf16 ? ew_launch(upsample2x_kernel<u16>, per, a, st) : ew_launch(upsample2x_kernel<float>, per, a, st);
+    return bf16 ? ew_launch(reinterpret_cast<const void *>(&upsample2x_kernel<u16>), per, a, sk) : ew_launch(reinterpret_cast<const void *>(&upsample2x_kernel<float>), per, a, sk);
 }
 
-hipError_t launch_concat(const EwArgs &a, bool bf16, hipStream_t st) {
+hipError_t launch_concat(const EwArgs &a, bool bf16, const Sink &sk) {
     if (!ew_ok(a, true) || a.C % 8 || a.C1 % 8 || a.Co != a.C + a.C1) return hipErrorInvalidValue;
     const long per = (long)a.H * a.W * (a.Co / 8);
-    return bf16 ? ew_launch(concat_kernel<u16>, per, a, st) : ew_launch(concat_kernel<float>, per, a, st);
+    return bf16 ? ew_launch(reinterpret_cast<const void *>(&concat_kernel<u16>), per, a, sk) : ew_launch(reinterpret_cast<const void *>(&concat_kernel<float>), per, a, sk);
 }
 
-hipError_t launch_export(const EwArgs &a, bool bf16, hipStream_t st) {
+hipError_t launch_export(const EwArgs &a, bool bf16, const Sink &sk) {
     if (!ew_ok(a, false) || a.c_logical > a.C || a.c_logical <= 0) return hipErrorInvalidValue;
     const long per = (long)a.c_logical * a.H * a.W;
-    return bf16 ? ew_launch(export_kernel<u16>, per, a, st) : ew_launch(export_kernel<float>, per, a, st);
+    return bf16 ? ew_launch(reinterpret_cast<const void *>(&export_kernel<u16>), per, a, sk) : ew_launch(reinterpret_cast<const void *>(&export_kernel<float>), per, a, sk);
 }
 
 }  // namespace gemel

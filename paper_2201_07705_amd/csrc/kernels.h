@@ -8,6 +8,33 @@
 
 namespace gemel {
 
+// Where a launcher puts its kernel: enqueued on a stream, or, when graph is
+// set, added to that HIP graph as a kernel node that runs after the ndeps
+// nodes in deps (the new node is returned in *node).
+struct Sink {
+    hipStream_t stream = nullptr;
+    hipGraph_t graph = nullptr;
+    const hipGraphNode_t *deps = nullptr;
+    size_t ndeps = 0;
+    hipGraphNode_t *node = nullptr;
+};
+
+// Launch kernel fn (one by-value argument block of type A, no dynamic LDS)
+// into the sink. Node parameters are copied when the node is added.
+template <typename A>
+inline hipError_t submit(const Sink &sk, const void *fn, dim3 grid, dim3 block, const A &args) {
+    void *params[] = {const_cast<A *>(&args)};
+    if (!sk.graph) return hipLaunchKernel(fn, grid, block, params, 0, sk.stream);
+    hipKernelNodeParams p{};
+    p.func = const_cast<void *>(fn);
+    p.gridDim = grid;
+    p.blockDim = block;
+    p.sharedMemBytes = 0;
+    p.kernelParams = params;
+    p.extra = nullptr;
+    return hipGraphAddKernelNode(sk.node, sk.graph, sk.deps, sk.ndeps, &p);
+}
+
 // Tile configurations of the bf16 implicit-GEMM convolution.
 enum ConvTile {
     TILE_128x128 = 0,  // 4 waves, 64x64 per wave
@@ -31,25 +58,25 @@ int conv_tile_bm(int tile);
 int conv_tile_bn(int tile);
 constexpr int CONV_BK = 64;
 
-hipError_t launch_conv_bf16(const ConvArgs &a, int tile, hipStream_t st);
+hipError_t launch_conv_bf16(const ConvArgs &a, int tile, const Sink &sk);
 bool conv_dma_supported(const ConvArgs &a);
-hipError_t launch_conv_dma(const ConvArgs &a, int tile, hipStream_t st);
+hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk);
 inline bool tile_is_dma(int tile) { return tile >= TILE_DMA_256x256 && tile < TILE_COUNT; }
-hipError_t launch_conv_f32(const ConvArgs &a, hipStream_t st);
+hipError_t launch_conv_f32(const ConvArgs &a, const Sink &sk);
 // Split-K reduction + fused epilogue (bf16 or f32 internal activations).
-hipError_t launch_conv_reduce(const ReduceArgs &a, bool bf16, hipStream_t st);
+hipError_t launch_conv_reduce(const ReduceArgs &a, bool bf16, const Sink &sk);
 
-hipError_t launch_fc_bf16(const FcArgs &a, hipStream_t st);
-hipError_t launch_fc_f32(const FcArgs &a, hipStream_t st);
-hipError_t launch_fc_reduce(const FcArgs &a, bool bf16, hipStream_t st);
+hipError_t launch_fc_bf16(const FcArgs &a, const Sink &sk);
+hipError_t launch_fc_f32(const FcArgs &a, const Sink &sk);
+hipError_t launch_fc_reduce(const FcArgs &a, bool bf16, const Sink &sk);
 
 // Input pack: caller NCHW f32 -> NHWC physical channels (bf16 or f32).
-hipError_t launch_pack(const EwArgs &a, bool bf16, hipStream_t st);
-hipError_t launch_maxpool(const EwArgs &a, bool bf16, hipStream_t st);
-hipError_t launch_avgpool(const EwArgs &a, bool bf16, hipStream_t st);
-hipError_t launch_upsample2x(const EwArgs &a, bool bf16, hipStream_t st);
-hipError_t launch_concat(const EwArgs &a, bool bf16, hipStream_t st);
+hipError_t launch_pack(const EwArgs &a, bool bf16, const Sink &sk);
+hipError_t launch_maxpool(const EwArgs &a, bool bf16, const Sink &sk);
+hipError_t launch_avgpool(const EwArgs &a, bool bf16, const Sink &sk);
+hipError_t launch_upsample2x(const EwArgs &a, bool bf16, const Sink &sk);
+hipError_t launch_concat(const EwArgs &a, bool bf16, const Sink &sk);
 // Internal NHWC tensor -> caller NCHW f32 output.
-hipError_t launch_export(const EwArgs &a, bool bf16, hipStream_t st);
+hipError_t launch_export(const EwArgs &a, bool bf16, const Sink &sk);
 
 }  // namespace gemel

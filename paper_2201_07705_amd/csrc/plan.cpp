@@ -16,10 +16,11 @@
 // Activations live in one arena whose offsets are assigned from tensor
 // lifetimes (tensors whose lifetimes overlap never share bytes).
 //
-// Round: the plan's launches are enqueued on the caller's stream (or a
-// captured HIP graph of them is replayed). Streamed weights are copied on a
-// side stream: copy i waits for the consumer of the chunk that last used
-// its slot, and consumer i waits for copy i.
+// Round: the plan's launches are enqueued on the caller's stream (or a HIP
+// graph of them, whose edges are the launches' data dependencies, is
+// replayed). Streamed weights are copied on a side stream: copy i waits for
+// the consumer of the chunk that last used its slot, and consumer i waits
+// for copy i.
 #include <algorithm>
 #include <functional>
 #include <cmath>
@@ -452,6 +453,11 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
     std::vector<double> est((size_t)NS, 5e-6);
     for (int i = 0; i < NN; ++i) {
         std::set<int> ps;
+        {   // the node's weights are read once, whatever its member count
+            const auto [s0, l0] = nodes[(size_t)order[(size_t)i]].mem[0];
+            const Layer &L0 = layer(s0, l0);
+            if (L0.eff) est[(size_t)i] += (double)L0.eff->rows * L0.eff->k * L0.eff->elem / 4e12;
+        }
         for (auto [s, l] : nodes[(size_t)order[(size_t)i]].mem) {
             const Layer &L = layer(s, l);
             if (L.src0 >= 0) ps.insert(step_of(s, L.src0));
@@ -467,9 +473,57 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
     }
     for (size_t e = 0; e < exports.size(); ++e) preds[(size_t)NN + e] = {step_of(exports[e].first, exports[e].second)};
 
+    // ---- happens-before: ancestors of each step in the dependency graph ----
+    const size_t WDS = ((size_t)NS + 63) / 64;
+    std::vector<uint64_t> anc((size_t)NS * WDS, 0);
+    for (int i = 0; i < NS; ++i)
+        for (int p : preds[(size_t)i]) {
+            uint64_t *dst = &anc[(size_t)i * WDS];
+            const uint64_t *src = &anc[(size_t)p * WDS];
+            for (size_t w = 0; w < WDS; ++w) dst[w] |= src[w];
+            dst[(size_t)p / 64] |= 1ull << (p % 64);
+        }
+
     // ---- streams: each step continues the stream of a predecessor it directly
-    // follows, else starts on the least loaded stream; cross-stream edges
-    // become event waits ----
+    // follows. A step that starts a branch opens the least loaded stream only
+    // when the work it dominates (the steps reachable from the round's start
+    // only through it: what can overlap with other branches before they
+    // join) is worth a fork, a cross-stream wait costing a few microseconds;
+    // else it queues behind its first predecessor. Cross-stream edges become
+    // event waits (graph edges in a graph round) ----
+    std::vector<int> idom((size_t)NS, -1), depth((size_t)NS, 0);  // -1: the round's start
+    for (int i = 0; i < NS; ++i) {
+        const auto &pr = preds[(size_t)i];
+        const bool from_start = pr.empty() || (i < NN && [&] {
+            for (auto [s, l] : nodes[(size_t)order[(size_t)i]].mem) {
+                const Layer &L = layer(s, l);
+                if (L.src0 < 0 || (L.op == GEMEL_OP_CONCAT && L.src1 < 0)) return true;
+            }
+            return false;
+        }());
+        int d = from_start ? -1 : pr[0];
+        for (size_t k = 1; k < pr.size() && d >= 0; ++k) {  // nearest common dominator
+            int x = d, y = pr[k];
+            while (x != y && x >= 0 && y >= 0) {
+                if (depth[(size_t)x] >= depth[(size_t)y]) x = idom[(size_t)x];
+                else y = idom[(size_t)y];
+            }
+            d = (x == y) ? x : -1;
+        }
+        idom[(size_t)i] = d;
+        depth[(size_t)i] = d < 0 ? 1 : depth[(size_t)d] + 1;
+    }
+    std::vector<double> owned(est);  // estimated work of the dominator subtree
+    std::vector<int> owned_steps((size_t)NS, 1);
+    for (int i = NS - 1; i >= 0; --i)
+        if (idom[(size_t)i] >= 0) {
+            owned[(size_t)idom[(size_t)i]] += owned[(size_t)i];
+            owned_steps[(size_t)idom[(size_t)i]] += owned_steps[(size_t)i];
+        }
+    // a chain of 3 or more launches overlaps usefully even when its FLOPs are
+    // few: small launches are latency bound
+    const double fork_work = ctx->opt.fork_us * 1e-6;
+    auto worth_fork = [&](int i) { return owned[(size_t)i] >= fork_work || owned_steps[(size_t)i] >= 3; };
     const int SMAX = std::max(1, std::min(ctx->opt.streams, 1 + (int)ctx->workers.size()));
     std::vector<int> stream_of((size_t)NS, 0), tail((size_t)SMAX, -2);
     std::vector<double> load((size_t)SMAX, 0.0);
@@ -480,6 +534,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 st = stream_of[(size_t)p];
                 break;
             }
+        if (st < 0 && !preds[(size_t)i].empty() && !worth_fork(i)) st = stream_of[(size_t)preds[(size_t)i][0]];
         if (st < 0) {
             st = 0;
             for (int k = 1; k < SMAX; ++k)
@@ -498,16 +553,6 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
             if (stream_of[(size_t)p] != stream_of[(size_t)i] && event_of[(size_t)p] < 0) event_of[(size_t)p] = n_events++;
     }
 
-    // ---- happens-before: ancestors of each step in the dependency graph ----
-    const size_t WDS = ((size_t)NS + 63) / 64;
-    std::vector<uint64_t> anc((size_t)NS * WDS, 0);
-    for (int i = 0; i < NS; ++i)
-        for (int p : preds[(size_t)i]) {
-            uint64_t *dst = &anc[(size_t)i * WDS];
-            const uint64_t *src = &anc[(size_t)p * WDS];
-            for (size_t w = 0; w < WDS; ++w) dst[w] |= src[w];
-            dst[(size_t)p / 64] |= 1ull << (p % 64);
-        }
     auto before = [&](int a_, int b_) {  // step a_ strictly precedes step b_
         if (a_ < 0) return b_ >= 0;          // the pack precedes every step
         if (b_ < 0) return false;
@@ -598,16 +643,21 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 return fail(ctx, GEMEL_EDEVICE, "event creation failed");
     }
     // stream, waits and event record of the launches of step i
+    std::vector<std::pair<size_t, size_t>> step_range((size_t)NS, {0, 0});
     auto tag_launches = [&](size_t first, int i) {
+        step_range[(size_t)i] = {first, P.launches.size()};
         if (first >= P.launches.size()) return;
-        for (size_t k = first; k < P.launches.size(); ++k) P.launches[k].stream = stream_of[(size_t)i];
+        for (size_t k = first; k < P.launches.size(); ++k) {
+            P.launches[k].stream = stream_of[(size_t)i];
+            P.launches[k].step = i;
+        }
         for (int p : preds[(size_t)i])
             if (stream_of[(size_t)p] != stream_of[(size_t)i]) P.launches[first].waits.push_back(event_of[(size_t)p]);
         P.launches.back().record = event_of[(size_t)i];
     };
 
     // ---- launches ----
-    size_t partial_need = 0;
+    std::vector<size_t> step_partial((size_t)NS, 0);  // split-K bytes per step
     // input pack, grouped by input shape, at most GEMEL_MAX_SEG models each
     {
         std::map<std::vector<int>, std::vector<int>> by_shape;
@@ -717,7 +767,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                         pick_fc_config(a.N, a.K, a.k_splits, a.k_per_split);
                         Lc.type = L_FC_BF16;
                         if (a.k_splits > 1)
-                            partial_need = std::max(partial_need, (size_t)a.k_splits * a.M * a.N * 4);
+                            step_partial[(size_t)step] = std::max(step_partial[(size_t)step], (size_t)a.k_splits * a.M * a.N * 4);
                     }
                     P.launches.push_back(Lc);
                     if (Lc.type == L_FC_BF16 && a.k_splits > 1) {
@@ -785,7 +835,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 }
                 P.launches.push_back(Lc);
                 if (a.k_splits > 1) {
-                    partial_need = std::max(partial_need, (size_t)a.k_splits * a.M * a.N * 4);
+                    step_partial[(size_t)step] = std::max(step_partial[(size_t)step], (size_t)a.k_splits * a.M * a.N * 4);
                     Launch R;
                     R.type = L_CONV_REDUCE;
                     R.kind = GEMEL_K_SPLITK_REDUCE;
@@ -863,24 +913,77 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
             const Launch &L = P.launches[i];
             const bool cv = L.type == L_CONV_BF16 || L.type == L_CONV_F32;
             const bool fcl = L.type == L_FC_BF16 || L.type == L_FC_F32;
-            std::fprintf(stderr, "plan %zu %s M=%d N=%d K=%d tile=%d splits=%d segs=%d gflop=%.3f mb=%.2f\n", i,
+            std::fprintf(stderr, "plan %zu %s M=%d N=%d K=%d tile=%d splits=%d segs=%d gflop=%.3f mb=%.2f st=%d\n", i,
                          names[L.type], cv ? L.conv.M : fcl ? L.fc.M : 0, cv ? L.conv.N : fcl ? L.fc.N : 0,
                          cv ? L.conv.K : fcl ? L.fc.K : 0, L.tile,
                          cv ? L.conv.k_splits : fcl ? L.fc.k_splits : 0,
-                         cv ? L.conv.nseg : fcl ? L.fc.nseg : L.ew.nseg, L.flops / 1e9, L.bytes / 1e6);
+                         cv ? L.conv.nseg : fcl ? L.fc.nseg : L.ew.nseg, L.flops / 1e9, L.bytes / 1e6, L.stream);
         }
     }
-    if (partial_need) {
-        if (hipMalloc((void **)&P.partial, partial_need) != hipSuccess) {
-            P.partial = nullptr;
-            (void)hipGetLastError();
-            return fail(ctx, GEMEL_ENOMEM, "device allocation of the split-K buffer failed");
+    // ---- split-K partial sums: a region per split-K step, first fit; two
+    // steps share bytes only when one precedes the other ----
+    {
+        std::vector<size_t> poff((size_t)NS, 0);
+        std::vector<int> ps;
+        for (int i = 0; i < NS; ++i)
+            if (step_partial[(size_t)i]) ps.push_back(i);
+        std::stable_sort(ps.begin(), ps.end(),
+                         [&](int x, int y) { return step_partial[(size_t)x] > step_partial[(size_t)y]; });
+        std::vector<int> done;
+        size_t total = 0;
+        for (int i : ps) {
+            std::vector<std::pair<size_t, size_t>> busy;
+            for (int j : done)
+                if (!before(i, j) && !before(j, i)) busy.push_back({poff[(size_t)j], poff[(size_t)j] + step_partial[(size_t)j]});
+            std::sort(busy.begin(), busy.end());
+            size_t cand = 0;
+            for (auto &bz : busy) {
+                if (cand + step_partial[(size_t)i] <= bz.first) break;
+                cand = std::max(cand, (size_t)round_up((int64_t)bz.second, 256));
+            }
+            poff[(size_t)i] = cand;
+            total = std::max(total, cand + (size_t)round_up((int64_t)step_partial[(size_t)i], 256));
+            done.push_back(i);
         }
-        P.partial_bytes = partial_need;
-        for (auto &L : P.launches) {
-            L.conv.partial = P.partial;
-            L.red.partial = P.partial;
-            L.fc.partial = P.partial;
+        if (total) {
+            if (hipMalloc((void **)&P.partial, total) != hipSuccess) {
+                P.partial = nullptr;
+                (void)hipGetLastError();
+                return fail(ctx, GEMEL_ENOMEM, "device allocation of the split-K buffer failed");
+            }
+            P.partial_bytes = total;
+            for (auto &L : P.launches) {
+                if (L.step < 0 || !step_partial[(size_t)L.step]) continue;
+                float *pp = P.partial + poff[(size_t)L.step] / sizeof(float);
+                L.conv.partial = pp;
+                L.red.partial = pp;
+                L.fc.partial = pp;
+            }
+        }
+    }
+
+    // ---- dependencies of each launch (the edges of a graph round) ----
+    {
+        std::vector<std::vector<int>> tails((size_t)NS);  // launches that complete step i
+        for (int i = 0; i < NS; ++i) {
+            std::set<int> d;
+            for (int p : preds[(size_t)i]) d.insert(tails[(size_t)p].begin(), tails[(size_t)p].end());
+            bool reads_input = false;
+            if (i < NN)
+                for (auto [s, l] : nodes[(size_t)order[(size_t)i]].mem) {
+                    const Layer &L = layer(s, l);
+                    reads_input |= L.src0 < 0 || (L.op == GEMEL_OP_CONCAT && L.src1 < 0);
+                }
+            if (reads_input)
+                for (int k = 0; k < P.n_pack; ++k) d.insert(k);
+            const auto [f, e] = step_range[(size_t)i];
+            if (f < e) {
+                P.launches[f].deps.assign(d.begin(), d.end());
+                for (size_t k = f + 1; k < e; ++k) P.launches[k].deps = {(int)k - 1};
+                tails[(size_t)i] = {(int)e - 1};
+            } else {
+                tails[(size_t)i].assign(d.begin(), d.end());
+            }
         }
     }
     return GEMEL_OK;
@@ -896,7 +999,7 @@ struct CallPtrs {
     std::vector<void *> outputs;       // per slot output, flattened by slot
 };
 
-hipError_t launch_one(Launch &L, const CallPtrs &cp, const Plan &P, void *wptr, hipStream_t st) {
+hipError_t launch_one(Launch &L, const CallPtrs &cp, const Plan &P, void *wptr, const Sink &st) {
     for (const Patch &p : L.patches) {
         if (p.kind == Patch::FRAMES) {
             L.ew.seg[p.seg].in0 = cp.frames[(size_t)p.slot];
@@ -993,7 +1096,9 @@ static gemel_status enqueue(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStre
             ctx->prof.pending.push_back(rec);
             HIPCHK(hipEventRecord(rec.a, ls), "hipEventRecord");
         }
-        hipError_t e = launch_one(L, cp, P, wptr, ls);
+        Sink sk;
+        sk.stream = ls;
+        hipError_t e = launch_one(L, cp, P, wptr, sk);
         if (e != hipSuccess) return fail(ctx, GEMEL_EDEVICE, std::string("kernel launch: ") + hipGetErrorString(e));
         if (ctx->opt.profile) {
             HIPCHK(hipEventRecord(rec.b, ls), "hipEventRecord");
@@ -1013,6 +1118,56 @@ static gemel_status enqueue(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStre
         HIPCHK(hipStreamWaitEvent(st, P.ev_join[(size_t)k], 0), "hipStreamWaitEvent");
     }
     return GEMEL_OK;
+}
+
+// The round as a HIP graph built node by node: one kernel node per launch,
+// after the nodes of the launches whose results it reads and, unless
+// data_only, after the previous launch of its plan stream (so the graph has
+// the shape of the multi-stream enqueue: one chain per stream plus the
+// cross-stream edges). Independent layers, e.g. of models that share
+// nothing, are then free to run concurrently. Only plans without streamed
+// weights are graphed.
+static gemel_status build_graph(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, bool data_only, hipGraphExec_t *out) {
+    hipGraph_t g = nullptr;
+    HIPCHK(hipGraphCreate(&g, 0), "hipGraphCreate");
+    const size_t n = P.launches.size();
+    // nodes that stand for launch i: its own node, or, when the launcher had
+    // nothing to do, the nodes its dependencies stand for
+    std::vector<std::vector<hipGraphNode_t>> done(n);
+    std::vector<hipGraphNode_t> deps;
+    std::vector<int> stream_last(8, -1);
+    gemel_status st = GEMEL_OK;
+    for (size_t i = 0; i < n && !st; ++i) {
+        deps.clear();
+        const Launch &L = P.launches[i];
+        for (int d : L.deps) deps.insert(deps.end(), done[(size_t)d].begin(), done[(size_t)d].end());
+        const int prev = stream_last[(size_t)L.stream];
+        if (!data_only && prev >= 0) deps.insert(deps.end(), done[(size_t)prev].begin(), done[(size_t)prev].end());
+        stream_last[(size_t)L.stream] = (int)i;
+        std::sort(deps.begin(), deps.end());
+        deps.erase(std::unique(deps.begin(), deps.end()), deps.end());
+        hipGraphNode_t node = nullptr;
+        Sink sk;
+        sk.graph = g;
+        sk.deps = deps.data();
+        sk.ndeps = deps.size();
+        sk.node = &node;
+        const hipError_t e = launch_one(P.launches[i], cp, P, nullptr, sk);
+        if (e != hipSuccess)
+            st = fail(ctx, GEMEL_EDEVICE, std::string("graph kernel node: ") + hipGetErrorString(e));
+        else if (node)
+            done[i] = {node};
+        else
+            done[i] = deps;
+    }
+    hipGraphExec_t ex = nullptr;
+    if (!st) {
+        const hipError_t e = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+        if (e != hipSuccess) st = fail(ctx, GEMEL_EDEVICE, std::string("hipGraphInstantiate: ") + hipGetErrorString(e));
+    }
+    (void)hipGraphDestroy(g);
+    if (!st) *out = ex;
+    return st;
 }
 
 gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, const void *const *frames,
@@ -1037,12 +1192,10 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
     DeviceScope scope(ctx->device);
     gemel_status st = materialise(ctx);
     if (st) return st;
-    // Several streams only for rounds enqueued directly: a round captured into
-    // a HIP graph always runs on the caller's stream alone (a captured
-    // fork/join over worker streams ended a test process with a host fault
-    // whose cause is not established, so that path is switched off).
+    // The null stream gets a single-stream plan (its implicit synchronisation
+    // with other streams would serialise the worker streams anyway).
     const bool will_graph = ctx->opt.use_graph && !ctx->opt.profile && stream != nullptr;
-    const int nstreams = (stream == nullptr || will_graph) ? 1 : ctx->opt.streams;
+    const int nstreams = stream == nullptr ? 1 : ctx->opt.streams;
     key.push_back(nstreams);
     auto it = ctx->plans.find(key);
     if (it == ctx->plans.end()) {
@@ -1071,13 +1224,14 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         const int no = (int)ctx->models[(size_t)id]->outputs.size();
         for (int o = 0; o < no; ++o) cp.outputs.push_back(outputs[caller_out_base[(size_t)ci] + o]);
     }
-    const bool graphable = will_graph && P.chunks.empty() && P.n_streams == 1;
+    const bool graphable = will_graph && P.chunks.empty();
     if (!graphable) {
         st = enqueue(ctx, P, cp, stream);
         if (!st && ctx->opt.profile) ctx->prof.rounds++;
         return st;
     }
-    if (P.graph && P.graph_stream == stream && P.graph_frames == cp.frames && P.graph_outputs == cp.outputs) {
+    if (P.graph && P.graph_stream == stream && P.graph_frames == cp.frames && P.graph_outputs == cp.outputs &&
+        P.graph_dag == ctx->opt.graph_dag) {
         HIPCHK(hipGraphLaunch(P.graph, stream), "hipGraphLaunch");
         ctx->graph_replays++;
         return GEMEL_OK;
@@ -1086,20 +1240,11 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         (void)hipGraphExecDestroy(P.graph);
         P.graph = nullptr;
     }
-    HIPCHK(hipStreamBeginCapture(stream, hipStreamCaptureModeThreadLocal), "hipStreamBeginCapture");
-    st = enqueue(ctx, P, cp, stream);
-    hipGraph_t g = nullptr;
-    hipError_t ec = hipStreamEndCapture(stream, &g);
-    if (st) {
-        if (g) (void)hipGraphDestroy(g);
-        return st;
-    }
-    if (ec != hipSuccess) return fail(ctx, GEMEL_EDEVICE, std::string("hipStreamEndCapture: ") + hipGetErrorString(ec));
     hipGraphExec_t ex = nullptr;
-    ec = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
-    (void)hipGraphDestroy(g);
-    if (ec != hipSuccess) return fail(ctx, GEMEL_EDEVICE, std::string("hipGraphInstantiate: ") + hipGetErrorString(ec));
+    st = build_graph(ctx, P, cp, ctx->opt.graph_dag != 0, &ex);
+    if (st) return st;
     P.graph = ex;
+    P.graph_dag = ctx->opt.graph_dag;
     P.graph_stream = stream;
     P.graph_frames = cp.frames;
     P.graph_outputs = cp.outputs;

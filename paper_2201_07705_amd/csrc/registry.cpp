@@ -431,6 +431,15 @@ gemel_status gemel_set_option(gemel_ctx *ctx, int32_t key, int64_t value) {
         ctx->opt.streams = (int)value;
         drop_plans(ctx);
         break;
+    case GEMEL_OPT_FORK_US:
+        if (value < 0 || value > 1000000) return fail(ctx, GEMEL_EINVAL, "fork_us is 0..1e6");
+        ctx->opt.fork_us = (int)value;
+        drop_plans(ctx);
+        break;
+    case GEMEL_OPT_GRAPH_DAG:
+        if (value != 0 && value != 1) return fail(ctx, GEMEL_EINVAL, "graph_dag is 0 or 1");
+        ctx->opt.graph_dag = (int)value;
+        break;
     case GEMEL_OPT_PROFILE:
         if (value != 0 && value != 1) return fail(ctx, GEMEL_EINVAL, "profile is 0 or 1");
         profile_reset(ctx);

@@ -23,7 +23,8 @@ def main():
     L = G.load(libpath)
     L.hipMalloc.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t]
     L.hipMalloc.restype = ctypes.c_int
-    for f in ("hoststub_violations", "hoststub_launches", "hoststub_live_bytes"):
+    for f in ("hoststub_violations", "hoststub_launches", "hoststub_live_bytes",
+              "hoststub_hazards", "hoststub_check_order", "hoststub_selftest"):
         getattr(L, f).restype = ctypes.c_long
     L.hoststub_last.restype = ctypes.c_char_p
     wl = configs.get(name, **kw)
@@ -57,7 +58,10 @@ def main():
     status = []
     for _ in range(rounds):
         status.append(ctx.infer_raw(ids, frames, nfr, outs, stream))
+    L.hoststub_check_order()
     print(json.dumps({
+        "selftest": L.hoststub_selftest(),
+        "hazards": L.hoststub_hazards(),
         "status": status,
         "violations": L.hoststub_violations(),
         "launches": L.hoststub_launches(),

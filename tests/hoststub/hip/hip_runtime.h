@@ -1,8 +1,9 @@
 // Minimal stand-in for the HIP runtime API used by libgemel's host sources,
 // so that the registry, planner and round executor can be compiled for the
 // CPU (with AddressSanitizer) and driven without a GPU. Device memory is
-// host memory; streams, events and graphs are bookkeeping only. Kernel
-// launchers are replaced by bounds checkers (hoststub.cpp).
+// host memory; streams, events and graphs only record the order they
+// impose. Kernel launchers are replaced by bounds and ordering checkers
+// (hoststub.cpp).
 #pragma once
 #include <cstddef>
 #include <cstdint>
@@ -21,8 +22,19 @@ typedef struct ihipGraphNode_t *hipGraphNode_t;
 struct hipDeviceProp_t {
     char gcnArchName[256];
 };
+struct dim3 {
+    unsigned x, y, z;
+    dim3(unsigned x_ = 1, unsigned y_ = 1, unsigned z_ = 1) : x(x_), y(y_), z(z_) {}
+};
+struct hipKernelNodeParams {
+    dim3 blockDim;
+    void **extra;
+    void *func;
+    dim3 gridDim;
+    void **kernelParams;
+    unsigned sharedMemBytes;
+};
 enum hipMemcpyKind { hipMemcpyHostToDevice = 1, hipMemcpyDeviceToHost = 2 };
-enum hipStreamCaptureMode { hipStreamCaptureModeGlobal = 0, hipStreamCaptureModeThreadLocal = 1 };
 #define hipHostMallocDefault 0u
 #define hipStreamNonBlocking 1u
 #define hipEventDisableTiming 2u
@@ -52,8 +64,10 @@ hipError_t hipMemcpyAsync(void *d, const void *s, size_t n, hipMemcpyKind k, hip
 hipError_t hipDeviceSynchronize();
 hipError_t hipGetLastError();
 const char *hipGetErrorString(hipError_t e);
-hipError_t hipStreamBeginCapture(hipStream_t s, hipStreamCaptureMode m);
-hipError_t hipStreamEndCapture(hipStream_t s, hipGraph_t *g);
+hipError_t hipLaunchKernel(const void *f, dim3 g, dim3 b, void **args, size_t shm, hipStream_t s);
+hipError_t hipGraphCreate(hipGraph_t *g, unsigned flags);
+hipError_t hipGraphAddKernelNode(hipGraphNode_t *n, hipGraph_t g, const hipGraphNode_t *deps, size_t ndeps,
+                                 const hipKernelNodeParams *p);
 hipError_t hipGraphInstantiate(hipGraphExec_t *e, hipGraph_t g, hipGraphNode_t *n, char *log, size_t sz);
 hipError_t hipGraphDestroy(hipGraph_t g);
 hipError_t hipGraphExecDestroy(hipGraphExec_t e);

@@ -63,38 +63,61 @@ def test_model_order_does_not_matter(r18):
     _same(_run(wl, params, frames), _run(wl, params, frames, order=[1, 0]))
 
 
-MULTISTREAM_OFF = ("multi-stream rounds are switched off on the GPU until the "
-                   "cause of a host fault seen with them is established")
-
-
 def test_graph_replays_bitwise(r18):
+    """A single-stream plan replayed as a HIP graph several times, against
+    rounds enqueued directly."""
     wl, params, frames = r18
     log("graph replays")
     base = _run(wl, params, frames, OPT_USE_GRAPH=0)
     _same(base, _run(wl, params, frames, repeat=5))
 
 
-@pytest.mark.skip(reason=MULTISTREAM_OFF)
-def test_streams_and_graph_replays_bitwise(r18):
-    wl, params, frames = r18
-    log("streams / graph")
-    base = _run(wl, params, frames, OPT_STREAMS=1, OPT_USE_GRAPH=0)
-    _same(base, _run(wl, params, frames, OPT_STREAMS=4, repeat=5))
-    _same(base, _run(wl, params, frames, OPT_STREAMS=8, OPT_USE_GRAPH=0))
-
-
-@pytest.mark.skip(reason=MULTISTREAM_OFF)
-def test_concurrent_branches_r50_vgg_reduced():
-    """Independent model chains run on different streams; outputs must match
-    the single-stream run bitwise and the oracle within tolerance."""
+@pytest.fixture(scope="module")
+def r50vgg():
     wl = configs.r50x2_vgg16x2(res=64, frames=2)
     params = [wl.params(i) for i in range(4)]
     frames = [wl.frames(i) for i in range(4)]
+    return wl, params, frames
+
+
+def test_concurrent_branches_r50_vgg_reduced(r50vgg):
+    """ResNet-50 and VGG-16 pairs share no layer: their chains (and each
+    model's own tail) run on separate streams by default, as graph branches
+    or enqueued directly. Every output must match the single-stream round
+    bitwise and the oracle within tolerance."""
+    wl, params, frames = r50vgg
     log("r50/vgg streams")
-    a = _run(wl, params, frames, OPT_STREAMS=1)
-    b = _run(wl, params, frames, OPT_STREAMS=4, repeat=3)
+    a = _run(wl, params, frames, OPT_STREAMS=1, OPT_USE_GRAPH=0)
+    b = _run(wl, params, frames, repeat=4)
     _same(a, b)
+    _same(a, _run(wl, params, frames, OPT_USE_GRAPH=0, repeat=2))
     compare(wl, b, oracle_outputs(wl, params, frames), tag="r50vgg-64px")
+
+
+@pytest.mark.parametrize("dag", [0, 1])
+def test_concurrent_branches_as_graph(r50vgg, dag):
+    """The multi-stream round as a HIP graph with edges following the plan
+    streams (0) or only the data dependencies (1), with 8 streams, replayed."""
+    wl, params, frames = r50vgg
+    log(f"r50/vgg graph dag={dag}")
+    a = _run(wl, params, frames, OPT_STREAMS=1, OPT_USE_GRAPH=0)
+    b = _run(wl, params, frames, OPT_STREAMS=8, OPT_FORK_US=0,
+             OPT_GRAPH_DAG=dag, repeat=4)
+    _same(a, b)
+
+
+def test_concurrent_branches_with_split_k(r50vgg):
+    """Forced split-K on every conv: concurrent branches each need their own
+    partial-sum region."""
+    wl, params, frames = r50vgg
+    log("r50/vgg streams, split-K 4")
+    a = _run(wl, params, frames, OPT_STREAMS=1, OPT_USE_GRAPH=0,
+             OPT_CONV_SPLITS=4)
+    b = _run(wl, params, frames, OPT_CONV_SPLITS=4, repeat=4)
+    _same(a, b)
+    c = _run(wl, params, frames, OPT_CONV_SPLITS=4, OPT_USE_GRAPH=0,
+             OPT_STREAMS=8, OPT_FORK_US=0, repeat=3)
+    _same(a, c)
 
 
 def test_swap_forced_equals_resident_bitwise():

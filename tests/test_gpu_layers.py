@@ -90,6 +90,39 @@ def test_conv_every_tile_shape(tile, case):
     run_case([lay], (cin, hw, hw), [n], "bf16", tile=tile)
 
 
+# One conv written straight to the fp32 output: inputs and weights are
+# bf16-exact and accumulation is fp32, so the only difference from the fp64
+# oracle is fp32 summation order (relative error ~ sqrt(K) * 2^-24 of the
+# terms' magnitude).
+EXACT_TOL = 5e-5
+
+
+@pytest.mark.parametrize("splits", [1, 3])
+@pytest.mark.parametrize("tile", range(len(TILES)), ids=lambda t: TILES[t])
+@pytest.mark.parametrize("case", CONV_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_conv_single_layer_exact(tile, case, splits):
+    """Every tile shape and split-K 1/3 on one conv + BN + residual-free
+    epilogue with the fp32 output store, against the oracle at fp32
+    accumulation precision."""
+    from paper_2201_07705_amd import gemel as G
+    cin, cout, k, s, p, hw, n = case
+    log(f"exact tile {TILES[tile]} splits {splits} conv {case}")
+    lay = [conv("c", -1, cin, cout, k, s, p, bn=True, act="leaky", out=True)]
+    models = [ModelSpec("m0", "custom", lay, n, (cin, hw, hw))]
+    wl = Workload("exact", 11, "bf16", models, [], "normal")
+    params = [wl.params(0)]
+    fr = [wl.frames(0)]
+    g = GpuWorkload(wl, params)
+    try:
+        g.ctx.set_option(G.OPT_CONV_TILE, tile)
+        g.ctx.set_option(G.OPT_CONV_SPLITS, splits)
+        got = g.run(fr)
+    finally:
+        g.close()
+    compare(wl, got, oracle_outputs(wl, params, fr), tol=EXACT_TOL,
+            check_argmax=False)
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("case", CONV_CASES[:6], ids=lambda c: "x".join(map(str, c)))
 def test_conv_layer_internal_store_and_export(dtype, case):

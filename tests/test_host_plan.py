@@ -2,7 +2,10 @@
 the CPU against a stub HIP runtime, with AddressSanitizer, and driven
 through whole inference rounds of every workload. The stub's kernel
 launchers check that every pointer range each kernel would read or write
-lies inside one live allocation; multi-stream plans, graph capture, the
+lies inside one live allocation, and that any two launches (or weight
+copies) that are not ordered by stream order, events or graph edges touch
+no common bytes unless both only read them. Multi-stream plans, graph
+rounds built from the launch dependencies (and as one chain), the
 weight-swap schedule and split-K are all exercised. No GPU is needed."""
 
 import json
@@ -51,6 +54,13 @@ CASES = [
     ("r50x2_vgg16x2", {}, {}),
     ("yolov3x3", {"res": 96, "frames": 2},
      {"OPT_STREAMS": 8, "OPT_USE_GRAPH": 0}),
+    ("yolov3x3", {"res": 96, "frames": 2}, {}),
+    ("yolov3x3", {"res": 96, "frames": 2},
+     {"OPT_STREAMS": 8, "OPT_FORK_US": 0}),
+    ("r50x2_vgg16x2", {"res": 64, "frames": 2},
+     {"OPT_STREAMS": 8, "OPT_FORK_US": 0, "OPT_GRAPH_DAG": 1}),
+    ("r50x2_vgg16x2", {"res": 64, "frames": 2},
+     {"OPT_CONV_SPLITS": 4, "OPT_STREAMS": 8, "OPT_FORK_US": 0}),
     ("mix8_budget40", {"res": 32, "frames": 2}, {}),
     ("mix8_budget40", {"res": 32, "frames": 2},
      {"OPT_SWAP_SLOT_BYTES": 1 << 20, "OPT_SWAP_SLOTS": 2,
@@ -63,6 +73,8 @@ CASES = [
 def test_every_kernel_access_in_bounds(hostlib, name, kw, opts):
     out = drive(hostlib, name, kw, opts)
     assert out["status"] == [0, 0], out["error"]
+    assert out["selftest"] == 1
+    assert out["hazards"] == 0, out["last"]
     assert out["violations"] == 0, out["last"]
     assert out["launches"] >= out["plan_launches"] > 0
     if name == "mix8_budget40":
