@@ -117,6 +117,11 @@ def main():
     log(f"timed {args.steps} steps")
     ev0, ev1 = torch.cuda.Event(enable_timing=True), \
         torch.cuda.Event(enable_timing=True)
+    # record both events once so that their lazy creation (which can stall
+    # the host for tens of milliseconds) happens outside the timed region
+    with torch.cuda.stream(stream):
+        ev0.record(stream)
+        ev1.record(stream)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     with torch.cuda.stream(stream):

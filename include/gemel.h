@@ -256,13 +256,16 @@ enum {
                                     it clears the collected statistics.    */
     GEMEL_OPT_CONV_TILE = 7,     /* -1 (default): pick each conv's tile
                                     shape and split-K by the cost model;
-                                    0..12: force one tile shape (128x128,
+                                    0..13: force one tile shape (128x128,
                                     128x64, 64x64, 256x256, 256x128,
                                     256x64, 64x64 and 128x64 with deeper
                                     prefetch, 64x128; then the LDS-DMA
                                     pipeline's 256x256, 256x128, 128x128,
-                                    128x64, used where Cin % 32 == 0) with
-                                    split-K still chosen                   */
+                                    128x64, used where Cin % 32 == 0; 13:
+                                    the 8-channel stem kernel, used where
+                                    the input has 8 physical channels and
+                                    without split-K) with split-K still
+                                    chosen                                 */
     GEMEL_OPT_CONV_SPLITS = 8,   /* 0 (default): split-K chosen per conv;
                                     n >= 1: force n depth splits (capped
                                     so that every split has work)          */
@@ -274,17 +277,35 @@ enum {
                                     when the work only it leads to is worth
                                     the fork; cross-stream dependencies are
                                     event waits                            */
-    GEMEL_OPT_GRAPH_DAG = 10,    /* graph edges: 0 (default): a node
-                                    follows the launches whose results it
-                                    reads and the previous launch of its
-                                    stream; 1: only the launches whose
-                                    results it reads (activation bytes are
-                                    reused only along such dependencies)   */
-    GEMEL_OPT_FORK_US = 11       /* a branch gets a stream of its own when
+    GEMEL_OPT_GRAPH_DAG = 10,    /* graph rounds over several streams with
+                                    autotune off: 0 (default): the launches
+                                    of each stream are cut where a cross-
+                                    stream wait or event record falls, and
+                                    each piece is a chain-shaped graph
+                                    launched on its stream (with the
+                                    round's fork, joins and events between
+                                    pieces); 1: one graph whose nodes
+                                    follow only the launches whose results
+                                    they read (activation bytes are reused
+                                    only along such dependencies)          */
+    GEMEL_OPT_FORK_US = 11,      /* a branch gets a stream of its own when
                                     the work only it leads to is estimated
                                     at this many microseconds or more
                                     (default 30), or spans 3 or more
                                     launch steps                           */
+    GEMEL_OPT_AUTOTUNE = 12      /* 1 (default): the first 12 rounds of a
+                                    graphable plan over several streams try
+                                    the two graph forms of GEMEL_OPT_GRAPH_DAG,
+                                    one graph with data edges plus each
+                                    stream's order, and direct enqueue, 3
+                                    rounds each (the first untimed), timing
+                                    each round with
+                                    HIP events on the caller's stream (the
+                                    timed rounds synchronise with it), and
+                                    later rounds use the fastest. Skipped
+                                    while the caller's stream is being
+                                    captured. 0: the mode set by
+                                    GEMEL_OPT_GRAPH_DAG                    */
 };
 
 /* Set an option; takes effect at the next gemel_infer. Errors: EINVAL. */

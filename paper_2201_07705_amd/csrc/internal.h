@@ -105,6 +105,17 @@ struct Chunk {
     size_t bytes() const { return (size_t)(nrows * blob->k) * blob->elem; }
 };
 
+// A run of one stream's launches with cross-stream waits only before its
+// first launch and an event record only after its last: one chain-shaped
+// HIP graph, launched on its stream.
+struct Segment {
+    int stream = 0;
+    std::vector<int> launches;
+    std::vector<int> waits;   // plan events waited for before the segment
+    int record = -1;          // plan event recorded after it
+    hipGraphExec_t exec = nullptr;
+};
+
 struct Plan {
     std::vector<int> model_ids, n_frames;  // active models (key)
     std::vector<int> out_base;             // first output index per slot
@@ -122,10 +133,17 @@ struct Plan {
     float *partial = nullptr;
     size_t partial_bytes = 0;
     size_t streamed_bytes = 0;
-    // HIP graph of the round for one set of caller pointers (edges: the
-    // launches' data dependencies, plus stream order unless graph_dag is 1)
-    hipGraphExec_t graph = nullptr;
-    int graph_dag = -1;
+    // HIP graphs of the round for one set of caller pointers: one chain per
+    // segment; one graph whose edges are the launches' data dependencies; one
+    // graph with those edges plus each plan stream's order
+    std::vector<Segment> segs;
+    hipGraphExec_t graph[2] = {nullptr, nullptr};
+    // execution mode of a multi-stream graphable plan, chosen by timing
+    // each candidate over its first rounds (autotune)
+    int tune_round = 0;
+    double tune_ms[4] = {0, 0, 0, 0};
+    int best_mode = -1;
+    hipEvent_t tune_ev[2] = {nullptr, nullptr};
     std::vector<const void *> graph_frames;
     std::vector<void *> graph_outputs;
     hipStream_t graph_stream = nullptr;
@@ -152,6 +170,7 @@ struct Options {
     int conv_splits = 0;
     int use_graph = 1;
     int graph_dag = 0;
+    int autotune = 1;
     int fork_us = 30;
     int64_t slot_bytes = 32ll << 20;
     int slots = 3;

@@ -479,7 +479,7 @@ struct TileShape {
 static const TileShape kTiles[TILE_COUNT] = {
     {128, 128, 256}, {128, 64, 256}, {64, 64, 256}, {256, 256, 512}, {256, 128, 512},
     {256, 64, 256},  {64, 64, 256},  {128, 64, 256}, {64, 128, 256},
-    {256, 256, 512}, {256, 128, 256}, {128, 128, 256}, {128, 64, 128}};
+    {256, 256, 512}, {256, 128, 256}, {128, 128, 256}, {128, 64, 128}, {256, 32, 256}};
 
 int conv_tile_bm(int tile) { return tile >= 0 && tile < TILE_COUNT ? kTiles[tile].bm : 0; }
 int conv_tile_bn(int tile) { return tile >= 0 && tile < TILE_COUNT ? kTiles[tile].bn : 0; }
@@ -523,6 +523,7 @@ static hipError_t launch_tile(int tile, dim3 grid, const Sink &sk, const ConvArg
 
 hipError_t launch_conv_bf16(const ConvArgs &a, int tile, const Sink &sk) {
     if (tile_is_dma(tile)) return launch_conv_dma(a, tile, sk);
+    if (tile == TILE_STEM) return launch_conv_stem(a, sk);
     if (!conv_args_ok(a) || !a.zero) return hipErrorInvalidValue;
     const int bm = conv_tile_bm(tile), bn = conv_tile_bn(tile);
     if (!bm) return hipErrorInvalidValue;

@@ -51,7 +51,9 @@ enum ConvTile {
     TILE_DMA_256x128 = 10, // 4 waves, 128x64 per wave
     TILE_DMA_128x128 = 11, // 4 waves, 64x64 per wave
     TILE_DMA_128x64 = 12,  // 2 waves, 64x64 per wave
-    TILE_COUNT = 13
+    // 8-channel inputs (k_stem.hip): 256 pixels x 32 channels, no LDS
+    TILE_STEM = 13,
+    TILE_COUNT = 14
 };
 int conv_tile_threads(int tile);
 int conv_tile_bm(int tile);
@@ -61,7 +63,10 @@ constexpr int CONV_BK = 64;
 hipError_t launch_conv_bf16(const ConvArgs &a, int tile, const Sink &sk);
 bool conv_dma_supported(const ConvArgs &a);
 hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk);
-inline bool tile_is_dma(int tile) { return tile >= TILE_DMA_256x256 && tile < TILE_COUNT; }
+inline bool tile_is_dma(int tile) { return tile >= TILE_DMA_256x256 && tile <= TILE_DMA_128x64; }
+// Stem kernel: Cin == in_cs == 8, no split-K.
+bool conv_stem_supported(const ConvArgs &a);
+hipError_t launch_conv_stem(const ConvArgs &a, const Sink &sk);
 hipError_t launch_conv_f32(const ConvArgs &a, const Sink &sk);
 // Split-K reduction + fused epilogue (bf16 or f32 internal activations).
 hipError_t launch_conv_reduce(const ReduceArgs &a, bool bf16, const Sink &sk);

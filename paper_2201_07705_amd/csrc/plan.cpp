@@ -103,7 +103,12 @@ void drop_plans(gemel_ctx *ctx) {
     if (!ctx->plans.empty()) (void)hipDeviceSynchronize();
     for (auto &kv : ctx->plans) {
         Plan &p = *kv.second;
-        if (p.graph) (void)hipGraphExecDestroy(p.graph);
+        for (auto g : p.graph)
+            if (g) (void)hipGraphExecDestroy(g);
+        for (auto &sg : p.segs)
+            if (sg.exec) (void)hipGraphExecDestroy(sg.exec);
+        for (auto ev : p.tune_ev)
+            if (ev) (void)hipEventDestroy(ev);
         for (auto ev : p.events)
             if (ev) (void)hipEventDestroy(ev);
         if (p.ev_fork) (void)hipEventDestroy(p.ev_fork);
@@ -822,8 +827,17 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     if (a.seg[i].scale != a.seg[0].scale || a.seg[i].shift != a.seg[0].shift) a.uni_affine = 0;
                 if (bf16) {
                     const bool dma_ok = a.Cin % 32 == 0 && a.in_cs % 8 == 0 && a.uni_affine;
-                    pick_conv_config(a.M, a.N, a.K, dma_ok, ctx->opt.conv_tile, ctx->opt.conv_splits, Lc.tile,
-                                     a.k_splits, a.k_per_split);
+                    // 8-channel inputs (the RGB stems) take the stem kernel
+                    const bool stem = a.Cin == 8 && a.in_cs == 8 && a.kh * a.kw <= 64 &&
+                                      (ctx->opt.conv_tile < 0 || ctx->opt.conv_tile == TILE_STEM);
+                    if (stem) {
+                        Lc.tile = TILE_STEM;
+                        a.k_splits = 1;
+                        a.k_per_split = a.K;
+                    } else {
+                        pick_conv_config(a.M, a.N, a.K, dma_ok, ctx->opt.conv_tile == TILE_STEM ? TILE_64x64 : ctx->opt.conv_tile,
+                                         ctx->opt.conv_splits, Lc.tile, a.k_splits, a.k_per_split);
+                    }
                     if (tile_is_dma(Lc.tile) && !conv_dma_supported(a)) Lc.tile = TILE_64x64;
                     Lc.type = L_CONV_BF16;
                     Lc.kind = L0.op == GEMEL_OP_CONV ? GEMEL_K_CONV_MFMA : GEMEL_K_FC;
@@ -1120,45 +1134,55 @@ static gemel_status enqueue(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStre
     return GEMEL_OK;
 }
 
-// The round as a HIP graph built node by node: one kernel node per launch,
-// after the nodes of the launches whose results it reads and, unless
-// data_only, after the previous launch of its plan stream (so the graph has
-// the shape of the multi-stream enqueue: one chain per stream plus the
-// cross-stream edges). Independent layers, e.g. of models that share
-// nothing, are then free to run concurrently. Only plans without streamed
-// weights are graphed.
-static gemel_status build_graph(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, bool data_only, hipGraphExec_t *out) {
+// Edges of a graph over plan launches.
+enum GraphEdges {
+    EDGES_CHAIN = 0,    // each launch follows the previous one of the list
+    EDGES_DATA = 1,     // each launch follows the launches whose results it reads
+    EDGES_STREAMS = 2   // data edges plus the previous launch of its plan stream
+};
+
+// A HIP graph built node by node over the launches `idx` (in plan order),
+// one kernel node per launch, with the given edges. Only plans without
+// streamed weights are graphed.
+static gemel_status build_graph(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, const std::vector<int> &idx,
+                                int edges, hipGraphExec_t *out) {
     hipGraph_t g = nullptr;
     HIPCHK(hipGraphCreate(&g, 0), "hipGraphCreate");
-    const size_t n = P.launches.size();
     // nodes that stand for launch i: its own node, or, when the launcher had
     // nothing to do, the nodes its dependencies stand for
-    std::vector<std::vector<hipGraphNode_t>> done(n);
+    std::vector<std::vector<hipGraphNode_t>> done(P.launches.size());
     std::vector<hipGraphNode_t> deps;
-    std::vector<int> stream_last(8, -1);
     gemel_status st = GEMEL_OK;
-    for (size_t i = 0; i < n && !st; ++i) {
+    int prev = -1;
+    std::vector<int> stream_last(8, -1);
+    for (size_t k = 0; k < idx.size() && !st; ++k) {
+        const int i = idx[k];
+        const Launch &L = P.launches[(size_t)i];
         deps.clear();
-        const Launch &L = P.launches[i];
-        for (int d : L.deps) deps.insert(deps.end(), done[(size_t)d].begin(), done[(size_t)d].end());
-        const int prev = stream_last[(size_t)L.stream];
-        if (!data_only && prev >= 0) deps.insert(deps.end(), done[(size_t)prev].begin(), done[(size_t)prev].end());
-        stream_last[(size_t)L.stream] = (int)i;
-        std::sort(deps.begin(), deps.end());
-        deps.erase(std::unique(deps.begin(), deps.end()), deps.end());
+        if (edges == EDGES_CHAIN) {
+            if (prev >= 0) deps = done[(size_t)prev];
+        } else {
+            for (int d : L.deps) deps.insert(deps.end(), done[(size_t)d].begin(), done[(size_t)d].end());
+            const int sp = stream_last[(size_t)L.stream];
+            if (edges == EDGES_STREAMS && sp >= 0) deps.insert(deps.end(), done[(size_t)sp].begin(), done[(size_t)sp].end());
+            std::sort(deps.begin(), deps.end());
+            deps.erase(std::unique(deps.begin(), deps.end()), deps.end());
+        }
+        prev = i;
+        stream_last[(size_t)L.stream] = i;
         hipGraphNode_t node = nullptr;
         Sink sk;
         sk.graph = g;
         sk.deps = deps.data();
         sk.ndeps = deps.size();
         sk.node = &node;
-        const hipError_t e = launch_one(P.launches[i], cp, P, nullptr, sk);
+        const hipError_t e = launch_one(P.launches[(size_t)i], cp, P, nullptr, sk);
         if (e != hipSuccess)
             st = fail(ctx, GEMEL_EDEVICE, std::string("graph kernel node: ") + hipGetErrorString(e));
         else if (node)
-            done[i] = {node};
+            done[(size_t)i] = {node};
         else
-            done[i] = deps;
+            done[(size_t)i] = deps;
     }
     hipGraphExec_t ex = nullptr;
     if (!st) {
@@ -1168,6 +1192,75 @@ static gemel_status build_graph(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, boo
     (void)hipGraphDestroy(g);
     if (!st) *out = ex;
     return st;
+}
+
+// Split the launches into segments (see Segment). With several streams the
+// input packs form a segment of their own, so that the other streams fork
+// right after them.
+static void build_segments(Plan &P) {
+    P.segs.clear();
+    std::vector<int> open(8, -1);  // open segment of each stream
+    for (size_t i = 0; i < P.launches.size(); ++i) {
+        const Launch &L = P.launches[i];
+        int &o = open[(size_t)L.stream];
+        const bool fork = (int)i == P.n_pack && P.n_streams > 1;
+        if (o < 0 || !L.waits.empty() || fork) {
+            for (int &x : open)
+                if (fork) x = -1;
+            Segment sg;
+            sg.stream = L.stream;
+            sg.waits = L.waits;
+            P.segs.push_back(sg);
+            o = (int)P.segs.size() - 1;
+        }
+        P.segs[(size_t)o].launches.push_back((int)i);
+        if (L.record >= 0) {
+            P.segs[(size_t)o].record = L.record;
+            o = -1;
+        }
+    }
+}
+
+// Execution modes of a round.
+enum RoundMode { MODE_EAGER = 0, MODE_SEGMENTS = 1, MODE_DAG = 2, MODE_STREAMGRAPH = 3 };
+
+// One graph round of the per-stream segments, launched in plan order, each
+// after its cross-stream waits, worker streams forked after the packs and
+// joined at the end.
+static gemel_status launch_segments(gemel_ctx *ctx, Plan &P, hipStream_t st) {
+    hipStream_t streams[8] = {st};
+    for (int k = 1; k < P.n_streams; ++k) streams[k] = ctx->workers[(size_t)k - 1];
+    bool forked = P.n_streams == 1;
+    for (const Segment &sg : P.segs) {
+        if (!forked && sg.launches.front() >= P.n_pack) {
+            HIPCHK(hipEventRecord(P.ev_fork, st), "hipEventRecord");
+            for (int k = 1; k < P.n_streams; ++k) HIPCHK(hipStreamWaitEvent(streams[k], P.ev_fork, 0), "hipStreamWaitEvent");
+            forked = true;
+        }
+        const hipStream_t ss = streams[sg.stream];
+        for (int ev : sg.waits) HIPCHK(hipStreamWaitEvent(ss, P.events[(size_t)ev], 0), "hipStreamWaitEvent");
+        HIPCHK(hipGraphLaunch(sg.exec, ss), "hipGraphLaunch");
+        if (sg.record >= 0) HIPCHK(hipEventRecord(P.events[(size_t)sg.record], ss), "hipEventRecord");
+    }
+    if (!forked) {
+        HIPCHK(hipEventRecord(P.ev_fork, st), "hipEventRecord");
+        for (int k = 1; k < P.n_streams; ++k) HIPCHK(hipStreamWaitEvent(streams[k], P.ev_fork, 0), "hipStreamWaitEvent");
+    }
+    for (int k = 1; k < P.n_streams; ++k) {
+        HIPCHK(hipEventRecord(P.ev_join[(size_t)k], streams[k]), "hipEventRecord");
+        HIPCHK(hipStreamWaitEvent(st, P.ev_join[(size_t)k], 0), "hipStreamWaitEvent");
+    }
+    return GEMEL_OK;
+}
+
+static void drop_graphs(Plan &P) {
+    for (auto &g : P.graph) {
+        if (g) (void)hipGraphExecDestroy(g);
+        g = nullptr;
+    }
+    for (auto &sg : P.segs)
+        if (sg.exec) (void)hipGraphExecDestroy(sg.exec);
+    P.segs.clear();
 }
 
 gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, const void *const *frames,
@@ -1230,25 +1323,85 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         if (!st && ctx->opt.profile) ctx->prof.rounds++;
         return st;
     }
-    if (P.graph && P.graph_stream == stream && P.graph_frames == cp.frames && P.graph_outputs == cp.outputs &&
-        P.graph_dag == ctx->opt.graph_dag) {
-        HIPCHK(hipGraphLaunch(P.graph, stream), "hipGraphLaunch");
-        ctx->graph_replays++;
-        return GEMEL_OK;
+    // mode of this round: a single-stream plan is one chain graph; a
+    // multi-stream plan uses the mode set by the options, or, with autotune,
+    // each candidate mode for kTuneEach rounds (the first of them untimed)
+    // and then the fastest
+    constexpr int kTuneEach = 3;
+    constexpr int kNCand = 4;
+    static const int kCand[kNCand] = {MODE_SEGMENTS, MODE_STREAMGRAPH, MODE_DAG, MODE_EAGER};
+    int mode = ctx->opt.graph_dag ? MODE_DAG : MODE_SEGMENTS;
+    bool timed = false, tuning = false;
+    if (P.n_streams == 1) {
+        mode = MODE_SEGMENTS;
+    } else if (ctx->opt.autotune) {
+        if (P.best_mode >= 0) {
+            mode = P.best_mode;
+        } else {
+            hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+            HIPCHK(hipStreamIsCapturing(stream, &cs), "hipStreamIsCapturing");
+            if (cs == hipStreamCaptureStatusNone) {
+                mode = kCand[P.tune_round / kTuneEach];
+                timed = P.tune_round % kTuneEach != 0;
+                tuning = true;
+                for (auto &ev : P.tune_ev)
+                    if (!ev) HIPCHK(hipEventCreate(&ev), "hipEventCreate");
+            }
+        }
     }
-    if (P.graph) {
-        (void)hipGraphExecDestroy(P.graph);
-        P.graph = nullptr;
+    // graphs for this set of caller pointers (rebuilt when they change)
+    if (P.graph_stream != stream || P.graph_frames != cp.frames || P.graph_outputs != cp.outputs) {
+        drop_graphs(P);
+        P.graph_stream = stream;
+        P.graph_frames = cp.frames;
+        P.graph_outputs = cp.outputs;
     }
-    hipGraphExec_t ex = nullptr;
-    st = build_graph(ctx, P, cp, ctx->opt.graph_dag != 0, &ex);
-    if (st) return st;
-    P.graph = ex;
-    P.graph_dag = ctx->opt.graph_dag;
-    P.graph_stream = stream;
-    P.graph_frames = cp.frames;
-    P.graph_outputs = cp.outputs;
-    HIPCHK(hipGraphLaunch(P.graph, stream), "hipGraphLaunch");
+    bool replay = true;
+    if (mode == MODE_SEGMENTS && P.segs.empty()) {
+        replay = false;
+        build_segments(P);
+        for (Segment &sg : P.segs) {
+            st = build_graph(ctx, P, cp, sg.launches, EDGES_CHAIN, &sg.exec);
+            if (st) {
+                drop_graphs(P);
+                return st;
+            }
+        }
+    } else if ((mode == MODE_DAG || mode == MODE_STREAMGRAPH) && !P.graph[mode == MODE_DAG ? 0 : 1]) {
+        replay = false;
+        std::vector<int> all(P.launches.size());
+        std::iota(all.begin(), all.end(), 0);
+        st = build_graph(ctx, P, cp, all, mode == MODE_DAG ? EDGES_DATA : EDGES_STREAMS, &P.graph[mode == MODE_DAG ? 0 : 1]);
+        if (st) return st;
+    }
+    if (timed) HIPCHK(hipEventRecord(P.tune_ev[0], stream), "hipEventRecord");
+    if (mode == MODE_EAGER) {
+        st = enqueue(ctx, P, cp, stream);
+        if (st) return st;
+    } else {
+        if (replay) ctx->graph_replays++;
+        if (mode == MODE_DAG || mode == MODE_STREAMGRAPH) {
+            HIPCHK(hipGraphLaunch(P.graph[mode == MODE_DAG ? 0 : 1], stream), "hipGraphLaunch");
+        } else {
+            st = launch_segments(ctx, P, stream);
+            if (st) return st;
+        }
+    }
+    if (timed) {
+        HIPCHK(hipEventRecord(P.tune_ev[1], stream), "hipEventRecord");
+        HIPCHK(hipEventSynchronize(P.tune_ev[1]), "hipEventSynchronize");
+        float ms = 0;
+        HIPCHK(hipEventElapsedTime(&ms, P.tune_ev[0], P.tune_ev[1]), "hipEventElapsedTime");
+        P.tune_ms[P.tune_round / kTuneEach] += ms;
+    }
+    if (tuning) {
+        if (++P.tune_round == kNCand * kTuneEach) {
+            int b = 0;
+            for (int c = 1; c < kNCand; ++c)
+                if (P.tune_ms[c] < P.tune_ms[b]) b = c;
+            P.best_mode = kCand[b];
+        }
+    }
     return GEMEL_OK;
 }
 

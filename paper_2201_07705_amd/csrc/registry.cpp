@@ -417,7 +417,7 @@ gemel_status gemel_set_option(gemel_ctx *ctx, int32_t key, int64_t value) {
         drop_plans(ctx);
         break;
     case GEMEL_OPT_CONV_TILE:
-        if (value < -1 || value >= TILE_COUNT) return fail(ctx, GEMEL_EINVAL, "conv tile is -1..12");
+        if (value < -1 || value >= TILE_COUNT) return fail(ctx, GEMEL_EINVAL, "conv tile is -1..13");
         ctx->opt.conv_tile = (int)value;
         drop_plans(ctx);
         break;
@@ -430,6 +430,10 @@ gemel_status gemel_set_option(gemel_ctx *ctx, int32_t key, int64_t value) {
         if (value < 1 || value > 8) return fail(ctx, GEMEL_EINVAL, "streams is 1..8");
         ctx->opt.streams = (int)value;
         drop_plans(ctx);
+        break;
+    case GEMEL_OPT_AUTOTUNE:
+        if (value != 0 && value != 1) return fail(ctx, GEMEL_EINVAL, "autotune is 0 or 1");
+        ctx->opt.autotune = (int)value;
         break;
     case GEMEL_OPT_FORK_US:
         if (value < 0 || value > 1000000) return fail(ctx, GEMEL_EINVAL, "fork_us is 0..1e6");

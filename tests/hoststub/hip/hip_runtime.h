@@ -35,6 +35,7 @@ struct hipKernelNodeParams {
     unsigned sharedMemBytes;
 };
 enum hipMemcpyKind { hipMemcpyHostToDevice = 1, hipMemcpyDeviceToHost = 2 };
+enum hipStreamCaptureStatus { hipStreamCaptureStatusNone = 0, hipStreamCaptureStatusActive = 1 };
 #define hipHostMallocDefault 0u
 #define hipStreamNonBlocking 1u
 #define hipEventDisableTiming 2u
@@ -64,6 +65,7 @@ hipError_t hipMemcpyAsync(void *d, const void *s, size_t n, hipMemcpyKind k, hip
 hipError_t hipDeviceSynchronize();
 hipError_t hipGetLastError();
 const char *hipGetErrorString(hipError_t e);
+hipError_t hipStreamIsCapturing(hipStream_t s, hipStreamCaptureStatus *st);
 hipError_t hipLaunchKernel(const void *f, dim3 g, dim3 b, void **args, size_t shm, hipStream_t s);
 hipError_t hipGraphCreate(hipGraph_t *g, unsigned flags);
 hipError_t hipGraphAddKernelNode(hipGraphNode_t *n, hipGraph_t g, const hipGraphNode_t *deps, size_t ndeps,

@@ -14,8 +14,9 @@
 // the dependency nodes it was added with (graph construction). Two nodes
 // that are not ordered either way may run concurrently; if one writes bytes
 // the other reads or writes, that is a hazard, counted as a violation.
-// Graphs are checked when instantiated, direct enqueue when the host asks
-// (hoststub_check_order).
+// Graphs are checked when instantiated; a graph launch is one node of the
+// stream it is launched on, with every range of the graph. Direct enqueue
+// and graph launches are checked when the host asks (hoststub_check_order).
 #include <algorithm>
 #include <cstdio>
 #include <cstdlib>
@@ -60,6 +61,7 @@ struct Universe {
 };
 Universe eager;                                      // direct enqueue
 std::map<hipGraph_t, Universe> graphs;               // graphs under construction
+std::map<hipGraphExec_t, std::vector<Rng>> execs;    // byte ranges of an instantiated graph
 std::map<hipStream_t, std::vector<int>> frontier;    // nodes the next op on a stream follows
 std::map<hipEvent_t, std::vector<int>> evstate;      // nodes an event's record follows
 size_t synced = 0;
@@ -234,6 +236,10 @@ hipError_t hipDeviceSynchronize() { synced = eager.nodes.size(); return hipSucce
 hipError_t hipGetLastError() { return hipSuccess; }
 const char *hipGetErrorString(hipError_t e) { return e == hipSuccess ? "success" : "stub error"; }
 hipError_t hipLaunchKernel(const void *, dim3, dim3, void **, size_t, hipStream_t) { return hipErrorInvalidValue; }
+hipError_t hipStreamIsCapturing(hipStream_t s, hipStreamCaptureStatus *st) {
+    *st = hipStreamCaptureStatusNone;
+    return s ? hipSuccess : hipErrorInvalidValue;
+}
 hipError_t hipGraphCreate(hipGraph_t *g, unsigned) {
     *g = (hipGraph_t)std::malloc(16);
     graphs[*g] = Universe{};
@@ -248,17 +254,30 @@ hipError_t hipGraphInstantiate(hipGraphExec_t *e, hipGraph_t g, hipGraphNode_t *
     if (it == graphs.end()) return hipErrorInvalidValue;
     check_universe(it->second, "graph");
     *e = (hipGraphExec_t)std::malloc(16);
+    auto &r = execs[*e];
+    for (const Node &n : it->second.nodes) r.insert(r.end(), n.rng.begin(), n.rng.end());
     return hipSuccess;
 }
 hipError_t hipGraphDestroy(hipGraph_t g) { graphs.erase(g); std::free(g); return hipSuccess; }
-hipError_t hipGraphExecDestroy(hipGraphExec_t e) { std::free(e); return hipSuccess; }
-hipError_t hipGraphLaunch(hipGraphExec_t, hipStream_t) { return hipSuccess; }
+hipError_t hipGraphExecDestroy(hipGraphExec_t e) { execs.erase(e); std::free(e); return hipSuccess; }
+hipError_t hipGraphLaunch(hipGraphExec_t e, hipStream_t s) {
+    auto it = execs.find(e);
+    if (it == execs.end() || !s) return hipErrorInvalidValue;
+    Node n;
+    n.kern = "graph";
+    n.deps = frontier[s];
+    n.synced = synced;
+    n.rng = it->second;
+    eager.nodes.push_back(n);
+    frontier[s] = {(int)eager.nodes.size() - 1};
+    return hipSuccess;
+}
 }  // extern "C"
 
 namespace gemel {
 
-static const int kBm[TILE_COUNT] = {128, 128, 64, 256, 256, 256, 64, 128, 64, 256, 256, 128, 128};
-static const int kBn[TILE_COUNT] = {128, 64, 64, 256, 128, 64, 64, 64, 128, 256, 128, 128, 64};
+static const int kBm[TILE_COUNT] = {128, 128, 64, 256, 256, 256, 64, 128, 64, 256, 256, 128, 128, 256};
+static const int kBn[TILE_COUNT] = {128, 64, 64, 256, 128, 64, 64, 64, 128, 256, 128, 128, 64, 32};
 int conv_tile_bm(int t) { return t >= 0 && t < TILE_COUNT ? kBm[t] : 0; }
 int conv_tile_bn(int t) { return t >= 0 && t < TILE_COUNT ? kBn[t] : 0; }
 int conv_tile_threads(int t) { return (t == TILE_256x256 || t == TILE_256x128) ? 512 : 256; }
@@ -309,6 +328,18 @@ bool conv_dma_supported(const ConvArgs &a) {
            a.uni_affine;
 }
 hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) { return launch_conv_bf16(a, tile, sk); }
+bool conv_stem_supported(const ConvArgs &a) {
+    return a.Cin == 8 && a.in_cs == 8 && a.k_splits <= 1 && a.kh * a.kw <= 64 && a.zero &&
+           (a.out_mode == OUT_NHWC || a.out_mode == OUT_NCHW_F32);
+}
+hipError_t launch_conv_stem(const ConvArgs &a, const Sink &sk) {
+    if (!conv_stem_supported(a)) {
+        ++violations;
+        last = "stem kernel on an unsupported conv";
+        return hipErrorInvalidValue;
+    }
+    return conv_common(a, 2, "conv_stem", true, sk);
+}
 hipError_t launch_conv_bf16(const ConvArgs &a, int tile, const Sink &sk) {
     if (tile < 0 || tile >= TILE_COUNT) return hipErrorInvalidValue;
     if (tile_is_dma(tile) && !conv_dma_supported(a)) {
@@ -316,6 +347,7 @@ hipError_t launch_conv_bf16(const ConvArgs &a, int tile, const Sink &sk) {
         last = "dma tile on an unsupported conv";
         return hipErrorInvalidValue;
     }
+    if (tile == TILE_STEM) return launch_conv_stem(a, sk);
     return conv_common(a, 2, "conv_bf16", true, sk);
 }
 hipError_t launch_conv_f32(const ConvArgs &a, const Sink &sk) { return conv_common(a, 4, "conv_f32", false, sk); }

@@ -102,8 +102,33 @@ def test_concurrent_branches_as_graph(r50vgg, dag):
     log(f"r50/vgg graph dag={dag}")
     a = _run(wl, params, frames, OPT_STREAMS=1, OPT_USE_GRAPH=0)
     b = _run(wl, params, frames, OPT_STREAMS=8, OPT_FORK_US=0,
-             OPT_GRAPH_DAG=dag, repeat=4)
+             OPT_AUTOTUNE=0, OPT_GRAPH_DAG=dag, repeat=4)
     _same(a, b)
+
+
+def test_autotuned_rounds_bitwise(r50vgg):
+    """The first rounds of a multi-stream plan cycle through the execution
+    modes while timing them; every round's outputs must equal the serial
+    round's."""
+    import torch
+    wl, params, frames = r50vgg
+    log("r50/vgg autotune rounds")
+    a = _run(wl, params, frames, OPT_STREAMS=1, OPT_USE_GRAPH=0)
+    g = _pinned(wl, params)
+    try:
+        dev = [torch.from_numpy(f).cuda() for f in frames]
+        s = torch.cuda.Stream()
+        outs = None
+        for r in range(14):
+            with torch.cuda.stream(s):
+                outs = g.ctx.infer(g.ids, dev, stream=s, outputs=outs)
+            s.synchronize()
+            got = [[o.cpu().numpy() for o in m] for m in outs]
+            for x, y in zip(a, got):
+                for u, v in zip(x, y):
+                    assert np.array_equal(u, v), r
+    finally:
+        g.close()
 
 
 def test_concurrent_branches_with_split_k(r50vgg):

@@ -60,6 +60,11 @@ CONV_CASES = [
     (32, 64, 3, 2, 1, 33, 1),
     (16, 40, 3, 1, 1, 9, 5),
     (1024, 64, 1, 1, 0, 5, 3),
+    # 8-channel (RGB stem) inputs: narrow N, ragged M, N beyond one tile
+    (3, 32, 3, 1, 1, 41, 3),
+    (3, 64, 3, 1, 1, 30, 2),
+    (8, 40, 5, 2, 2, 23, 2),
+    (3, 96, 3, 2, 1, 17, 1),
 ]
 
 
@@ -74,7 +79,7 @@ def test_conv_layer_output_store(dtype, case):
 
 TILES = ["128x128", "128x64", "64x64", "256x256", "256x128", "256x64",
          "64x64d2", "128x64d2", "64x128", "dma256x256", "dma256x128",
-         "dma128x128", "dma128x64"]
+         "dma128x128", "dma128x64", "stem"]
 
 
 @pytest.mark.parametrize("tile", range(len(TILES)), ids=lambda t: TILES[t])
