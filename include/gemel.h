@@ -227,7 +227,8 @@ enum {
     GEMEL_Q_ACTIVATION_BYTES = 5, /* activation arena of the last plan    */
     GEMEL_Q_LAUNCHES = 6,       /* kernel launches per round, last plan   */
     GEMEL_Q_N_MODELS = 7,       /* registered models                      */
-    GEMEL_Q_GRAPH_REPLAYS = 8   /* rounds served by a replayed HIP graph  */
+    GEMEL_Q_GRAPH_REPLAYS = 8,  /* rounds served by a replayed HIP graph  */
+    GEMEL_Q_STREAMS = 9         /* GEMEL_OPT_STREAMS now in force         */
 };
 
 /* Read a counter. Errors: EINVAL (unknown key, null val). */

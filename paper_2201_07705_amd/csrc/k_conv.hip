@@ -175,6 +175,18 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a
     const size_t frame_elems = (size_t)a.H * a.W * a.in_cs;
     const u16 *const zp = (const u16 *)a.zero;
     const int H = a.H, W = a.W, in_cs = a.in_cs, N = a.N, K = a.K, Cin = a.Cin, kw = a.kw;
+    // segment of the tile's first and last row (wave-uniform, scalar loads):
+    // rows of a tile inside one segment (the common case: segments are
+    // whole frames) take its fields as uniform values; per-row lookups only
+    // for a tile that straddles segments
+    const int m_first = tm * BM, m_last = min(a.M, m_first + BM) - 1;
+    int s_first = 0, s_last = 0;
+    for (int i = 1; i < a.nseg; ++i) {
+        s_first += m_first >= a.seg[i].m_start ? 1 : 0;
+        s_last += m_last >= a.seg[i].m_start ? 1 : 0;
+    }
+    const bool one_seg = s_first == s_last;
+    const ConvSeg &useg = a.seg[s_first];
 
     // ---- loader set-up: thread owns K chunk q of rows r0 + RPP j ----
     const int q = tid & 7, r0 = tid >> 3;
@@ -187,11 +199,15 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a
         ahi[j] = -(1 << 28);
         awi[j] = 0;
         if (gm < a.M) {
-            const int sg = seg_of_row(a, gm);
             const int fr = gm / HWo;
             const int pix = gm - fr * HWo;
             const int ho = pix / a.Wo, wo = pix - (pix / a.Wo) * a.Wo;
-            abase[j] = (const u16 *)a.seg[sg].in + (size_t)(fr - a.seg[sg].f_start) * frame_elems;
+            if (one_seg) {
+                abase[j] = (const u16 *)useg.in + (size_t)(fr - useg.f_start) * frame_elems;
+            } else {
+                const int sg = seg_of_row(a, gm);
+                abase[j] = (const u16 *)a.seg[sg].in + (size_t)(fr - a.seg[sg].f_start) * frame_elems;
+            }
             ahi[j] = ho * a.stride - a.pad;
             awi[j] = wo * a.stride - a.pad;
         }
@@ -300,8 +316,12 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a
             const int gm = tm * BM + (tid + NT * i) / CH;
             const u16 *p = zp;
             if (gm < a.M) {
-                const ConvSeg &sg = a.seg[seg_of_row(a, gm)];
-                p = (const u16 *)sg.res + (size_t)(gm - sg.m_start) * e.out_cs + my_gn;
+                if (one_seg) {
+                    p = (const u16 *)useg.res + (size_t)(gm - useg.m_start) * e.out_cs + my_gn;
+                } else {
+                    const ConvSeg &sg = a.seg[seg_of_row(a, gm)];
+                    p = (const u16 *)sg.res + (size_t)(gm - sg.m_start) * e.out_cs + my_gn;
+                }
             }
             rpf[i] = *(const u32x4 *)p;
         }
@@ -374,16 +394,28 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a
                 const float4 v0 = *(const float4 *)(Cs + rl * LDC + ch * 8);
                 const float4 v1 = *(const float4 *)(Cs + rl * LDC + ch * 8 + 4);
                 float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-                const ConvSeg &sg = a.seg[seg_of_row(a, gm)];
                 if (pre) {
-                    const size_t off = (size_t)(gm - sg.m_start) * e.out_cs + gn;
+                    const u16 *resp;
+                    u16 *outp;
+                    int ms;
+                    if (one_seg) {
+                        resp = (const u16 *)useg.res;
+                        outp = (u16 *)useg.out;
+                        ms = useg.m_start;
+                    } else {
+                        const ConvSeg &sg = a.seg[seg_of_row(a, gm)];
+                        resp = (const u16 *)sg.res;
+                        outp = (u16 *)sg.out;
+                        ms = sg.m_start;
+                    }
+                    const size_t off = (size_t)(gm - ms) * e.out_cs + gn;
                     u16 rv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
                     if (e.has_res) {
                         u32x4 r4;
                         if constexpr (RES_PF)
                             r4 = rpf[(item - tid) / NT];
                         else
-                            r4 = *(const u32x4 *)((const u16 *)sg.res + off);
+                            r4 = *(const u32x4 *)(resp + off);
 #pragma unroll
                         for (int jj = 0; jj < 4; ++jj) {
                             rv[2 * jj] = (u16)(r4[jj] & 0xffffu);
@@ -395,9 +427,11 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a
 #pragma unroll
                     for (int jj = 0; jj < 8; ++jj)
                         op[jj] = f2bf(epi(v[jj] * sc[jj] + sh[jj], bf2f(rv[jj]), e.has_res, e.res_mode, e.act, e.slope));
-                    *(uint4 *)((u16 *)sg.out + off) = o;
+                    *(uint4 *)(outp + off) = o;
+                } else if (one_seg) {
+                    store8_nhwc_bf16(useg, e, gm, gn, v);
                 } else {
-                    store8_nhwc_bf16(sg, e, gm, gn, v);
+                    store8_nhwc_bf16(a.seg[seg_of_row(a, gm)], e, gm, gn, v);
                 }
             }
         } else {
@@ -405,7 +439,10 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a
                 const int col = item / nrows, rl = item - (item / nrows) * nrows;
                 const int gm = tm * BM + row0 + rl, gn = tn * BN + col;
                 if (gm >= a.M || gn >= a.N) continue;
-                store1_nchw_f32<true>(a.seg[seg_of_row(a, gm)], e, gm, gn, Cs[rl * LDC + col]);
+                if (one_seg)
+                    store1_nchw_f32<true>(useg, e, gm, gn, Cs[rl * LDC + col]);
+                else
+                    store1_nchw_f32<true>(a.seg[seg_of_row(a, gm)], e, gm, gn, Cs[rl * LDC + col]);
             }
         }
         __syncthreads();

@@ -116,6 +116,17 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
     const int H = a.H, W = a.W, in_cs = a.in_cs, N = a.N, K = a.K, Cin = a.Cin, kw = a.kw;
     const size_t frame_elems = (size_t)H * W * in_cs;
     const u16 *const zp = (const u16 *)a.zero;
+    // segment of the tile's first and last row (wave-uniform, scalar loads):
+    // rows of a tile inside one segment take its fields as uniform values;
+    // per-row lookups only for a tile that straddles segments
+    const int m_first = tm * BM, m_last = min(a.M, m_first + BM) - 1;
+    int s_first = 0, s_last = 0;
+    for (int i = 1; i < a.nseg; ++i) {
+        s_first += m_first >= a.seg[i].m_start ? 1 : 0;
+        s_last += m_last >= a.seg[i].m_start ? 1 : 0;
+    }
+    const bool one_seg = s_first == s_last;
+    const ConvSeg &useg = a.seg[s_first];
 
     // ---- DMA assignment: instruction i of this thread fills slot
     // (i*NW + wave)*64 + lane: row ((i*NW + wave)*16 + lane/4), chunk cq ----
@@ -129,11 +140,15 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
         ahi[i] = -(1 << 28);
         awi[i] = 0;
         if (gm < a.M) {
-            const int sg = d_seg(a, gm);
             const int fr = gm / HWo;
             const int pix = gm - fr * HWo;
             const int ho = pix / a.Wo, wo = pix - (pix / a.Wo) * a.Wo;
-            abase[i] = (const u16 *)a.seg[sg].in + (size_t)(fr - a.seg[sg].f_start) * frame_elems;
+            if (one_seg) {
+                abase[i] = (const u16 *)useg.in + (size_t)(fr - useg.f_start) * frame_elems;
+            } else {
+                const int sg = d_seg(a, gm);
+                abase[i] = (const u16 *)a.seg[sg].in + (size_t)(fr - a.seg[sg].f_start) * frame_elems;
+            }
             ahi[i] = ho * a.stride - a.pad;
             awi[i] = wo * a.stride - a.pad;
         }
@@ -258,20 +273,32 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
             const float *src = ew + rl * EPI_LD + ch * 8;
             const float4 v0 = *(const float4 *)src, v1 = *(const float4 *)(src + 4);
             float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-            const ConvSeg &sg = a.seg[d_seg(a, gm)];
-            const int lr_ = gm - sg.m_start;
             if (a.k_splits > 1) {
                 float4 *dst = (float4 *)(a.partial + ((size_t)blockIdx.y * a.M + gm) * N + gn);
                 dst[0] = v0;
                 dst[1] = v1;
                 continue;
             }
+            const u16 *resp;
+            void *outp;
+            int ms;
+            if (one_seg) {
+                resp = (const u16 *)useg.res;
+                outp = useg.out;
+                ms = useg.m_start;
+            } else {
+                const ConvSeg &sg = a.seg[d_seg(a, gm)];
+                resp = (const u16 *)sg.res;
+                outp = sg.out;
+                ms = sg.m_start;
+            }
+            const int lr_ = gm - ms;
             const float s8[8] = {sc0[0], sc0[1], sc0[2], sc0[3], sc1[0], sc1[1], sc1[2], sc1[3]};
             const float h8[8] = {sh0[0], sh0[1], sh0[2], sh0[3], sh1[0], sh1[1], sh1[2], sh1[3]};
             if (a.out_mode == OUT_NHWC) {
                 const size_t off = (size_t)lr_ * out_cs + gn;
                 u32x4 r4 = {0u, 0u, 0u, 0u};
-                if (a.has_res) r4 = *(const u32x4 *)((const u16 *)sg.res + off);
+                if (a.has_res) r4 = *(const u32x4 *)(resp + off);
                 u32x4 o;
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
@@ -281,15 +308,15 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
                                                 a.act, a.slope));
                     o[q] = (uint32_t)y0 | ((uint32_t)y1 << 16);
                 }
-                *(u32x4 *)((u16 *)sg.out + off) = o;
+                *(u32x4 *)((u16 *)outp + off) = o;
             } else {
                 const int f = lr_ / HWo, pix = lr_ - (lr_ / HWo) * HWo;
 #pragma unroll
                 for (int q = 0; q < 8; ++q) {
                     const int c = gn + q;
                     if (c >= a.cout) break;
-                    const float r = a.has_res ? d_bf2f(((const u16 *)sg.res)[(size_t)lr_ * out_cs + c]) : 0.f;
-                    ((float *)sg.out)[((size_t)f * a.cout + c) * HWo + pix] =
+                    const float r = a.has_res ? d_bf2f(resp[(size_t)lr_ * out_cs + c]) : 0.f;
+                    ((float *)outp)[((size_t)f * a.cout + c) * HWo + pix] =
                         d_epi(v[q] * s8[q] + h8[q], r, a.has_res, a.res_mode, a.act, a.slope);
                 }
             }

@@ -8,11 +8,18 @@
 // registers: no LDS staging and no im2col. A depth step of 32 covers 4 taps
 // (the last step of a filter is padded with zero taps). The weight
 // fragment is the MFMA's first operand and the pixel fragment its second,
-// so a lane's result is 4 consecutive output channels of one pixel, stored
-// as one 8-byte write (NHWC) or 4 coalesced fp32 writes (NCHW output).
+// so a lane's result is 4 output channels of one pixel. The weight rows of
+// each pair of channel fragments are interleaved so that those are channels
+// 8q..8q+3 in one fragment and 8q+4..8q+7 in the other: a lane writes 8
+// consecutive channels as one 16-byte store (NHWC) or 8 coalesced fp32
+// writes (NCHW output). Epilogue scale/shift (one pair of arrays shared by
+// every segment) are fetched together once the depth loop ends.
 //
-// Tile: 4 waves x 64 pixels (four 16-pixel fragments each) by 32 output
-// channels; the depth loop loads step k+1 while the MFMAs of step k run.
+// Tile: 4 waves x PF 16-pixel fragments by NF 16-channel fragments: 64
+// channels (PF 2) or 32 (PF 4) per workgroup, so that a pixel's output
+// channels are written whole by one workgroup. The depth loop loads step
+// k+1 while the MFMAs of step k run; with three steps (3x3 filters) every
+// load is issued before the first MFMA.
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
@@ -27,7 +34,7 @@ namespace {
 typedef unsigned short u16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float s_bf2f(u16 h) { return __uint_as_float((uint32_t)h << 16); }
 __device__ __forceinline__ u16 s_f2bf(float f) { return __builtin_bit_cast(u16, (__bf16)f); }
@@ -56,13 +63,11 @@ struct SFor<0> {
     __device__ __forceinline__ static void run(F &&) {}
 };
 
-constexpr int STEM_PX = 256;   // pixels per workgroup (4 waves x 64)
-
 }  // namespace
 
-template <int NF>
+template <int PF, int NF, int S>
 __global__ __launch_bounds__(256) void conv_stem_kernel(const ConvArgs a) {
-    constexpr int BN = NF * 16;
+    constexpr int BN = NF * 16, STEM_PX = 4 * PF * 16;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int tiles_n = (a.N + BN - 1) / BN;
@@ -77,40 +82,75 @@ __global__ __launch_bounds__(256) void conv_stem_kernel(const ConvArgs a) {
     const int l16 = lane & 15, kq = lane >> 4;   // fragment row/column, tap within a step
     const u16 *const zp = (const u16 *)a.zero;
 
-    // this lane's pixel in each of the wave's 4 pixel fragments
-    const u16 *pbase[4];
-    int phi[4], pwi[4];
-    SFor<4>::run([&](auto I) {
-        const int m = tm * STEM_PX + wave * 64 + I * 16 + l16;
+    // segment of the tile's first and last pixel (wave-uniform, scalar
+    // loads). A tile inside one segment (the common case: segments are whole
+    // frames) takes that segment's fields as uniform values; only a tile
+    // that straddles segments looks them up per pixel.
+    const int m_first = tm * STEM_PX, m_last = min(a.M, m_first + STEM_PX) - 1;
+    int s_first = 0, s_last = 0;
+    for (int i = 1; i < a.nseg; ++i) {
+        s_first += m_first >= a.seg[i].m_start ? 1 : 0;
+        s_last += m_last >= a.seg[i].m_start ? 1 : 0;
+    }
+    const bool one_seg = s_first == s_last;
+    auto seg_of = [&](int m) __attribute__((always_inline)) {
+        int sx = 0;
+        for (int i = 1; i < a.nseg; ++i) sx += (m >= a.seg[i].m_start) ? 1 : 0;
+        return sx;
+    };
+
+    // this lane's pixel in each of the wave's PF pixel fragments
+    const u16 *pbase[PF];
+    int phi[PF], pwi[PF];
+    const u16 *const in_u = (const u16 *)a.seg[s_first].in;
+    const int f_u = a.seg[s_first].f_start;
+    SFor<PF>::run([&](auto I) __attribute__((always_inline)) {
+        const int m = tm * STEM_PX + wave * PF * 16 + I * 16 + l16;
         pbase[I] = zp;
         phi[I] = -(1 << 28);
         pwi[I] = 0;
         if (m < a.M) {
-            int s = 0;
-            for (int i = 1; i < a.nseg; ++i) s += (m >= a.seg[i].m_start) ? 1 : 0;
             const int fr = m / HWo, pix = m - (m / HWo) * HWo;
             const int ho = pix / a.Wo, wo = pix - (pix / a.Wo) * a.Wo;
-            pbase[I] = (const u16 *)a.seg[s].in + (size_t)(fr - a.seg[s].f_start) * H * W * 8;
+            if (one_seg) {
+                pbase[I] = in_u + (size_t)(fr - f_u) * H * W * 8;
+            } else {
+                const int sx = seg_of(m);
+                pbase[I] = (const u16 *)a.seg[sx].in + (size_t)(fr - a.seg[sx].f_start) * H * W * 8;
+            }
             phi[I] = ho * a.stride - a.pad;
             pwi[I] = wo * a.stride - a.pad;
         }
     });
-    // this lane's weight row in each of the NF channel fragments
+    // this lane's weight row in each of the NF channel fragments: MFMA row r
+    // of fragment J holds channel 32*(J/2) + 8*(r/4) + 4*(J%2) + r%4
+    static_assert(NF % 2 == 0, "channel fragments come in pairs");
     const u16 *wrow[NF];
-    SFor<NF>::run([&](auto J) {
-        const int n = tn * BN + J * 16 + l16;
+    SFor<NF>::run([&](auto J) __attribute__((always_inline)) {
+        const int n = tn * BN + (J / 2) * 32 + (l16 >> 2) * 8 + (J % 2) * 4 + (l16 & 3);
         wrow[J] = n < N ? (const u16 *)a.w + (size_t)n * K : nullptr;
     });
+    // epilogue constants of this lane's channels c = 32*j + 8*kq .. +7 of
+    // fragment pair j (every segment shares them; loaded from an in-range
+    // channel), in named registers per pair
+    struct Aff {
+        f32x4 s0, s1, h0, h1;
+    };
+    auto load_aff = [&](int c) __attribute__((always_inline)) {
+        const int cc = c < N ? c : 0;
+        const float *sp = a.seg[0].scale + cc, *hp = a.seg[0].shift + cc;
+        return Aff{*(const f32x4 *)sp, *(const f32x4 *)(sp + 4), *(const f32x4 *)hp, *(const f32x4 *)(hp + 4)};
+    };
 
-    auto load = [&](int step, bf16x8 (&wf)[NF], bf16x8 (&pf)[4]) __attribute__((always_inline)) {
+    auto load = [&](int step, bf16x8 (&wf)[NF], bf16x8 (&pf)[PF]) __attribute__((always_inline)) {
         const int tap = step * 4 + kq;
         const bool tok = tap < taps;
         const int r = tok ? tap / kw : 0, s = tok ? tap - (tap / kw) * kw : 0;
-        SFor<NF>::run([&](auto J) {
+        SFor<NF>::run([&](auto J) __attribute__((always_inline)) {
             const u16 *p = (tok && wrow[J]) ? wrow[J] + tap * 8 : zp;
             wf[J] = *(const bf16x8 *)p;
         });
-        SFor<4>::run([&](auto I) {
+        SFor<PF>::run([&](auto I) __attribute__((always_inline)) {
             const int hi = phi[I] + r, wi = pwi[I] + s;
             const bool ok = tok && (unsigned)hi < (unsigned)H && (unsigned)wi < (unsigned)W;
             const u16 *p = ok ? pbase[I] + (size_t)(hi * W + wi) * 8 : zp;
@@ -118,61 +158,100 @@ __global__ __launch_bounds__(256) void conv_stem_kernel(const ConvArgs a) {
         });
     };
 
-    f32x4 acc[4][NF];
-    SFor<4>::run([&](auto I) { SFor<NF>::run([&](auto J) { acc[I][J] = f32x4{0.f, 0.f, 0.f, 0.f}; }); });
-    bf16x8 w0[NF], p0[4], w1[NF], p1[4];
+    f32x4 acc[PF][NF];
+    SFor<PF>::run([&](auto I) __attribute__((always_inline)) { SFor<NF>::run([&](auto J) __attribute__((always_inline)) { acc[I][J] = f32x4{0.f, 0.f, 0.f, 0.f}; }); });
+    bf16x8 w0[NF], p0[PF], w1[NF], p1[PF];
     load(0, w0, p0);
-    auto mma = [&](const bf16x8 (&wf)[NF], const bf16x8 (&pf)[4]) __attribute__((always_inline)) {
-        SFor<4>::run([&](auto I) {
-            SFor<NF>::run([&](auto J) {
+    auto mma = [&](const bf16x8 (&wf)[NF], const bf16x8 (&pf)[PF]) __attribute__((always_inline)) {
+        SFor<PF>::run([&](auto I) __attribute__((always_inline)) {
+            SFor<NF>::run([&](auto J) __attribute__((always_inline)) {
                 acc[I][J] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[J], pf[I], acc[I][J], 0, 0, 0);
             });
         });
     };
-    for (int st = 0; st < steps; st += 2) {
-        if (st + 1 < steps) load(st + 1, w1, p1);
+    if constexpr (S == 3) {
+        // 3 depth steps (3x3 filters): every load in flight at once
+        bf16x8 w2[NF], p2[PF];
+        load(1, w1, p1);
+        load(2, w2, p2);
         mma(w0, p0);
-        if (st + 1 < steps) {
-            if (st + 2 < steps) load(st + 2, w0, p0);
-            mma(w1, p1);
+        mma(w1, p1);
+        mma(w2, p2);
+    } else {
+        for (int st = 0; st < steps; st += 2) {
+            if (st + 1 < steps) load(st + 1, w1, p1);
+            mma(w0, p0);
+            if (st + 1 < steps) {
+                if (st + 2 < steps) load(st + 2, w0, p0);
+                mma(w1, p1);
+            }
         }
     }
 
-    // epilogue: lane holds channels c0..c0+3 of pixel m for each (I, J)
-    SFor<4>::run([&](auto I) {
-        const int m = tm * STEM_PX + wave * 64 + I * 16 + l16;
+    // all epilogue constants at once, after the depth loop (held across it
+    // they would be spilled; the empty asm keeps the compiler from hoisting
+    // the loads above the loop)
+    asm volatile("" ::: "memory");
+    const Aff aff0 = load_aff(tn * BN + kq * 8);
+    const Aff aff1 = NF > 2 ? load_aff(tn * BN + 32 + kq * 8) : aff0;
+    void *const out_u = a.seg[s_first].out;
+    const void *const res_u = a.seg[s_first].res;
+    const int ms_u = a.seg[s_first].m_start;
+
+    // epilogue: for each pixel fragment I and fragment pair j the lane holds
+    // channels c0..c0+7 of pixel m (acc[I][2j] then acc[I][2j+1])
+    SFor<PF>::run([&](auto I) __attribute__((always_inline)) {
+        const int m = tm * STEM_PX + wave * PF * 16 + I * 16 + l16;
         if (m >= a.M) return;
-        int sidx = 0;
-        for (int i = 1; i < a.nseg; ++i) sidx += (m >= a.seg[i].m_start) ? 1 : 0;
-        const ConvSeg &sg = a.seg[sidx];
-        const int ml = m - sg.m_start;
-        SFor<NF>::run([&](auto J) {
-            const int c0 = tn * BN + J * 16 + kq * 4;
+        void *outp;
+        const void *resp;
+        int ml;
+        if (one_seg) {
+            outp = out_u;
+            resp = res_u;
+            ml = m - ms_u;
+        } else {
+            const int sx = seg_of(m);
+            outp = a.seg[sx].out;
+            resp = a.seg[sx].res;
+            ml = m - a.seg[sx].m_start;
+        }
+        SFor<NF / 2>::run([&](auto JP) __attribute__((always_inline)) {
+            constexpr int j0 = 2 * JP, j1 = 2 * JP + 1;
+            const int c0 = tn * BN + JP * 32 + kq * 8;
             if (c0 >= N) return;
-            const f32x4 sc = *(const f32x4 *)(sg.scale + c0);
-            const f32x4 sh = *(const f32x4 *)(sg.shift + c0);
-            float rv[4] = {0.f, 0.f, 0.f, 0.f};
-            if (a.has_res) {
-                const u32x2 rr = *(const u32x2 *)((const u16 *)sg.res + (size_t)ml * a.out_cs + c0);
-                rv[0] = s_bf2f((u16)(rr.x & 0xffff));
-                rv[1] = s_bf2f((u16)(rr.x >> 16));
-                rv[2] = s_bf2f((u16)(rr.y & 0xffff));
-                rv[3] = s_bf2f((u16)(rr.y >> 16));
+            f32x4 sc0, sc1, sh0, sh1;
+            if constexpr (decltype(JP)::value == 0) {
+                sc0 = aff0.s0; sc1 = aff0.s1; sh0 = aff0.h0; sh1 = aff0.h1;
+            } else {
+                sc0 = aff1.s0; sc1 = aff1.s1; sh0 = aff1.h0; sh1 = aff1.h1;
             }
-            float y[4];
-            SFor<4>::run([&](auto V) {
+            float rv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+            if (a.has_res) {
+                const u32x4 rr = *(const u32x4 *)((const u16 *)resp + (size_t)ml * a.out_cs + c0);
+                SFor<4>::run([&](auto Q) __attribute__((always_inline)) {
+                    constexpr int q = Q;
+                    rv[2 * q] = s_bf2f((u16)(rr[q] & 0xffff));
+                    rv[2 * q + 1] = s_bf2f((u16)(rr[q] >> 16));
+                });
+            }
+            float y[8];
+            SFor<4>::run([&](auto V) __attribute__((always_inline)) {
                 constexpr int v = V;
-                y[v] = s_epi(acc[I][J][v] * sc[v] + sh[v], rv[v], a.has_res, a.res_mode, a.act, a.slope);
+                y[v] = s_epi(acc[I][j0][v] * sc0[v] + sh0[v], rv[v], a.has_res, a.res_mode, a.act, a.slope);
+                y[4 + v] = s_epi(acc[I][j1][v] * sc1[v] + sh1[v], rv[4 + v], a.has_res, a.res_mode, a.act, a.slope);
             });
             if (a.out_mode == OUT_NHWC) {
-                u32x2 o;
-                o.x = (uint32_t)s_f2bf(y[0]) | ((uint32_t)s_f2bf(y[1]) << 16);
-                o.y = (uint32_t)s_f2bf(y[2]) | ((uint32_t)s_f2bf(y[3]) << 16);
-                *(u32x2 *)((u16 *)sg.out + (size_t)ml * a.out_cs + c0) = o;
+                u32x4 o;
+                SFor<4>::run([&](auto Q) __attribute__((always_inline)) {
+                    constexpr int q = Q;
+                    o[q] = (uint32_t)s_f2bf(y[2 * q]) | ((uint32_t)s_f2bf(y[2 * q + 1]) << 16);
+                });
+                *(u32x4 *)((u16 *)outp + (size_t)ml * a.out_cs + c0) = o;
             } else {
                 const int fl = ml / HWo, pix = ml - (ml / HWo) * HWo;
-                float *o = (float *)sg.out + (size_t)fl * a.cout * HWo + pix;
-                SFor<4>::run([&](auto V) {
+                float *o = (float *)outp + (size_t)fl * a.cout * HWo + pix;
+                SFor<8>::run([&](auto V) __attribute__((always_inline)) {
                     constexpr int v = V;
                     if (c0 + v < a.cout) o[(size_t)(c0 + v) * HWo] = y[v];
                 });
@@ -182,28 +261,35 @@ __global__ __launch_bounds__(256) void conv_stem_kernel(const ConvArgs a) {
 }
 
 bool conv_stem_supported(const ConvArgs &a) {
-    return a.Cin == 8 && a.in_cs == 8 && a.k_splits <= 1 && a.kh * a.kw <= 64 && a.zero &&
+    return a.Cin == 8 && a.in_cs == 8 && a.k_splits <= 1 && a.kh * a.kw <= 64 && a.zero && a.uni_affine &&
            (a.out_mode == OUT_NHWC || a.out_mode == OUT_NCHW_F32);
 }
 
 hipError_t launch_conv_stem(const ConvArgs &a, const Sink &sk) {
     if (!conv_stem_supported(a) || a.M <= 0 || a.N <= 0 || a.N % 8 || a.nseg < 1 || a.nseg > GEMEL_MAX_SEG)
         return hipErrorInvalidValue;
-    if (a.K != a.kh * a.kw * 8 || a.out_cs < a.N || a.out_cs % 4 || a.seg[0].m_start != 0) return hipErrorInvalidValue;
+    if (a.K != a.kh * a.kw * 8 || a.out_cs < a.N || a.out_cs % 8 || a.seg[0].m_start != 0) return hipErrorInvalidValue;
     if (a.out_mode == OUT_NCHW_F32 && a.cout > a.N) return hipErrorInvalidValue;
     for (int i = 0; i < a.nseg; ++i) {
         const ConvSeg &s = a.seg[i];
         if (!s.in || !s.out || !s.scale || !s.shift || (a.has_res && !s.res)) return hipErrorInvalidValue;
         if (s.m_start != s.f_start * a.Ho * a.Wo || (i && s.m_start < a.seg[i - 1].m_start)) return hipErrorInvalidValue;
     }
-    // 32 output channels per tile: the pixel loads of a wider tile would be
-    // re-used across more MFMAs, but its registers spill
-    constexpr int NF = 2;
-    const long tiles = (long)((a.M + STEM_PX - 1) / STEM_PX) * ((a.N + NF * 16 - 1) / (NF * 16));
+    // up to 32 channels: 4 pixel fragments x 2 channel fragments per wave;
+    // more: 2 x 4 (a wider tile holds its pixels' whole output rows; 4 x 4
+    // would spill registers)
+    const bool narrow = a.N <= 32;
+    const int px = narrow ? 256 : 128, bn = narrow ? 32 : 64;
+    const long tiles = (long)((a.M + px - 1) / px) * ((a.N + bn - 1) / bn);
     const long blocks = tiles >= 8 ? (tiles + 7) / 8 * 8 : tiles;
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
     const dim3 grid((unsigned)blocks), block(256);
-    return submit(sk, reinterpret_cast<const void *>(&conv_stem_kernel<NF>), grid, block, a);
+    const bool three = (a.kh * a.kw + 3) / 4 == 3;   // 9..12 taps: three depth steps
+    const void *k = narrow ? (three ? reinterpret_cast<const void *>(&conv_stem_kernel<4, 2, 3>)
+                                    : reinterpret_cast<const void *>(&conv_stem_kernel<4, 2, 0>))
+                           : (three ? reinterpret_cast<const void *>(&conv_stem_kernel<2, 4, 3>)
+                                    : reinterpret_cast<const void *>(&conv_stem_kernel<2, 4, 0>));
+    return submit(sk, k, grid, block, a);
 }
 
 }  // namespace gemel

@@ -51,7 +51,8 @@ enum ConvTile {
     TILE_DMA_256x128 = 10, // 4 waves, 128x64 per wave
     TILE_DMA_128x128 = 11, // 4 waves, 64x64 per wave
     TILE_DMA_128x64 = 12,  // 2 waves, 64x64 per wave
-    // 8-channel inputs (k_stem.hip): 256 pixels x 32 channels, no LDS
+    // 8-channel inputs (k_stem.hip): 128 pixels x 64 channels (256 x 32
+    // when N <= 32), no LDS
     TILE_STEM = 13,
     TILE_COUNT = 14
 };

@@ -828,7 +828,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 if (bf16) {
                     const bool dma_ok = a.Cin % 32 == 0 && a.in_cs % 8 == 0 && a.uni_affine;
                     // 8-channel inputs (the RGB stems) take the stem kernel
-                    const bool stem = a.Cin == 8 && a.in_cs == 8 && a.kh * a.kw <= 64 &&
+                    const bool stem = a.Cin == 8 && a.in_cs == 8 && a.kh * a.kw <= 64 && a.uni_affine &&
                                       (ctx->opt.conv_tile < 0 || ctx->opt.conv_tile == TILE_STEM);
                     if (stem) {
                         Lc.tile = TILE_STEM;

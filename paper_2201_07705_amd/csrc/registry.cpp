@@ -383,6 +383,7 @@ gemel_status gemel_query(gemel_ctx *ctx, int32_t key, int64_t *val) {
     case GEMEL_Q_LAUNCHES: *val = ctx->last_plan ? (int64_t)ctx->last_plan->launches.size() : 0; break;
     case GEMEL_Q_N_MODELS: *val = (int64_t)ctx->models.size(); break;
     case GEMEL_Q_GRAPH_REPLAYS: *val = ctx->graph_replays; break;
+    case GEMEL_Q_STREAMS: *val = ctx->opt.streams; break;
     default: return fail(ctx, GEMEL_EINVAL, "unknown query key");
     }
     return GEMEL_OK;
