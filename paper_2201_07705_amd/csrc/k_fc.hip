@@ -76,26 +76,41 @@ __global__ __launch_bounds__(256) void fc_bf16_kernel(const FcArgs a) {
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    if (n0 < a.N) {
-        for (int k = k_begin; k < k_end; k += 128) {
-            uint4 wv[4];
+    // depth steps of 256: 8 weight chunks of 16 bytes per lane (lane g of a
+    // row covers 32 contiguous bytes of every 128), the next step's weights
+    // loaded while the current step's MFMAs run
+    constexpr int KS = 256, WJ = KS / 32;
+    auto wload = [&](int k, uint4 (&wv)[WJ]) __attribute__((always_inline)) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int kk = k + g * 32 + j * 8;
-                wv[j] = (row_ok && kk < k_end) ? *(const uint4 *)(wrow + kk) : make_uint4(0, 0, 0, 0);
+        for (int j = 0; j < WJ; ++j) {
+            const int kk = k + j * 32 + g * 8;
+            wv[j] = (row_ok && kk < k_end) ? *(const uint4 *)(wrow + kk) : make_uint4(0, 0, 0, 0);
+        }
+    };
+    auto step = [&](int k, const uint4 (&wv)[WJ]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            uint4 xv[WJ];
+#pragma unroll
+            for (int j = 0; j < WJ; ++j) {
+                const int kk = k + j * 32 + g * 8;
+                xv[j] = (xrow[mb] && kk < k_end) ? *(const uint4 *)(xrow[mb] + kk) : make_uint4(0, 0, 0, 0);
             }
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb) {
-                uint4 xv[4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int kk = k + g * 32 + j * 8;
-                    xv[j] = (xrow[mb] && kk < k_end) ? *(const uint4 *)(xrow[mb] + kk) : make_uint4(0, 0, 0, 0);
-                }
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        __builtin_bit_cast(bf16x8, wv[j]), __builtin_bit_cast(bf16x8, xv[j]), acc[mb], 0, 0, 0);
+            for (int j = 0; j < WJ; ++j)
+                acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    __builtin_bit_cast(bf16x8, wv[j]), __builtin_bit_cast(bf16x8, xv[j]), acc[mb], 0, 0, 0);
+        }
+    };
+    if (n0 < a.N) {
+        uint4 w0[WJ], w1[WJ];
+        wload(k_begin, w0);
+        for (int k = k_begin; k < k_end; k += 2 * KS) {
+            if (k + KS < k_end) wload(k + KS, w1);
+            step(k, w0);
+            if (k + KS < k_end) {
+                if (k + 2 * KS < k_end) wload(k + 2 * KS, w0);
+                step(k + KS, w1);
             }
         }
     }

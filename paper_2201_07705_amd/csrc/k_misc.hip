@@ -93,28 +93,39 @@ __global__ __launch_bounds__(256) void maxpool_kernel(const EwArgs a) {
     store8((T *)sg.out + idx * 8, m);
 }
 
-// Global average pool: [f][H][W][C] -> [f][C], fp32 sum.
+// Global average pool: [f][H][W][C] -> [f][C], fp32 sums. A workgroup
+// covers one frame and 64 8-channel chunks; its 4 waves take every 4th
+// pixel (independent loads in flight), and the 4 partial sums meet in LDS.
+// Grid: x = frames * ceil(chunks / 64), y = segment.
 template <typename T>
 __global__ __launch_bounds__(256) void avgpool_kernel(const EwArgs a) {
+    __shared__ float part[4][64][9];
     const EwSeg &sg = a.seg[blockIdx.y];
-    const int ch = a.C / 8;
-    const long idx = (long)blockIdx.x * 256 + threadIdx.x;
-    if (idx >= (long)sg.frames * ch) return;
-    const long f = idx / ch;
-    const int cc = (int)(idx - f * ch);
+    const int ch = a.C / 8, cblocks = (ch + 63) / 64;
+    const long f = blockIdx.x / cblocks;
+    if (f >= sg.frames) return;
+    const int lane = threadIdx.x & 63, pg = threadIdx.x >> 6;
+    const int cc = (int)(blockIdx.x - f * cblocks) * 64 + lane;
     const long hw = (long)a.H * a.W;
-    const T *in = (const T *)sg.in0 + f * hw * a.C + cc * 8;
     float s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    for (long p = 0; p < hw; ++p) {
-        float v[8];
-        load8(in + p * a.C, v);
+    if (cc < ch) {
+        const T *in = (const T *)sg.in0 + f * hw * a.C + cc * 8;
+        for (long p = pg; p < hw; p += 4) {
+            float v[8];
+            load8(in + p * a.C, v);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) s[j] += v[j];
+            for (int j = 0; j < 8; ++j) s[j] += v[j];
+        }
     }
-    const float inv = 1.0f / (float)hw;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) s[j] *= inv;
-    store8((T *)sg.out + f * a.C + cc * 8, s);
+    for (int j = 0; j < 8; ++j) part[pg][lane][j] = s[j];
+    __syncthreads();
+    if (pg == 0 && cc < ch) {
+        const float inv = 1.0f / (float)hw;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) s[j] = (part[0][lane][j] + part[1][lane][j] + part[2][lane][j] + part[3][lane][j]) * inv;
+        store8((T *)sg.out + f * a.C + cc * 8, s);
+    }
 }
 
 // Nearest-neighbour 2x upsample.
@@ -149,23 +160,26 @@ __global__ __launch_bounds__(256) void concat_kernel(const EwArgs a) {
 }
 
 // Internal NHWC (C physical) -> caller NCHW f32 with c_logical channels.
+// One thread per (frame, 8-channel chunk, pixel), pixels fastest: a 16-byte
+// load of the pixel's 8 channels, then 8 plane writes that consecutive
+// threads make to consecutive addresses.
 template <typename T>
 __global__ __launch_bounds__(256) void export_kernel(const EwArgs a) {
     const EwSeg &sg = a.seg[blockIdx.y];
     const long hw = (long)a.H * a.W;
+    const int ch = (a.c_logical + 7) / 8;
     const long idx = (long)blockIdx.x * 256 + threadIdx.x;
-    if (idx >= (long)sg.frames * a.c_logical * hw) return;
+    if (idx >= (long)sg.frames * ch * hw) return;
     const long p = idx % hw;
     const long t = idx / hw;
-    const int c = (int)(t % a.c_logical);
-    const long f = t / a.c_logical;
-    const T v = ((const T *)sg.in0)[(f * hw + p) * a.C + c];
-    float x;
-    if constexpr (sizeof(T) == 2)
-        x = m_bf2f(v);
-    else
-        x = v;
-    ((float *)sg.out)[idx] = x;
+    const int cc = (int)(t % ch);
+    const long f = t / ch;
+    float v[8];
+    load8((const T *)sg.in0 + (f * hw + p) * a.C + cc * 8, v);
+    float *o = (float *)sg.out + (f * a.c_logical + cc * 8) * hw + p;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        if (cc * 8 + j < a.c_logical) o[j * hw] = v[j];
 }
 
 static bool ew_ok(const EwArgs &a, bool need_in1) {
@@ -201,8 +215,12 @@ hipError_t launch_maxpool(const EwArgs &a, bool bf16, const Sink &sk) {
 
 hipError_t launch_avgpool(const EwArgs &a, bool bf16, const Sink &sk) {
     if (!ew_ok(a, false) || a.C % 8 || a.H <= 0 || a.W <= 0) return hipErrorInvalidValue;
-    const long per = a.C / 8;
-    return bf16 ? ew_launch(reinterpret_cast<const void *>(&avgpool_kernel<u16>), per, a, sk) : ew_launch(reinterpret_cast<const void *>(&avgpool_kernel<float>), per, a, sk);
+    const long blocks = (long)a.max_frames * ((a.C / 8 + 63) / 64);
+    if (blocks <= 0) return hipSuccess;
+    if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
+    const void *k = bf16 ? reinterpret_cast<const void *>(&avgpool_kernel<u16>)
+                         : reinterpret_cast<const void *>(&avgpool_kernel<float>);
+    return submit(sk, k, dim3((unsigned)blocks, (unsigned)a.nseg), dim3(256), a);
 }
 
 hipError_t launch_upsample2x(const EwArgs &a, bool bf16, const Sink &sk) {
@@ -219,7 +237,7 @@ hipError_t launch_concat(const EwArgs &a, bool bf16, const Sink &sk) {
 
 hipError_t launch_export(const EwArgs &a, bool bf16, const Sink &sk) {
     if (!ew_ok(a, false) || a.c_logical > a.C || a.c_logical <= 0) return hipErrorInvalidValue;
-    const long per = (long)a.c_logical * a.H * a.W;
+    const long per = (long)((a.c_logical + 7) / 8) * a.H * a.W;
     return bf16 ? ew_launch(reinterpret_cast<const void *>(&export_kernel<u16>), per, a, sk) : ew_launch(reinterpret_cast<const void *>(&export_kernel<float>), per, a, sk);
 }
 
