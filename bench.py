@@ -197,6 +197,8 @@ def main():
 
     streamed = ctx.query(G.Q_STREAMED_BYTES)
     launches = ctx.query(G.Q_LAUNCHES)
+    round_mode = ["enqueue", "stream_segments", "data_graph", "stream_graph"][
+        ctx.query(G.Q_ROUND_MODE)]
 
     # per-kernel-family HIP-event timings (separate, untimed passes): on one
     # stream (each kernel alone on the GPU: the roofline figure, comparable
@@ -271,6 +273,7 @@ def main():
         "event_ms_per_step": ev_ms / args.steps,
         "roofline": roof, "roofline_concurrent": roof_conc, "kernels": kern,
         "cpu_baseline": cpu,
+        "round_mode": round_mode,
         "streamed_bytes_per_step": streamed,
         "launches_per_step": launches,
     }

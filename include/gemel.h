@@ -228,7 +228,11 @@ enum {
     GEMEL_Q_LAUNCHES = 6,       /* kernel launches per round, last plan   */
     GEMEL_Q_N_MODELS = 7,       /* registered models                      */
     GEMEL_Q_GRAPH_REPLAYS = 8,  /* rounds served by a replayed HIP graph  */
-    GEMEL_Q_STREAMS = 9         /* GEMEL_OPT_STREAMS now in force         */
+    GEMEL_Q_STREAMS = 9,        /* GEMEL_OPT_STREAMS now in force         */
+    GEMEL_Q_ROUND_MODE = 10     /* how the last round ran: 0 enqueued
+                                   directly, 1 per-stream chain graphs,
+                                   2 one graph with data edges, 3 one graph
+                                   with data edges and stream order       */
 };
 
 /* Read a counter. Errors: EINVAL (unknown key, null val). */

@@ -204,6 +204,7 @@ struct gemel_ctx {
     size_t resident_bytes = 0, peak_bytes = 0;
     int64_t copies_issued = 0;
     int64_t graph_replays = 0;
+    int last_mode = 0;   // execution mode of the last round (GEMEL_Q_ROUND_MODE)
     std::map<std::vector<int>, std::unique_ptr<gemel::Plan>> plans;
     gemel::Plan *last_plan = nullptr;
     gemel::Profile prof;

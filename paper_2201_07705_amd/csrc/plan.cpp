@@ -1319,6 +1319,7 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
     }
     const bool graphable = will_graph && P.chunks.empty();
     if (!graphable) {
+        ctx->last_mode = MODE_EAGER;
         st = enqueue(ctx, P, cp, stream);
         if (!st && ctx->opt.profile) ctx->prof.rounds++;
         return st;
@@ -1374,6 +1375,7 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         st = build_graph(ctx, P, cp, all, mode == MODE_DAG ? EDGES_DATA : EDGES_STREAMS, &P.graph[mode == MODE_DAG ? 0 : 1]);
         if (st) return st;
     }
+    ctx->last_mode = mode;
     if (timed) HIPCHK(hipEventRecord(P.tune_ev[0], stream), "hipEventRecord");
     if (mode == MODE_EAGER) {
         st = enqueue(ctx, P, cp, stream);

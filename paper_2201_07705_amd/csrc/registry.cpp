@@ -384,6 +384,7 @@ gemel_status gemel_query(gemel_ctx *ctx, int32_t key, int64_t *val) {
     case GEMEL_Q_N_MODELS: *val = (int64_t)ctx->models.size(); break;
     case GEMEL_Q_GRAPH_REPLAYS: *val = ctx->graph_replays; break;
     case GEMEL_Q_STREAMS: *val = ctx->opt.streams; break;
+    case GEMEL_Q_ROUND_MODE: *val = ctx->last_mode; break;
     default: return fail(ctx, GEMEL_EINVAL, "unknown query key");
     }
     return GEMEL_OK;
