@@ -123,6 +123,10 @@ def main():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device to device once (the "
                          "reference kernel for byte-counter scaling)")
+    ap.add_argument("--option", action="append", default=[],
+                    metavar="NAME=VALUE",
+                    help="library option set before the first round, e.g. "
+                         "SPLITK_FUSED=0 (repeatable)")
     ap.add_argument("--sources-hash", action="store_true",
                     help="print the hash recorded with traffic figures")
     args = ap.parse_args()
@@ -159,6 +163,11 @@ def main():
     ids = [ctx.register_model(m.layers, params[i], m.in_chw)
            for i, m in enumerate(wl.models)]
     ctx.merge([[(ids[a], b) for a, b in g] for g in wl.groups])
+    options = {}
+    for o in args.option:
+        name, _, value = o.partition("=")
+        ctx.set_option(getattr(G, "OPT_" + name.upper()), int(value))
+        options[name.upper()] = int(value)
     budget = 0
     if wl.budget_frac:
         budget = int(wl.budget_frac * ctx.query(G.Q_UNMERGED_BYTES))
@@ -276,6 +285,7 @@ def main():
         "round_mode": round_mode,
         "streamed_bytes_per_step": streamed,
         "launches_per_step": launches,
+        "options": options,
     }
     ctx.close()
     print(json.dumps(line), flush=True)

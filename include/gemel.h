@@ -298,7 +298,7 @@ enum {
                                     at this many microseconds or more
                                     (default 30), or spans 3 or more
                                     launch steps                           */
-    GEMEL_OPT_AUTOTUNE = 12      /* 1 (default): the first 12 rounds of a
+    GEMEL_OPT_AUTOTUNE = 12,     /* 1 (default): the first 12 rounds of a
                                     graphable plan over several streams try
                                     the two graph forms of GEMEL_OPT_GRAPH_DAG,
                                     one graph with data edges plus each
@@ -311,6 +311,16 @@ enum {
                                     while the caller's stream is being
                                     captured. 0: the mode set by
                                     GEMEL_OPT_GRAPH_DAG                    */
+    GEMEL_OPT_SPLITK_FUSED = 13  /* how split-K layers reduce their fp32
+                                    partial sums: 1 (default) inside the
+                                    GEMM launch (the last split of each
+                                    output tile to finish sums the tile and
+                                    applies the epilogue) for FC layers and
+                                    for convs of 256 output tiles or more,
+                                    else in a separate reduction launch;
+                                    2: inside the GEMM launch always; 0: in
+                                    a separate launch always. Every form
+                                    sums in split order: same bits         */
 };
 
 /* Set an option; takes effect at the next gemel_infer. Errors: EINVAL. */

@@ -1,0 +1,179 @@
+// Device helpers shared by the implicit-GEMM conv kernels: the fused
+// epilogue (per-channel scale/shift, residual before or after the
+// activation, ReLU / leaky ReLU, bf16 NHWC or fp32 NCHW stores), the
+// segment lookup of a GEMM row, and the fused split-K reduction.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include "kargs.h"
+#include "splitk.h"
+
+namespace gemel {
+
+typedef unsigned short u16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf2f(u16 h) {
+    return __uint_as_float((uint32_t)h << 16);
+}
+__device__ __forceinline__ u16 f2bf(float f) {
+    return __builtin_bit_cast(u16, (__bf16)f);
+}
+__device__ __forceinline__ float act_fn(float y, int act, float slope) {
+    if (act == 1) return fmaxf(y, 0.f);
+    if (act == 2) return y > 0.f ? y : y * slope;
+    return y;
+}
+__device__ __forceinline__ float epi(float z, float r, int has_res,
+                                     int res_mode, int act, float slope) {
+    if (!has_res) return act_fn(z, act, slope);
+    if (res_mode == 0) return act_fn(z + r, act, slope);
+    return act_fn(z, act, slope) + r;
+}
+
+// Segment of GEMM row gm: the last segment whose m_start <= gm.
+template <typename Args>
+__device__ __forceinline__ int seg_of_row(const Args &a, int gm) {
+    int s = 0;
+    for (int i = 1; i < a.nseg; ++i) s += (gm >= a.seg[i].m_start) ? 1 : 0;
+    return s;
+}
+
+// Scalars of the fused epilogue.
+struct Epi {
+    int out_cs, cout, act, res_mode, has_res, HWo;
+    float slope;
+};
+template <typename Args>
+__device__ __forceinline__ Epi epi_of(const Args &a, int HWo) {
+    Epi e;
+    e.out_cs = a.out_cs; e.cout = a.cout; e.act = a.act; e.res_mode = a.res_mode;
+    e.has_res = a.has_res; e.HWo = HWo; e.slope = a.slope;
+    return e;
+}
+
+// Epilogue of 8 consecutive channels [gn, gn+8) of row gm into NHWC bf16.
+__device__ __forceinline__ void store8_nhwc_bf16(const ConvSeg &sg, const Epi &e,
+                                                 int gm, int gn, const float *v) {
+    const size_t off = (size_t)(gm - sg.m_start) * e.out_cs + gn;
+    const float4 sc0 = *(const float4 *)(sg.scale + gn);
+    const float4 sc1 = *(const float4 *)(sg.scale + gn + 4);
+    const float4 sh0 = *(const float4 *)(sg.shift + gn);
+    const float4 sh1 = *(const float4 *)(sg.shift + gn + 4);
+    const float sc[8] = {sc0.x, sc0.y, sc0.z, sc0.w, sc1.x, sc1.y, sc1.z, sc1.w};
+    const float sh[8] = {sh0.x, sh0.y, sh0.z, sh0.w, sh1.x, sh1.y, sh1.z, sh1.w};
+    u16 rv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (e.has_res) {
+        const uint4 r4 = *(const uint4 *)((const u16 *)sg.res + off);
+        const u16 *rp = (const u16 *)&r4;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) rv[j] = rp[j];
+    }
+    uint4 o;
+    u16 *op = (u16 *)&o;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const float z = v[j] * sc[j] + sh[j];
+        op[j] = f2bf(epi(z, bf2f(rv[j]), e.has_res, e.res_mode, e.act, e.slope));
+    }
+    *(uint4 *)((u16 *)sg.out + off) = o;
+}
+
+// Epilogue of 8 consecutive channels of row gm into NHWC fp32.
+__device__ __forceinline__ void store8_nhwc_f32(const ConvSeg &sg, const Epi &e,
+                                                int gm, int gn, const float *v) {
+    const size_t off = (size_t)(gm - sg.m_start) * e.out_cs + gn;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const float r = e.has_res ? ((const float *)sg.res)[off + j] : 0.f;
+        const float z = v[j] * sg.scale[gn + j] + sg.shift[gn + j];
+        ((float *)sg.out)[off + j] = epi(z, r, e.has_res, e.res_mode, e.act, e.slope);
+    }
+}
+
+// Epilogue of one element into a caller-owned fp32 NCHW output.
+template <bool BF16>
+__device__ __forceinline__ void store1_nchw_f32(const ConvSeg &sg, const Epi &e,
+                                                int gm, int gn, float v) {
+    if (gn >= e.cout) return;
+    const int lr = gm - sg.m_start;
+    const int f = lr / e.HWo, pix = lr - f * e.HWo;
+    float r = 0.f;
+    if (e.has_res) {
+        const size_t roff = (size_t)lr * e.out_cs + gn;
+        r = BF16 ? bf2f(((const u16 *)sg.res)[roff]) : ((const float *)sg.res)[roff];
+    }
+    const float z = v * sg.scale[gn] + sg.shift[gn];
+    ((float *)sg.out)[((size_t)f * e.cout + gn) * e.HWo + pix] =
+        epi(z, r, e.has_res, e.res_mode, e.act, e.slope);
+}
+
+// Fused split-K reduction of output tile `tile` (rows [m0, m0 + bm),
+// columns [n0, n0 + bn)): the last split to arrive sums the partials in
+// split order and applies the epilogue with the arithmetic of the separate
+// reduction kernel, so both give the same bits. The launcher guarantees
+// that the partial sums span less than 2^31 bytes.
+template <int NT>
+__device__ __forceinline__ void splitk_fixup(const ConvArgs &a, int tile, int m0, int bm, int n0, int bn,
+                                             int *flag) {
+    if (!splitk_arrive(a.counters + tile, a.k_splits, flag)) return;
+    const Epi e = epi_of(a, a.Ho * a.Wo);
+    const __amdgpu_buffer_rsrc_t pr = partial_rsrc(a.partial, (uint32_t)a.k_splits * a.M * a.N * 4u);
+    const int chunks = bn / 8, items = bm * chunks;
+    const uint32_t split_bytes = (uint32_t)a.M * a.N * 4u;
+    // two items per thread and four splits per batch: the 16 loads of a
+    // batch are issued together, then summed in split order
+    for (int i0 = threadIdx.x; i0 < items; i0 += 2 * NT) {
+        int gm[2], gn[2];
+        bool ok[2];
+        uint32_t off[2];
+        float v[2][8];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int item = i0 + u * NT;
+            const int rl = item / chunks;
+            gm[u] = m0 + rl;
+            gn[u] = n0 + (item - rl * chunks) * 8;
+            ok[u] = item < items && gm[u] < a.M && gn[u] < a.N;
+            off[u] = ok[u] ? (uint32_t)((gm[u] * a.N + gn[u]) * 4u) : 0u;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[u][j] = 0.f;
+        }
+        for (int sp0 = 0; sp0 < a.k_splits; sp0 += 4) {
+            float4 p[2][4][2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    if (ok[u] && sp0 + q < a.k_splits) {
+                        const uint32_t o = off[u] + (uint32_t)(sp0 + q) * split_bytes;
+                        p[u][q][0] = load_partial4(pr, o);
+                        p[u][q][1] = load_partial4(pr, o + 16);
+                    }
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    if (ok[u] && sp0 + q < a.k_splits) {
+                        v[u][0] += p[u][q][0].x; v[u][1] += p[u][q][0].y;
+                        v[u][2] += p[u][q][0].z; v[u][3] += p[u][q][0].w;
+                        v[u][4] += p[u][q][1].x; v[u][5] += p[u][q][1].y;
+                        v[u][6] += p[u][q][1].z; v[u][7] += p[u][q][1].w;
+                    }
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            if (!ok[u]) continue;
+            const ConvSeg &sg = a.seg[seg_of_row(a, gm[u])];
+            if (a.out_mode == OUT_NHWC) {
+                store8_nhwc_bf16(sg, e, gm[u], gn[u], v[u]);
+            } else {
+                for (int j = 0; j < 8; ++j) store1_nchw_f32<true>(sg, e, gm[u], gn[u] + j, v[u][j]);
+            }
+        }
+    }
+}
+
+}  // namespace gemel

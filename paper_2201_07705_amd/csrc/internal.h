@@ -85,6 +85,7 @@ struct Launch {
     std::vector<Patch> patches;
     // weight streaming: >= 0 when the weights come from a staging slot
     int chunk = -1;
+    int ctr_n = 0;  // arrival counters of a fused split-K launch
     // concurrency: stream index, plan events waited for before the launch,
     // plan event recorded after it (-1 = none)
     int stream = 0;
@@ -132,6 +133,9 @@ struct Plan {
     // concurrently get disjoint regions
     float *partial = nullptr;
     size_t partial_bytes = 0;
+    // arrival counters of the fused split-K reductions, a disjoint range per
+    // launch (never shared: a counter must read zero when its launch starts)
+    int32_t *counters = nullptr;
     size_t streamed_bytes = 0;
     // HIP graphs of the round for one set of caller pointers: one chain per
     // segment; one graph whose edges are the launches' data dependencies; one
@@ -172,6 +176,7 @@ struct Options {
     int graph_dag = 0;
     int autotune = 1;
     int fork_us = 30;
+    int splitk_fused = 1;
     int64_t slot_bytes = 32ll << 20;
     int slots = 3;
     int64_t fail_copy_at = 0;

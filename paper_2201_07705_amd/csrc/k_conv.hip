@@ -14,117 +14,19 @@
 // LDS and applies per-channel scale/shift (bias and batch norm), the
 // residual (before or after the activation) and ReLU / leaky ReLU, then
 // writes bf16 NHWC with 16-byte stores (or fp32 NCHW for model outputs).
-// With k_splits > 1 each split writes fp32 partial sums instead and
-// conv_reduce applies the epilogue.
+// With k_splits > 1 each split writes fp32 partial sums instead; the last
+// split of a tile to finish reduces them and applies the epilogue
+// (splitk_fixup), or, without arrival counters, conv_reduce does.
 //
 // conv_f32: direct convolution in fp32 FMA (no reduced-precision products)
 // for float32 contexts.
 #include <hip/hip_runtime.h>
 
+#include "conv_epi.h"
 #include "kargs.h"
 #include "kernels.h"
 
 namespace gemel {
-
-typedef unsigned short u16;
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ float bf2f(u16 h) {
-    return __uint_as_float((uint32_t)h << 16);
-}
-__device__ __forceinline__ u16 f2bf(float f) {
-    return __builtin_bit_cast(u16, (__bf16)f);
-}
-__device__ __forceinline__ float act_fn(float y, int act, float slope) {
-    if (act == 1) return fmaxf(y, 0.f);
-    if (act == 2) return y > 0.f ? y : y * slope;
-    return y;
-}
-__device__ __forceinline__ float epi(float z, float r, int has_res,
-                                     int res_mode, int act, float slope) {
-    if (!has_res) return act_fn(z, act, slope);
-    if (res_mode == 0) return act_fn(z + r, act, slope);
-    return act_fn(z, act, slope) + r;
-}
-
-// Segment of GEMM row gm: the last segment whose m_start <= gm.
-template <typename Args>
-__device__ __forceinline__ int seg_of_row(const Args &a, int gm) {
-    int s = 0;
-    for (int i = 1; i < a.nseg; ++i) s += (gm >= a.seg[i].m_start) ? 1 : 0;
-    return s;
-}
-
-// Scalars of the fused epilogue.
-struct Epi {
-    int out_cs, cout, act, res_mode, has_res, HWo;
-    float slope;
-};
-template <typename Args>
-__device__ __forceinline__ Epi epi_of(const Args &a, int HWo) {
-    Epi e;
-    e.out_cs = a.out_cs; e.cout = a.cout; e.act = a.act; e.res_mode = a.res_mode;
-    e.has_res = a.has_res; e.HWo = HWo; e.slope = a.slope;
-    return e;
-}
-
-// Epilogue of 8 consecutive channels [gn, gn+8) of row gm into NHWC bf16.
-__device__ __forceinline__ void store8_nhwc_bf16(const ConvSeg &sg, const Epi &e,
-                                                 int gm, int gn, const float *v) {
-    const size_t off = (size_t)(gm - sg.m_start) * e.out_cs + gn;
-    const float4 sc0 = *(const float4 *)(sg.scale + gn);
-    const float4 sc1 = *(const float4 *)(sg.scale + gn + 4);
-    const float4 sh0 = *(const float4 *)(sg.shift + gn);
-    const float4 sh1 = *(const float4 *)(sg.shift + gn + 4);
-    const float sc[8] = {sc0.x, sc0.y, sc0.z, sc0.w, sc1.x, sc1.y, sc1.z, sc1.w};
-    const float sh[8] = {sh0.x, sh0.y, sh0.z, sh0.w, sh1.x, sh1.y, sh1.z, sh1.w};
-    u16 rv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    if (e.has_res) {
-        const uint4 r4 = *(const uint4 *)((const u16 *)sg.res + off);
-        const u16 *rp = (const u16 *)&r4;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) rv[j] = rp[j];
-    }
-    uint4 o;
-    u16 *op = (u16 *)&o;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const float z = v[j] * sc[j] + sh[j];
-        op[j] = f2bf(epi(z, bf2f(rv[j]), e.has_res, e.res_mode, e.act, e.slope));
-    }
-    *(uint4 *)((u16 *)sg.out + off) = o;
-}
-
-// Epilogue of 8 consecutive channels of row gm into NHWC fp32.
-__device__ __forceinline__ void store8_nhwc_f32(const ConvSeg &sg, const Epi &e,
-                                                int gm, int gn, const float *v) {
-    const size_t off = (size_t)(gm - sg.m_start) * e.out_cs + gn;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const float r = e.has_res ? ((const float *)sg.res)[off + j] : 0.f;
-        const float z = v[j] * sg.scale[gn + j] + sg.shift[gn + j];
-        ((float *)sg.out)[off + j] = epi(z, r, e.has_res, e.res_mode, e.act, e.slope);
-    }
-}
-
-// Epilogue of one element into a caller-owned fp32 NCHW output.
-template <bool BF16>
-__device__ __forceinline__ void store1_nchw_f32(const ConvSeg &sg, const Epi &e,
-                                                int gm, int gn, float v) {
-    if (gn >= e.cout) return;
-    const int lr = gm - sg.m_start;
-    const int f = lr / e.HWo, pix = lr - f * e.HWo;
-    float r = 0.f;
-    if (e.has_res) {
-        const size_t roff = (size_t)lr * e.out_cs + gn;
-        r = BF16 ? bf2f(((const u16 *)sg.res)[roff]) : ((const float *)sg.res)[roff];
-    }
-    const float z = v * sg.scale[gn] + sg.shift[gn];
-    ((float *)sg.out)[((size_t)f * e.cout + gn) * e.HWo + pix] =
-        epi(z, r, e.has_res, e.res_mode, e.act, e.slope);
-}
 
 // Implicit-GEMM tile kernel. BM x BN output tile, WM x WN waves (each a
 // (BM/WM) x (BN/WN) wave tile of 16x16 MFMA blocks), depth 64 per step.
@@ -376,15 +278,15 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a
         const int row0 = pass * TM;
         const int nrows = min(EPI_ROWS, BM - row0);
         if (a.k_splits > 1) {
-            float *P = a.partial + (size_t)blockIdx.y * a.M * a.N;
+            const __amdgpu_buffer_rsrc_t pr = partial_rsrc(a.partial, (uint32_t)a.k_splits * a.M * a.N * 4u);
             for (int item = tid; item < nrows * CH; item += NT) {
                 const int rl = item / CH, ch = item - (item / CH) * CH;
                 const int gm = tm * BM + row0 + rl, gn = tn * BN + ch * 8;
                 if (gm >= a.M || gn >= a.N) continue;
                 const float *src = Cs + rl * LDC + ch * 8;
-                float4 *dst = (float4 *)(P + (size_t)gm * a.N + gn);
-                dst[0] = *(const float4 *)src;
-                dst[1] = *(const float4 *)(src + 4);
+                const uint32_t off = (uint32_t)((((int)blockIdx.y * a.M + gm) * a.N + gn) * 4u);
+                store_partial4(pr, off, *(const float4 *)src);
+                store_partial4(pr, off + 16, *(const float4 *)(src + 4));
             }
         } else if (a.out_mode == OUT_NHWC) {
             for (int item = tid; item < nrows * CH; item += NT) {
@@ -447,6 +349,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a
         }
         __syncthreads();
     }
+    if (a.k_splits > 1 && a.counters) splitk_fixup<NT>(a, t, tm * BM, BM, tn * BN, BN, (int *)smem);
 }
 
 // Split-K reduction: sum the partial tiles, then the same epilogue.
@@ -530,12 +433,13 @@ static bool conv_args_ok(const ConvArgs &a) {
     if (a.seg[0].m_start != 0) return false;
     for (int i = 0; i < a.nseg; ++i) {
         if (!a.seg[i].in || !a.seg[i].scale || !a.seg[i].shift) return false;
-        if (a.k_splits <= 1 && !a.seg[i].out) return false;
+        if ((a.k_splits <= 1 || a.counters) && !a.seg[i].out) return false;
         if (a.has_res && !a.seg[i].res) return false;
         if (i && a.seg[i].m_start < a.seg[i - 1].m_start) return false;
         if (a.seg[i].m_start != a.seg[i].f_start * a.Ho * a.Wo) return false;
     }
     if (a.k_splits > 1 && (!a.partial || a.k_per_split % CONV_BK)) return false;
+    if (a.k_splits > 1 && (long)a.k_splits * a.M * a.N * 4 > 0x7fffffffL) return false;
     if (a.k_per_split <= 0 || (long)a.k_per_split * a.k_splits < a.K) return false;
     if (a.out_mode == OUT_NCHW_F32 && a.cout > a.N) return false;
     return true;

@@ -24,6 +24,7 @@
 
 #include <type_traits>
 
+#include "conv_epi.h"
 #include "kargs.h"
 #include "kernels.h"
 
@@ -31,29 +32,7 @@ namespace gemel {
 
 namespace {
 
-typedef unsigned short u16;
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) unsigned char lds_u8;
-
-__device__ __forceinline__ float d_bf2f(u16 h) { return __uint_as_float((uint32_t)h << 16); }
-__device__ __forceinline__ u16 d_f2bf(float f) { return __builtin_bit_cast(u16, (__bf16)f); }
-__device__ __forceinline__ float d_act(float y, int act, float slope) {
-    if (act == 1) return fmaxf(y, 0.f);
-    if (act == 2) return y > 0.f ? y : y * slope;
-    return y;
-}
-__device__ __forceinline__ float d_epi(float z, float r, int has_res, int res_mode, int act, float slope) {
-    if (!has_res) return d_act(z, act, slope);
-    if (res_mode == 0) return d_act(z + r, act, slope);
-    return d_act(z, act, slope) + r;
-}
-__device__ __forceinline__ int d_seg(const ConvArgs &a, int gm) {
-    int s = 0;
-    for (int i = 1; i < a.nseg; ++i) s += (gm >= a.seg[i].m_start) ? 1 : 0;
-    return s;
-}
 
 // Calls f(std::integral_constant<int, i>) for i = 0 .. I-1 with a
 // compile-time i, so that register arrays are indexed statically.
@@ -146,7 +125,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
             if (one_seg) {
                 abase[i] = (const u16 *)useg.in + (size_t)(fr - useg.f_start) * frame_elems;
             } else {
-                const int sg = d_seg(a, gm);
+                const int sg = seg_of_row(a, gm);
                 abase[i] = (const u16 *)a.seg[sg].in + (size_t)(fr - a.seg[sg].f_start) * frame_elems;
             }
             ahi[i] = ho * a.stride - a.pad;
@@ -256,6 +235,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
     __builtin_amdgcn_s_barrier();
     float *ew = (float *)((wave < HALF ? st0 : st1) + (wave < HALF ? wave : wave - HALF) * 16 * EPI_LD * 4);
     const int out_cs = a.out_cs;
+    const __amdgpu_buffer_rsrc_t pr = partial_rsrc(a.partial, (uint32_t)a.k_splits * a.M * N * 4u);
     StaticFor<FM>::run([&](auto ic) __attribute__((always_inline)) {
         constexpr int i = decltype(ic)::value;
 #pragma unroll
@@ -274,9 +254,9 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
             const float4 v0 = *(const float4 *)src, v1 = *(const float4 *)(src + 4);
             float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
             if (a.k_splits > 1) {
-                float4 *dst = (float4 *)(a.partial + ((size_t)blockIdx.y * a.M + gm) * N + gn);
-                dst[0] = v0;
-                dst[1] = v1;
+                const uint32_t off = (uint32_t)((((int)blockIdx.y * a.M + gm) * N + gn) * 4u);
+                store_partial4(pr, off, v0);
+                store_partial4(pr, off + 16, v1);
                 continue;
             }
             const u16 *resp;
@@ -287,7 +267,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
                 outp = useg.out;
                 ms = useg.m_start;
             } else {
-                const ConvSeg &sg = a.seg[d_seg(a, gm)];
+                const ConvSeg &sg = a.seg[seg_of_row(a, gm)];
                 resp = (const u16 *)sg.res;
                 outp = sg.out;
                 ms = sg.m_start;
@@ -302,9 +282,9 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
                 u32x4 o;
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const float r0 = d_bf2f((u16)(r4[q] & 0xffffu)), r1 = d_bf2f((u16)(r4[q] >> 16));
-                    const u16 y0 = d_f2bf(d_epi(v[2 * q] * s8[2 * q] + h8[2 * q], r0, a.has_res, a.res_mode, a.act, a.slope));
-                    const u16 y1 = d_f2bf(d_epi(v[2 * q + 1] * s8[2 * q + 1] + h8[2 * q + 1], r1, a.has_res, a.res_mode,
+                    const float r0 = bf2f((u16)(r4[q] & 0xffffu)), r1 = bf2f((u16)(r4[q] >> 16));
+                    const u16 y0 = f2bf(epi(v[2 * q] * s8[2 * q] + h8[2 * q], r0, a.has_res, a.res_mode, a.act, a.slope));
+                    const u16 y1 = f2bf(epi(v[2 * q + 1] * s8[2 * q + 1] + h8[2 * q + 1], r1, a.has_res, a.res_mode,
                                                 a.act, a.slope));
                     o[q] = (uint32_t)y0 | ((uint32_t)y1 << 16);
                 }
@@ -315,9 +295,9 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
                 for (int q = 0; q < 8; ++q) {
                     const int c = gn + q;
                     if (c >= a.cout) break;
-                    const float r = a.has_res ? d_bf2f(resp[(size_t)lr_ * out_cs + c]) : 0.f;
+                    const float r = a.has_res ? bf2f(resp[(size_t)lr_ * out_cs + c]) : 0.f;
                     ((float *)outp)[((size_t)f * a.cout + c) * HWo + pix] =
-                        d_epi(v[q] * s8[q] + h8[q], r, a.has_res, a.res_mode, a.act, a.slope);
+                        epi(v[q] * s8[q] + h8[q], r, a.has_res, a.res_mode, a.act, a.slope);
                 }
             }
         }
@@ -325,6 +305,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     });
+    if (a.k_splits > 1 && a.counters) splitk_fixup<64 * WM * WN>(a, t, tm * BM, BM, tn * BN, BN, (int *)st2);
 }
 
 bool conv_dma_supported(const ConvArgs &a) {
@@ -337,10 +318,11 @@ hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) {
         return hipErrorInvalidValue;
     if (a.K != a.kh * a.kw * a.Cin || a.out_cs < a.N || a.seg[0].m_start != 0) return hipErrorInvalidValue;
     if (a.k_splits > 1 && !a.partial) return hipErrorInvalidValue;
+    if (a.k_splits > 1 && (long)a.k_splits * a.M * a.N * 4 > 0x7fffffffL) return hipErrorInvalidValue;
     if ((long)a.k_per_split * a.k_splits < a.K) return hipErrorInvalidValue;
     for (int i = 0; i < a.nseg; ++i) {
         if (!a.seg[i].in || !a.seg[i].scale || !a.seg[i].shift) return hipErrorInvalidValue;
-        if (a.k_splits <= 1 && !a.seg[i].out) return hipErrorInvalidValue;
+        if ((a.k_splits <= 1 || a.counters) && !a.seg[i].out) return hipErrorInvalidValue;
         if (a.has_res && !a.seg[i].res) return hipErrorInvalidValue;
         if (a.seg[i].m_start != a.seg[i].f_start * a.Ho * a.Wo) return hipErrorInvalidValue;
     }

@@ -9,13 +9,15 @@
 // multiply-adds (weights as the 16-row A operand, frames as the 16-column B
 // operand; the K order inside a step is the same for A and B, so any order
 // is correct). K is split over blockIdx.y so that enough waves are in flight
-// to saturate HBM; partial sums go to a [splits][M][N] fp32 buffer and
-// fc_reduce applies bias, activation and the store. With one split the
-// epilogue is applied directly.
+// to saturate HBM; partial sums go to a [splits][M][N] fp32 buffer and the
+// last split of each column of 64 neurons to finish reduces them and
+// applies bias, activation and the store (or, without arrival counters,
+// fc_reduce does). With one split the epilogue is applied directly.
 #include <hip/hip_runtime.h>
 
 #include "kargs.h"
 #include "kernels.h"
+#include "splitk.h"
 
 namespace gemel {
 
@@ -124,9 +126,47 @@ __global__ __launch_bounds__(256) void fc_bf16_kernel(const FcArgs a) {
             const int n = n0 + g * 4 + v;
             if (n >= a.N) continue;
             if (a.k_splits > 1)
-                a.partial[((size_t)blockIdx.y * a.M + f) * a.N + n] = acc[mb][v];
+                store_partial1(a.partial + ((size_t)blockIdx.y * a.M + f) * a.N + n, acc[mb][v]);
             else
                 fc_store(a, f, n, acc[mb][v], true);
+        }
+    }
+    // fused split-K reduction: the last split of this column of 64 neurons
+    // sums the partials in split order, as fc_reduce does
+    if (a.k_splits > 1 && a.counters) {
+        __shared__ int flag;
+        if (!splitk_arrive(a.counters + blockIdx.x, a.k_splits, &flag)) return;
+        // four items per thread, eight splits per batch of loads
+        for (int i0 = threadIdx.x; i0 < a.M * 64; i0 += 4 * 256) {
+            float sum[4] = {0.f, 0.f, 0.f, 0.f};
+            bool ok[4];
+            const float *base[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int item = i0 + u * 256;
+                const int f = item >> 6, n = blockIdx.x * 64 + (item & 63);
+                ok[u] = item < a.M * 64 && n < a.N;
+                base[u] = a.partial + (ok[u] ? (size_t)f * a.N + n : 0);
+            }
+            const size_t split_elems = (size_t)a.M * a.N;
+            for (int sp0 = 0; sp0 < a.k_splits; sp0 += 8) {
+                float p[4][8];
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+#pragma unroll
+                    for (int q = 0; q < 8; ++q)
+                        if (ok[u] && sp0 + q < a.k_splits) p[u][q] = load_partial1(base[u] + (sp0 + q) * split_elems);
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+#pragma unroll
+                    for (int q = 0; q < 8; ++q)
+                        if (ok[u] && sp0 + q < a.k_splits) sum[u] += p[u][q];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int item = i0 + u * 256;
+                if (ok[u]) fc_store(a, item >> 6, blockIdx.x * 64 + (item & 63), sum[u], true);
+            }
         }
     }
 }

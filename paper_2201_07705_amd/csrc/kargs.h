@@ -43,6 +43,10 @@ struct ConvArgs {
     int32_t k_splits;     // >1: write fp32 partials to `partial`
     int32_t k_per_split;  // depth handled by one split (multiple of BK)
     float *partial;       // [k_splits][M][N] when k_splits > 1
+    int32_t *counters;    // split-K: one arrival counter per output tile,
+                          // zero between launches; the last split of a tile
+                          // reduces the partials. Null: a separate reduce
+                          // launch does.
     ConvSeg seg[GEMEL_MAX_SEG];
 };
 
@@ -75,6 +79,8 @@ struct FcArgs {
     int32_t nseg;
     int32_t k_splits, k_per_split;
     float *partial;       // [k_splits][M][N]
+    int32_t *counters;    // split-K: one arrival counter per workgroup
+                          // column (64 neurons), as in ConvArgs
     FcSeg seg[GEMEL_MAX_SEG];
 };
 

@@ -116,6 +116,7 @@ void drop_plans(gemel_ctx *ctx) {
             if (ev) (void)hipEventDestroy(ev);
         if (p.arena) (void)hipFree(p.arena);
         if (p.partial) (void)hipFree(p.partial);
+        if (p.counters) (void)hipFree(p.counters);
     }
     ctx->plans.clear();
     ctx->last_plan = nullptr;
@@ -312,6 +313,9 @@ static const TileCost kTileCost[] = {
     {TILE_DMA_128x64, 0.379, 3, 5.06e-6},
 };
 
+// Partial sums of one split-K launch are addressed with 32-bit byte offsets.
+constexpr int64_t kMaxPartialBytes = 0x7fffffff;
+
 void pick_conv_config(int64_t M, int64_t N, int64_t K, bool dma_ok, int force, int force_splits, int &tile,
                       int &splits, int &kps) {
     const double cu_flops = 4096.0 * 2.4e9;   // per CU, dense bf16
@@ -327,6 +331,7 @@ void pick_conv_config(int64_t M, int64_t N, int64_t K, bool dma_ok, int force, i
             if (s > 1 && K / s < 4 * CONV_BK) break;
             const int64_t k_s = round_up((K + s - 1) / s, CONV_BK);
             const int64_t s_eff = (K + k_s - 1) / k_s;
+            if (s_eff > 1 && s_eff * M * N * 4 > kMaxPartialBytes) break;
             const double waves = std::ceil((double)(tiles * s_eff) / (256.0 * tc.occ));
             double t = waves * (tc.occ * (2.0 * bm * bn * k_s) / (cu_flops * tc.eff) + tc.lat);
             if (s_eff > 1) t += (double)s_eff * M * N * 4.0 * 2.0 / 4e12 + 2e-6;
@@ -338,6 +343,7 @@ void pick_conv_config(int64_t M, int64_t N, int64_t K, bool dma_ok, int force, i
         }
     }
     if (force_splits > 0) splits = (int)std::min<int64_t>(force_splits, (K + CONV_BK - 1) / CONV_BK);
+    while (splits > 1 && (int64_t)splits * M * N * 4 > kMaxPartialBytes) --splits;
     kps = (int)round_up((K + splits - 1) / splits, CONV_BK);
     splits = (int)((K + kps - 1) / kps);
 }
@@ -771,11 +777,13 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     } else {
                         pick_fc_config(a.N, a.K, a.k_splits, a.k_per_split);
                         Lc.type = L_FC_BF16;
-                        if (a.k_splits > 1)
+                        if (a.k_splits > 1) {
                             step_partial[(size_t)step] = std::max(step_partial[(size_t)step], (size_t)a.k_splits * a.M * a.N * 4);
+                            if (ctx->opt.splitk_fused) Lc.ctr_n = (a.N + 63) / 64;
+                        }
                     }
                     P.launches.push_back(Lc);
-                    if (Lc.type == L_FC_BF16 && a.k_splits > 1) {
+                    if (Lc.type == L_FC_BF16 && a.k_splits > 1 && !Lc.ctr_n) {
                         Launch R = Lc;
                         R.type = L_FC_REDUCE;
                         R.kind = GEMEL_K_SPLITK_REDUCE;
@@ -847,9 +855,18 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     Lc.type = L_CONV_F32;
                     Lc.kind = L0.op == GEMEL_OP_CONV ? GEMEL_K_CONV_F32 : GEMEL_K_FC;
                 }
-                P.launches.push_back(Lc);
                 if (a.k_splits > 1) {
                     step_partial[(size_t)step] = std::max(step_partial[(size_t)step], (size_t)a.k_splits * a.M * a.N * 4);
+                    // fused reduction: the last split of each tile reduces it, so
+                    // only as many workgroups as tiles share that work; with
+                    // fewer tiles than compute units a separate reduction
+                    // launch (one workgroup per 2048 outputs) is faster
+                    const int bm = conv_tile_bm(Lc.tile), bn = conv_tile_bn(Lc.tile);
+                    const int tiles = ((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn);
+                    if (ctx->opt.splitk_fused == 2 || (ctx->opt.splitk_fused == 1 && tiles >= 256)) Lc.ctr_n = tiles;
+                }
+                P.launches.push_back(Lc);
+                if (a.k_splits > 1 && !Lc.ctr_n) {
                     Launch R;
                     R.type = L_CONV_REDUCE;
                     R.kind = GEMEL_K_SPLITK_REDUCE;
@@ -972,6 +989,30 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 L.conv.partial = pp;
                 L.red.partial = pp;
                 L.fc.partial = pp;
+            }
+        }
+    }
+
+    // ---- arrival counters of the fused split-K launches: zeroed once here;
+    // each launch leaves its counters at zero again ----
+    {
+        size_t total = 0;
+        for (auto &L : P.launches) total += (size_t)L.ctr_n;
+        if (total) {
+            if (hipMalloc((void **)&P.counters, total * sizeof(int32_t)) != hipSuccess) {
+                P.counters = nullptr;
+                (void)hipGetLastError();
+                return fail(ctx, GEMEL_ENOMEM, "device allocation of the split-K counters failed");
+            }
+            const std::vector<int32_t> zeros(total, 0);
+            if (hipMemcpy(P.counters, zeros.data(), total * sizeof(int32_t), hipMemcpyHostToDevice) != hipSuccess)
+                return fail(ctx, GEMEL_EDEVICE, "clearing the split-K counters failed");
+            size_t off = 0;
+            for (auto &L : P.launches) {
+                if (!L.ctr_n) continue;
+                L.conv.counters = P.counters + off;
+                L.fc.counters = P.counters + off;
+                off += (size_t)L.ctr_n;
             }
         }
     }
@@ -1300,6 +1341,7 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         if (st) {
             if (P->arena) (void)hipFree(P->arena);
             if (P->partial) (void)hipFree(P->partial);
+            if (P->counters) (void)hipFree(P->counters);
             for (auto ev : P->events)
                 if (ev) (void)hipEventDestroy(ev);
             if (P->ev_fork) (void)hipEventDestroy(P->ev_fork);

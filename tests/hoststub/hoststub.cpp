@@ -287,7 +287,7 @@ static long long seg_rows(const Seg *seg, int nseg, int i, int M) {
     return (long long)((i + 1 < nseg ? seg[i + 1].m_start : M) - seg[i].m_start);
 }
 
-static hipError_t conv_common(const ConvArgs &a, int esz, const char *kern, bool need_zero, const Sink &sk) {
+static hipError_t conv_common(const ConvArgs &a, int tile, int esz, const char *kern, bool need_zero, const Sink &sk) {
     ++launches;
     begin_node(sk, kern);
     bool ok = a.M > 0 && a.N > 0 && a.N % 8 == 0 && a.K == a.kh * a.kw * a.Cin && a.Cin % 8 == 0 &&
@@ -312,7 +312,7 @@ static hipError_t conv_common(const ConvArgs &a, int esz, const char *kern, bool
         ok &= chk(s.in, frames * a.H * a.W * a.in_cs * esz, "input", kern);
         ok &= chk(s.scale, (long long)a.N * 4, "scale", kern) & chk(s.shift, (long long)a.N * 4, "shift", kern);
         if (a.has_res) ok &= chk(s.res, ((rows - 1) * a.out_cs + a.N) * esz, "residual", kern);
-        if (a.k_splits <= 1) {
+        if (a.k_splits <= 1 || a.counters) {
             if (a.out_mode == OUT_NHWC)
                 ok &= chk(s.out, ((rows - 1) * a.out_cs + a.N) * esz, "output", kern, true);
             else
@@ -320,6 +320,10 @@ static hipError_t conv_common(const ConvArgs &a, int esz, const char *kern, bool
         }
     }
     if (a.k_splits > 1) ok &= chk(a.partial, (long long)a.k_splits * a.M * a.N * 4, "partial", kern, true);
+    if (a.k_splits > 1 && a.counters) {
+        const long long bm = conv_tile_bm(tile), bn = conv_tile_bn(tile);
+        ok &= chk(a.counters, ((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn) * 4, "counters", kern, true);
+    }
     return verdict(ok);
 }
 
@@ -338,7 +342,7 @@ hipError_t launch_conv_stem(const ConvArgs &a, const Sink &sk) {
         last = "stem kernel on an unsupported conv";
         return hipErrorInvalidValue;
     }
-    return conv_common(a, 2, "conv_stem", true, sk);
+    return conv_common(a, TILE_STEM, 2, "conv_stem", true, sk);
 }
 hipError_t launch_conv_bf16(const ConvArgs &a, int tile, const Sink &sk) {
     if (tile < 0 || tile >= TILE_COUNT) return hipErrorInvalidValue;
@@ -348,9 +352,9 @@ hipError_t launch_conv_bf16(const ConvArgs &a, int tile, const Sink &sk) {
         return hipErrorInvalidValue;
     }
     if (tile == TILE_STEM) return launch_conv_stem(a, sk);
-    return conv_common(a, 2, "conv_bf16", true, sk);
+    return conv_common(a, tile, 2, "conv_bf16", true, sk);
 }
-hipError_t launch_conv_f32(const ConvArgs &a, const Sink &sk) { return conv_common(a, 4, "conv_f32", false, sk); }
+hipError_t launch_conv_f32(const ConvArgs &a, const Sink &sk) { return conv_common(a, -1, 4, "conv_f32", false, sk); }
 
 hipError_t launch_conv_reduce(const ReduceArgs &a, bool bf16, const Sink &sk) {
     ++launches;
@@ -382,7 +386,7 @@ static hipError_t fc_common(const FcArgs &a, int esz, const char *kern, bool rea
         return hipErrorInvalidValue;
     }
     const bool split = a.k_splits > 1;
-    const bool writes_out = !reads_w || !split;
+    const bool writes_out = !reads_w || !split || a.counters;
     if (reads_w) ok &= chk(a.w, (long long)a.N * a.K * esz, "weights", kern);
     for (int i = 0; i < a.nseg; ++i) {
         const FcSeg &s = a.seg[i];
@@ -395,6 +399,7 @@ static hipError_t fc_common(const FcArgs &a, int esz, const char *kern, bool rea
         ok &= chk(s.scale, (long long)a.N * 4, "scale", kern);
     }
     if (split) ok &= chk(a.partial, (long long)a.k_splits * a.M * a.N * 4, "partial", kern, reads_w);
+    if (split && reads_w && a.counters) ok &= chk(a.counters, (long long)(a.N + 63) / 64 * 4, "counters", kern, true);
     return verdict(ok);
 }
 hipError_t launch_fc_bf16(const FcArgs &a, const Sink &sk) { return fc_common(a, 2, "fc_bf16", true, sk); }

@@ -145,6 +145,32 @@ def test_concurrent_branches_with_split_k(r50vgg):
     _same(a, c)
 
 
+@pytest.mark.parametrize("tile", [2, 11], ids=["generic64x64", "dma128x128"])
+def test_fused_split_k_equals_separate_reduce(r50vgg, tile):
+    """The last split of each tile reduces the partial sums inside the GEMM
+    launch (conv and FC); the separate reduction launch sums them in the
+    same order, so both give the same bits. Two rounds on one input and a
+    third on another: a counter not cleared after a launch would leave the
+    third round's outputs unwritten."""
+    wl, params, frames = r50vgg
+    other = [np.ascontiguousarray(f[..., ::-1]) for f in frames]
+    log(f"fused split-K tile {tile}")
+    ref = _run(wl, params, other, OPT_CONV_TILE=tile, OPT_CONV_SPLITS=4,
+               OPT_SPLITK_FUSED=0)
+    g = _pinned(wl, params, OPT_CONV_TILE=tile, OPT_CONV_SPLITS=4,
+                OPT_SPLITK_FUSED=2)
+    try:
+        g.run(frames, repeat=2)
+        got = g.run(other)
+    finally:
+        g.close()
+    _same(ref, got)
+    c = _run(wl, params, other, OPT_CONV_TILE=tile, OPT_CONV_SPLITS=4,
+             OPT_SPLITK_FUSED=2, OPT_USE_GRAPH=0, OPT_STREAMS=8,
+             OPT_FORK_US=0, repeat=2)
+    _same(ref, c)
+
+
 def test_swap_forced_equals_resident_bitwise():
     """A budget far below the unmerged weight bytes streams most layers
     through the staging slots every round; outputs must not change."""

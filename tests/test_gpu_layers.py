@@ -102,11 +102,13 @@ def test_conv_every_tile_shape(tile, case):
 EXACT_TOL = 5e-5
 
 
-@pytest.mark.parametrize("splits", [1, 3])
+@pytest.mark.parametrize("splits,fused", [(1, 0), (3, 0), (3, 2)],
+                         ids=["split1", "split3", "split3fused"])
 @pytest.mark.parametrize("tile", range(len(TILES)), ids=lambda t: TILES[t])
 @pytest.mark.parametrize("case", CONV_CASES, ids=lambda c: "x".join(map(str, c)))
-def test_conv_single_layer_exact(tile, case, splits):
-    """Every tile shape and split-K 1/3 on one conv + BN + residual-free
+def test_conv_single_layer_exact(tile, case, splits, fused):
+    """Every tile shape and split-K 1/3 (partial sums reduced by a separate
+    launch or inside the GEMM launch) on one conv + BN + residual-free
     epilogue with the fp32 output store, against the oracle at fp32
     accumulation precision."""
     from paper_2201_07705_amd import gemel as G
@@ -121,6 +123,7 @@ def test_conv_single_layer_exact(tile, case, splits):
     try:
         g.ctx.set_option(G.OPT_CONV_TILE, tile)
         g.ctx.set_option(G.OPT_CONV_SPLITS, splits)
+        g.ctx.set_option(G.OPT_SPLITK_FUSED, fused)
         got = g.run(fr)
     finally:
         g.close()

@@ -62,7 +62,11 @@ CASES = [
       "OPT_AUTOTUNE": 0}),
     ("r50x2_vgg16x2", {"res": 64, "frames": 2}, {"ROUNDS": 14}),
     ("r50x2_vgg16x2", {"res": 64, "frames": 2},
-     {"OPT_CONV_SPLITS": 4, "OPT_STREAMS": 8, "OPT_FORK_US": 0}),
+     {"OPT_CONV_SPLITS": 4, "OPT_STREAMS": 8, "OPT_FORK_US": 0,
+      "OPT_SPLITK_FUSED": 2}),
+    ("r50x2_vgg16x2", {"res": 64, "frames": 2},
+     {"OPT_CONV_SPLITS": 4, "OPT_STREAMS": 8, "OPT_FORK_US": 0,
+      "OPT_SPLITK_FUSED": 0}),
     ("mix8_budget40", {"res": 32, "frames": 2}, {}),
     ("mix8_budget40", {"res": 32, "frames": 2},
      {"OPT_SWAP_SLOT_BYTES": 1 << 20, "OPT_SWAP_SLOTS": 2,
