@@ -57,15 +57,22 @@ __device__ __forceinline__ void wait_vm() {
     __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// lgkmcnt(0) only: vmcnt and expcnt left at their maxima (gfx9 encoding).
+__device__ __forceinline__ void wait_lgkm0() {
+    __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));
+}
+
 }  // namespace
 
-template <int BM, int BN, int WM, int WN, int STAGES>
+template <int BM, int BN, int WM, int WN, int STAGES, int BK>
 __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a) {
     constexpr int NW = WM * WN, NT = 64 * NW;
-    constexpr int BK = 32;
+    static_assert(BK == 32 || BK == 64, "step depth");
+    constexpr int CPR = BK / 8;                                 // 16-byte chunks per row
+    constexpr int RPI = 64 / CPR;                               // rows per DMA instruction
     constexpr int TM = BM / WM, TN = BN / WN;
     constexpr int FM = TM / 16, FN = TN / 16;
-    constexpr int A_SLOTS = BM * 4, B_SLOTS = BN * 4;          // 16-byte slots per stage
+    constexpr int A_SLOTS = BM * CPR, B_SLOTS = BN * CPR;      // 16-byte slots per stage
     constexpr int AI = A_SLOTS / NT, BI = B_SLOTS / NT;        // DMA instructions per thread
     static_assert(AI * NT == A_SLOTS && BI * NT == B_SLOTS && AI >= 1 && BI >= 1, "tile/threads");
     constexpr int STAGE_BYTES = (A_SLOTS + B_SLOTS) * 16;
@@ -108,13 +115,16 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
     const ConvSeg &useg = a.seg[s_first];
 
     // ---- DMA assignment: instruction i of this thread fills slot
-    // (i*NW + wave)*64 + lane: row ((i*NW + wave)*16 + lane/4), chunk cq ----
-    const int cq = (lane & 3) ^ ((lane >> 3) & 3);
+    // (i*NW + wave)*64 + lane: row (i*NW + wave)*RPI + lane/CPR; the slot's
+    // chunk position lane%CPR holds logical chunk (lane%CPR) ^ sw(row) ----
+    auto sw = [](int row) __attribute__((always_inline)) { return (row >> 1) & (CPR - 1); };
     const u16 *abase[AI];
-    int ahi[AI], awi[AI];
+    int ahi[AI], awi[AI], acq[AI];
 #pragma unroll
     for (int i = 0; i < AI; ++i) {
-        const int gm = tm * BM + (i * NW + wave) * 16 + (lane >> 2);
+        const int rl = (i * NW + wave) * RPI + lane / CPR;
+        acq[i] = (lane % CPR) ^ sw(rl);
+        const int gm = tm * BM + rl;
         abase[i] = zp;
         ahi[i] = -(1 << 28);
         awi[i] = 0;
@@ -135,8 +145,9 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
     const u16 *bbase[BI];
 #pragma unroll
     for (int i = 0; i < BI; ++i) {
-        const int gn = tn * BN + (i * NW + wave) * 16 + (lane >> 2);
-        bbase[i] = gn < N ? (const u16 *)a.w + (size_t)gn * K + cq * 8 : nullptr;
+        const int rl = (i * NW + wave) * RPI + lane / CPR;
+        const int gn = tn * BN + rl;
+        bbase[i] = gn < N ? (const u16 *)a.w + (size_t)gn * K + ((lane % CPR) ^ sw(rl)) * 8 : nullptr;
     }
     // loader position (uniform): next step's tap (lr, ls) and channel base lc
     int kb = k_begin, lc, lr, ls;
@@ -147,12 +158,11 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
         ls = rs - lr * kw;
     }
     auto issue = [&](unsigned char *stage) __attribute__((always_inline)) {
-        const int c = lc + cq * 8;
 #pragma unroll
         for (int i = 0; i < AI; ++i) {
             const int hi = ahi[i] + lr, wi = awi[i] + ls;
             const bool ok = (unsigned)hi < (unsigned)H && (unsigned)wi < (unsigned)W;
-            const u16 *p = ok ? abase[i] + ((size_t)(hi * W + wi) * in_cs + c) : zp;
+            const u16 *p = ok ? abase[i] + ((size_t)(hi * W + wi) * in_cs + lc + acq[i] * 8) : zp;
             __builtin_amdgcn_global_load_lds((const void *)p, (lds_u8 *)(stage + (i * NW + wave) * 1024), 16, 0, 0);
         }
 #pragma unroll
@@ -175,25 +185,44 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // fragment read offsets inside a stage (swizzled slots)
+    // fragment read offsets inside a stage (swizzled slots): a fragment row
+    // is wave-tile row 16*i + lane%16 (a multiple of 16 plus lane%16), so
+    // its swizzle depends on the lane only
     const int g = lane >> 4;
-    auto frag_off = [&](int row) __attribute__((always_inline)) { return (row * 4 + (g ^ ((row >> 1) & 3))) * 16; };
+    const int swl = sw(lane & 15);
     int aoff[FM], boff[FN];
 #pragma unroll
-    for (int i = 0; i < FM; ++i) aoff[i] = frag_off(wm * TM + i * 16 + (lane & 15));
+    for (int i = 0; i < FM; ++i) aoff[i] = (wm * TM + i * 16 + (lane & 15)) * CPR * 16;
 #pragma unroll
-    for (int j = 0; j < FN; ++j) boff[j] = A_SLOTS * 16 + frag_off(wn * TN + j * 16 + (lane & 15));
-    auto compute = [&](const unsigned char *stage) __attribute__((always_inline)) {
-        bf16x8 bfr[FN];
+    for (int j = 0; j < FN; ++j) boff[j] = A_SLOTS * 16 + (wn * TN + j * 16 + (lane & 15)) * CPR * 16;
+    // fragments of one depth step in registers: H halves of 32
+    constexpr int NH = BK / 32;
+    typedef bf16x8 FragA[NH][FM];
+    typedef bf16x8 FragB[NH][FN];
+    auto read_frags = [&](const unsigned char *stage, FragA &fa, FragB &fb) __attribute__((always_inline)) {
 #pragma unroll
-        for (int j = 0; j < FN; ++j) bfr[j] = *(const bf16x8 *)(stage + boff[j]);
+        for (int h = 0; h < NH; ++h) {
+            const int pos = ((h * 4 + g) ^ swl) * 16;
 #pragma unroll
-        for (int i = 0; i < FM; ++i) {
-            const bf16x8 af = *(const bf16x8 *)(stage + aoff[i]);
+            for (int j = 0; j < FN; ++j) fb[h][j] = *(const bf16x8 *)(stage + boff[j] + pos);
 #pragma unroll
-            for (int j = 0; j < FN; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bfr[j], acc[i][j], 0, 0, 0);
+            for (int i = 0; i < FM; ++i) fa[h][i] = *(const bf16x8 *)(stage + aoff[i] + pos);
         }
+    };
+    auto mfmas = [&](const FragA &fa, const FragB &fb) __attribute__((always_inline)) {
+#pragma unroll
+        for (int h = 0; h < NH; ++h)
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[h][i], fb[h][j], acc[i][j], 0, 0, 0);
+    };
+    auto compute = [&](const unsigned char *stage) __attribute__((always_inline)) {
+        FragA fa;
+        FragB fb;
+        read_frags(stage, fa, fb);
+        mfmas(fa, fb);
     };
 
     // epilogue constants of this lane's 8 channels (every segment shares
@@ -214,18 +243,79 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
     for (int s = 0; s < STAGES - 1; ++s)
         if (s < nk) issue(stg[s]);
 
-    // main loop, unrolled by STAGES so that every buffer index is static
-    for (int base = 0; base < nk; base += STAGES) {
+    // register double-buffering needs a second fragment set: only where it
+    // fits beside the accumulators (512-thread workgroups have 256
+    // registers per lane)
+    constexpr bool PIPE = STAGES == 4 && (NT <= 256 || FM * FN <= 16);
+    if constexpr (PIPE) {
+        // Fragments double-buffered in registers: iteration it reads step
+        // it+1's fragments from LDS, then issues step it's MFMAs from the
+        // registers filled one iteration earlier, so the LDS reads overlap
+        // the MFMAs. The DMA issued in iteration it refills the buffer of
+        // step it-1, whose fragments every wave read before this
+        // iteration's barrier.
+        FragA fa[2];
+        FragB fb[2];
+        if (nk > 0) {
+            if (STAGES - 2 < nk) wait_vm<(STAGES - 2) * PER_STEP>();
+            else wait_vm<0>();
+            __builtin_amdgcn_s_barrier();
+            read_frags(stg[0], fa[0], fb[0]);
+        }
+        int base = 0;
+        // steady state: every iteration of the group waits, issues the DMA
+        // three steps ahead and reads the next fragments (no branches, so
+        // the compiler's wait placement sees one path)
+        for (; base + 2 * STAGES - 1 <= nk; base += STAGES) {
 #pragma unroll
-        for (int s = 0; s < STAGES; ++s) {
-            const int it = base + s;
-            if (it < nk) {
-                // step it must have landed; the newer steps may still fly
-                if (it + STAGES - 2 < nk) wait_vm<(STAGES - 2) * PER_STEP>();
-                else wait_vm<0>();
+            for (int s = 0; s < STAGES; ++s) {
+                wait_vm<(STAGES - 3) * PER_STEP>();
                 __builtin_amdgcn_s_barrier();
-                if (it + STAGES - 1 < nk) issue(stg[(s + STAGES - 1) % STAGES]);
-                compute(stg[s]);
+                issue(stg[(s + STAGES - 1) % STAGES]);
+                wait_lgkm0();
+                read_frags(stg[(s + 1) % STAGES], fa[(s + 1) & 1], fb[(s + 1) & 1]);
+                mfmas(fa[s & 1], fb[s & 1]);
+            }
+        }
+        // the last groups, with the bounds checks
+        for (; base < nk; base += STAGES) {
+#pragma unroll
+            for (int s = 0; s < STAGES; ++s) {
+                const int it = base + s;
+                if (it < nk) {
+                    if (it + 1 < nk) {
+                        // step it+1 must have landed; newer steps may fly
+                        if (it + STAGES - 2 < nk) wait_vm<(STAGES - 3) * PER_STEP>();
+                        else wait_vm<0>();
+                        __builtin_amdgcn_s_barrier();
+                        if (it + STAGES - 1 < nk) issue(stg[(s + STAGES - 1) % STAGES]);
+                        // the fragments read one iteration ago (the operands
+                        // of the MFMAs below) have long arrived: waiting for
+                        // them here, before the next reads are issued, keeps
+                        // the compiler from waiting for those after them
+                        wait_lgkm0();
+                        read_frags(stg[(s + 1) % STAGES], fa[(s + 1) & 1], fb[(s + 1) & 1]);
+                    } else {
+                        wait_lgkm0();   // both paths reach the MFMAs with no read pending on their operands
+                    }
+                    mfmas(fa[s & 1], fb[s & 1]);
+                }
+            }
+        }
+    } else {
+        // main loop, unrolled by STAGES so that every buffer index is static
+        for (int base = 0; base < nk; base += STAGES) {
+#pragma unroll
+            for (int s = 0; s < STAGES; ++s) {
+                const int it = base + s;
+                if (it < nk) {
+                    // step it must have landed; the newer steps may still fly
+                    if (it + STAGES - 2 < nk) wait_vm<(STAGES - 2) * PER_STEP>();
+                    else wait_vm<0>();
+                    __builtin_amdgcn_s_barrier();
+                    if (it + STAGES - 1 < nk) issue(stg[(s + STAGES - 1) % STAGES]);
+                    compute(stg[s]);
+                }
             }
         }
     }
@@ -312,9 +402,14 @@ bool conv_dma_supported(const ConvArgs &a) {
     return a.Cin % 32 == 0 && a.in_cs % 8 == 0 && a.K % 32 == 0 && a.k_per_split % 32 == 0 && a.zero &&
            a.uni_affine;
 }
+bool conv_dma_supported(const ConvArgs &a, int tile) {
+    if (!conv_dma_supported(a)) return false;
+    if (tile_dma_depth(tile) == 64) return a.Cin % 64 == 0 && a.k_per_split % 64 == 0;
+    return true;
+}
 
 hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) {
-    if (!conv_dma_supported(a) || a.M <= 0 || a.N <= 0 || a.N % 8 || a.nseg < 1 || a.nseg > GEMEL_MAX_SEG)
+    if (!conv_dma_supported(a, tile) || a.M <= 0 || a.N <= 0 || a.N % 8 || a.nseg < 1 || a.nseg > GEMEL_MAX_SEG)
         return hipErrorInvalidValue;
     if (a.K != a.kh * a.kw * a.Cin || a.out_cs < a.N || a.seg[0].m_start != 0) return hipErrorInvalidValue;
     if (a.k_splits > 1 && !a.partial) return hipErrorInvalidValue;
@@ -334,10 +429,14 @@ hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) {
     dim3 grid((unsigned)blocks, (unsigned)a.k_splits);
     hipError_t e = hipErrorInvalidValue;
     switch (tile) {
-    case TILE_DMA_256x256: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<256, 256, 2, 4, 4>), grid, dim3(512), a); break;
-    case TILE_DMA_256x128: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<256, 128, 2, 2, 4>), grid, dim3(256), a); break;
-    case TILE_DMA_128x128: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<128, 128, 2, 2, 4>), grid, dim3(256), a); break;
-    case TILE_DMA_128x64: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<128, 64, 2, 1, 4>), grid, dim3(128), a); break;
+    case TILE_DMA_256x256: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<256, 256, 2, 4, 4, 32>), grid, dim3(512), a); break;
+    case TILE_DMA_256x128: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<256, 128, 2, 2, 4, 32>), grid, dim3(256), a); break;
+    case TILE_DMA_128x128: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<128, 128, 2, 2, 4, 32>), grid, dim3(256), a); break;
+    case TILE_DMA_128x64: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<128, 64, 2, 1, 4, 32>), grid, dim3(128), a); break;
+    case TILE_DMA64_256x256: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<256, 256, 2, 4, 2, 64>), grid, dim3(512), a); break;
+    case TILE_DMA64_256x128: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<256, 128, 2, 2, 3, 64>), grid, dim3(256), a); break;
+    case TILE_DMA64_128x128: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<128, 128, 2, 2, 2, 64>), grid, dim3(256), a); break;
+    case TILE_DMA64_128x64: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<128, 64, 2, 1, 3, 64>), grid, dim3(128), a); break;
     default: break;
     }
     return e;

@@ -54,7 +54,13 @@ enum ConvTile {
     // 8-channel inputs (k_stem.hip): 128 pixels x 64 channels (256 x 32
     // when N <= 32), no LDS
     TILE_STEM = 13,
-    TILE_COUNT = 14
+    // LDS-DMA pipeline with depth steps of 64 (each row load a whole
+    // 128-byte line), Cin a multiple of 64
+    TILE_DMA64_256x256 = 14, // 8 waves, 2 stages
+    TILE_DMA64_256x128 = 15, // 4 waves, 3 stages
+    TILE_DMA64_128x128 = 16, // 4 waves, 2 stages
+    TILE_DMA64_128x64 = 17,  // 2 waves, 3 stages
+    TILE_COUNT = 18
 };
 int conv_tile_threads(int tile);
 int conv_tile_bm(int tile);
@@ -62,9 +68,14 @@ int conv_tile_bn(int tile);
 constexpr int CONV_BK = 64;
 
 hipError_t launch_conv_bf16(const ConvArgs &a, int tile, const Sink &sk);
-bool conv_dma_supported(const ConvArgs &a);
+bool conv_dma_supported(const ConvArgs &a);             // any DMA tile of depth 32
+bool conv_dma_supported(const ConvArgs &a, int tile);   // this DMA tile
 hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk);
-inline bool tile_is_dma(int tile) { return tile >= TILE_DMA_256x256 && tile <= TILE_DMA_128x64; }
+inline bool tile_is_dma(int tile) {
+    return (tile >= TILE_DMA_256x256 && tile <= TILE_DMA_128x64) ||
+           (tile >= TILE_DMA64_256x256 && tile <= TILE_DMA64_128x64);
+}
+inline int tile_dma_depth(int tile) { return tile >= TILE_DMA64_256x256 ? 64 : 32; }
 // Stem kernel: Cin == in_cs == 8, no split-K.
 bool conv_stem_supported(const ConvArgs &a);
 hipError_t launch_conv_stem(const ConvArgs &a, const Sink &sk);

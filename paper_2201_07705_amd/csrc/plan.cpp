@@ -311,12 +311,17 @@ static const TileCost kTileCost[] = {
     {TILE_DMA_256x128, 0.330, 1, 7.72e-6},
     {TILE_DMA_128x128, 0.526, 2, 4.83e-6},
     {TILE_DMA_128x64, 0.379, 3, 5.06e-6},
+    {TILE_DMA64_256x256, 0.520, 1, 7.94e-6},
+    {TILE_DMA64_256x128, 0.320, 1, 7.72e-6},
+    {TILE_DMA64_128x128, 0.520, 1, 4.83e-6},
+    {TILE_DMA64_128x64, 0.370, 3, 5.06e-6},
 };
 
 // Partial sums of one split-K launch are addressed with 32-bit byte offsets.
 constexpr int64_t kMaxPartialBytes = 0x7fffffff;
 
-void pick_conv_config(int64_t M, int64_t N, int64_t K, bool dma_ok, int force, int force_splits, int &tile,
+// dma_depth: deepest LDS-DMA step the conv allows (0: no DMA tile, 32 or 64).
+void pick_conv_config(int64_t M, int64_t N, int64_t K, int dma_depth, int force, int force_splits, int &tile,
                       int &splits, int &kps) {
     const double cu_flops = 4096.0 * 2.4e9;   // per CU, dense bf16
     double best = 1e300;
@@ -324,7 +329,7 @@ void pick_conv_config(int64_t M, int64_t N, int64_t K, bool dma_ok, int force, i
     splits = 1;
     for (const TileCost &tc : kTileCost) {
         if (force >= 0 && tc.tile != force) continue;
-        if (force < 0 && tile_is_dma(tc.tile) && !dma_ok) continue;
+        if (force < 0 && tile_is_dma(tc.tile) && tile_dma_depth(tc.tile) > dma_depth) continue;
         const int64_t bm = conv_tile_bm(tc.tile), bn = conv_tile_bn(tc.tile);
         const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
         for (int s = 1; s <= 16; s *= 2) {
@@ -834,7 +839,10 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 for (int i = 1; i < a.nseg; ++i)
                     if (a.seg[i].scale != a.seg[0].scale || a.seg[i].shift != a.seg[0].shift) a.uni_affine = 0;
                 if (bf16) {
-                    const bool dma_ok = a.Cin % 32 == 0 && a.in_cs % 8 == 0 && a.uni_affine;
+                    const int dma_depth = !(a.in_cs % 8 == 0 && a.uni_affine) ? 0
+                                          : a.Cin % 64 == 0                      ? 64
+                                          : a.Cin % 32 == 0                      ? 32
+                                                                                 : 0;
                     // 8-channel inputs (the RGB stems) take the stem kernel
                     const bool stem = a.Cin == 8 && a.in_cs == 8 && a.kh * a.kw <= 64 && a.uni_affine &&
                                       (ctx->opt.conv_tile < 0 || ctx->opt.conv_tile == TILE_STEM);
@@ -843,10 +851,10 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                         a.k_splits = 1;
                         a.k_per_split = a.K;
                     } else {
-                        pick_conv_config(a.M, a.N, a.K, dma_ok, ctx->opt.conv_tile == TILE_STEM ? TILE_64x64 : ctx->opt.conv_tile,
+                        pick_conv_config(a.M, a.N, a.K, dma_depth, ctx->opt.conv_tile == TILE_STEM ? TILE_64x64 : ctx->opt.conv_tile,
                                          ctx->opt.conv_splits, Lc.tile, a.k_splits, a.k_per_split);
                     }
-                    if (tile_is_dma(Lc.tile) && !conv_dma_supported(a)) Lc.tile = TILE_64x64;
+                    if (tile_is_dma(Lc.tile) && !conv_dma_supported(a, Lc.tile)) Lc.tile = TILE_64x64;
                     Lc.type = L_CONV_BF16;
                     Lc.kind = L0.op == GEMEL_OP_CONV ? GEMEL_K_CONV_MFMA : GEMEL_K_FC;
                 } else {

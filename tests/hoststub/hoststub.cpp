@@ -276,8 +276,10 @@ hipError_t hipGraphLaunch(hipGraphExec_t e, hipStream_t s) {
 
 namespace gemel {
 
-static const int kBm[TILE_COUNT] = {128, 128, 64, 256, 256, 256, 64, 128, 64, 256, 256, 128, 128, 256};
-static const int kBn[TILE_COUNT] = {128, 64, 64, 256, 128, 64, 64, 64, 128, 256, 128, 128, 64, 32};
+static const int kBm[TILE_COUNT] = {128, 128, 64, 256, 256, 256, 64, 128, 64, 256, 256, 128, 128, 256,
+                                    256, 256, 128, 128};
+static const int kBn[TILE_COUNT] = {128, 64, 64, 256, 128, 64, 64, 64, 128, 256, 128, 128, 64, 32,
+                                    256, 128, 128, 64};
 int conv_tile_bm(int t) { return t >= 0 && t < TILE_COUNT ? kBm[t] : 0; }
 int conv_tile_bn(int t) { return t >= 0 && t < TILE_COUNT ? kBn[t] : 0; }
 int conv_tile_threads(int t) { return (t == TILE_256x256 || t == TILE_256x128) ? 512 : 256; }
@@ -331,6 +333,10 @@ bool conv_dma_supported(const ConvArgs &a) {
     return a.Cin % 32 == 0 && a.in_cs % 8 == 0 && a.K % 32 == 0 && a.k_per_split % 32 == 0 && a.zero &&
            a.uni_affine;
 }
+bool conv_dma_supported(const ConvArgs &a, int tile) {
+    if (!conv_dma_supported(a)) return false;
+    return tile_dma_depth(tile) == 32 || (a.Cin % 64 == 0 && a.k_per_split % 64 == 0);
+}
 hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) { return launch_conv_bf16(a, tile, sk); }
 bool conv_stem_supported(const ConvArgs &a) {
     return a.Cin == 8 && a.in_cs == 8 && a.k_splits <= 1 && a.kh * a.kw <= 64 && a.zero && a.uni_affine &&
@@ -346,7 +352,7 @@ hipError_t launch_conv_stem(const ConvArgs &a, const Sink &sk) {
 }
 hipError_t launch_conv_bf16(const ConvArgs &a, int tile, const Sink &sk) {
     if (tile < 0 || tile >= TILE_COUNT) return hipErrorInvalidValue;
-    if (tile_is_dma(tile) && !conv_dma_supported(a)) {
+    if (tile_is_dma(tile) && !conv_dma_supported(a, tile)) {
         ++violations;
         last = "dma tile on an unsupported conv";
         return hipErrorInvalidValue;
