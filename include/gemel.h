@@ -273,8 +273,8 @@ enum {
                                     pipeline with depth steps of 64,
                                     256x256, 256x128, 128x128, 128x64, used
                                     where Cin % 64 == 0) with split-K still
-                                    chosen. A forced tile a conv cannot
-                                    use falls back to 64x64                */
+                                    chosen. A forced tile a conv cannot use
+                                    falls back to 64x64                    */
     GEMEL_OPT_CONV_SPLITS = 8,   /* 0 (default): split-K chosen per conv;
                                     n >= 1: force n depth splits (capped
                                     so that every split has work)          */
@@ -315,7 +315,7 @@ enum {
                                     while the caller's stream is being
                                     captured. 0: the mode set by
                                     GEMEL_OPT_GRAPH_DAG                    */
-    GEMEL_OPT_SPLITK_FUSED = 13  /* how split-K layers reduce their fp32
+    GEMEL_OPT_SPLITK_FUSED = 13, /* how split-K layers reduce their fp32
                                     partial sums: 1 (default) inside the
                                     GEMM launch (the last split of each
                                     output tile to finish sums the tile and
@@ -325,6 +325,20 @@ enum {
                                     2: inside the GEMM launch always; 0: in
                                     a separate launch always. Every form
                                     sums in split order: same bits         */
+    GEMEL_OPT_TUNE = 14          /* 1 (default): when a plan is built, each
+                                    bf16 conv shape whose tile and split-K
+                                    are not forced (and whose weights are
+                                    resident and whose output is internal)
+                                    times the cost model's best estimated
+                                    configurations (up to 4, those within
+                                    2x of the best estimate) on the device
+                                    and keeps the fastest; choices are kept
+                                    for the context's life. Not while the
+                                    caller's stream is being captured. 0:
+                                    the cost model alone; 2..16: as 1, up
+                                    to that many candidates. Different
+                                    choices change fp32 summation order,
+                                    so bits may differ between contexts    */
 };
 
 /* Set an option; takes effect at the next gemel_infer. Errors: EINVAL. */

@@ -21,16 +21,77 @@ __device__ __forceinline__ float bf2f(u16 h) {
 __device__ __forceinline__ u16 f2bf(float f) {
     return __builtin_bit_cast(u16, (__bf16)f);
 }
+// Activation (0 none, 1 ReLU, 2 leaky ReLU) and the residual epilogue,
+// written with selects rather than branches: the flags are the same for a
+// whole launch, and branches on them let the compiler duplicate every
+// unrolled store loop once per flag combination (code that outgrows the
+// instruction cache). The arithmetic of each case is unchanged.
 __device__ __forceinline__ float act_fn(float y, int act, float slope) {
-    if (act == 1) return fmaxf(y, 0.f);
-    if (act == 2) return y > 0.f ? y : y * slope;
-    return y;
+    const float relu = fmaxf(y, 0.f);
+    const float leaky = y > 0.f ? y : y * slope;
+    return act == 1 ? relu : act == 2 ? leaky : y;
 }
 __device__ __forceinline__ float epi(float z, float r, int has_res,
                                      int res_mode, int act, float slope) {
-    if (!has_res) return act_fn(z, act, slope);
-    if (res_mode == 0) return act_fn(z + r, act, slope);
-    return act_fn(z, act, slope) + r;
+    const bool pre = has_res && res_mode == 0, post = has_res && res_mode != 0;
+    const float u = act_fn(pre ? z + r : z, act, slope);
+    return post ? u + r : u;
+}
+
+// Epilogue kinds with their own short instruction sequence; everything
+// else takes the general form (epi). The flags are launch-wide, so the
+// switch in epi8_bf16 is a uniform branch.
+enum { EK_NONE = 0, EK_RELU = 1, EK_RELU_RES = 2, EK_LEAKY = 3, EK_GENERAL = 4 };
+__device__ __forceinline__ int epi_kind(int act, int has_res, int res_mode, float slope) {
+    if (!has_res && act == 0) return EK_NONE;
+    if (!has_res && act == 1) return EK_RELU;
+    if (has_res && res_mode == 0 && act == 1) return EK_RELU_RES;
+    // for 0 <= slope <= 1, max(y, slope * y) is y for y > 0 and slope * y
+    // otherwise (the leaky ReLU), one select fewer
+    if (!has_res && act == 2 && slope >= 0.f && slope <= 1.f) return EK_LEAKY;
+    return EK_GENERAL;
+}
+// z = v * scale + shift, the activation / residual of `kind`, rounded to
+// bf16 and packed in channel order. r4 holds the residual's 8 bf16 values
+// (ignored unless the kind has a residual).
+__device__ __forceinline__ u32x4 epi8_bf16(const float *v, const float *sc, const float *sh, const u32x4 &r4,
+                                           int kind, int has_res, int res_mode, int act, float slope) {
+    float y[8];
+    // the residual is unpacked only where a kind reads it, so that kinds
+    // without one never wait for its load
+    auto res = [&](int j) __attribute__((always_inline)) {
+        const uint32_t w = r4[j >> 1];
+        return __uint_as_float((j & 1) ? (w & 0xffff0000u) : (w << 16));
+    };
+    switch (kind) {
+    case EK_NONE:
+#pragma unroll
+        for (int j = 0; j < 8; ++j) y[j] = v[j] * sc[j] + sh[j];
+        break;
+    case EK_RELU:
+#pragma unroll
+        for (int j = 0; j < 8; ++j) y[j] = fmaxf(v[j] * sc[j] + sh[j], 0.f);
+        break;
+    case EK_RELU_RES:
+#pragma unroll
+        for (int j = 0; j < 8; ++j) y[j] = fmaxf((v[j] * sc[j] + sh[j]) + res(j), 0.f);
+        break;
+    case EK_LEAKY:
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const float z = v[j] * sc[j] + sh[j];
+            y[j] = fmaxf(z, z * slope);
+        }
+        break;
+    default:
+#pragma unroll
+        for (int j = 0; j < 8; ++j) y[j] = epi(v[j] * sc[j] + sh[j], res(j), has_res, res_mode, act, slope);
+        break;
+    }
+    u32x4 o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q] = (uint32_t)f2bf(y[2 * q]) | ((uint32_t)f2bf(y[2 * q + 1]) << 16);
+    return o;
 }
 
 // Segment of GEMM row gm: the last segment whose m_start <= gm.
@@ -41,9 +102,43 @@ __device__ __forceinline__ int seg_of_row(const Args &a, int gm) {
     return s;
 }
 
+// Fields of one segment. The segment table lives in the kernel argument
+// block: indexing it with a per-lane segment number turns every field
+// access into a per-lane global load on the critical path, so per-row
+// fields are gathered by row_seg with uniform (scalar) loads and selects.
+struct RowSeg {
+    const void *in;
+    const void *res;
+    void *out;
+    const float *scale;
+    const float *shift;
+    int m_start, f_start;
+};
+template <typename Args>
+__device__ __forceinline__ RowSeg uni_seg(const Args &a, int s) {
+    const ConvSeg &g = a.seg[s];
+    return RowSeg{g.in, g.res, g.out, g.scale, g.shift, g.m_start, g.f_start};
+}
+template <typename Args>
+__device__ __forceinline__ RowSeg row_seg(const Args &a, int gm) {
+    RowSeg r = uni_seg(a, 0);
+    for (int i = 1; i < a.nseg; ++i) {
+        const RowSeg c = uni_seg(a, i);
+        const bool hit = gm >= c.m_start;
+        r.in = hit ? c.in : r.in;
+        r.res = hit ? c.res : r.res;
+        r.out = hit ? c.out : r.out;
+        r.scale = hit ? c.scale : r.scale;
+        r.shift = hit ? c.shift : r.shift;
+        r.m_start = hit ? c.m_start : r.m_start;
+        r.f_start = hit ? c.f_start : r.f_start;
+    }
+    return r;
+}
+
 // Scalars of the fused epilogue.
 struct Epi {
-    int out_cs, cout, act, res_mode, has_res, HWo;
+    int out_cs, cout, act, res_mode, has_res, HWo, kind;
     float slope;
 };
 template <typename Args>
@@ -51,11 +146,12 @@ __device__ __forceinline__ Epi epi_of(const Args &a, int HWo) {
     Epi e;
     e.out_cs = a.out_cs; e.cout = a.cout; e.act = a.act; e.res_mode = a.res_mode;
     e.has_res = a.has_res; e.HWo = HWo; e.slope = a.slope;
+    e.kind = epi_kind(a.act, a.has_res, a.res_mode, a.slope);
     return e;
 }
 
 // Epilogue of 8 consecutive channels [gn, gn+8) of row gm into NHWC bf16.
-__device__ __forceinline__ void store8_nhwc_bf16(const ConvSeg &sg, const Epi &e,
+__device__ __forceinline__ void store8_nhwc_bf16(const RowSeg &sg, const Epi &e,
                                                  int gm, int gn, const float *v) {
     const size_t off = (size_t)(gm - sg.m_start) * e.out_cs + gn;
     const float4 sc0 = *(const float4 *)(sg.scale + gn);
@@ -64,25 +160,13 @@ __device__ __forceinline__ void store8_nhwc_bf16(const ConvSeg &sg, const Epi &e
     const float4 sh1 = *(const float4 *)(sg.shift + gn + 4);
     const float sc[8] = {sc0.x, sc0.y, sc0.z, sc0.w, sc1.x, sc1.y, sc1.z, sc1.w};
     const float sh[8] = {sh0.x, sh0.y, sh0.z, sh0.w, sh1.x, sh1.y, sh1.z, sh1.w};
-    u16 rv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    if (e.has_res) {
-        const uint4 r4 = *(const uint4 *)((const u16 *)sg.res + off);
-        const u16 *rp = (const u16 *)&r4;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) rv[j] = rp[j];
-    }
-    uint4 o;
-    u16 *op = (u16 *)&o;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const float z = v[j] * sc[j] + sh[j];
-        op[j] = f2bf(epi(z, bf2f(rv[j]), e.has_res, e.res_mode, e.act, e.slope));
-    }
-    *(uint4 *)((u16 *)sg.out + off) = o;
+    u32x4 r4 = {0u, 0u, 0u, 0u};
+    if (e.has_res) r4 = *(const u32x4 *)((const u16 *)sg.res + off);
+    *(u32x4 *)((u16 *)sg.out + off) = epi8_bf16(v, sc, sh, r4, e.kind, e.has_res, e.res_mode, e.act, e.slope);
 }
 
 // Epilogue of 8 consecutive channels of row gm into NHWC fp32.
-__device__ __forceinline__ void store8_nhwc_f32(const ConvSeg &sg, const Epi &e,
+__device__ __forceinline__ void store8_nhwc_f32(const RowSeg &sg, const Epi &e,
                                                 int gm, int gn, const float *v) {
     const size_t off = (size_t)(gm - sg.m_start) * e.out_cs + gn;
 #pragma unroll
@@ -95,7 +179,7 @@ __device__ __forceinline__ void store8_nhwc_f32(const ConvSeg &sg, const Epi &e,
 
 // Epilogue of one element into a caller-owned fp32 NCHW output.
 template <bool BF16>
-__device__ __forceinline__ void store1_nchw_f32(const ConvSeg &sg, const Epi &e,
+__device__ __forceinline__ void store1_nchw_f32(const RowSeg &sg, const Epi &e,
                                                 int gm, int gn, float v) {
     if (gn >= e.cout) return;
     const int lr = gm - sg.m_start;
@@ -166,7 +250,7 @@ __device__ __forceinline__ void splitk_fixup(const ConvArgs &a, int tile, int m0
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
             if (!ok[u]) continue;
-            const ConvSeg &sg = a.seg[seg_of_row(a, gm[u])];
+            const RowSeg sg = row_seg(a, gm[u]);
             if (a.out_mode == OUT_NHWC) {
                 store8_nhwc_bf16(sg, e, gm[u], gn[u], v[u]);
             } else {

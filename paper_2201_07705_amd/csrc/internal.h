@@ -177,6 +177,8 @@ struct Options {
     int autotune = 1;
     int fork_us = 30;
     int splitk_fused = 1;
+    int tune = 1;             // measured conv configuration at plan time
+    int tune_candidates = 4;  // configurations timed per conv shape
     int64_t slot_bytes = 32ll << 20;
     int slots = 3;
     int64_t fail_copy_at = 0;
@@ -213,6 +215,15 @@ struct gemel_ctx {
     std::map<std::vector<int>, std::unique_ptr<gemel::Plan>> plans;
     gemel::Plan *last_plan = nullptr;
     gemel::Profile prof;
+    // plan-time conv tuning: chosen (tile, splits) per conv shape, and the
+    // stream, events and scratch the timing runs use
+    std::map<std::vector<int64_t>, std::pair<int, int>> tune_cache;
+    hipStream_t tune_stream = nullptr;
+    hipEvent_t tune_ev[2] = {nullptr, nullptr};
+    void *tune_partial = nullptr;
+    size_t tune_partial_bytes = 0;
+    void *tune_ctr = nullptr;
+    size_t tune_ctr_bytes = 0;
 };
 
 namespace gemel {

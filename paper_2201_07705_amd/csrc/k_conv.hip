@@ -88,7 +88,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a
         s_last += m_last >= a.seg[i].m_start ? 1 : 0;
     }
     const bool one_seg = s_first == s_last;
-    const ConvSeg &useg = a.seg[s_first];
+    const RowSeg useg = uni_seg(a, s_first);
 
     // ---- loader set-up: thread owns K chunk q of rows r0 + RPP j ----
     const int q = tid & 7, r0 = tid >> 3;
@@ -107,8 +107,8 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a
             if (one_seg) {
                 abase[j] = (const u16 *)useg.in + (size_t)(fr - useg.f_start) * frame_elems;
             } else {
-                const int sg = seg_of_row(a, gm);
-                abase[j] = (const u16 *)a.seg[sg].in + (size_t)(fr - a.seg[sg].f_start) * frame_elems;
+                const RowSeg sg = row_seg(a, gm);
+                abase[j] = (const u16 *)sg.in + (size_t)(fr - sg.f_start) * frame_elems;
             }
             ahi[j] = ho * a.stride - a.pad;
             awi[j] = wo * a.stride - a.pad;
@@ -221,7 +221,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a
                 if (one_seg) {
                     p = (const u16 *)useg.res + (size_t)(gm - useg.m_start) * e.out_cs + my_gn;
                 } else {
-                    const ConvSeg &sg = a.seg[seg_of_row(a, gm)];
+                    const RowSeg sg = row_seg(a, gm);
                     p = (const u16 *)sg.res + (size_t)(gm - sg.m_start) * e.out_cs + my_gn;
                 }
             }
@@ -305,35 +305,24 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a
                         outp = (u16 *)useg.out;
                         ms = useg.m_start;
                     } else {
-                        const ConvSeg &sg = a.seg[seg_of_row(a, gm)];
+                        const RowSeg sg = row_seg(a, gm);
                         resp = (const u16 *)sg.res;
                         outp = (u16 *)sg.out;
                         ms = sg.m_start;
                     }
                     const size_t off = (size_t)(gm - ms) * e.out_cs + gn;
-                    u16 rv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                    u32x4 r4 = {0u, 0u, 0u, 0u};
                     if (e.has_res) {
-                        u32x4 r4;
                         if constexpr (RES_PF)
                             r4 = rpf[(item - tid) / NT];
                         else
                             r4 = *(const u32x4 *)(resp + off);
-#pragma unroll
-                        for (int jj = 0; jj < 4; ++jj) {
-                            rv[2 * jj] = (u16)(r4[jj] & 0xffffu);
-                            rv[2 * jj + 1] = (u16)(r4[jj] >> 16);
-                        }
                     }
-                    uint4 o;
-                    u16 *op = (u16 *)&o;
-#pragma unroll
-                    for (int jj = 0; jj < 8; ++jj)
-                        op[jj] = f2bf(epi(v[jj] * sc[jj] + sh[jj], bf2f(rv[jj]), e.has_res, e.res_mode, e.act, e.slope));
-                    *(uint4 *)(outp + off) = o;
+                    *(u32x4 *)(outp + off) = epi8_bf16(v, sc, sh, r4, e.kind, e.has_res, e.res_mode, e.act, e.slope);
                 } else if (one_seg) {
                     store8_nhwc_bf16(useg, e, gm, gn, v);
                 } else {
-                    store8_nhwc_bf16(a.seg[seg_of_row(a, gm)], e, gm, gn, v);
+                    store8_nhwc_bf16(row_seg(a, gm), e, gm, gn, v);
                 }
             }
         } else {
@@ -344,7 +333,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a
                 if (one_seg)
                     store1_nchw_f32<true>(useg, e, gm, gn, Cs[rl * LDC + col]);
                 else
-                    store1_nchw_f32<true>(a.seg[seg_of_row(a, gm)], e, gm, gn, Cs[rl * LDC + col]);
+                    store1_nchw_f32<true>(row_seg(a, gm), e, gm, gn, Cs[rl * LDC + col]);
             }
         }
         __syncthreads();
@@ -367,7 +356,7 @@ __global__ __launch_bounds__(256) void conv_reduce_kernel(const ReduceArgs ra) {
         v[4] += p1.x; v[5] += p1.y; v[6] += p1.z; v[7] += p1.w;
     }
     const Epi e = epi_of(ra, ra.HWo);
-    const ConvSeg &sg = ra.seg[seg_of_row(ra, gm)];
+    const RowSeg sg = row_seg(ra, gm);
     if (ra.out_mode == OUT_NHWC) {
         if (BF16)
             store8_nhwc_bf16(sg, e, gm, gn, v);
@@ -384,8 +373,7 @@ __global__ __launch_bounds__(256) void conv_f32_kernel(const ConvArgs a) {
     if (idx >= (long)a.M * a.N) return;
     const int gm = (int)(idx / a.N), gn = (int)(idx - (long)gm * a.N);
     const int HWo = a.Ho * a.Wo;
-    const int s = seg_of_row(a, gm);
-    const ConvSeg &sg = a.seg[s];
+    const RowSeg sg = row_seg(a, gm);
     const int fr = gm / HWo, pix = gm - fr * HWo;
     const int ho = pix / a.Wo, wo = pix - ho * a.Wo;
     const float *in = (const float *)sg.in + (size_t)(fr - sg.f_start) * a.H * a.W * a.in_cs;

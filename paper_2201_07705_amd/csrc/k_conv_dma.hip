@@ -77,10 +77,9 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
     static_assert(AI * NT == A_SLOTS && BI * NT == B_SLOTS && AI >= 1 && BI >= 1, "tile/threads");
     constexpr int STAGE_BYTES = (A_SLOTS + B_SLOTS) * 16;
     constexpr int EPI_LD = TN + 4;                              // fp32 row pitch of a wave's staging
-    constexpr int HALF = (NW + 1) / 2;                          // waves staging in each of st0, st1
-    static_assert(HALF * 16 * EPI_LD * 4 <= STAGE_BYTES, "epilogue staging must fit two stages");
     static_assert(STAGES >= 2 && STAGES <= 4, "stages");
-    static_assert(TN == 64, "a lane owns one 8-channel chunk of its wave's 64 columns");
+    static_assert(TN % 8 == 0 && 64 % (TN / 8) == 0 && TN <= 512,
+                  "every epilogue item of a lane is the same 8-channel chunk of its wave's columns");
     constexpr int PER_STEP = AI + BI;                           // vm ops per thread per step
     __shared__ __attribute__((aligned(1024))) unsigned char st0[STAGE_BYTES];
     __shared__ __attribute__((aligned(1024))) unsigned char st1[STAGE_BYTES];
@@ -112,7 +111,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
         s_last += m_last >= a.seg[i].m_start ? 1 : 0;
     }
     const bool one_seg = s_first == s_last;
-    const ConvSeg &useg = a.seg[s_first];
+    const RowSeg useg = uni_seg(a, s_first);
 
     // ---- DMA assignment: instruction i of this thread fills slot
     // (i*NW + wave)*64 + lane: row (i*NW + wave)*RPI + lane/CPR; the slot's
@@ -132,12 +131,8 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
             const int fr = gm / HWo;
             const int pix = gm - fr * HWo;
             const int ho = pix / a.Wo, wo = pix - (pix / a.Wo) * a.Wo;
-            if (one_seg) {
-                abase[i] = (const u16 *)useg.in + (size_t)(fr - useg.f_start) * frame_elems;
-            } else {
-                const int sg = seg_of_row(a, gm);
-                abase[i] = (const u16 *)a.seg[sg].in + (size_t)(fr - a.seg[sg].f_start) * frame_elems;
-            }
+            const RowSeg sg = one_seg ? useg : row_seg(a, gm);
+            abase[i] = (const u16 *)sg.in + (size_t)(fr - sg.f_start) * frame_elems;
             ahi[i] = ho * a.stride - a.pad;
             awi[i] = wo * a.stride - a.pad;
         }
@@ -227,7 +222,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
 
     // epilogue constants of this lane's 8 channels (every segment shares
     // one scale/shift pair), fetched ahead of the depth loop
-    const int my_gn = tn * BN + wn * TN + (lane & 7) * 8;
+    const int my_gn = tn * BN + wn * TN + (lane % (TN / 8)) * 8;
     f32x4 sc0 = {1.f, 1.f, 1.f, 1.f}, sc1 = sc0, sh0 = {0.f, 0.f, 0.f, 0.f}, sh1 = sh0;
     if (a.k_splits <= 1 && my_gn < N) {
         const float *scl = a.seg[0].scale + my_gn, *shl = a.seg[0].shift + my_gn;
@@ -320,73 +315,99 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
         }
     }
 
-    // ---- epilogue: each wave stages 16 rows of its tile at a time ----
+    // ---- epilogue: each wave stages PG passes of 16 rows of its tile at a
+    // time in its share of the stage buffers. Only the accumulator dump is
+    // unrolled per pass; the store code exists once (a kernel larger than
+    // the instruction cache pays for its cold misses on every launch).
+    constexpr int WPS = (NW + STAGES - 1) / STAGES;             // waves per stage buffer
+    constexpr int PASS_FLOATS = 16 * EPI_LD;
+    constexpr int GMAX = STAGE_BYTES / (WPS * PASS_FLOATS * 4);
+    static_assert(GMAX >= 1, "a 16-row pass must fit a wave's share of a stage buffer");
+    constexpr int PG = (GMAX >= 4 && FM % 4 == 0) ? 4 : (GMAX >= 2 && FM % 2 == 0) ? 2 : 1;
+    constexpr int NGRP = FM / PG;
+    constexpr int CHW = TN / 8;                                 // 8-channel chunks per wave row
+    constexpr int ITEMS = PG * 16 * CHW / 64;                    // (row, chunk) items per lane per group
+    static_assert(ITEMS * 64 == PG * 16 * CHW, "items per lane");
     wait_vm<0>();
     __builtin_amdgcn_s_barrier();
-    float *ew = (float *)((wave < HALF ? st0 : st1) + (wave < HALF ? wave : wave - HALF) * 16 * EPI_LD * 4);
+    const int sidx = wave % STAGES;
+    unsigned char *const sbuf = sidx == 0 ? st0 : sidx == 1 ? st1 : sidx == 2 ? st2 : st3;
+    float *const ew = (float *)(sbuf + (wave / STAGES) * PG * PASS_FLOATS * 4);
     const int out_cs = a.out_cs;
     const __amdgpu_buffer_rsrc_t pr = partial_rsrc(a.partial, (uint32_t)a.k_splits * a.M * N * 4u);
-    StaticFor<FM>::run([&](auto ic) __attribute__((always_inline)) {
-        constexpr int i = decltype(ic)::value;
+    const int ch = lane % CHW;                                  // this lane's chunk in every item
+    const int gn = my_gn;
+    const bool col_ok = gn < N;
+    const bool pre_res = a.has_res && a.out_mode == OUT_NHWC && a.k_splits <= 1;
+    const int ekind = epi_kind(a.act, a.has_res, a.res_mode, a.slope);
+    const float s8[8] = {sc0[0], sc0[1], sc0[2], sc0[3], sc1[0], sc1[1], sc1[2], sc1[3]};
+    const float h8[8] = {sh0[0], sh0[1], sh0[2], sh0[3], sh1[0], sh1[1], sh1[2], sh1[3]};
+#pragma nounroll
+    for (int grp = 0; grp < NGRP; ++grp) {
+        const int row0 = tm * BM + wm * TM + grp * PG * 16;
+        // residuals of the group's items, loaded ahead of the staging
+        u32x4 rv[ITEMS];
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
+        for (int u = 0; u < ITEMS; ++u) {
+            rv[u] = u32x4{0u, 0u, 0u, 0u};
+            const int gm = row0 + (lane + u * 64) / CHW;
+            if (pre_res && col_ok && gm < a.M) {
+                const RowSeg sg = one_seg ? useg : row_seg(a, gm);
+                rv[u] = *(const u32x4 *)((const u16 *)sg.res + (size_t)(gm - sg.m_start) * out_cs + gn);
+            }
+        }
+        StaticFor<NGRP>::run([&](auto gc) __attribute__((always_inline)) {
+            constexpr int gi = decltype(gc)::value;
+            if (grp == gi) {
+                StaticFor<PG>::run([&](auto pc) __attribute__((always_inline)) {
+                    constexpr int pp = decltype(pc)::value;
+                    constexpr int i = gi * PG + pp;
 #pragma unroll
-            for (int v = 0; v < 4; ++v) ew[((lane >> 4) * 4 + v) * EPI_LD + j * 16 + (lane & 15)] = acc[i][j][v];
+                    for (int j = 0; j < FN; ++j)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v)
+                            ew[(pp * 16 + (lane >> 4) * 4 + v) * EPI_LD + j * 16 + (lane & 15)] = acc[i][j][v];
+                });
+            }
+        });
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        for (int item = lane; item < 16 * (TN / 8); item += 64) {
-            const int rl = item / (TN / 8), ch = item - (item / (TN / 8)) * (TN / 8);
-            const int gm = tm * BM + wm * TM + i * 16 + rl;
-            const int gn = tn * BN + wn * TN + ch * 8;
-            if (gm >= a.M || gn >= N) continue;
+        // the residual loads (and the previous group's stores) complete
+        // here, once: with none pending, the compiler needs no wait between
+        // the stores below (vmcnt counts loads and stores together, so a
+        // wait for a load would also wait for every earlier store). Without
+        // a residual nothing is waited for: the epilogue kinds without one
+        // never read the residual registers.
+        if (pre_res) wait_vm<0>();
+#pragma unroll
+        for (int u = 0; u < ITEMS; ++u) {
+            const int rl = (lane + u * 64) / CHW;
+            const int gm = row0 + rl;
+            if (!col_ok || gm >= a.M) continue;
             const float *src = ew + rl * EPI_LD + ch * 8;
             const float4 v0 = *(const float4 *)src, v1 = *(const float4 *)(src + 4);
-            float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
             if (a.k_splits > 1) {
                 const uint32_t off = (uint32_t)((((int)blockIdx.y * a.M + gm) * N + gn) * 4u);
                 store_partial4(pr, off, v0);
                 store_partial4(pr, off + 16, v1);
                 continue;
             }
-            const u16 *resp;
-            void *outp;
-            int ms;
-            if (one_seg) {
-                resp = (const u16 *)useg.res;
-                outp = useg.out;
-                ms = useg.m_start;
-            } else {
-                const ConvSeg &sg = a.seg[seg_of_row(a, gm)];
-                resp = (const u16 *)sg.res;
-                outp = sg.out;
-                ms = sg.m_start;
-            }
-            const int lr_ = gm - ms;
-            const float s8[8] = {sc0[0], sc0[1], sc0[2], sc0[3], sc1[0], sc1[1], sc1[2], sc1[3]};
-            const float h8[8] = {sh0[0], sh0[1], sh0[2], sh0[3], sh1[0], sh1[1], sh1[2], sh1[3]};
+            const float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+            const RowSeg sg = one_seg ? useg : row_seg(a, gm);
+            const int lr_ = gm - sg.m_start;
             if (a.out_mode == OUT_NHWC) {
                 const size_t off = (size_t)lr_ * out_cs + gn;
-                u32x4 r4 = {0u, 0u, 0u, 0u};
-                if (a.has_res) r4 = *(const u32x4 *)(resp + off);
-                u32x4 o;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const float r0 = bf2f((u16)(r4[q] & 0xffffu)), r1 = bf2f((u16)(r4[q] >> 16));
-                    const u16 y0 = f2bf(epi(v[2 * q] * s8[2 * q] + h8[2 * q], r0, a.has_res, a.res_mode, a.act, a.slope));
-                    const u16 y1 = f2bf(epi(v[2 * q + 1] * s8[2 * q + 1] + h8[2 * q + 1], r1, a.has_res, a.res_mode,
-                                                a.act, a.slope));
-                    o[q] = (uint32_t)y0 | ((uint32_t)y1 << 16);
-                }
-                *(u32x4 *)((u16 *)outp + off) = o;
+                *(u32x4 *)((u16 *)sg.out + off) =
+                    epi8_bf16(v, s8, h8, rv[u], ekind, a.has_res, a.res_mode, a.act, a.slope);
             } else {
                 const int f = lr_ / HWo, pix = lr_ - (lr_ / HWo) * HWo;
-#pragma unroll
+                const u16 *resp = (const u16 *)sg.res;
                 for (int q = 0; q < 8; ++q) {
                     const int c = gn + q;
                     if (c >= a.cout) break;
                     const float r = a.has_res ? bf2f(resp[(size_t)lr_ * out_cs + c]) : 0.f;
-                    ((float *)outp)[((size_t)f * a.cout + c) * HWo + pix] =
+                    ((float *)sg.out)[((size_t)f * a.cout + c) * HWo + pix] =
                         epi(v[q] * s8[q] + h8[q], r, a.has_res, a.res_mode, a.act, a.slope);
                 }
             }
@@ -394,7 +415,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    });
+    }
     if (a.k_splits > 1 && a.counters) splitk_fixup<64 * WM * WN>(a, t, tm * BM, BM, tn * BN, BN, (int *)st2);
 }
 

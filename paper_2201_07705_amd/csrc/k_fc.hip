@@ -28,9 +28,9 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ float fc_bf2f(u16 h) { return __uint_as_float((uint32_t)h << 16); }
 __device__ __forceinline__ u16 fc_f2bf(float f) { return __builtin_bit_cast(u16, (__bf16)f); }
 __device__ __forceinline__ float fc_act(float y, int act, float slope) {
-    if (act == 1) return fmaxf(y, 0.f);
-    if (act == 2) return y > 0.f ? y : y * slope;
-    return y;
+    const float relu = fmaxf(y, 0.f);
+    const float leaky = y > 0.f ? y : y * slope;
+    return act == 1 ? relu : act == 2 ? leaky : y;
 }
 
 // Segment holding launch frame f: the last one with f_start <= f.

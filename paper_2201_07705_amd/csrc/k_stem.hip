@@ -38,15 +38,17 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float s_bf2f(u16 h) { return __uint_as_float((uint32_t)h << 16); }
 __device__ __forceinline__ u16 s_f2bf(float f) { return __builtin_bit_cast(u16, (__bf16)f); }
+// Epilogue with selects on the launch-wide flags (branches would let the
+// compiler duplicate the unrolled store code per flag combination).
 __device__ __forceinline__ float s_act(float y, int act, float slope) {
-    if (act == 1) return fmaxf(y, 0.f);
-    if (act == 2) return y > 0.f ? y : y * slope;
-    return y;
+    const float relu = fmaxf(y, 0.f);
+    const float leaky = y > 0.f ? y : y * slope;
+    return act == 1 ? relu : act == 2 ? leaky : y;
 }
 __device__ __forceinline__ float s_epi(float z, float r, int has_res, int res_mode, int act, float slope) {
-    if (!has_res) return s_act(z, act, slope);
-    if (res_mode == 0) return s_act(z + r, act, slope);
-    return s_act(z, act, slope) + r;
+    const bool pre = has_res && res_mode == 0, post = has_res && res_mode != 0;
+    const float u = s_act(pre ? z + r : z, act, slope);
+    return post ? u + r : u;
 }
 
 template <int I>
@@ -93,10 +95,25 @@ __global__ __launch_bounds__(256) void conv_stem_kernel(const ConvArgs a) {
         s_last += m_last >= a.seg[i].m_start ? 1 : 0;
     }
     const bool one_seg = s_first == s_last;
-    auto seg_of = [&](int m) __attribute__((always_inline)) {
-        int sx = 0;
-        for (int i = 1; i < a.nseg; ++i) sx += (m >= a.seg[i].m_start) ? 1 : 0;
-        return sx;
+    // fields of the segment holding pixel m, gathered with uniform loads and
+    // selects (a per-lane index into the argument block's segment table
+    // would make each field a per-lane global load)
+    struct SegF {
+        const void *in, *res;
+        void *out;
+        int m_start, f_start;
+    };
+    auto seg_at = [&](int m) __attribute__((always_inline)) {
+        SegF r{a.seg[0].in, a.seg[0].res, a.seg[0].out, a.seg[0].m_start, a.seg[0].f_start};
+        for (int i = 1; i < a.nseg; ++i) {
+            const bool hit = m >= a.seg[i].m_start;
+            r.in = hit ? a.seg[i].in : r.in;
+            r.res = hit ? a.seg[i].res : r.res;
+            r.out = hit ? a.seg[i].out : r.out;
+            r.m_start = hit ? a.seg[i].m_start : r.m_start;
+            r.f_start = hit ? a.seg[i].f_start : r.f_start;
+        }
+        return r;
     };
 
     // this lane's pixel in each of the wave's PF pixel fragments
@@ -115,8 +132,8 @@ __global__ __launch_bounds__(256) void conv_stem_kernel(const ConvArgs a) {
             if (one_seg) {
                 pbase[I] = in_u + (size_t)(fr - f_u) * H * W * 8;
             } else {
-                const int sx = seg_of(m);
-                pbase[I] = (const u16 *)a.seg[sx].in + (size_t)(fr - a.seg[sx].f_start) * H * W * 8;
+                const SegF g = seg_at(m);
+                pbase[I] = (const u16 *)g.in + (size_t)(fr - g.f_start) * H * W * 8;
             }
             phi[I] = ho * a.stride - a.pad;
             pwi[I] = wo * a.stride - a.pad;
@@ -198,6 +215,13 @@ __global__ __launch_bounds__(256) void conv_stem_kernel(const ConvArgs a) {
     const void *const res_u = a.seg[s_first].res;
     const int ms_u = a.seg[s_first].m_start;
 
+    // epilogue kind: 0 none, 1 ReLU, 2 ReLU after the residual add, 3 leaky
+    // ReLU with 0 <= slope <= 1 (max(y, slope * y)), 4 anything else
+    const int skind = (!a.has_res && a.act == 0)                                  ? 0
+                      : (!a.has_res && a.act == 1)                                ? 1
+                      : (a.has_res && a.res_mode == 0 && a.act == 1)              ? 2
+                      : (!a.has_res && a.act == 2 && a.slope >= 0.f && a.slope <= 1.f) ? 3
+                                                                                  : 4;
     // epilogue: for each pixel fragment I and fragment pair j the lane holds
     // channels c0..c0+7 of pixel m (acc[I][2j] then acc[I][2j+1])
     SFor<PF>::run([&](auto I) __attribute__((always_inline)) {
@@ -211,10 +235,10 @@ __global__ __launch_bounds__(256) void conv_stem_kernel(const ConvArgs a) {
             resp = res_u;
             ml = m - ms_u;
         } else {
-            const int sx = seg_of(m);
-            outp = a.seg[sx].out;
-            resp = a.seg[sx].res;
-            ml = m - a.seg[sx].m_start;
+            const SegF g = seg_at(m);
+            outp = g.out;
+            resp = g.res;
+            ml = m - g.m_start;
         }
         SFor<NF / 2>::run([&](auto JP) __attribute__((always_inline)) {
             constexpr int j0 = 2 * JP, j1 = 2 * JP + 1;
@@ -235,12 +259,30 @@ __global__ __launch_bounds__(256) void conv_stem_kernel(const ConvArgs a) {
                     rv[2 * q + 1] = s_bf2f((u16)(rr[q] >> 16));
                 });
             }
-            float y[8];
+            float z[8], y[8];
             SFor<4>::run([&](auto V) __attribute__((always_inline)) {
                 constexpr int v = V;
-                y[v] = s_epi(acc[I][j0][v] * sc0[v] + sh0[v], rv[v], a.has_res, a.res_mode, a.act, a.slope);
-                y[4 + v] = s_epi(acc[I][j1][v] * sc1[v] + sh1[v], rv[4 + v], a.has_res, a.res_mode, a.act, a.slope);
+                z[v] = acc[I][j0][v] * sc0[v] + sh0[v];
+                z[4 + v] = acc[I][j1][v] * sc1[v] + sh1[v];
             });
+            // short sequences for the common epilogues (uniform switch)
+            switch (skind) {
+            case 0:
+                for (int v = 0; v < 8; ++v) y[v] = z[v];
+                break;
+            case 1:
+                for (int v = 0; v < 8; ++v) y[v] = fmaxf(z[v], 0.f);
+                break;
+            case 2:
+                for (int v = 0; v < 8; ++v) y[v] = fmaxf(z[v] + rv[v], 0.f);
+                break;
+            case 3:
+                for (int v = 0; v < 8; ++v) y[v] = fmaxf(z[v], z[v] * a.slope);
+                break;
+            default:
+                for (int v = 0; v < 8; ++v) y[v] = s_epi(z[v], rv[v], a.has_res, a.res_mode, a.act, a.slope);
+                break;
+            }
             if (a.out_mode == OUT_NHWC) {
                 u32x4 o;
                 SFor<4>::run([&](auto Q) __attribute__((always_inline)) {

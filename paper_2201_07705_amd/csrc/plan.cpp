@@ -125,6 +125,17 @@ void drop_plans(gemel_ctx *ctx) {
 void release_device(gemel_ctx *ctx) {
     drop_plans(ctx);
     free_placement(ctx);
+    if (ctx->tune_stream) (void)hipStreamSynchronize(ctx->tune_stream);
+    if (ctx->tune_stream) (void)hipStreamDestroy(ctx->tune_stream);
+    ctx->tune_stream = nullptr;
+    for (auto &ev : ctx->tune_ev) {
+        if (ev) (void)hipEventDestroy(ev);
+        ev = nullptr;
+    }
+    if (ctx->tune_partial) (void)hipFree(ctx->tune_partial);
+    if (ctx->tune_ctr) (void)hipFree(ctx->tune_ctr);
+    ctx->tune_partial = ctx->tune_ctr = nullptr;
+    ctx->tune_partial_bytes = ctx->tune_ctr_bytes = 0;
     if (ctx->side) (void)hipStreamDestroy(ctx->side);
     ctx->side = nullptr;
     for (auto w : ctx->workers) (void)hipStreamDestroy(w);
@@ -320,37 +331,180 @@ static const TileCost kTileCost[] = {
 // Partial sums of one split-K launch are addressed with 32-bit byte offsets.
 constexpr int64_t kMaxPartialBytes = 0x7fffffff;
 
-// dma_depth: deepest LDS-DMA step the conv allows (0: no DMA tile, 32 or 64).
-void pick_conv_config(int64_t M, int64_t N, int64_t K, int dma_depth, int force, int force_splits, int &tile,
-                      int &splits, int &kps) {
+// One launch configuration of a conv and its estimated time.
+struct ConvCand {
+    double est;
+    int tile, splits;
+};
+
+// Every (tile, split-K) configuration the conv may use, fastest estimate
+// first. dma_depth: deepest LDS-DMA step the conv allows (0: no DMA tile,
+// 32 or 64); force >= 0 restricts the tile.
+std::vector<ConvCand> conv_candidates(int64_t M, int64_t N, int64_t K, int dma_depth, int force) {
     const double cu_flops = 4096.0 * 2.4e9;   // per CU, dense bf16
-    double best = 1e300;
-    tile = force >= 0 ? force : TILE_64x64;
-    splits = 1;
+    std::vector<ConvCand> out;
     for (const TileCost &tc : kTileCost) {
         if (force >= 0 && tc.tile != force) continue;
         if (force < 0 && tile_is_dma(tc.tile) && tile_dma_depth(tc.tile) > dma_depth) continue;
         const int64_t bm = conv_tile_bm(tc.tile), bn = conv_tile_bn(tc.tile);
         const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+        int last = 0;
         for (int s = 1; s <= 16; s *= 2) {
             if (s > 1 && K / s < 4 * CONV_BK) break;
             const int64_t k_s = round_up((K + s - 1) / s, CONV_BK);
             const int64_t s_eff = (K + k_s - 1) / k_s;
             if (s_eff > 1 && s_eff * M * N * 4 > kMaxPartialBytes) break;
+            if (s_eff == last) continue;
+            last = (int)s_eff;
             const double waves = std::ceil((double)(tiles * s_eff) / (256.0 * tc.occ));
             double t = waves * (tc.occ * (2.0 * bm * bn * k_s) / (cu_flops * tc.eff) + tc.lat);
             if (s_eff > 1) t += (double)s_eff * M * N * 4.0 * 2.0 / 4e12 + 2e-6;
-            if (t < best) {
-                best = t;
-                tile = tc.tile;
-                splits = (int)s_eff;
-            }
+            out.push_back({t, tc.tile, (int)s_eff});
         }
     }
-    if (force_splits > 0) splits = (int)std::min<int64_t>(force_splits, (K + CONV_BK - 1) / CONV_BK);
-    while (splits > 1 && (int64_t)splits * M * N * 4 > kMaxPartialBytes) --splits;
+    std::stable_sort(out.begin(), out.end(), [](const ConvCand &x, const ConvCand &y) { return x.est < y.est; });
+    return out;
+}
+
+// Depth per split for `splits` splits (a multiple of the conv step); the
+// split count is then the number of splits that depth needs.
+void conv_split_depth(int64_t K, int &splits, int &kps) {
     kps = (int)round_up((K + splits - 1) / splits, CONV_BK);
     splits = (int)((K + kps - 1) / kps);
+}
+
+// Launch configuration of a bf16 implicit-GEMM conv of size M x N x K:
+// the candidate with the smallest estimated time (or the forced tile /
+// split count).
+void pick_conv_config(int64_t M, int64_t N, int64_t K, int dma_depth, int force, int force_splits, int &tile,
+                      int &splits, int &kps) {
+    const std::vector<ConvCand> c = conv_candidates(M, N, K, dma_depth, force);
+    tile = c.empty() ? (force >= 0 ? force : TILE_64x64) : c[0].tile;
+    splits = c.empty() ? 1 : c[0].splits;
+    if (force_splits > 0) splits = (int)std::min<int64_t>(force_splits, (K + CONV_BK - 1) / CONV_BK);
+    while (splits > 1 && (int64_t)splits * M * N * 4 > kMaxPartialBytes) --splits;
+    conv_split_depth(K, splits, kps);
+}
+
+// Split-K partial sums reduced inside the GEMM launch (by the last split of
+// each tile): only as many workgroups as tiles share that work, so with
+// fewer tiles than compute units a separate reduction launch (one
+// workgroup per 2048 outputs) is faster (measured).
+bool fuse_splitk(const gemel_ctx *ctx, int tiles) {
+    return ctx->opt.splitk_fused == 2 || (ctx->opt.splitk_fused == 1 && tiles >= 256);
+}
+
+// Argument block of the separate split-K reduction of conv launch a.
+ReduceArgs reduce_args(const ConvArgs &a) {
+    ReduceArgs r{};
+    r.partial = a.partial;
+    r.M = a.M; r.N = a.N; r.splits = a.k_splits; r.HWo = a.Ho * a.Wo;
+    r.out_cs = a.out_cs; r.cout = a.cout; r.act = a.act; r.slope = a.slope;
+    r.res_mode = a.res_mode; r.has_res = a.has_res; r.out_mode = a.out_mode;
+    r.nseg = a.nseg;
+    for (int i = 0; i < a.nseg; ++i) r.seg[i] = a.seg[i];
+    return r;
+}
+
+// Measured choice among the best-estimated configurations of one conv
+// launch: each candidate runs on the context's tuning stream over the
+// plan's own tensors (their contents are overwritten by every round), one
+// untimed run then three timed with HIP events; the fastest wins. Results
+// are cached per conv shape for the life of the context. Returns false
+// (leaving tile/splits/kps alone) if nothing could be timed.
+bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int &tile, int &splits, int &kps) {
+    std::vector<int64_t> key = {a0.M, a0.N, a0.K, a0.H, a0.W, a0.Cin, a0.in_cs, a0.kh, a0.kw, a0.stride, a0.pad,
+                                a0.out_cs, a0.has_res, a0.out_mode, a0.nseg > 1, dma_depth, ctx->opt.splitk_fused};
+    auto hit = ctx->tune_cache.find(key);
+    if (hit != ctx->tune_cache.end()) {
+        tile = hit->second.first;
+        splits = hit->second.second;
+        conv_split_depth(a0.K, splits, kps);
+        return true;
+    }
+    std::vector<ConvCand> c = conv_candidates(a0.M, a0.N, a0.K, dma_depth, -1);
+    if (c.empty()) return false;
+    const double cut = 2.0 * c[0].est;
+    size_t n = 0;
+    while (n < c.size() && n < (size_t)ctx->opt.tune_candidates && c[n].est <= cut) ++n;
+    if (n < 2) return false;
+    c.resize(n);
+    // scratch: partial sums and arrival counters of the largest candidate
+    size_t pbytes = 0, cbytes = 0;
+    for (const ConvCand &k : c) {
+        const int64_t bm = conv_tile_bm(k.tile), bn = conv_tile_bn(k.tile);
+        if (k.splits > 1) pbytes = std::max(pbytes, (size_t)k.splits * a0.M * a0.N * 4);
+        cbytes = std::max(cbytes, (size_t)(((a0.M + bm - 1) / bm) * ((a0.N + bn - 1) / bn)) * 4);
+    }
+    if (!ctx->tune_stream && hipStreamCreateWithFlags(&ctx->tune_stream, hipStreamNonBlocking) != hipSuccess)
+        return false;
+    if (!ctx->tune_ev[0] && (hipEventCreate(&ctx->tune_ev[0]) != hipSuccess ||
+                             hipEventCreate(&ctx->tune_ev[1]) != hipSuccess))
+        return false;
+    if (pbytes > ctx->tune_partial_bytes) {
+        if (ctx->tune_partial) (void)hipFree(ctx->tune_partial);
+        ctx->tune_partial = nullptr;
+        ctx->tune_partial_bytes = 0;
+        if (hipMalloc(&ctx->tune_partial, pbytes) != hipSuccess) {
+            (void)hipGetLastError();
+            return false;
+        }
+        ctx->tune_partial_bytes = pbytes;
+    }
+    if (cbytes > ctx->tune_ctr_bytes) {
+        if (ctx->tune_ctr) (void)hipFree(ctx->tune_ctr);
+        ctx->tune_ctr = nullptr;
+        ctx->tune_ctr_bytes = 0;
+        if (hipMalloc(&ctx->tune_ctr, cbytes) != hipSuccess) {
+            (void)hipGetLastError();
+            return false;
+        }
+        const std::vector<char> zeros(cbytes, 0);
+        if (hipMemcpy(ctx->tune_ctr, zeros.data(), cbytes, hipMemcpyHostToDevice) != hipSuccess) return false;
+        ctx->tune_ctr_bytes = cbytes;
+    }
+    Sink sk;
+    sk.stream = ctx->tune_stream;
+    double best = 1e300;
+    int bi = -1;
+    for (size_t i = 0; i < c.size(); ++i) {
+        ConvArgs a = a0;
+        int sp = c[i].splits, kp = 0;
+        conv_split_depth(a.K, sp, kp);
+        a.k_splits = sp;
+        a.k_per_split = kp;
+        const int64_t bm = conv_tile_bm(c[i].tile), bn = conv_tile_bn(c[i].tile);
+        const int tiles = (int)(((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn));
+        const bool fuse = sp > 1 && fuse_splitk(ctx, tiles);
+        a.partial = sp > 1 ? (float *)ctx->tune_partial : nullptr;
+        a.counters = fuse ? (int32_t *)ctx->tune_ctr : nullptr;
+        const ReduceArgs r = reduce_args(a);
+        auto once = [&]() {
+            hipError_t e = launch_conv_bf16(a, c[i].tile, sk);
+            if (e == hipSuccess && sp > 1 && !fuse) e = launch_conv_reduce(r, bf16, sk);
+            return e;
+        };
+        bool ok = once() == hipSuccess && hipEventRecord(ctx->tune_ev[0], sk.stream) == hipSuccess;
+        for (int rep = 0; ok && rep < 3; ++rep) ok = once() == hipSuccess;
+        ok = ok && hipEventRecord(ctx->tune_ev[1], sk.stream) == hipSuccess &&
+             hipEventSynchronize(ctx->tune_ev[1]) == hipSuccess;
+        float ms = 0.f;
+        ok = ok && hipEventElapsedTime(&ms, ctx->tune_ev[0], ctx->tune_ev[1]) == hipSuccess;
+        if (!ok) {
+            (void)hipGetLastError();
+            continue;
+        }
+        if (ms < best) {
+            best = ms;
+            bi = (int)i;
+        }
+    }
+    if (hipStreamSynchronize(ctx->tune_stream) != hipSuccess || bi < 0) return false;
+    tile = c[(size_t)bi].tile;
+    splits = c[(size_t)bi].splits;
+    conv_split_depth(a0.K, splits, kps);
+    ctx->tune_cache[key] = {tile, c[(size_t)bi].splits};
+    return true;
 }
 
 void pick_fc_config(int64_t N, int64_t K, int &splits, int &kps) {
@@ -364,8 +518,10 @@ void pick_fc_config(int64_t N, int64_t K, int &splits, int &kps) {
 
 }  // namespace
 
+// can_tune: conv configurations may be timed on the device (not while the
+// caller's stream is being captured into a graph).
 static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, const std::vector<int> &nfr,
-                               Plan &P) {
+                               Plan &P, bool can_tune) {
     const bool bf16 = ctx->dtype == GEMEL_BF16;
     const size_t esz = bf16 ? 2 : 4;
     const int S = (int)ids.size();
@@ -853,6 +1009,11 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     } else {
                         pick_conv_config(a.M, a.N, a.K, dma_depth, ctx->opt.conv_tile == TILE_STEM ? TILE_64x64 : ctx->opt.conv_tile,
                                          ctx->opt.conv_splits, Lc.tile, a.k_splits, a.k_per_split);
+                        // measured choice where nothing is forced and the
+                        // launch's tensors all exist at plan time
+                        if (ctx->opt.tune && can_tune && ctx->opt.conv_tile < 0 && ctx->opt.conv_splits <= 0 && !direct &&
+                            blob->w_dev)
+                            tune_conv(ctx, a, dma_depth, bf16, Lc.tile, a.k_splits, a.k_per_split);
                     }
                     if (tile_is_dma(Lc.tile) && !conv_dma_supported(a, Lc.tile)) Lc.tile = TILE_64x64;
                     Lc.type = L_CONV_BF16;
@@ -865,13 +1026,9 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 }
                 if (a.k_splits > 1) {
                     step_partial[(size_t)step] = std::max(step_partial[(size_t)step], (size_t)a.k_splits * a.M * a.N * 4);
-                    // fused reduction: the last split of each tile reduces it, so
-                    // only as many workgroups as tiles share that work; with
-                    // fewer tiles than compute units a separate reduction
-                    // launch (one workgroup per 2048 outputs) is faster
                     const int bm = conv_tile_bm(Lc.tile), bn = conv_tile_bn(Lc.tile);
                     const int tiles = ((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn);
-                    if (ctx->opt.splitk_fused == 2 || (ctx->opt.splitk_fused == 1 && tiles >= 256)) Lc.ctr_n = tiles;
+                    if (fuse_splitk(ctx, tiles)) Lc.ctr_n = tiles;
                 }
                 P.launches.push_back(Lc);
                 if (a.k_splits > 1 && !Lc.ctr_n) {
@@ -881,12 +1038,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     R.bytes = (double)a.k_splits * a.M * a.N * 4.0;
                     R.bf16 = bf16;
                     R.patches = Lc.patches;
-                    ReduceArgs &r = R.red;
-                    r.M = a.M; r.N = a.N; r.splits = a.k_splits; r.HWo = a.Ho * a.Wo;
-                    r.out_cs = a.out_cs; r.cout = a.cout; r.act = a.act; r.slope = a.slope;
-                    r.res_mode = a.res_mode; r.has_res = a.has_res; r.out_mode = a.out_mode;
-                    r.nseg = a.nseg;
-                    for (int i = 0; i < a.nseg; ++i) r.seg[i] = a.seg[i];
+                    R.red = reduce_args(a);
                     P.launches.push_back(R);
                 }
             }
@@ -1344,7 +1496,10 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         auto P = std::make_unique<Plan>();
         const int saved = ctx->opt.streams;
         ctx->opt.streams = nstreams;
-        st = build_plan(ctx, ids, nfr, *P);
+        hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+        const bool can_tune = stream == nullptr || (hipStreamIsCapturing(stream, &cap) == hipSuccess &&
+                                                    cap == hipStreamCaptureStatusNone);
+        st = build_plan(ctx, ids, nfr, *P, can_tune);
         ctx->opt.streams = saved;
         if (st) {
             if (P->arena) (void)hipFree(P->arena);

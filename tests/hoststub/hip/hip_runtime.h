@@ -74,6 +74,7 @@ hipError_t hipGraphInstantiate(hipGraphExec_t *e, hipGraph_t g, hipGraphNode_t *
 hipError_t hipGraphDestroy(hipGraph_t g);
 hipError_t hipGraphExecDestroy(hipGraphExec_t e);
 hipError_t hipGraphLaunch(hipGraphExec_t e, hipStream_t s);
+hipError_t hipStreamSynchronize(hipStream_t s);
 #ifdef __cplusplus
 }
 #endif

@@ -65,6 +65,7 @@ std::map<hipGraphExec_t, std::vector<Rng>> execs;    // byte ranges of an instan
 std::map<hipStream_t, std::vector<int>> frontier;    // nodes the next op on a stream follows
 std::map<hipEvent_t, std::vector<int>> evstate;      // nodes an event's record follows
 size_t synced = 0;
+std::vector<int> host_done;                          // nodes the host has waited for
 Node *cur = nullptr;                                 // node of the launch being checked
 
 void begin_node(const gemel::Sink &sk, const char *kern) {
@@ -78,6 +79,7 @@ void begin_node(const gemel::Sink &sk, const char *kern) {
         cur = &u.nodes.back();
     } else {
         n.deps = frontier[sk.stream];
+        n.deps.insert(n.deps.end(), host_done.begin(), host_done.end());
         n.synced = synced;
         eager.nodes.push_back(n);
         frontier[sk.stream] = {(int)eager.nodes.size() - 1};
@@ -182,7 +184,18 @@ hipError_t hipEventCreate(hipEvent_t *e) { *e = (hipEvent_t)std::malloc(16); ret
 hipError_t hipEventCreateWithFlags(hipEvent_t *e, unsigned) { return hipEventCreate(e); }
 hipError_t hipEventDestroy(hipEvent_t e) { evstate.erase(e); std::free(e); return hipSuccess; }
 hipError_t hipEventRecord(hipEvent_t e, hipStream_t s) { evstate[e] = frontier[s]; return hipSuccess; }
-hipError_t hipEventSynchronize(hipEvent_t) { return hipSuccess; }
+// A host wait orders every later operation after what the waited-for event
+// or stream had reached.
+hipError_t hipEventSynchronize(hipEvent_t e) {
+    auto it = evstate.find(e);
+    if (it != evstate.end()) host_done.insert(host_done.end(), it->second.begin(), it->second.end());
+    return hipSuccess;
+}
+hipError_t hipStreamSynchronize(hipStream_t s) {
+    auto it = frontier.find(s);
+    if (it != frontier.end()) host_done.insert(host_done.end(), it->second.begin(), it->second.end());
+    return hipSuccess;
+}
 hipError_t hipEventElapsedTime(float *ms, hipEvent_t, hipEvent_t) { *ms = 0.001f; return hipSuccess; }
 hipError_t hipStreamWaitEvent(hipStream_t s, hipEvent_t e, unsigned) {
     if (!s || !e) return hipErrorInvalidValue;
@@ -266,6 +279,7 @@ hipError_t hipGraphLaunch(hipGraphExec_t e, hipStream_t s) {
     Node n;
     n.kern = "graph";
     n.deps = frontier[s];
+    n.deps.insert(n.deps.end(), host_done.begin(), host_done.end());
     n.synced = synced;
     n.rng = it->second;
     eager.nodes.push_back(n);
