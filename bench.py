@@ -54,7 +54,7 @@ DESCRIPTIONS = {
 # launch shapes; the figure is reported only while they are unchanged.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_conv_r50x2_vgg16x2.md")
 TRAFFIC_SOURCES = ["k_conv.hip", "k_conv_dma.hip", "k_stem.hip", "kernels.h",
-                   "kargs.h", "plan.cpp"]
+                   "kargs.h", "conv_epi.h", "splitk.h", "plan.cpp"]
 
 
 def sources_hash():
