@@ -261,7 +261,7 @@ enum {
                                     it clears the collected statistics.    */
     GEMEL_OPT_CONV_TILE = 7,     /* -1 (default): pick each conv's tile
                                     shape and split-K by the cost model;
-                                    0..17: force one tile shape (128x128,
+                                    0..19: force one tile shape (128x128,
                                     128x64, 64x64, 256x256, 256x128,
                                     256x64, 64x64 and 128x64 with deeper
                                     prefetch, 64x128; then the LDS-DMA
@@ -272,9 +272,10 @@ enum {
                                     without split-K; 14..17: the LDS-DMA
                                     pipeline with depth steps of 64,
                                     256x256, 256x128, 128x128, 128x64, used
-                                    where Cin % 64 == 0) with split-K still
-                                    chosen. A forced tile a conv cannot use
-                                    falls back to 64x64                    */
+                                    where Cin % 64 == 0; 18, 19: LDS-DMA
+                                    64x64 of depth 32 and 64) with split-K
+                                    still chosen. A forced tile a conv
+                                    cannot use falls back to 64x64         */
     GEMEL_OPT_CONV_SPLITS = 8,   /* 0 (default): split-K chosen per conv;
                                     n >= 1: force n depth splits (capped
                                     so that every split has work)          */

@@ -454,6 +454,8 @@ hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) {
     case TILE_DMA_256x128: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<256, 128, 2, 2, 4, 32>), grid, dim3(256), a); break;
     case TILE_DMA_128x128: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<128, 128, 2, 2, 4, 32>), grid, dim3(256), a); break;
     case TILE_DMA_128x64: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<128, 64, 2, 1, 4, 32>), grid, dim3(128), a); break;
+    case TILE_DMA_64x64: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<64, 64, 2, 2, 4, 32>), grid, dim3(256), a); break;
+    case TILE_DMA64_64x64: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<64, 64, 2, 2, 4, 64>), grid, dim3(256), a); break;
     case TILE_DMA64_256x256: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<256, 256, 2, 4, 2, 64>), grid, dim3(512), a); break;
     case TILE_DMA64_256x128: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<256, 128, 2, 2, 3, 64>), grid, dim3(256), a); break;
     case TILE_DMA64_128x128: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<128, 128, 2, 2, 2, 64>), grid, dim3(256), a); break;

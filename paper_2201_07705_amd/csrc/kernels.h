@@ -60,7 +60,10 @@ enum ConvTile {
     TILE_DMA64_256x128 = 15, // 4 waves, 3 stages
     TILE_DMA64_128x128 = 16, // 4 waves, 2 stages
     TILE_DMA64_128x64 = 17,  // 2 waves, 3 stages
-    TILE_COUNT = 18
+    // small tiles for latency-bound layers: 4 waves of 32x32, 4 stages
+    TILE_DMA_64x64 = 18,     // depth 32 (4 workgroups per CU)
+    TILE_DMA64_64x64 = 19,   // depth 64 (2 workgroups per CU)
+    TILE_COUNT = 20
 };
 int conv_tile_threads(int tile);
 int conv_tile_bm(int tile);
@@ -73,9 +76,11 @@ bool conv_dma_supported(const ConvArgs &a, int tile);   // this DMA tile
 hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk);
 inline bool tile_is_dma(int tile) {
     return (tile >= TILE_DMA_256x256 && tile <= TILE_DMA_128x64) ||
-           (tile >= TILE_DMA64_256x256 && tile <= TILE_DMA64_128x64);
+           (tile >= TILE_DMA64_256x256 && tile <= TILE_DMA64_64x64);
 }
-inline int tile_dma_depth(int tile) { return tile >= TILE_DMA64_256x256 ? 64 : 32; }
+inline int tile_dma_depth(int tile) {
+    return (tile >= TILE_DMA64_256x256 && tile <= TILE_DMA64_128x64) || tile == TILE_DMA64_64x64 ? 64 : 32;
+}
 // Stem kernel: Cin == in_cs == 8, no split-K.
 bool conv_stem_supported(const ConvArgs &a);
 hipError_t launch_conv_stem(const ConvArgs &a, const Sink &sk);

@@ -326,6 +326,8 @@ static const TileCost kTileCost[] = {
     {TILE_DMA64_256x128, 0.320, 1, 7.72e-6},
     {TILE_DMA64_128x128, 0.520, 1, 4.83e-6},
     {TILE_DMA64_128x64, 0.370, 3, 5.06e-6},
+    {TILE_DMA_64x64, 0.380, 4, 2.50e-6},
+    {TILE_DMA64_64x64, 0.420, 2, 2.20e-6},
 };
 
 // Partial sums of one split-K launch are addressed with 32-bit byte offsets.

@@ -419,7 +419,7 @@ gemel_status gemel_set_option(gemel_ctx *ctx, int32_t key, int64_t value) {
         drop_plans(ctx);
         break;
     case GEMEL_OPT_CONV_TILE:
-        if (value < -1 || value >= TILE_COUNT) return fail(ctx, GEMEL_EINVAL, "conv tile is -1..17");
+        if (value < -1 || value >= TILE_COUNT) return fail(ctx, GEMEL_EINVAL, "conv tile is -1..19");
         ctx->opt.conv_tile = (int)value;
         drop_plans(ctx);
         break;

@@ -291,9 +291,9 @@ hipError_t hipGraphLaunch(hipGraphExec_t e, hipStream_t s) {
 namespace gemel {
 
 static const int kBm[TILE_COUNT] = {128, 128, 64, 256, 256, 256, 64, 128, 64, 256, 256, 128, 128, 256,
-                                    256, 256, 128, 128};
+                                    256, 256, 128, 128, 64, 64};
 static const int kBn[TILE_COUNT] = {128, 64, 64, 256, 128, 64, 64, 64, 128, 256, 128, 128, 64, 32,
-                                    256, 128, 128, 64};
+                                    256, 128, 128, 64, 64, 64};
 int conv_tile_bm(int t) { return t >= 0 && t < TILE_COUNT ? kBm[t] : 0; }
 int conv_tile_bn(int t) { return t >= 0 && t < TILE_COUNT ? kBn[t] : 0; }
 int conv_tile_threads(int t) { return (t == TILE_256x256 || t == TILE_256x128) ? 512 : 256; }

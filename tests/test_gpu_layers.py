@@ -80,7 +80,7 @@ def test_conv_layer_output_store(dtype, case):
 TILES = ["128x128", "128x64", "64x64", "256x256", "256x128", "256x64",
          "64x64d2", "128x64d2", "64x128", "dma256x256", "dma256x128",
          "dma128x128", "dma128x64", "stem", "dma64_256x256", "dma64_256x128",
-         "dma64_128x128", "dma64_128x64"]
+         "dma64_128x128", "dma64_128x64", "dma64x64", "dma64_64x64"]
 
 
 @pytest.mark.parametrize("tile", range(len(TILES)), ids=lambda t: TILES[t])
