@@ -202,7 +202,7 @@ struct gemel_ctx {
     std::vector<hipStream_t> workers;  // extra streams for concurrent steps
     std::vector<hipEvent_t> ev_copied, ev_free;
     void *wpool = nullptr;           // resident weights + all scale/shift
-    void *zero_page = nullptr;       // 256 zero bytes inside wpool
+    void *zero_page = nullptr;       // GEMEL_ZERO_PAGE_BYTES zero bytes inside wpool
     size_t wpool_bytes = 0;
     void *staging = nullptr;         // slots x slot_bytes
     int staging_slots = 0;

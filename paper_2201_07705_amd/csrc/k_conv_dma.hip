@@ -137,12 +137,13 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
             awi[i] = wo * a.stride - a.pad;
         }
     }
+    // weight rows beyond N read row 0 instead (their columns are never stored)
     const u16 *bbase[BI];
 #pragma unroll
     for (int i = 0; i < BI; ++i) {
         const int rl = (i * NW + wave) * RPI + lane / CPR;
         const int gn = tn * BN + rl;
-        bbase[i] = gn < N ? (const u16 *)a.w + (size_t)gn * K + ((lane % CPR) ^ sw(rl)) * 8 : nullptr;
+        bbase[i] = (const u16 *)a.w + (size_t)(gn < N ? gn : 0) * K + ((lane % CPR) ^ sw(rl)) * 8;
     }
     // loader position (uniform): next step's tap (lr, ls) and channel base lc
     int kb = k_begin, lc, lr, ls;
@@ -152,25 +153,35 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
         lr = rs / kw;
         ls = rs - lr * kw;
     }
-    auto issue = [&](unsigned char *stage) __attribute__((always_inline)) {
+    // each row's source for the current tap, the lane's chunk included: the
+    // pixel, or the zero page where the tap falls outside the image (or the
+    // row beyond M). Recomputed when the tap changes; a depth step only adds
+    // the uniform channel offset (the zero page spans any row's channels).
+    const u16 *arow[AI];
+    auto set_tap = [&]() __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < AI; ++i) {
             const int hi = ahi[i] + lr, wi = awi[i] + ls;
             const bool ok = (unsigned)hi < (unsigned)H && (unsigned)wi < (unsigned)W;
-            const u16 *p = ok ? abase[i] + ((size_t)(hi * W + wi) * in_cs + lc + acq[i] * 8) : zp;
-            __builtin_amdgcn_global_load_lds((const void *)p, (lds_u8 *)(stage + (i * NW + wave) * 1024), 16, 0, 0);
+            arow[i] = (ok ? abase[i] + (size_t)(hi * W + wi) * in_cs : zp) + acq[i] * 8;
         }
+    };
+    set_tap();
+    auto issue = [&](unsigned char *stage) __attribute__((always_inline)) {
 #pragma unroll
-        for (int i = 0; i < BI; ++i) {
-            const u16 *p = bbase[i] ? bbase[i] + kb : zp;
-            __builtin_amdgcn_global_load_lds((const void *)p,
+        for (int i = 0; i < AI; ++i)
+            __builtin_amdgcn_global_load_lds((const void *)(arow[i] + lc), (lds_u8 *)(stage + (i * NW + wave) * 1024),
+                                             16, 0, 0);
+#pragma unroll
+        for (int i = 0; i < BI; ++i)
+            __builtin_amdgcn_global_load_lds((const void *)(bbase[i] + kb),
                                              (lds_u8 *)(stage + A_SLOTS * 16 + (i * NW + wave) * 1024), 16, 0, 0);
-        }
         kb += BK;
         lc += BK;
         if (lc == Cin) {
             lc = 0;
             if (++ls == kw) { ls = 0; ++lr; }
+            set_tap();
         }
     };
 
@@ -420,8 +431,9 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
 }
 
 bool conv_dma_supported(const ConvArgs &a) {
+    // a row outside the image reads the zero page at its channel offset
     return a.Cin % 32 == 0 && a.in_cs % 8 == 0 && a.K % 32 == 0 && a.k_per_split % 32 == 0 && a.zero &&
-           a.uni_affine;
+           a.uni_affine && (long)a.in_cs * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES;
 }
 bool conv_dma_supported(const ConvArgs &a, int tile) {
     if (!conv_dma_supported(a)) return false;

@@ -10,6 +10,9 @@
 #include <stdint.h>
 
 #define GEMEL_MAX_SEG 16
+// Bytes of zeros behind ConvArgs::zero (masked-off loads read there, at up
+// to a pixel's channel offset).
+#define GEMEL_ZERO_PAGE_BYTES 16384
 
 enum { OUT_NHWC = 0, OUT_NCHW_F32 = 1, OUT_PARTIAL_F32 = 2 };
 
@@ -25,7 +28,7 @@ struct ConvSeg {
 
 struct ConvArgs {
     const void *w;        // [N][K], k = (r * kw + s) * Cin + c
-    const void *zero;     // >= 16 zero bytes (target of masked-off loads)
+    const void *zero;     // GEMEL_ZERO_PAGE_BYTES zero bytes (target of masked-off loads)
     int32_t M, N, K;      // rows = frames*Ho*Wo, cols = out channels, depth
     int32_t H, W, Cin;    // input spatial size, physical input channels
     int32_t in_cs;        // input pixel stride in elements (>= Cin)

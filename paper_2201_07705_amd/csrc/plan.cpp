@@ -202,7 +202,7 @@ gemel_status materialise(gemel_ctx *ctx) {
                 return fail(ctx, GEMEL_EBUDGET, "a weight row block does not fit one staging slot");
     }
 
-    size_t pool = aff_total + 256;  // + zero page
+    size_t pool = aff_total + GEMEL_ZERO_PAGE_BYTES;  // + zero page
     for (size_t i = 0; i < blobs.size(); ++i)
         if (resident[i]) pool += (size_t)round_up((int64_t)blobs[i]->w_bytes(), 256);
     if (hipMalloc(&ctx->wpool, pool) != hipSuccess) {
@@ -212,14 +212,14 @@ gemel_status materialise(gemel_ctx *ctx) {
     }
     ctx->wpool_bytes = pool;
     {
-        static const uint8_t zeros[256] = {};
+        static const uint8_t zeros[GEMEL_ZERO_PAGE_BYTES] = {};
         ctx->zero_page = ctx->wpool;
         if (hipMemcpy(ctx->zero_page, zeros, sizeof(zeros), hipMemcpyHostToDevice) != hipSuccess) {
             free_placement(ctx);
             return fail(ctx, GEMEL_EDEVICE, "zero page upload failed");
         }
     }
-    size_t off = 256;
+    size_t off = GEMEL_ZERO_PAGE_BYTES;
     for (size_t i = 0; i < blobs.size(); ++i) {
         Blob &b = *blobs[i];
         ctx->placed.push_back(blobs[i]);

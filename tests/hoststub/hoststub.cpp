@@ -315,7 +315,7 @@ static hipError_t conv_common(const ConvArgs &a, int tile, int esz, const char *
     }
     const long long hwo = (long long)a.Ho * a.Wo;
     ok &= chk(a.w, (long long)a.N * a.K * esz, "weights", kern);
-    if (need_zero) ok &= chk(a.zero, 16, "zero page", kern);
+    if (need_zero) ok &= chk(a.zero, GEMEL_ZERO_PAGE_BYTES, "zero page", kern);
     for (int i = 0; i < a.nseg; ++i) {
         const ConvSeg &s = a.seg[i];
         const long long rows = seg_rows(a.seg, a.nseg, i, a.M);
@@ -345,7 +345,7 @@ static hipError_t conv_common(const ConvArgs &a, int tile, int esz, const char *
 
 bool conv_dma_supported(const ConvArgs &a) {
     return a.Cin % 32 == 0 && a.in_cs % 8 == 0 && a.K % 32 == 0 && a.k_per_split % 32 == 0 && a.zero &&
-           a.uni_affine;
+           a.uni_affine && (long)a.in_cs * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES;
 }
 bool conv_dma_supported(const ConvArgs &a, int tile) {
     if (!conv_dma_supported(a)) return false;
