@@ -15,6 +15,8 @@
 // fc_reduce does). With one split the epilogue is applied directly.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "kargs.h"
 #include "kernels.h"
 #include "splitk.h"
@@ -54,6 +56,10 @@ __device__ __forceinline__ void fc_store(const FcArgs &a, int f, int n, float ac
     }
 }
 
+// Elements of the LDS input slice: frames (16 per block) x (depth per split
+// + 8). The planner keeps MB * 16 * (k_per_split + 8) within it.
+constexpr int FC_X_ELEMS = 32768;
+
 template <int MB>  // frame blocks of 16
 __global__ __launch_bounds__(256) void fc_bf16_kernel(const FcArgs a) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -64,16 +70,25 @@ __global__ __launch_bounds__(256) void fc_bf16_kernel(const FcArgs a) {
     const int g = lane >> 4;
     const bool row_ok = row < a.N;
     const u16 *wrow = (const u16 *)a.w + (size_t)(row_ok ? row : 0) * a.K;
-    const u16 *xrow[MB];
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-        const int f = mb * 16 + (lane & 15);
-        xrow[mb] = nullptr;
-        if (f < a.M) {
+    // the workgroup's slice of the inputs, [frame][k_begin, k_end), staged
+    // in LDS once: every wave reads it, and from LDS its reads need no wait
+    // on a global round trip inside the depth loop. Rows are padded by 16
+    // bytes so that the 16 frames of a fragment fall on distinct banks.
+    // Frames beyond M are left unset: they only feed output columns that are
+    // never stored.
+    __shared__ __attribute__((aligned(16))) u16 xs[FC_X_ELEMS];
+    const int kn = k_end - k_begin;
+    const int pitch = kn + 8;
+    {
+        const int chunks = kn / 8;
+        for (int idx = threadIdx.x; idx < a.M * chunks; idx += 256) {
+            const int f = idx / chunks, c = idx - (idx / chunks) * chunks;
             const FcSeg &sg = a.seg[fc_seg(a, f)];
-            xrow[mb] = (const u16 *)sg.in + (size_t)(f - sg.f_start) * a.K;
+            *(uint4 *)(xs + f * pitch + c * 8) =
+                *(const uint4 *)((const u16 *)sg.in + (size_t)(f - sg.f_start) * a.K + k_begin + c * 8);
         }
     }
+    __syncthreads();
     f32x4 acc[MB];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -93,10 +108,11 @@ __global__ __launch_bounds__(256) void fc_bf16_kernel(const FcArgs a) {
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
             uint4 xv[WJ];
+            const u16 *xr = xs + (mb * 16 + (lane & 15)) * pitch - k_begin;
 #pragma unroll
             for (int j = 0; j < WJ; ++j) {
                 const int kk = k + j * 32 + g * 8;
-                xv[j] = (xrow[mb] && kk < k_end) ? *(const uint4 *)(xrow[mb] + kk) : make_uint4(0, 0, 0, 0);
+                xv[j] = kk < k_end ? *(const uint4 *)(xr + kk) : make_uint4(0, 0, 0, 0);
             }
 #pragma unroll
             for (int j = 0; j < WJ; ++j)
@@ -209,6 +225,7 @@ static bool fc_args_ok(const FcArgs &a) {
 
 hipError_t launch_fc_bf16(const FcArgs &a, const Sink &sk) {
     if (!fc_args_ok(a) || a.M > 64 || (a.k_splits > 1 && a.k_per_split % 128)) return hipErrorInvalidValue;
+    if (((a.M + 15) / 16) * 16 * (long)(std::min(a.K, a.k_per_split) + 8) > FC_X_ELEMS) return hipErrorInvalidValue;
     dim3 grid((unsigned)((a.N + 63) / 64), (unsigned)a.k_splits), block(256);
     const int mb = (a.M + 15) / 16;
     hipError_t e;

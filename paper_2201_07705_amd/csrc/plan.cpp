@@ -509,11 +509,17 @@ bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int
     return true;
 }
 
-void pick_fc_config(int64_t N, int64_t K, int &splits, int &kps) {
+// Split-K of the small-batch FC kernel: enough workgroups to keep HBM busy
+// (about 1024), with each split's input slice (16-frame blocks x depth) fitting
+// the kernel's 64 KB of LDS.
+void pick_fc_config(int64_t M, int64_t N, int64_t K, int &splits, int &kps) {
     const int64_t blocks = (N + 63) / 64;
     const int64_t want = (1024 + blocks - 1) / blocks;
     const int64_t maxs = std::max<int64_t>(1, K / 1024);
+    const int64_t fb = (M + 15) / 16 * 16;
+    const int64_t kps_cap = std::max<int64_t>(128, (32768 / fb - 8) / 128 * 128);
     splits = (int)std::max<int64_t>(1, std::min(want, maxs));
+    splits = (int)std::max<int64_t>(splits, (K + kps_cap - 1) / kps_cap);
     kps = (int)round_up((K + splits - 1) / splits, 128);
     splits = (int)((K + kps - 1) / kps);
 }
@@ -938,7 +944,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                         a.k_per_split = a.K;
                         Lc.type = L_FC_F32;
                     } else {
-                        pick_fc_config(a.N, a.K, a.k_splits, a.k_per_split);
+                        pick_fc_config(a.M, a.N, a.K, a.k_splits, a.k_per_split);
                         Lc.type = L_FC_BF16;
                         if (a.k_splits > 1) {
                             step_partial[(size_t)step] = std::max(step_partial[(size_t)step], (size_t)a.k_splits * a.M * a.N * 4);
