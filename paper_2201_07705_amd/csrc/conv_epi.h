@@ -1,7 +1,8 @@
 // Device helpers shared by the implicit-GEMM conv kernels: the fused
 // epilogue (per-channel scale/shift, residual before or after the
 // activation, ReLU / leaky ReLU, bf16 NHWC or fp32 NCHW stores), the
-// segment lookup of a GEMM row, and the fused split-K reduction.
+// segment fields of a GEMM row (the last segment whose m_start <= row), and
+// the fused split-K reduction.
 #pragma once
 #include <hip/hip_runtime.h>
 
@@ -92,14 +93,6 @@ __device__ __forceinline__ u32x4 epi8_bf16(const float *v, const float *sc, cons
 #pragma unroll
     for (int q = 0; q < 4; ++q) o[q] = (uint32_t)f2bf(y[2 * q]) | ((uint32_t)f2bf(y[2 * q + 1]) << 16);
     return o;
-}
-
-// Segment of GEMM row gm: the last segment whose m_start <= gm.
-template <typename Args>
-__device__ __forceinline__ int seg_of_row(const Args &a, int gm) {
-    int s = 0;
-    for (int i = 1; i < a.nseg; ++i) s += (gm >= a.seg[i].m_start) ? 1 : 0;
-    return s;
 }
 
 // Fields of one segment. The segment table lives in the kernel argument

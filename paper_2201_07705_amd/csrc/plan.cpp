@@ -1003,10 +1003,11 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 for (int i = 1; i < a.nseg; ++i)
                     if (a.seg[i].scale != a.seg[0].scale || a.seg[i].shift != a.seg[0].shift) a.uni_affine = 0;
                 if (bf16) {
-                    const int dma_depth = !(a.in_cs % 8 == 0 && a.uni_affine) ? 0
-                                          : a.Cin % 64 == 0                      ? 64
-                                          : a.Cin % 32 == 0                      ? 32
-                                                                                 : 0;
+                    // DMA tiles: masked rows read the zero page at their
+                    // channel offset, so the pixel stride must fit it
+                    const bool dma_ok = a.in_cs % 8 == 0 && a.uni_affine &&
+                                        (int64_t)a.in_cs * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES;
+                    const int dma_depth = !dma_ok ? 0 : a.Cin % 64 == 0 ? 64 : a.Cin % 32 == 0 ? 32 : 0;
                     // 8-channel inputs (the RGB stems) take the stem kernel
                     const bool stem = a.Cin == 8 && a.in_cs == 8 && a.kh * a.kw <= 64 && a.uni_affine &&
                                       (ctx->opt.conv_tile < 0 || ctx->opt.conv_tile == TILE_STEM);
