@@ -67,6 +67,7 @@ CASES = [
     ("r50x2_vgg16x2", {"res": 64, "frames": 2},
      {"OPT_CONV_SPLITS": 4, "OPT_STREAMS": 8, "OPT_FORK_US": 0,
       "OPT_SPLITK_FUSED": 0}),
+    ("yolov3x3", {"res": 96, "frames": 2}, {"OPT_TUNE": 0}),
     ("mix8_budget40", {"res": 32, "frames": 2}, {}),
     ("mix8_budget40", {"res": 32, "frames": 2},
      {"OPT_SWAP_SLOT_BYTES": 1 << 20, "OPT_SWAP_SLOTS": 2,
