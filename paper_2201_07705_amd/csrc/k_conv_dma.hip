@@ -57,6 +57,17 @@ __device__ __forceinline__ void wait_vm() {
     __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// Waits until at most n steps of PER vm operations each are in flight, for a
+// uniform n in 0 .. MAXN-1 (s_waitcnt takes an immediate, so one branch per
+// count).
+template <int PER, int MAXN>
+__device__ __forceinline__ void wait_steps(int n) {
+    StaticFor<MAXN>::run([&](auto c) __attribute__((always_inline)) {
+        constexpr int i = decltype(c)::value;
+        if (n == i) wait_vm<i * PER>();
+    });
+}
+
 // lgkmcnt(0) only: vmcnt and expcnt left at their maxima (gfx9 encoding).
 __device__ __forceinline__ void wait_lgkm0() {
     __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));
@@ -263,14 +274,14 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
         FragA fa[2];
         FragB fb[2];
         if (nk > 0) {
-            if (STAGES - 2 < nk) wait_vm<(STAGES - 2) * PER_STEP>();
-            else wait_vm<0>();
+            // steps 0 .. min(nk, STAGES-1)-1 were issued; step 0 must land
+            wait_steps<PER_STEP, STAGES - 1>(min(nk - 1, STAGES - 2));
             __builtin_amdgcn_s_barrier();
             read_frags(stg[0], fa[0], fb[0]);
         }
         int base = 0;
         // steady state: every iteration of the group waits, issues the DMA
-        // three steps ahead and reads the next fragments (no branches, so
+        // STAGES-1 steps ahead and reads the next fragments (no branches, so
         // the compiler's wait placement sees one path)
         for (; base + 2 * STAGES - 1 <= nk; base += STAGES) {
 #pragma unroll
@@ -290,9 +301,9 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
                 const int it = base + s;
                 if (it < nk) {
                     if (it + 1 < nk) {
-                        // step it+1 must have landed; newer steps may fly
-                        if (it + STAGES - 2 < nk) wait_vm<(STAGES - 3) * PER_STEP>();
-                        else wait_vm<0>();
+                        // step it+1 must have landed; the newer steps issued
+                        // (up to it+STAGES-2, none beyond nk-1) may fly
+                        wait_steps<PER_STEP, STAGES - 2>(min(nk - it - 2, STAGES - 3));
                         __builtin_amdgcn_s_barrier();
                         if (it + STAGES - 1 < nk) issue(stg[(s + STAGES - 1) % STAGES]);
                         // the fragments read one iteration ago (the operands
@@ -315,9 +326,9 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
             for (int s = 0; s < STAGES; ++s) {
                 const int it = base + s;
                 if (it < nk) {
-                    // step it must have landed; the newer steps may still fly
-                    if (it + STAGES - 2 < nk) wait_vm<(STAGES - 2) * PER_STEP>();
-                    else wait_vm<0>();
+                    // step it must have landed; the newer steps issued (up
+                    // to it+STAGES-2, none beyond nk-1) may still fly
+                    wait_steps<PER_STEP, STAGES - 1>(min(nk - it - 1, STAGES - 2));
                     __builtin_amdgcn_s_barrier();
                     if (it + STAGES - 1 < nk) issue(stg[(s + STAGES - 1) % STAGES]);
                     compute(stg[s]);

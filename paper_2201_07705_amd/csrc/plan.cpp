@@ -410,8 +410,8 @@ ReduceArgs reduce_args(const ConvArgs &a) {
 
 // Measured choice among the best-estimated configurations of one conv
 // launch: each candidate runs on the context's tuning stream over the
-// plan's own tensors (their contents are overwritten by every round), one
-// untimed run then three timed with HIP events; the fastest wins. Results
+// plan's own tensors (their contents are overwritten by every round), timed
+// launch by launch with HIP events; the smallest median wins. Results
 // are cached per conv shape for the life of the context. Returns false
 // (leaving tile/splits/kps alone) if nothing could be timed.
 bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int &tile, int &splits, int &kps) {
@@ -467,9 +467,8 @@ bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int
     }
     Sink sk;
     sk.stream = ctx->tune_stream;
-    double best = 1e300;
-    int bi = -1;
-    for (size_t i = 0; i < c.size(); ++i) {
+    // launch of candidate i
+    auto once = [&](size_t i) {
         ConvArgs a = a0;
         int sp = c[i].splits, kp = 0;
         conv_split_depth(a.K, sp, kp);
@@ -480,24 +479,38 @@ bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int
         const bool fuse = sp > 1 && fuse_splitk(ctx, tiles);
         a.partial = sp > 1 ? (float *)ctx->tune_partial : nullptr;
         a.counters = fuse ? (int32_t *)ctx->tune_ctr : nullptr;
-        const ReduceArgs r = reduce_args(a);
-        auto once = [&]() {
-            hipError_t e = launch_conv_bf16(a, c[i].tile, sk);
-            if (e == hipSuccess && sp > 1 && !fuse) e = launch_conv_reduce(r, bf16, sk);
-            return e;
-        };
-        bool ok = once() == hipSuccess && hipEventRecord(ctx->tune_ev[0], sk.stream) == hipSuccess;
-        for (int rep = 0; ok && rep < 3; ++rep) ok = once() == hipSuccess;
-        ok = ok && hipEventRecord(ctx->tune_ev[1], sk.stream) == hipSuccess &&
-             hipEventSynchronize(ctx->tune_ev[1]) == hipSuccess;
-        float ms = 0.f;
-        ok = ok && hipEventElapsedTime(&ms, ctx->tune_ev[0], ctx->tune_ev[1]) == hipSuccess;
-        if (!ok) {
-            (void)hipGetLastError();
-            continue;
+        hipError_t e = launch_conv_bf16(a, c[i].tile, sk);
+        if (e == hipSuccess && sp > 1 && !fuse) e = launch_conv_reduce(reduce_args(a), bf16, sk);
+        return e;
+    };
+    // one untimed pass over every candidate, then kTuneReps passes timing
+    // each launch on its own with the candidates interleaved (a clock that
+    // is still rising, or any other drift, then affects all of them alike);
+    // the median of a candidate's times decides
+    constexpr int kTuneReps = 7;
+    std::vector<bool> ok(c.size(), true);
+    std::vector<std::vector<float>> ms(c.size());
+    for (size_t i = 0; i < c.size(); ++i) ok[i] = once(i) == hipSuccess;
+    for (int rep = 0; rep < kTuneReps; ++rep) {
+        for (size_t i = 0; i < c.size(); ++i) {
+            if (!ok[i]) continue;
+            float t = 0.f;
+            ok[i] = hipEventRecord(ctx->tune_ev[0], sk.stream) == hipSuccess && once(i) == hipSuccess &&
+                    hipEventRecord(ctx->tune_ev[1], sk.stream) == hipSuccess &&
+                    hipEventSynchronize(ctx->tune_ev[1]) == hipSuccess &&
+                    hipEventElapsedTime(&t, ctx->tune_ev[0], ctx->tune_ev[1]) == hipSuccess;
+            if (ok[i]) ms[i].push_back(t);
         }
-        if (ms < best) {
-            best = ms;
+    }
+    (void)hipGetLastError();
+    double best = 1e300;
+    int bi = -1;
+    for (size_t i = 0; i < c.size(); ++i) {
+        if (!ok[i] || ms[i].empty()) continue;
+        std::vector<float> v = ms[i];
+        std::nth_element(v.begin(), v.begin() + v.size() / 2, v.end());
+        if (v[v.size() / 2] < best) {
+            best = v[v.size() / 2];
             bi = (int)i;
         }
     }

@@ -27,8 +27,10 @@ def hostlib():
            "-fno-omit-frame-pointer", "-fPIC", "-shared", f"-I{STUB}",
            f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}",
            os.path.join(CSRC, "registry.cpp"), os.path.join(CSRC, "plan.cpp"),
-           os.path.join(STUB, "hoststub.cpp"), "-o", LIB]
+           os.path.join(STUB, "hoststub.cpp"), "-o", LIB + f".{os.getpid()}"]
     subprocess.check_call(cmd)
+    # atomic: parallel test workers may build and load it at the same time
+    os.replace(LIB + f".{os.getpid()}", LIB)
     return LIB
 
 
