@@ -5,7 +5,11 @@
 // With 8 channels per pixel, the 8 depth values a lane supplies to a
 // 16x16x32 MFMA operand (one 16-byte chunk) are exactly one filter tap of
 // one pixel, so both operands are loaded straight from global memory into
-// registers: no LDS staging and no im2col. A depth step of 32 covers 4 taps
+// registers (no im2col). With 64-channel tiles the weight fragments are
+// staged in LDS once per workgroup instead (all four waves use the same
+// ones; fetched by every wave they are two thirds of the loads, 5% of the
+// time measured on the VGG and ResNet stems; with 32-channel tiles the
+// staging costs more than it saves). A depth step of 32 covers 4 taps
 // (the last step of a filter is padded with zero taps). The weight
 // fragment is the MFMA's first operand and the pixel fragment its second,
 // so a lane's result is 4 output channels of one pixel. The weight rows of
@@ -116,19 +120,33 @@ __global__ __launch_bounds__(256) void conv_stem_kernel(const ConvArgs a) {
         return r;
     };
 
-    // this lane's pixel in each of the wave's PF pixel fragments
+    // this lane's pixel in each of the wave's PF pixel fragments. The
+    // coordinates of the wave's first pixel come from uniform (scalar)
+    // divisions; a lane's then follow by carrying its offset through the
+    // columns, rows and frames (at most once per fragment for outputs at
+    // least 16 wide), which costs far fewer vector instructions than a
+    // division per lane and fragment
     const u16 *pbase[PF];
     int phi[PF], pwi[PF];
     const u16 *const in_u = (const u16 *)a.seg[s_first].in;
     const int f_u = a.seg[s_first].f_start;
+    const int mw = tm * STEM_PX + wave * PF * 16;
+    const int fw = mw / HWo, pw = mw - fw * HWo, how = pw / a.Wo;
+    int fr = fw, ho = how, wo = pw - how * a.Wo + l16;
     SFor<PF>::run([&](auto I) __attribute__((always_inline)) {
-        const int m = tm * STEM_PX + wave * PF * 16 + I * 16 + l16;
+        if (I > 0) wo += 16;
+        while (wo >= a.Wo) {
+            wo -= a.Wo;
+            if (++ho == a.Ho) {
+                ho = 0;
+                ++fr;
+            }
+        }
+        const int m = mw + I * 16 + l16;
         pbase[I] = zp;
         phi[I] = -(1 << 28);
         pwi[I] = 0;
         if (m < a.M) {
-            const int fr = m / HWo, pix = m - (m / HWo) * HWo;
-            const int ho = pix / a.Wo, wo = pix - (pix / a.Wo) * a.Wo;
             if (one_seg) {
                 pbase[I] = in_u + (size_t)(fr - f_u) * H * W * 8;
             } else {
@@ -142,11 +160,6 @@ __global__ __launch_bounds__(256) void conv_stem_kernel(const ConvArgs a) {
     // this lane's weight row in each of the NF channel fragments: MFMA row r
     // of fragment J holds channel 32*(J/2) + 8*(r/4) + 4*(J%2) + r%4
     static_assert(NF % 2 == 0, "channel fragments come in pairs");
-    const u16 *wrow[NF];
-    SFor<NF>::run([&](auto J) __attribute__((always_inline)) {
-        const int n = tn * BN + (J / 2) * 32 + (l16 >> 2) * 8 + (J % 2) * 4 + (l16 & 3);
-        wrow[J] = n < N ? (const u16 *)a.w + (size_t)n * K : nullptr;
-    });
     // epilogue constants of this lane's channels c = 32*j + 8*kq .. +7 of
     // fragment pair j (every segment shares them; loaded from an in-range
     // channel), in named registers per pair
@@ -159,14 +172,49 @@ __global__ __launch_bounds__(256) void conv_stem_kernel(const ConvArgs a) {
         return Aff{*(const f32x4 *)sp, *(const f32x4 *)(sp + 4), *(const f32x4 *)hp, *(const f32x4 *)(hp + 4)};
     };
 
-    auto load = [&](int step, bf16x8 (&wf)[NF], bf16x8 (&pf)[PF]) __attribute__((always_inline)) {
+    // weight fragments of the channel tile: with 64-channel tiles staged in
+    // LDS once per workgroup (fragment J of step st for lane l at
+    // wl[(st * NF + J) * 64 + l]), else read by each wave from global memory
+    constexpr bool WLDS = NF == 4;
+    constexpr int MAX_STEPS = S > 0 ? S : (STEM_MAX_TAPS + 3) / 4;
+    __shared__ bf16x8 wl[WLDS ? MAX_STEPS * NF * 64 : 1];
+    const u16 *wrow[NF];
+    SFor<NF>::run([&](auto J) __attribute__((always_inline)) {
+        const int n = tn * BN + (J / 2) * 32 + (l16 >> 2) * 8 + (J % 2) * 4 + (l16 & 3);
+        wrow[J] = n < N ? (const u16 *)a.w + (size_t)n * K : nullptr;
+    });
+    auto stage_weights = [&]() __attribute__((always_inline)) {
+        if constexpr (!WLDS) return;
+        for (int e = threadIdx.x; e < steps * NF * 64; e += 256) {
+            const int l = e & 63, sj = e >> 6, st = sj / NF, J = sj - (sj / NF) * NF;
+            // MFMA row r of fragment J holds channel 32*(J/2) + 8*(r/4) + 4*(J%2) + r%4
+            const int n = tn * BN + (J / 2) * 32 + ((l & 15) >> 2) * 8 + (J % 2) * 4 + (l & 3);
+            const int tap = st * 4 + (l >> 4);
+            wl[e] = *(const bf16x8 *)((n < N && tap < taps) ? (const u16 *)a.w + (size_t)n * K + tap * 8 : zp);
+        }
+        __syncthreads();
+    };
+    auto read_w = [&](int step, bf16x8 (&wf)[NF]) __attribute__((always_inline)) {
+        if constexpr (WLDS) {
+            SFor<NF>::run([&](auto J) __attribute__((always_inline)) { wf[J] = wl[(step * NF + J) * 64 + lane]; });
+        } else {
+            const int tap = step * 4 + kq;
+            SFor<NF>::run([&](auto J) __attribute__((always_inline)) {
+                wf[J] = *(const bf16x8 *)((tap < taps && wrow[J]) ? wrow[J] + tap * 8 : zp);
+            });
+        }
+    };
+    auto load = [&](int step, bf16x8 (&pf)[PF]) __attribute__((always_inline)) {
+        // filter row and column of this lane's tap: the step's first tap
+        // (uniform) carried by kq < 4 columns
         const int tap = step * 4 + kq;
         const bool tok = tap < taps;
-        const int r = tok ? tap / kw : 0, s = tok ? tap - (tap / kw) * kw : 0;
-        SFor<NF>::run([&](auto J) __attribute__((always_inline)) {
-            const u16 *p = (tok && wrow[J]) ? wrow[J] + tap * 8 : zp;
-            wf[J] = *(const bf16x8 *)p;
-        });
+        const int r0 = (step * 4) / kw;
+        int r = r0, s = step * 4 - r0 * kw + kq;
+        while (s >= kw) {
+            s -= kw;
+            ++r;
+        }
         SFor<PF>::run([&](auto I) __attribute__((always_inline)) {
             const int hi = phi[I] + r, wi = pwi[I] + s;
             const bool ok = tok && (unsigned)hi < (unsigned)H && (unsigned)wi < (unsigned)W;
@@ -178,7 +226,6 @@ __global__ __launch_bounds__(256) void conv_stem_kernel(const ConvArgs a) {
     f32x4 acc[PF][NF];
     SFor<PF>::run([&](auto I) __attribute__((always_inline)) { SFor<NF>::run([&](auto J) __attribute__((always_inline)) { acc[I][J] = f32x4{0.f, 0.f, 0.f, 0.f}; }); });
     bf16x8 w0[NF], p0[PF], w1[NF], p1[PF];
-    load(0, w0, p0);
     auto mma = [&](const bf16x8 (&wf)[NF], const bf16x8 (&pf)[PF]) __attribute__((always_inline)) {
         SFor<PF>::run([&](auto I) __attribute__((always_inline)) {
             SFor<NF>::run([&](auto J) __attribute__((always_inline)) {
@@ -186,20 +233,41 @@ __global__ __launch_bounds__(256) void conv_stem_kernel(const ConvArgs a) {
             });
         });
     };
-    if constexpr (S == 3) {
-        // 3 depth steps (3x3 filters): every load in flight at once
-        bf16x8 w2[NF], p2[PF];
-        load(1, w1, p1);
-        load(2, w2, p2);
-        mma(w0, p0);
-        mma(w1, p1);
-        mma(w2, p2);
+    // the first pixel loads are issued before the weights are staged, so
+    // that both wait out one memory latency together
+    if constexpr (S > 0) {
+        // S depth steps known at compile time (3x3 and 7x7 filters):
+        // straight-line code with the pixel loads issued D steps ahead of
+        // their MFMAs (3x3: all at once). A loop would carry the
+        // accumulators, and the register allocator copies those between
+        // register files on every iteration (64 instructions per two
+        // steps, measured as half of the 7x7 stem's vector instructions).
+        constexpr int D = S < 4 ? S : 4;
+        bf16x8 pf[S][PF];
+        SFor<D>::run([&](auto st) __attribute__((always_inline)) { load(st, pf[st]); });
+        stage_weights();
+        SFor<S>::run([&](auto st) __attribute__((always_inline)) {
+            constexpr int si = decltype(st)::value;
+            if constexpr (si + D < S) load(si + D, pf[si + D]);
+            bf16x8 wf[NF];
+            read_w(si, wf);
+            mma(wf, pf[si]);
+        });
     } else {
+        load(0, p0);
+        stage_weights();
+        read_w(0, w0);
         for (int st = 0; st < steps; st += 2) {
-            if (st + 1 < steps) load(st + 1, w1, p1);
+            if (st + 1 < steps) {
+                load(st + 1, p1);
+                read_w(st + 1, w1);
+            }
             mma(w0, p0);
             if (st + 1 < steps) {
-                if (st + 2 < steps) load(st + 2, w0, p0);
+                if (st + 2 < steps) {
+                    load(st + 2, p0);
+                    read_w(st + 2, w0);
+                }
                 mma(w1, p1);
             }
         }
@@ -303,7 +371,7 @@ __global__ __launch_bounds__(256) void conv_stem_kernel(const ConvArgs a) {
 }
 
 bool conv_stem_supported(const ConvArgs &a) {
-    return a.Cin == 8 && a.in_cs == 8 && a.k_splits <= 1 && a.kh * a.kw <= 64 && a.zero && a.uni_affine &&
+    return a.Cin == 8 && a.in_cs == 8 && a.k_splits <= 1 && a.kh * a.kw <= STEM_MAX_TAPS && a.zero && a.uni_affine &&
            (a.out_mode == OUT_NHWC || a.out_mode == OUT_NCHW_F32);
 }
 
@@ -326,11 +394,14 @@ hipError_t launch_conv_stem(const ConvArgs &a, const Sink &sk) {
     const long blocks = tiles >= 8 ? (tiles + 7) / 8 * 8 : tiles;
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
     const dim3 grid((unsigned)blocks), block(256);
-    const bool three = (a.kh * a.kw + 3) / 4 == 3;   // 9..12 taps: three depth steps
-    const void *k = narrow ? (three ? reinterpret_cast<const void *>(&conv_stem_kernel<4, 2, 3>)
-                                    : reinterpret_cast<const void *>(&conv_stem_kernel<4, 2, 0>))
-                           : (three ? reinterpret_cast<const void *>(&conv_stem_kernel<2, 4, 3>)
-                                    : reinterpret_cast<const void *>(&conv_stem_kernel<2, 4, 0>));
+    // straight-line forms for 3 and 13 depth steps (3x3 and 7x7 filters)
+    const int steps = (a.kh * a.kw + 3) / 4;
+    const void *k = narrow ? (steps == 3    ? reinterpret_cast<const void *>(&conv_stem_kernel<4, 2, 3>)
+                              : steps == 13 ? reinterpret_cast<const void *>(&conv_stem_kernel<4, 2, 13>)
+                                            : reinterpret_cast<const void *>(&conv_stem_kernel<4, 2, 0>))
+                           : (steps == 3    ? reinterpret_cast<const void *>(&conv_stem_kernel<2, 4, 3>)
+                              : steps == 13 ? reinterpret_cast<const void *>(&conv_stem_kernel<2, 4, 13>)
+                                            : reinterpret_cast<const void *>(&conv_stem_kernel<2, 4, 0>));
     return submit(sk, k, grid, block, a);
 }
 

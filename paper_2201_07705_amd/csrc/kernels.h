@@ -81,7 +81,9 @@ inline bool tile_is_dma(int tile) {
 inline int tile_dma_depth(int tile) {
     return (tile >= TILE_DMA64_256x256 && tile <= TILE_DMA64_128x64) || tile == TILE_DMA64_64x64 ? 64 : 32;
 }
-// Stem kernel: Cin == in_cs == 8, no split-K.
+// Stem kernel: Cin == in_cs == 8, at most STEM_MAX_TAPS filter taps (7x7
+// and smaller), no split-K.
+constexpr int STEM_MAX_TAPS = 52;
 bool conv_stem_supported(const ConvArgs &a);
 hipError_t launch_conv_stem(const ConvArgs &a, const Sink &sk);
 hipError_t launch_conv_f32(const ConvArgs &a, const Sink &sk);

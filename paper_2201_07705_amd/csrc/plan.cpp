@@ -1022,7 +1022,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                                         (int64_t)a.in_cs * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES;
                     const int dma_depth = !dma_ok ? 0 : a.Cin % 64 == 0 ? 64 : a.Cin % 32 == 0 ? 32 : 0;
                     // 8-channel inputs (the RGB stems) take the stem kernel
-                    const bool stem = a.Cin == 8 && a.in_cs == 8 && a.kh * a.kw <= 64 && a.uni_affine &&
+                    const bool stem = a.Cin == 8 && a.in_cs == 8 && a.kh * a.kw <= STEM_MAX_TAPS && a.uni_affine &&
                                       (ctx->opt.conv_tile < 0 || ctx->opt.conv_tile == TILE_STEM);
                     if (stem) {
                         Lc.tile = TILE_STEM;

@@ -353,7 +353,7 @@ bool conv_dma_supported(const ConvArgs &a, int tile) {
 }
 hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) { return launch_conv_bf16(a, tile, sk); }
 bool conv_stem_supported(const ConvArgs &a) {
-    return a.Cin == 8 && a.in_cs == 8 && a.k_splits <= 1 && a.kh * a.kw <= 64 && a.zero && a.uni_affine &&
+    return a.Cin == 8 && a.in_cs == 8 && a.k_splits <= 1 && a.kh * a.kw <= STEM_MAX_TAPS && a.zero && a.uni_affine &&
            (a.out_mode == OUT_NHWC || a.out_mode == OUT_NCHW_F32);
 }
 hipError_t launch_conv_stem(const ConvArgs &a, const Sink &sk) {
