@@ -182,6 +182,40 @@ gemel_status gemel_merge(gemel_ctx *ctx, const gemel_group *groups,
                          int32_t n_groups);
 
 /*
+ * Candidate groups of a workload (Section 5.3, the merging heuristic's first
+ * step): every appearance of a parametric layer (CONV, FC) in the models
+ * `model_ids`, grouped by architectural identity (exactly the properties
+ * gemel_merge checks, so any returned group is accepted by it), each group
+ * with the memory its appearances consume in total, and the groups listed
+ * in descending order of that memory, so that the groups whose merging
+ * would save the most come first. Only groups with at least two
+ * appearances are listed (a layer that appears once has nothing to share).
+ * The memory of one appearance is its parameter count (weights, plus cout
+ * for a bias, plus 4 * cout for batch norm) times the context's element
+ * size (2 bytes for GEMEL_BF16, 4 for GEMEL_F32).
+ *  model_ids, n_models   distinct registered model ids.
+ *  groups, groups_cap    caller array receiving the groups in order; each
+ *                        group's members point into `members`.
+ *  members, members_cap  caller array receiving all members back to back,
+ *                        group after group; within a group in order of the
+ *                        model's position in model_ids, then layer index
+ *                        (so members[0], the weight source gemel_merge
+ *                        uses, is the first appearance).
+ *  group_bytes           NULL, or groups_cap int64 receiving each group's
+ *                        total memory.
+ *  *n_groups, *n_members receive the counts. With groups and members both
+ *                        NULL the call only reports the counts.
+ * The context is not changed (the current sharing map plays no part).
+ * Errors: EINVAL (null counts, bad or repeated model id, arrays smaller
+ * than the counts, which are still reported), ENOMEM.
+ */
+gemel_status gemel_enumerate_groups(gemel_ctx *ctx, const int32_t *model_ids,
+                                    int32_t n_models, gemel_group *groups,
+                                    int32_t groups_cap, gemel_member *members,
+                                    int32_t members_cap, int64_t *group_bytes,
+                                    int32_t *n_groups, int32_t *n_members);
+
+/*
  * Run one inference round over `n_models` registered models.
  *  model_ids   distinct model ids; their order does not change any output.
  *  frames      per model: device pointer to float32 NCHW

@@ -3,8 +3,11 @@
 // merging (architectural-identity check, one copy per group), byte
 // accounting and options. Nothing here calls the HIP runtime except
 // gemel_infer (through run()) and gemel_destroy.
+#include <algorithm>
+#include <climits>
 #include <cmath>
 #include <cstring>
+#include <map>
 #include <new>
 #include <set>
 
@@ -314,6 +317,87 @@ gemel_status gemel_merge(gemel_ctx *ctx, const gemel_group *groups, int32_t n_gr
     ctx->weights_ready = false;
     drop_plans(ctx);
     return GEMEL_OK;
+}
+
+gemel_status gemel_enumerate_groups(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models,
+                                    gemel_group *groups, int32_t groups_cap, gemel_member *members,
+                                    int32_t members_cap, int64_t *group_bytes, int32_t *n_groups,
+                                    int32_t *n_members) {
+    if (!ctx) return GEMEL_EINVAL;
+    if (!n_groups || !n_members) return fail(ctx, GEMEL_EINVAL, "null count pointer");
+    *n_groups = 0;
+    *n_members = 0;
+    if (n_models <= 0 || !model_ids) return fail(ctx, GEMEL_EINVAL, "no models");
+    std::set<int> ids;
+    for (int i = 0; i < n_models; ++i) {
+        if (model_ids[i] < 0 || model_ids[i] >= (int)ctx->models.size())
+            return fail(ctx, GEMEL_EINVAL, "unknown model id " + std::to_string(model_ids[i]));
+        if (!ids.insert(model_ids[i]).second) return fail(ctx, GEMEL_EINVAL, "a model id appears twice");
+    }
+    try {
+        // one candidate per architectural identity (the properties gemel_merge
+        // compares), its appearances in model-position then layer order
+        struct Cand {
+            std::vector<gemel_member> mem;
+            int64_t bytes = 0;
+            int first_pos = 0, first_layer = 0;
+        };
+        const int64_t elem = ctx->dtype == GEMEL_BF16 ? 2 : 4;
+        std::map<std::vector<int64_t>, size_t> index;
+        std::vector<Cand> cands;
+        for (int p = 0; p < n_models; ++p) {
+            const Model &m = *ctx->models[(size_t)model_ids[p]];
+            for (int l = 0; l < (int)m.layers.size(); ++l) {
+                const Layer &L = m.layers[(size_t)l];
+                if (L.op != GEMEL_OP_CONV && L.op != GEMEL_OP_FC) continue;
+                const bool fc = L.op == GEMEL_OP_FC;
+                const std::vector<int64_t> key = {L.op,      L.cin,      L.cout,         L.kh,
+                                                  L.kw,      L.stride,   L.pad,          L.has_bias,
+                                                  L.has_bn,  fc ? L.in_c : 0, fc ? L.in_h : 0, fc ? L.in_w : 0};
+                const int64_t params = (int64_t)L.cout * L.cin * (fc ? 1 : (int64_t)L.kh * L.kw) +
+                                       (L.has_bias ? L.cout : 0) + (L.has_bn ? 4 * (int64_t)L.cout : 0);
+                auto it = index.find(key);
+                if (it == index.end()) {
+                    it = index.emplace(key, cands.size()).first;
+                    cands.push_back(Cand{{}, 0, p, l});
+                }
+                Cand &c = cands[it->second];
+                c.mem.push_back(gemel_member{model_ids[p], l});
+                c.bytes += params * elem;
+            }
+        }
+        std::vector<size_t> order;
+        int64_t total = 0;
+        for (size_t i = 0; i < cands.size(); ++i)
+            if (cands[i].mem.size() >= 2) {
+                order.push_back(i);
+                total += (int64_t)cands[i].mem.size();
+            }
+        // most memory first; ties in order of first appearance
+        std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) {
+            const Cand &x = cands[a], &y = cands[b];
+            if (x.bytes != y.bytes) return x.bytes > y.bytes;
+            if (x.first_pos != y.first_pos) return x.first_pos < y.first_pos;
+            return x.first_layer < y.first_layer;
+        });
+        if (total > INT32_MAX) return fail(ctx, GEMEL_EINVAL, "too many appearances");
+        *n_groups = (int32_t)order.size();
+        *n_members = (int32_t)total;
+        if (!groups && !members) return GEMEL_OK;
+        if (!groups || !members || groups_cap < *n_groups || members_cap < *n_members)
+            return fail(ctx, GEMEL_EINVAL, "group or member array smaller than the counts");
+        int32_t at = 0;
+        for (size_t g = 0; g < order.size(); ++g) {
+            const Cand &c = cands[order[g]];
+            groups[g].n_members = (int32_t)c.mem.size();
+            groups[g].members = members + at;
+            for (const gemel_member &mb : c.mem) members[at++] = mb;
+            if (group_bytes) group_bytes[g] = c.bytes;
+        }
+        return GEMEL_OK;
+    } catch (const std::bad_alloc &) {
+        return fail(ctx, GEMEL_ENOMEM, "out of host memory");
+    }
 }
 
 gemel_status gemel_infer(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models,

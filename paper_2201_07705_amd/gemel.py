@@ -44,7 +44,7 @@ KERNEL_FAMILIES = ("conv_mfma", "conv_f32", "splitk_reduce", "fc", "pack",
                    "pool", "route", "export")
 
 EXPORTED = ("gemel_create", "gemel_register_model", "gemel_merge",
-            "gemel_infer", "gemel_model_outputs", "gemel_output_shape",
+            "gemel_enumerate_groups", "gemel_infer", "gemel_model_outputs", "gemel_output_shape",
             "gemel_query", "gemel_set_option", "gemel_profile",
             "gemel_last_error", "gemel_destroy")
 
@@ -116,6 +116,10 @@ def _configure(L):
                                        i32, i32, i32,
                                        ctypes.POINTER(i32)]
     L.gemel_merge.argtypes = [vp, ctypes.POINTER(Group), i32]
+    L.gemel_enumerate_groups.argtypes = [
+        vp, ctypes.POINTER(i32), i32, ctypes.POINTER(Group), i32,
+        ctypes.POINTER(Member), i32, ctypes.POINTER(i64),
+        ctypes.POINTER(i32), ctypes.POINTER(i32)]
     L.gemel_infer.argtypes = [vp, ctypes.POINTER(i32), i32,
                               ctypes.POINTER(vp), ctypes.POINTER(i32),
                               ctypes.POINTER(vp), vp]
@@ -243,6 +247,30 @@ class Context:
             garr[i].n_members = len(g)
             garr[i].members = ctypes.cast(m, ctypes.POINTER(Member))
         self._check(self._lib.gemel_merge(self._h, garr, n))
+
+    def enumerate_groups(self, model_ids):
+        """Candidate groups of the models (Section 5.3): a list of
+        (total_bytes, [(model_id, layer_index), ...]) in descending order of
+        memory, each accepted by merge() as it is."""
+        n = len(model_ids)
+        ids = (ctypes.c_int32 * max(n, 1))(*model_ids)
+        ng, nm = ctypes.c_int32(), ctypes.c_int32()
+        self._check(self._lib.gemel_enumerate_groups(
+            self._h, ids, n, None, 0, None, 0, None, ctypes.byref(ng),
+            ctypes.byref(nm)))
+        garr = (Group * max(ng.value, 1))()
+        marr = (Member * max(nm.value, 1))()
+        nbytes = (ctypes.c_int64 * max(ng.value, 1))()
+        self._check(self._lib.gemel_enumerate_groups(
+            self._h, ids, n, garr, ng.value, marr, nm.value, nbytes,
+            ctypes.byref(ng), ctypes.byref(nm)))
+        out, at = [], 0
+        for g in range(ng.value):
+            k = garr[g].n_members
+            out.append((nbytes[g], [(marr[at + j].model_id, marr[at + j].layer)
+                                    for j in range(k)]))
+            at += k
+        return out
 
     def n_outputs(self, model_id):
         n = ctypes.c_int32()

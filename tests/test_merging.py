@@ -1,0 +1,227 @@
+"""Candidate merge groups of a workload (Section 5.3, the merging heuristic's
+first step), on the CPU.
+
+The oracle (oracle/merging.py) is pinned to the figures the paper prints:
+VGG16 and VGG19 share 16 of VGG19's 19 layers, ResNet-18 and ResNet-34 share
+41 of ResNet-34's 73 (batch norm counted as layers of their own), VGG16's
+largest layer takes 392 MB, and a 100 MB layer in four models is listed
+before a 120 MB layer in three; and to a brute-force pairwise identity check.
+The library's gemel_enumerate_groups must then return exactly the oracle's
+groups (members, order and bytes) for the workloads' model sets, and its
+groups must be accepted by gemel_merge.
+"""
+
+import ctypes
+import itertools
+
+import numpy as np
+import pytest
+
+from oracle import merging as OM
+from paper_2201_07705_amd import gemel as G
+from workloads import configs, zoo
+
+IN224 = (3, 224, 224)
+
+
+# ---- the oracle against the paper's figures ----
+
+def test_vgg16_vgg19_share_16_of_19_layers():
+    """Appendix figure on VGG variants: 16 of 19 layers (13 conv, 3 fc)."""
+    v16, v19 = zoo.vgg(16), zoo.vgg(19)
+    assert OM.layer_count(v19) == 19
+    assert OM.shared_layer_count([(v16, IN224), (v19, IN224)]) == 16
+
+
+def test_resnet18_resnet34_share_41_of_73_layers():
+    """Appendix figure on ResNet variants: 41 of 73 layers (20 conv, 20 batch
+    norm, 1 fc), batch norm counted as layers of their own."""
+    r18, r34 = zoo.resnet(18), zoo.resnet(34)
+    assert OM.layer_count(r34, count_bn_separately=True) == 73
+    assert OM.shared_layer_count([(r18, IN224), (r34, IN224)],
+                                 count_bn_separately=True) == 41
+    # without batch norm as separate layers: the 20 convs and the fc
+    assert OM.shared_layer_count([(r18, IN224), (r34, IN224)]) == 21
+
+
+def test_vgg16_largest_layer_is_392_mb():
+    """Section 4.2, Observation 1: one VGG16 layer takes 392 MB (float32)."""
+    v16 = zoo.vgg(16)
+    groups = OM.candidate_groups([(0, v16, IN224), (1, v16, IN224)], 4)
+    total, members = groups[0]
+    fc6 = [l["name"] for l in v16].index("classifier.fc6")
+    assert members == [(0, fc6), (1, fc6)]
+    assert round(total / 2 / 2**20) == 392
+
+
+def _fc_model(sizes):
+    layers = []
+    for i, cin in enumerate(sizes):
+        layers.append(dict(name=f"fc{i}", op="fc", src0=-1, src1=-1, cin=cin,
+                           cout=1000, kh=1, kw=1, stride=1, pad=0, bias=False,
+                           bn=False))
+    return layers
+
+
+def _fc_models(counts):
+    """One single-fc model per appearance: counts = [(cin, appearances)],
+    each fc cin -> 1000 reading its model's (cin, 1, 1) input."""
+    models = []
+    for cin, n in counts:
+        for _ in range(n):
+            models.append((len(models), _fc_model([cin]), (cin, 1, 1)))
+    return models
+
+
+def test_memory_order_counts_every_appearance():
+    """Section 5.3's example: a 100 MB layer appearing in 4 models comes
+    before a 120 MB layer appearing 3 times (float32; fc 25000->1000 is
+    100 MB, fc 30000->1000 is 120 MB)."""
+    a, b = 25000, 30000
+    groups = OM.candidate_groups(_fc_models([(b, 3), (a, 4)]), 4)
+    assert [g[0] for g in groups] == [400_000_000, 360_000_000]
+    assert [len(g[1]) for g in groups] == [4, 3]
+
+
+def _signature_brute(la, sa, ina, i, lb, sb, inb, j):
+    """Identity of two layers compared field by field (no hashing)."""
+    x, y = la[i], lb[j]
+    if x["op"] not in ("conv", "fc") or y["op"] != x["op"]:
+        return False
+    for f in ("cin", "cout", "kh", "kw", "stride", "pad"):
+        if x.get(f, 0) != y.get(f, 0):
+            return False
+    if bool(x.get("bias")) != bool(y.get("bias")) or bool(x.get("bn")) != bool(y.get("bn")):
+        return False
+    if x["op"] == "fc":
+        px = ina if x["src0"] < 0 else sa[x["src0"]]
+        py = inb if y["src0"] < 0 else sb[y["src0"]]
+        return tuple(px) == tuple(py)
+    return True
+
+
+@pytest.mark.parametrize("archs", [("resnet18", "resnet34"), ("vgg16", "vgg19"),
+                                   ("resnet50", "resnet152"), ("yolov3", "resnet50")])
+def test_groups_partition_equals_brute_force(archs):
+    """Every pair of appearances is in one group iff identical field by field,
+    and no single-appearance group is listed."""
+    models = [(k, zoo.build(a), (3, 224, 224) if a != "yolov3" else (3, 416, 416))
+              for k, a in enumerate(archs)]
+    shapes = [OM.output_shapes(l, c) for _, l, c in models]
+    groups = OM.candidate_groups(models, 2)
+    where = {}
+    for gi, (_, mem) in enumerate(groups):
+        for m in mem:
+            where[m] = gi
+    apps = [(k, i) for k, (_, l, _) in enumerate(models) for i in range(len(l))
+            if l[i]["op"] in ("conv", "fc")]
+    for (ka, i), (kb, j) in itertools.combinations(apps, 2):
+        same = _signature_brute(models[ka][1], shapes[ka], models[ka][2], i,
+                                models[kb][1], shapes[kb], models[kb][2], j)
+        ga, gb = where.get((ka, i)), where.get((kb, j))
+        if same:
+            assert ga is not None and ga == gb, ((ka, i), (kb, j))
+        else:
+            assert ga is None or gb is None or ga != gb, ((ka, i), (kb, j))
+    for (ka, i) in apps:   # unlisted appearances have no identical partner
+        if (ka, i) not in where:
+            assert not any(_signature_brute(models[ka][1], shapes[ka], models[ka][2], i,
+                                            models[kb][1], shapes[kb], models[kb][2], j)
+                           for (kb, j) in apps if (kb, j) != (ka, i))
+
+
+def test_planted_mistake_is_caught():
+    """A plausible bug (sorting by one appearance's size instead of the
+    group total) reorders the Section 5.3 example, so the test above would
+    fail on it."""
+    groups = OM.candidate_groups(_fc_models([(30000, 3), (25000, 4)]), 4)
+    per_app = sorted(groups, key=lambda g: -g[0] / len(g[1]))
+    assert [g[0] for g in per_app] != [g[0] for g in groups]
+
+
+# ---- the library against the oracle ----
+
+def _zero_params(layers):
+    out = []
+    for l in layers:
+        if l["op"] == "conv":
+            p = {"w": np.zeros((l["cout"], l["cin"], l["kh"], l["kw"]), np.float32),
+                 "b": np.zeros(l["cout"], np.float32) if l.get("bias") else None,
+                 "bn": None}
+            if l.get("bn"):
+                one = np.ones(l["cout"], np.float32)
+                p["bn"] = (one, one * 0, one * 0, one, 1e-5)
+            out.append(p)
+        elif l["op"] == "fc":
+            out.append({"w": np.zeros((l["cout"], l["cin"]), np.float32),
+                        "b": np.zeros(l["cout"], np.float32) if l.get("bias") else None,
+                        "bn": None})
+        else:
+            out.append(None)
+    return out
+
+
+def _library_vs_oracle(specs, dtype):
+    ctx = G.Context(0, dtype)
+    try:
+        ids = [ctx.register_model(l, _zero_params(l), chw) for l, chw in specs]
+        got = ctx.enumerate_groups(ids)
+        want = OM.candidate_groups([(i, l, chw) for i, (l, chw) in zip(ids, specs)],
+                                   2 if dtype == "bf16" else 4)
+        assert got == want
+        # the groups install as they are, and merging them saves memory
+        before = ctx.query(G.Q_MERGED_BYTES)
+        ctx.merge([m for _, m in got])
+        assert ctx.query(G.Q_MERGED_BYTES) < before or not got
+        return got
+    finally:
+        ctx.close()
+
+
+@pytest.mark.parametrize("name", ["r50x2_vgg16x2", "yolov3x3", "mix8_budget40", "resnet18x2"])
+def test_library_groups_equal_oracle_on_workloads(name):
+    wl = configs.get(name, res=32 if name != "yolov3x3" else 64)
+    _library_vs_oracle([(m.layers, m.in_chw) for m in wl.models], wl.dtype)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_library_groups_equal_oracle_on_model_variants(dtype):
+    chw = (3, 32, 32)
+    got = _library_vs_oracle([(zoo.resnet(18), chw), (zoo.resnet(34), chw),
+                              (zoo.vgg(16, 1000, 32), chw), (zoo.vgg(19, 1000, 32), chw)],
+                             dtype)
+    assert got and all(len(m) >= 2 for _, m in got)
+
+
+def test_enumerate_errors_and_count_query():
+    ctx = G.Context(0, "bf16")
+    try:
+        l = zoo.resnet(18)
+        a = ctx.register_model(l, _zero_params(l), (3, 32, 32))
+        b = ctx.register_model(l, _zero_params(l), (3, 32, 32))
+        L = ctx._lib
+        ng, nm = ctypes.c_int32(-5), ctypes.c_int32(-5)
+        ids = (ctypes.c_int32 * 2)(a, b)
+        assert L.gemel_enumerate_groups(ctx._h, ids, 2, None, 0, None, 0, None,
+                                        ctypes.byref(ng), ctypes.byref(nm)) == G.OK
+        # ResNet-18 twice: every one of its 21 parametric layers' identities
+        # pairs up, and repeated identities within a model join their group
+        assert nm.value == 2 * 21 and 0 < ng.value <= 21
+        small = (G.Group * 1)()
+        mem = (G.Member * 1)()
+        assert L.gemel_enumerate_groups(ctx._h, ids, 2, small, 1, mem, 1, None,
+                                        ctypes.byref(ng), ctypes.byref(nm)) == G.EINVAL
+        assert nm.value == 42                      # counts still reported
+        rep = (ctypes.c_int32 * 2)(a, a)
+        assert L.gemel_enumerate_groups(ctx._h, rep, 2, None, 0, None, 0, None,
+                                        ctypes.byref(ng), ctypes.byref(nm)) == G.EINVAL
+        bad = (ctypes.c_int32 * 1)(7)
+        assert L.gemel_enumerate_groups(ctx._h, bad, 1, None, 0, None, 0, None,
+                                        ctypes.byref(ng), ctypes.byref(nm)) == G.EINVAL
+        assert L.gemel_enumerate_groups(ctx._h, ids, 2, None, 0, None, 0, None,
+                                        None, ctypes.byref(nm)) == G.EINVAL
+        # one model alone: repeated identities inside it still form groups
+        one = ctx.enumerate_groups([a])
+        assert one and all(m[0][0] == a for _, m in one)
+    finally:
+        ctx.close()
