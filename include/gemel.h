@@ -360,7 +360,7 @@ enum {
                                     2: inside the GEMM launch always; 0: in
                                     a separate launch always. Every form
                                     sums in split order: same bits         */
-    GEMEL_OPT_TUNE = 14          /* 1 (default): when a plan is built, each
+    GEMEL_OPT_TUNE = 14,         /* 1 (default): when a plan is built, each
                                     bf16 conv shape whose tile and split-K
                                     are not forced (and whose weights are
                                     resident and whose output is internal)
@@ -374,6 +374,15 @@ enum {
                                     to that many candidates. Different
                                     choices change fp32 summation order,
                                     so bits may differ between contexts    */
+    GEMEL_OPT_FUSE_POOL = 15     /* 1 (default): a bf16 conv whose only
+                                    consumer is a 2x2 stride-2 max pool
+                                    (even output size, no residual, not an
+                                    output, input channels a multiple of
+                                    32) writes the pooled tensor from its
+                                    epilogue, and the pool launch and the
+                                    full-size tensor disappear. Results are
+                                    bit-identical to the separate pool. 0:
+                                    off                                    */
 };
 
 /* Set an option; takes effect at the next gemel_infer. Errors: EINVAL. */

@@ -52,12 +52,11 @@ __device__ __forceinline__ int epi_kind(int act, int has_res, int res_mode, floa
     if (!has_res && act == 2 && slope >= 0.f && slope <= 1.f) return EK_LEAKY;
     return EK_GENERAL;
 }
-// z = v * scale + shift, the activation / residual of `kind`, rounded to
-// bf16 and packed in channel order. r4 holds the residual's 8 bf16 values
-// (ignored unless the kind has a residual).
-__device__ __forceinline__ u32x4 epi8_bf16(const float *v, const float *sc, const float *sh, const u32x4 &r4,
-                                           int kind, int has_res, int res_mode, int act, float slope) {
-    float y[8];
+// y = the activation / residual of `kind` applied to z = v * scale + shift,
+// in fp32. r4 holds the residual's 8 bf16 values (ignored unless the kind
+// has a residual).
+__device__ __forceinline__ void epi8_f32(const float *v, const float *sc, const float *sh, const u32x4 &r4,
+                                         int kind, int has_res, int res_mode, int act, float slope, float *y) {
     // the residual is unpacked only where a kind reads it, so that kinds
     // without one never wait for its load
     auto res = [&](int j) __attribute__((always_inline)) {
@@ -89,10 +88,20 @@ __device__ __forceinline__ u32x4 epi8_bf16(const float *v, const float *sc, cons
         for (int j = 0; j < 8; ++j) y[j] = epi(v[j] * sc[j] + sh[j], res(j), has_res, res_mode, act, slope);
         break;
     }
+}
+// 8 fp32 values rounded to bf16 and packed in channel order.
+__device__ __forceinline__ u32x4 pack8_bf16(const float *y) {
     u32x4 o;
 #pragma unroll
     for (int q = 0; q < 4; ++q) o[q] = (uint32_t)f2bf(y[2 * q]) | ((uint32_t)f2bf(y[2 * q + 1]) << 16);
     return o;
+}
+// epi8_f32, rounded to bf16 and packed in channel order.
+__device__ __forceinline__ u32x4 epi8_bf16(const float *v, const float *sc, const float *sh, const u32x4 &r4,
+                                           int kind, int has_res, int res_mode, int act, float slope) {
+    float y[8];
+    epi8_f32(v, sc, sh, r4, kind, has_res, res_mode, act, slope, y);
+    return pack8_bf16(y);
 }
 
 // Fields of one segment. The segment table lives in the kernel argument

@@ -179,6 +179,7 @@ struct Options {
     int splitk_fused = 1;
     int tune = 1;             // measured conv configuration at plan time
     int tune_candidates = 4;  // configurations timed per conv shape
+    int fuse_pool = 1;        // 2x2 max pools fused into their conv
     int64_t slot_bytes = 32ll << 20;
     int slots = 3;
     int64_t fail_copy_at = 0;

@@ -432,6 +432,8 @@ static bool conv_args_ok(const ConvArgs &a) {
     if (a.k_splits > 1 && (long)a.k_splits * a.M * a.N * 4 > 0x7fffffffL) return false;
     if (a.k_per_split <= 0 || (long)a.k_per_split * a.k_splits < a.K) return false;
     if (a.out_mode == OUT_NCHW_F32 && a.cout > a.N) return false;
+    // the fused 2x2 pool exists only in the LDS-DMA kernel
+    if (a.out_mode != OUT_NHWC && a.out_mode != OUT_NCHW_F32) return false;
     return true;
 }
 
@@ -476,6 +478,7 @@ hipError_t launch_conv_f32(const ConvArgs &a, const Sink &sk) {
 hipError_t launch_conv_reduce(const ReduceArgs &a, bool bf16, const Sink &sk) {
     if (a.M <= 0 || a.N <= 0 || a.N % 8 || a.splits < 1 || !a.partial || a.nseg < 1 || a.nseg > GEMEL_MAX_SEG)
         return hipErrorInvalidValue;
+    if (a.out_mode != OUT_NHWC && a.out_mode != OUT_NCHW_F32) return hipErrorInvalidValue;
     for (int i = 0; i < a.nseg; ++i)
         if (!a.seg[i].out || !a.seg[i].scale || !a.seg[i].shift || (a.has_res && !a.seg[i].res))
             return hipErrorInvalidValue;

@@ -75,7 +75,9 @@ __device__ __forceinline__ void wait_lgkm0() {
 
 }  // namespace
 
-template <int BM, int BN, int WM, int WN, int STAGES, int BK>
+// POOL: the 2x2 stride-2 max pool fused (out_mode OUT_NHWC_POOL2), a
+// separate instantiation so that the other kernels keep their code size
+template <int BM, int BN, int WM, int WN, int STAGES, int BK, bool POOL>
 __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a) {
     constexpr int NW = WM * WN, NT = 64 * NW;
     static_assert(BK == 32 || BK == 64, "step depth");
@@ -128,6 +130,10 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
     // (i*NW + wave)*64 + lane: row (i*NW + wave)*RPI + lane/CPR; the slot's
     // chunk position lane%CPR holds logical chunk (lane%CPR) ^ sw(row) ----
     auto sw = [](int row) __attribute__((always_inline)) { return (row >> 1) & (CPR - 1); };
+    // with the 2x2 max pool fused, rows run over the output in window
+    // order: row 4g + 2dy + dx is pixel (2hp + dy, 2wp + dx) of pooled pixel g
+    constexpr bool pool2 = POOL;
+    const int Wp = a.Wo >> 1, HWp = HWo >> 2;
     const u16 *abase[AI];
     int ahi[AI], awi[AI], acq[AI];
 #pragma unroll
@@ -139,9 +145,19 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
         ahi[i] = -(1 << 28);
         awi[i] = 0;
         if (gm < a.M) {
-            const int fr = gm / HWo;
-            const int pix = gm - fr * HWo;
-            const int ho = pix / a.Wo, wo = pix - (pix / a.Wo) * a.Wo;
+            int fr, ho, wo;
+            if constexpr (pool2) {
+                const int g = gm >> 2;
+                fr = g / HWp;
+                const int pp = g - fr * HWp, hp = pp / Wp;
+                ho = 2 * hp + ((gm >> 1) & 1);
+                wo = 2 * (pp - hp * Wp) + (gm & 1);
+            } else {
+                fr = gm / HWo;
+                const int pix = gm - fr * HWo;
+                ho = pix / a.Wo;
+                wo = pix - ho * a.Wo;
+            }
             const RowSeg sg = one_seg ? useg : row_seg(a, gm);
             abase[i] = (const u16 *)sg.in + (size_t)(fr - sg.f_start) * frame_elems;
             ahi[i] = ho * a.stride - a.pad;
@@ -402,6 +418,34 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
         // a residual nothing is waited for: the epilogue kinds without one
         // never read the residual registers.
         if (pre_res) wait_vm<0>();
+        if constexpr (pool2) {
+            // pooled items (window, chunk): the window's 4 staged rows through
+            // the epilogue, each rounded to bf16 as stored unfused, then their
+            // max in window order (what the separate pool computes)
+            constexpr int NPI = PG * 4 * CHW;
+#pragma unroll
+            for (int u = 0; u < (NPI + 63) / 64; ++u) {
+                const int idx = lane + u * 64;
+                const int pr = idx / CHW;
+                const int gm = row0 + 4 * pr;
+                if (idx >= NPI || !col_ok || gm >= a.M) continue;
+                float mx[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) mx[j] = -INFINITY;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const float *src = ew + (4 * pr + q) * EPI_LD + ch * 8;
+                    const float4 v0 = *(const float4 *)src, v1 = *(const float4 *)(src + 4);
+                    const float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+                    float y[8];
+                    epi8_f32(v, s8, h8, u32x4{0u, 0u, 0u, 0u}, ekind, 0, 0, a.act, a.slope, y);
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) mx[j] = fmaxf(mx[j], bf2f(f2bf(y[j])));
+                }
+                const RowSeg sg = one_seg ? useg : row_seg(a, gm);
+                *(u32x4 *)((u16 *)sg.out + (size_t)((gm - sg.m_start) >> 2) * out_cs + gn) = pack8_bf16(mx);
+            }
+        } else {
 #pragma unroll
         for (int u = 0; u < ITEMS; ++u) {
             const int rl = (lane + u * 64) / CHW;
@@ -434,6 +478,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
                 }
             }
         }
+        }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -457,6 +502,10 @@ hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) {
         return hipErrorInvalidValue;
     if (a.K != a.kh * a.kw * a.Cin || a.out_cs < a.N || a.seg[0].m_start != 0) return hipErrorInvalidValue;
     if (a.k_splits > 1 && !a.partial) return hipErrorInvalidValue;
+    // fused 2x2 pool: whole windows, no split-K, no residual
+    if (a.out_mode == OUT_NHWC_POOL2 &&
+        (a.k_splits > 1 || a.has_res || (a.Ho & 1) || (a.Wo & 1) || a.Ho <= 0 || a.Wo <= 0))
+        return hipErrorInvalidValue;
     if (a.k_splits > 1 && (long)a.k_splits * a.M * a.N * 4 > 0x7fffffffL) return hipErrorInvalidValue;
     if ((long)a.k_per_split * a.k_splits < a.K) return hipErrorInvalidValue;
     for (int i = 0; i < a.nseg; ++i) {
@@ -472,19 +521,28 @@ hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) {
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
     dim3 grid((unsigned)blocks, (unsigned)a.k_splits);
     hipError_t e = hipErrorInvalidValue;
+    const bool pool = a.out_mode == OUT_NHWC_POOL2;
+#define GEMEL_DMA_CASE(T, BM_, BN_, WM_, WN_, ST_, BK_, NT_)                                                    \
+    case T:                                                                                                     \
+        e = submit(sk,                                                                                          \
+                   pool ? reinterpret_cast<const void *>(&conv_dma_kernel<BM_, BN_, WM_, WN_, ST_, BK_, true>)  \
+                        : reinterpret_cast<const void *>(&conv_dma_kernel<BM_, BN_, WM_, WN_, ST_, BK_, false>), \
+                   grid, dim3(NT_), a);                                                                         \
+        break;
     switch (tile) {
-    case TILE_DMA_256x256: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<256, 256, 2, 4, 4, 32>), grid, dim3(512), a); break;
-    case TILE_DMA_256x128: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<256, 128, 2, 2, 4, 32>), grid, dim3(256), a); break;
-    case TILE_DMA_128x128: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<128, 128, 2, 2, 4, 32>), grid, dim3(256), a); break;
-    case TILE_DMA_128x64: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<128, 64, 2, 1, 4, 32>), grid, dim3(128), a); break;
-    case TILE_DMA_64x64: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<64, 64, 2, 2, 4, 32>), grid, dim3(256), a); break;
-    case TILE_DMA64_64x64: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<64, 64, 2, 2, 4, 64>), grid, dim3(256), a); break;
-    case TILE_DMA64_256x256: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<256, 256, 2, 4, 2, 64>), grid, dim3(512), a); break;
-    case TILE_DMA64_256x128: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<256, 128, 2, 2, 3, 64>), grid, dim3(256), a); break;
-    case TILE_DMA64_128x128: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<128, 128, 2, 2, 2, 64>), grid, dim3(256), a); break;
-    case TILE_DMA64_128x64: e = submit(sk, reinterpret_cast<const void *>(&conv_dma_kernel<128, 64, 2, 1, 3, 64>), grid, dim3(128), a); break;
+        GEMEL_DMA_CASE(TILE_DMA_256x256, 256, 256, 2, 4, 4, 32, 512)
+        GEMEL_DMA_CASE(TILE_DMA_256x128, 256, 128, 2, 2, 4, 32, 256)
+        GEMEL_DMA_CASE(TILE_DMA_128x128, 128, 128, 2, 2, 4, 32, 256)
+        GEMEL_DMA_CASE(TILE_DMA_128x64, 128, 64, 2, 1, 4, 32, 128)
+        GEMEL_DMA_CASE(TILE_DMA_64x64, 64, 64, 2, 2, 4, 32, 256)
+        GEMEL_DMA_CASE(TILE_DMA64_64x64, 64, 64, 2, 2, 4, 64, 256)
+        GEMEL_DMA_CASE(TILE_DMA64_256x256, 256, 256, 2, 4, 2, 64, 512)
+        GEMEL_DMA_CASE(TILE_DMA64_256x128, 256, 128, 2, 2, 3, 64, 256)
+        GEMEL_DMA_CASE(TILE_DMA64_128x128, 128, 128, 2, 2, 2, 64, 256)
+        GEMEL_DMA_CASE(TILE_DMA64_128x64, 128, 64, 2, 1, 3, 64, 128)
     default: break;
     }
+#undef GEMEL_DMA_CASE
     return e;
 }
 

@@ -14,7 +14,12 @@
 // to a pixel's channel offset).
 #define GEMEL_ZERO_PAGE_BYTES 16384
 
-enum { OUT_NHWC = 0, OUT_NCHW_F32 = 1, OUT_PARTIAL_F32 = 2 };
+// OUT_NHWC_POOL2: the conv's 2x2 stride-2 max pool fused into its
+// epilogue. GEMM rows then run over the output in window order: row
+// 4*g + 2*dy + dx of a frame is output pixel (2*hp + dy, 2*wp + dx) of
+// pooled pixel g = hp * Wo/2 + wp, and the output tensor is the pooled one
+// (Ho/2 x Wo/2 pixels per frame, out_cs channels).
+enum { OUT_NHWC = 0, OUT_NCHW_F32 = 1, OUT_PARTIAL_F32 = 2, OUT_NHWC_POOL2 = 3 };
 
 struct ConvSeg {
     const void *in;       // NHWC [frames][H][W][in_cs], frame 0 of the segment

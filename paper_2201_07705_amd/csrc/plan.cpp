@@ -341,13 +341,16 @@ struct ConvCand {
 
 // Every (tile, split-K) configuration the conv may use, fastest estimate
 // first. dma_depth: deepest LDS-DMA step the conv allows (0: no DMA tile,
-// 32 or 64); force >= 0 restricts the tile.
-std::vector<ConvCand> conv_candidates(int64_t M, int64_t N, int64_t K, int dma_depth, int force) {
+// 32 or 64); force >= 0 restricts the tile; pooled: the conv's 2x2 pool is
+// fused (LDS-DMA tiles, no split-K).
+std::vector<ConvCand> conv_candidates(int64_t M, int64_t N, int64_t K, int dma_depth, int force, bool pooled) {
     const double cu_flops = 4096.0 * 2.4e9;   // per CU, dense bf16
     std::vector<ConvCand> out;
     for (const TileCost &tc : kTileCost) {
         if (force >= 0 && tc.tile != force) continue;
         if (force < 0 && tile_is_dma(tc.tile) && tile_dma_depth(tc.tile) > dma_depth) continue;
+        // a fused pool runs in the LDS-DMA kernel without split-K
+        if (pooled && (!tile_is_dma(tc.tile) || tile_dma_depth(tc.tile) > dma_depth)) continue;
         const int64_t bm = conv_tile_bm(tc.tile), bn = conv_tile_bn(tc.tile);
         const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
         int last = 0;
@@ -357,6 +360,7 @@ std::vector<ConvCand> conv_candidates(int64_t M, int64_t N, int64_t K, int dma_d
             const int64_t s_eff = (K + k_s - 1) / k_s;
             if (s_eff > 1 && s_eff * M * N * 4 > kMaxPartialBytes) break;
             if (s_eff == last) continue;
+            if (pooled && s_eff > 1) break;
             last = (int)s_eff;
             const double waves = std::ceil((double)(tiles * s_eff) / (256.0 * tc.occ));
             double t = waves * (tc.occ * (2.0 * bm * bn * k_s) / (cu_flops * tc.eff) + tc.lat);
@@ -378,12 +382,12 @@ void conv_split_depth(int64_t K, int &splits, int &kps) {
 // Launch configuration of a bf16 implicit-GEMM conv of size M x N x K:
 // the candidate with the smallest estimated time (or the forced tile /
 // split count).
-void pick_conv_config(int64_t M, int64_t N, int64_t K, int dma_depth, int force, int force_splits, int &tile,
-                      int &splits, int &kps) {
-    const std::vector<ConvCand> c = conv_candidates(M, N, K, dma_depth, force);
+void pick_conv_config(int64_t M, int64_t N, int64_t K, int dma_depth, int force, int force_splits, bool pooled,
+                      int &tile, int &splits, int &kps) {
+    const std::vector<ConvCand> c = conv_candidates(M, N, K, dma_depth, force, pooled);
     tile = c.empty() ? (force >= 0 ? force : TILE_64x64) : c[0].tile;
     splits = c.empty() ? 1 : c[0].splits;
-    if (force_splits > 0) splits = (int)std::min<int64_t>(force_splits, (K + CONV_BK - 1) / CONV_BK);
+    if (force_splits > 0 && !pooled) splits = (int)std::min<int64_t>(force_splits, (K + CONV_BK - 1) / CONV_BK);
     while (splits > 1 && (int64_t)splits * M * N * 4 > kMaxPartialBytes) --splits;
     conv_split_depth(K, splits, kps);
 }
@@ -424,7 +428,7 @@ bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int
         conv_split_depth(a0.K, splits, kps);
         return true;
     }
-    std::vector<ConvCand> c = conv_candidates(a0.M, a0.N, a0.K, dma_depth, -1);
+    std::vector<ConvCand> c = conv_candidates(a0.M, a0.N, a0.K, dma_depth, -1, a0.out_mode == OUT_NHWC_POOL2);
     if (c.empty()) return false;
     const double cut = 2.0 * c[0].est;
     size_t n = 0;
@@ -556,6 +560,34 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
     auto model = [&](int s) -> const Model & { return *ctx->models[(size_t)ids[(size_t)s]]; };
     auto layer = [&](int s, int l) -> const Layer & { return model(s).layers[(size_t)l]; };
 
+    // ---- 2x2 max pools fused into their conv: pool_of[s][l] is the pool
+    // that conv (s, l) writes from its epilogue (-1: none). The conv is its
+    // pool's only producer input, the pool its only consumer; the pool
+    // layer then belongs to the conv's node and has no launch of its own ----
+    std::vector<std::vector<int>> pool_of((size_t)S), fused_into((size_t)S);
+    const int forced = ctx->opt.conv_tile;
+    for (int s = 0; s < S; ++s) {
+        const Model &m = model(s);
+        pool_of[(size_t)s].assign(m.layers.size(), -1);
+        fused_into[(size_t)s].assign(m.layers.size(), -1);
+        if (!bf16 || !ctx->opt.fuse_pool || (forced >= 0 && !tile_is_dma(forced))) continue;
+        for (int p = 0; p < (int)m.layers.size(); ++p) {
+            const Layer &Pl = m.layers[(size_t)p];
+            if (Pl.op != GEMEL_OP_MAXPOOL || Pl.kh != 2 || Pl.kw != 2 || Pl.stride != 2 || Pl.pad != 0 || Pl.src0 < 0)
+                continue;
+            const int l = Pl.src0;
+            const Layer &L = m.layers[(size_t)l];
+            // the LDS-DMA kernel's requirements (as for its tiles below)
+            const bool dma = L.in_cp % 32 == 0 && (int64_t)L.in_cp * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES &&
+                             (forced < 0 || tile_dma_depth(forced) == 32 || L.in_cp % 64 == 0);
+            if (L.op != GEMEL_OP_CONV || L.res >= 0 || L.is_output || L.consumers != 1 || !dma || L.out_h % 2 ||
+                L.out_w % 2 || L.out_h < 2 || L.out_w < 2)
+                continue;
+            pool_of[(size_t)s][(size_t)l] = p;
+            fused_into[(size_t)s][(size_t)p] = l;
+        }
+    }
+
     // ---- nodes: merged groups batched when compatible ----
     std::vector<Node> nodes;
     std::map<std::vector<int64_t>, int> group_node;
@@ -565,11 +597,15 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
         node_of[(size_t)s].assign(m.layers.size(), -1);
         for (int l = 0; l < (int)m.layers.size(); ++l) {
             const Layer &L = m.layers[(size_t)l];
+            if (fused_into[(size_t)s][(size_t)l] >= 0) {   // a fused pool: part of its conv's node
+                node_of[(size_t)s][(size_t)l] = node_of[(size_t)s][(size_t)fused_into[(size_t)s][(size_t)l]];
+                continue;
+            }
             int nid = -1;
             if (L.group >= 0 && !ctx->opt.split_merged) {
                 std::vector<int64_t> key = {L.group, L.in_h, L.in_w, L.in_c, L.act,
                                             (int64_t)(L.slope * 1e6f), L.res >= 0, L.res_mode,
-                                            direct_output(L), L.src1_cp};
+                                            direct_output(L), L.src1_cp, pool_of[(size_t)s][(size_t)l] >= 0};
                 auto it = group_node.find(key);
                 if (it != group_node.end() && nodes[(size_t)it->second].mem.size() < GEMEL_MAX_SEG) {
                     nid = it->second;
@@ -628,6 +664,10 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 single.push_back(Node{nd.op, {mb}});
             }
         nodes.swap(single);
+        for (int s = 0; s < S; ++s)
+            for (size_t p = 0; p < fused_into[(size_t)s].size(); ++p)
+                if (fused_into[(size_t)s][p] >= 0)
+                    node_of[(size_t)s][p] = node_of[(size_t)s][(size_t)fused_into[(size_t)s][p]];
         if (!topo(order)) return fail(ctx, GEMEL_ESTATE, "internal: layer graph has a cycle");
     }
 
@@ -767,7 +807,13 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
     for (int i = 0; i < NN; ++i)
         for (auto [s, l] : nodes[(size_t)order[(size_t)i]].mem) {
             const Layer &L = layer(s, l);
-            if (!direct_output(L)) {
+            const int p = pool_of[(size_t)s][(size_t)l];
+            if (p >= 0) {   // the conv writes its pool's (pooled) tensor only
+                const Layer &Pl = layer(s, p);
+                TInfo &t = T[{s, p}];
+                t.bytes = (size_t)nfr[(size_t)s] * Pl.out_h * Pl.out_w * Pl.out_cp * esz;
+                t.prod = i;
+            } else if (!direct_output(L)) {
                 TInfo &t = T[{s, l}];
                 t.bytes = (size_t)nfr[(size_t)s] * L.out_h * L.out_w * L.out_cp * esz;
                 t.prod = i;
@@ -896,6 +942,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
         const Layer &L0 = layer(s0, l0);
         if (L0.op == GEMEL_OP_CONV || L0.op == GEMEL_OP_FC) {
             Blob *blob = L0.eff.get();
+            const bool pooled = pool_of[(size_t)s0][(size_t)l0] >= 0;   // alike for every member
             int64_t M = 0;
             for (auto [s, l] : nd.mem) M += (int64_t)nfr[(size_t)s] * layer(s, l).out_h * layer(s, l).out_w;
             const bool direct = direct_output(L0);
@@ -922,7 +969,8 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 Lc.bf16 = bf16;
                 const double co = (double)std::max<int64_t>(0, std::min<int64_t>(nrows, L0.out_c - row0));
                 Lc.flops = 2.0 * (double)M * co * kdepth;
-                Lc.bytes = co * kdepth * esz + in_elems * esz + (double)M * co * (direct ? 4.0 : esz) +
+                Lc.bytes = co * kdepth * esz + in_elems * esz +
+                           (double)M * co * (direct ? 4.0 : esz) / (pooled ? 4.0 : 1.0) +
                            (L0.res >= 0 ? (double)M * co * esz : 0.0);
                 if (!blob->w_dev) {
                     Lc.chunk = (int)P.chunks.size();
@@ -993,7 +1041,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 a.cout = direct ? std::min<int>((int)nrows, L0.out_c - (int)row0) : L0.out_c;
                 a.act = L0.act; a.slope = L0.slope;
                 a.res_mode = L0.res_mode; a.has_res = L0.res >= 0;
-                a.out_mode = direct ? OUT_NCHW_F32 : OUT_NHWC;
+                a.out_mode = direct ? OUT_NCHW_F32 : pooled ? OUT_NHWC_POOL2 : OUT_NHWC;
                 a.nseg = 0;
                 int f = 0;
                 for (auto [s, l] : nd.mem) {
@@ -1002,7 +1050,8 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     ConvSeg &sg = a.seg[a.nseg];
                     sg.in = in_ptr(s, L.src0);
                     sg.res = L.res >= 0 ? (const void *)((char *)tptr(s, L.res) + row0 * esz) : nullptr;
-                    sg.out = direct ? nullptr : (void *)((char *)tptr(s, l) + row0 * esz);
+                    const int wl = pooled ? pool_of[(size_t)s][(size_t)l] : l;   // the tensor written
+                    sg.out = direct ? nullptr : (void *)((char *)tptr(s, wl) + row0 * esz);
                     sg.scale = blob->aff_dev + row0;
                     sg.shift = blob->aff_dev + blob->rows + row0;
                     sg.f_start = f;
@@ -1030,14 +1079,17 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                         a.k_per_split = a.K;
                     } else {
                         pick_conv_config(a.M, a.N, a.K, dma_depth, ctx->opt.conv_tile == TILE_STEM ? TILE_64x64 : ctx->opt.conv_tile,
-                                         ctx->opt.conv_splits, Lc.tile, a.k_splits, a.k_per_split);
+                                         ctx->opt.conv_splits, pooled, Lc.tile, a.k_splits, a.k_per_split);
                         // measured choice where nothing is forced and the
                         // launch's tensors all exist at plan time
-                        if (ctx->opt.tune && can_tune && ctx->opt.conv_tile < 0 && ctx->opt.conv_splits <= 0 && !direct &&
-                            blob->w_dev)
+                        if (ctx->opt.tune && can_tune && ctx->opt.conv_tile < 0 && (ctx->opt.conv_splits <= 0 || pooled) &&
+                            !direct && blob->w_dev)
                             tune_conv(ctx, a, dma_depth, bf16, Lc.tile, a.k_splits, a.k_per_split);
                     }
-                    if (tile_is_dma(Lc.tile) && !conv_dma_supported(a, Lc.tile)) Lc.tile = TILE_64x64;
+                    if (tile_is_dma(Lc.tile) && !conv_dma_supported(a, Lc.tile)) {
+                        if (pooled) return fail(ctx, GEMEL_ESTATE, "internal: fused pool without an LDS-DMA tile");
+                        Lc.tile = TILE_64x64;
+                    }
                     Lc.type = L_CONV_BF16;
                     Lc.kind = L0.op == GEMEL_OP_CONV ? GEMEL_K_CONV_MFMA : GEMEL_K_FC;
                 } else {

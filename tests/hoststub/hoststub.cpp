@@ -331,9 +331,16 @@ static hipError_t conv_common(const ConvArgs &a, int tile, int esz, const char *
         if (a.k_splits <= 1 || a.counters) {
             if (a.out_mode == OUT_NHWC)
                 ok &= chk(s.out, ((rows - 1) * a.out_cs + a.N) * esz, "output", kern, true);
+            else if (a.out_mode == OUT_NHWC_POOL2)   // the pooled tensor: a quarter of the rows
+                ok &= chk(s.out, ((rows / 4 - 1) * a.out_cs + a.N) * esz, "pooled output", kern, true);
             else
                 ok &= chk(s.out, frames * a.cout * hwo * 4, "output nchw", kern, true);
         }
+    }
+    if (a.out_mode == OUT_NHWC_POOL2 && (!tile_is_dma(tile) || a.k_splits > 1 || a.has_res || a.Ho % 2 || a.Wo % 2)) {
+        ++violations;
+        last = std::string(kern) + ": fused pool outside the LDS-DMA kernel's conditions";
+        return hipErrorInvalidValue;
     }
     if (a.k_splits > 1) ok &= chk(a.partial, (long long)a.k_splits * a.M * a.N * 4, "partial", kern, true);
     if (a.k_splits > 1 && a.counters) {

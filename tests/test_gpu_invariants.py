@@ -171,6 +171,43 @@ def test_fused_split_k_equals_separate_reduce(r50vgg, tile):
     _same(ref, c)
 
 
+DMA_TILES = [9, 10, 11, 12, 14, 15, 16, 17, 18, 19]
+
+
+@pytest.mark.parametrize("tile", DMA_TILES)
+def test_fused_pool_equals_separate_pool(r50vgg, tile):
+    """A 2x2 max pool fused into its conv's epilogue (GEMM rows in window
+    order, the max of the four activated and bf16-rounded values) gives the
+    bits of the conv's stored output pooled by the separate kernel, for
+    every LDS-DMA tile shape; the merged VGG pair puts two segments in each
+    launch, and every VGG conv/pool pair at 64 px is fused."""
+    wl, params, frames = r50vgg
+    log(f"fused pool tile {tile}")
+    ref = _run(wl, params, frames, OPT_CONV_TILE=tile, OPT_FUSE_POOL=0)
+    got = _run(wl, params, frames, OPT_CONV_TILE=tile, OPT_FUSE_POOL=1,
+               repeat=2)
+    _same(ref, got)
+
+
+def test_fused_pool_odd_sizes_and_default_plan():
+    """At 48 px the VGG conv outputs are 48, 24, 12, 6 and 3 pixels: the
+    last pair (odd output) stays separate, the others fuse. Pinned tile:
+    bitwise against no fusion; default plan (tuned tiles): the oracle."""
+    wl = configs.r50x2_vgg16x2(res=48, frames=2)
+    params = [wl.params(i) for i in range(4)]
+    frames = [wl.frames(i) for i in range(4)]
+    log("fused pool 48 px")
+    ref = _run(wl, params, frames, OPT_CONV_TILE=18, OPT_FUSE_POOL=0)
+    got = _run(wl, params, frames, OPT_CONV_TILE=18, OPT_FUSE_POOL=1)
+    _same(ref, got)
+    g = GpuWorkload(wl, params)
+    try:
+        out = g.run(frames)
+    finally:
+        g.close()
+    compare(wl, out, oracle_outputs(wl, params, frames), tag="r50vgg-48px-fused")
+
+
 def test_swap_forced_equals_resident_bitwise():
     """A budget far below the unmerged weight bytes streams most layers
     through the staging slots every round; outputs must not change."""
