@@ -1,0 +1,53 @@
+"""Every candidate group of a workload merged at once, on the GPU.
+
+gemel_enumerate_groups lists all appearances of each architecturally
+identical layer (Section 5.3); installing all of them makes one weight copy
+serve layers at different positions of one model and at different spatial
+sizes (VGG-19's 512->512 convs at 8x8 and 4x4, ResNet-34's repeated blocks),
+which the plan runs as separate launches over the one copy. The outputs must
+match the oracle evaluated with the same effective weights (each member
+takes its group's first member's parameters)."""
+
+import pytest
+
+from harness import GpuWorkload, compare, log, oracle_outputs
+from oracle import merging as OM
+from workloads import configs, zoo
+
+pytestmark = pytest.mark.gpu
+
+
+def _variants_workload(res=64, frames=2):
+    chw = (3, res, res)
+    models = [configs.ModelSpec("r18", "resnet18", zoo.resnet(18), frames, chw),
+              configs.ModelSpec("r34", "resnet34", zoo.resnet(34), frames, chw),
+              configs.ModelSpec("v16", "vgg16", zoo.vgg(16, 1000, res), frames, chw),
+              configs.ModelSpec("v19", "vgg19", zoo.vgg(19, 1000, res), frames, chw)]
+    groups = [m for _, m in OM.candidate_groups(
+        [(i, m.layers, m.in_chw) for i, m in enumerate(models)], 2)]
+    return configs.Workload("variants", 7, "bf16", models, groups, "normal")
+
+
+def test_all_candidate_groups_merged_match_oracle():
+    wl = _variants_workload()
+    # heterogeneous groups exist: a weight copy used at several spatial sizes
+    sizes = {}
+    for gi, g in enumerate(wl.groups):
+        for mi, li in g:
+            sh = OM.output_shapes(wl.models[mi].layers, wl.models[mi].in_chw)
+            src = wl.models[mi].layers[li]["src0"]
+            hw = wl.models[mi].in_chw[1:] if src < 0 else sh[src][1:]
+            sizes.setdefault(gi, set()).add(tuple(hw))
+    assert any(len(v) > 1 for v in sizes.values())
+    params = [wl.params(i) for i in range(len(wl.models))]
+    frames = [wl.frames(i) for i in range(len(wl.models))]
+    log(f"variants: {len(wl.groups)} groups")
+    g = GpuWorkload(wl, params)
+    try:
+        got = g.run(frames, repeat=2)
+        # the library lists the same groups for the registered models
+        lib_groups = [m for _, m in g.ctx.enumerate_groups(g.ids)]
+        assert lib_groups == [[(g.ids[a], b) for a, b in gr] for gr in wl.groups]
+    finally:
+        g.close()
+    compare(wl, got, oracle_outputs(wl, params, frames), tag="variants-64px")
