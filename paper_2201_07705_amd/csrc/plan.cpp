@@ -589,8 +589,12 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
     }
 
     // ---- nodes: merged groups batched when compatible ----
+    // A node batches at most one appearance of a group per model: the k-th
+    // appearance in each model goes with the k-th of the others (appearances
+    // within one model may depend on each other, e.g. repeated blocks).
     std::vector<Node> nodes;
     std::map<std::vector<int64_t>, int> group_node;
+    std::map<std::pair<int, int>, int> occurrence;   // (model slot, group) -> appearances so far
     std::vector<std::vector<int>> node_of((size_t)S);
     for (int s = 0; s < S; ++s) {
         const Model &m = model(s);
@@ -605,7 +609,8 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
             if (L.group >= 0 && !ctx->opt.split_merged) {
                 std::vector<int64_t> key = {L.group, L.in_h, L.in_w, L.in_c, L.act,
                                             (int64_t)(L.slope * 1e6f), L.res >= 0, L.res_mode,
-                                            direct_output(L), L.src1_cp, pool_of[(size_t)s][(size_t)l] >= 0};
+                                            direct_output(L), L.src1_cp, pool_of[(size_t)s][(size_t)l] >= 0,
+                                            occurrence[{s, L.group}]++};
                 auto it = group_node.find(key);
                 if (it != group_node.end() && nodes[(size_t)it->second].mem.size() < GEMEL_MAX_SEG) {
                     nid = it->second;
@@ -623,7 +628,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
         }
     }
 
-    // ---- topological order of nodes (Kahn); dissolve merged nodes on a cycle ----
+    // ---- topological order of nodes (Kahn) ----
     auto topo = [&](std::vector<int> &order) -> bool {
         const size_t n = nodes.size();
         std::vector<std::set<int>> out(n);
@@ -655,20 +660,32 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
         }
         return order.size() == n;
     };
+    // a merged node that takes part in a cycle (its members' models order
+    // their layers differently) runs its members separately: the nodes Kahn
+    // leaves unordered are on a cycle or behind one, and each round splits
+    // the merged ones among them until an order exists
     std::vector<int> order;
-    if (!topo(order)) {
-        std::vector<Node> single;
-        for (auto &nd : nodes)
-            for (auto &mb : nd.mem) {
-                node_of[(size_t)mb.first][(size_t)mb.second] = (int)single.size();
-                single.push_back(Node{nd.op, {mb}});
+    while (!topo(order)) {
+        std::vector<char> done(nodes.size(), 0);
+        for (int v : order) done[(size_t)v] = 1;
+        std::vector<Node> next;
+        bool split = false;
+        for (size_t v = 0; v < nodes.size(); ++v) {
+            if (!done[v] && nodes[v].mem.size() > 1) {
+                split = true;
+                for (auto &mb : nodes[v].mem) next.push_back(Node{nodes[v].op, {mb}});
+            } else {
+                next.push_back(nodes[v]);
             }
-        nodes.swap(single);
+        }
+        if (!split) return fail(ctx, GEMEL_ESTATE, "internal: layer graph has a cycle");
+        nodes.swap(next);
+        for (size_t v = 0; v < nodes.size(); ++v)
+            for (auto &mb : nodes[v].mem) node_of[(size_t)mb.first][(size_t)mb.second] = (int)v;
         for (int s = 0; s < S; ++s)
             for (size_t p = 0; p < fused_into[(size_t)s].size(); ++p)
                 if (fused_into[(size_t)s][p] >= 0)
                     node_of[(size_t)s][p] = node_of[(size_t)s][(size_t)fused_into[(size_t)s][p]];
-        if (!topo(order)) return fail(ctx, GEMEL_ESTATE, "internal: layer graph has a cycle");
     }
 
     // ---- steps: the ordered nodes, then one export step per output that is

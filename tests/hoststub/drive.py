@@ -27,7 +27,12 @@ def main():
               "hoststub_hazards", "hoststub_check_order", "hoststub_selftest"):
         getattr(L, f).restype = ctypes.c_long
     L.hoststub_last.restype = ctypes.c_char_p
-    wl = configs.get(name, **kw)
+    if name == "variants":   # every candidate group merged (tests/test_gpu_merging.py)
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        from test_gpu_merging import _variants_workload
+        wl = _variants_workload(**kw)
+    else:
+        wl = configs.get(name, **kw)
     ctx = G.Context(0, wl.dtype, 0, library=L)
     ids = [ctx.register_model(m.layers, wl.params(i), m.in_chw)
            for i, m in enumerate(wl.models)]
