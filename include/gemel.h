@@ -374,7 +374,7 @@ enum {
                                     to that many candidates. Different
                                     choices change fp32 summation order,
                                     so bits may differ between contexts    */
-    GEMEL_OPT_FUSE_POOL = 15     /* 1 (default): a bf16 conv whose only
+    GEMEL_OPT_FUSE_POOL = 15,    /* 1 (default): a bf16 conv whose only
                                     consumer is a 2x2 stride-2 max pool
                                     (even output size, no residual, not an
                                     output, input channels a multiple of
@@ -383,6 +383,15 @@ enum {
                                     full-size tensor disappear. Results are
                                     bit-identical to the separate pool. 0:
                                     off                                    */
+    GEMEL_OPT_MIXED_SIZES = 16   /* 1 (default): members of a merged group
+                                    whose inputs differ in spatial size
+                                    (one weight copy at several positions
+                                    or input sizes) run as one launch whose
+                                    segments keep their own sizes, where
+                                    the conv takes the LDS-DMA kernel (bf16,
+                                    input channels a multiple of 32,
+                                    internal output, no fused pool). 0: one
+                                    launch per size                        */
 };
 
 /* Set an option; takes effect at the next gemel_infer. Errors: EINVAL. */

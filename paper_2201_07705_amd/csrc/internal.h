@@ -180,6 +180,7 @@ struct Options {
     int tune = 1;             // measured conv configuration at plan time
     int tune_candidates = 4;  // configurations timed per conv shape
     int fuse_pool = 1;        // 2x2 max pools fused into their conv
+    int mixed_sizes = 1;      // merged members of different sizes in one launch
     int64_t slot_bytes = 32ll << 20;
     int slots = 3;
     int64_t fail_copy_at = 0;

@@ -432,8 +432,9 @@ static bool conv_args_ok(const ConvArgs &a) {
     if (a.k_splits > 1 && (long)a.k_splits * a.M * a.N * 4 > 0x7fffffffL) return false;
     if (a.k_per_split <= 0 || (long)a.k_per_split * a.k_splits < a.K) return false;
     if (a.out_mode == OUT_NCHW_F32 && a.cout > a.N) return false;
-    // the fused 2x2 pool exists only in the LDS-DMA kernel
-    if (a.out_mode != OUT_NHWC && a.out_mode != OUT_NCHW_F32) return false;
+    // the fused 2x2 pool and segments of mixed sizes exist only in the
+    // LDS-DMA kernel
+    if ((a.out_mode != OUT_NHWC && a.out_mode != OUT_NCHW_F32) || a.hetero) return false;
     return true;
 }
 

@@ -75,9 +75,10 @@ __device__ __forceinline__ void wait_lgkm0() {
 
 }  // namespace
 
-// POOL: the 2x2 stride-2 max pool fused (out_mode OUT_NHWC_POOL2), a
-// separate instantiation so that the other kernels keep their code size
-template <int BM, int BN, int WM, int WN, int STAGES, int BK, bool POOL>
+// MODE 1: the 2x2 stride-2 max pool fused (out_mode OUT_NHWC_POOL2);
+// MODE 2: segments of different spatial sizes (ConvArgs::hetero). Separate
+// instantiations, so that the plain kernels keep their code and registers.
+template <int BM, int BN, int WM, int WN, int STAGES, int BK, int MODE>
 __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a) {
     constexpr int NW = WM * WN, NT = 64 * NW;
     static_assert(BK == 32 || BK == 64, "step depth");
@@ -132,10 +133,14 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
     auto sw = [](int row) __attribute__((always_inline)) { return (row >> 1) & (CPR - 1); };
     // with the 2x2 max pool fused, rows run over the output in window
     // order: row 4g + 2dy + dx is pixel (2hp + dy, 2wp + dx) of pooled pixel g
-    constexpr bool pool2 = POOL;
+    constexpr bool pool2 = MODE == 1;
+    // with segments of different sizes, each row takes its segment's sizes
+    // (and its frame within the segment from the rows before it)
+    constexpr bool hetero = MODE == 2;
     const int Wp = a.Wo >> 1, HWp = HWo >> 2;
     const u16 *abase[AI];
     int ahi[AI], awi[AI], acq[AI];
+    int aH[hetero ? AI : 1], aW[hetero ? AI : 1];
 #pragma unroll
     for (int i = 0; i < AI; ++i) {
         const int rl = (i * NW + wave) * RPI + lane / CPR;
@@ -144,7 +149,31 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
         abase[i] = zp;
         ahi[i] = -(1 << 28);
         awi[i] = 0;
-        if (gm < a.M) {
+        if constexpr (hetero) {
+            aH[i] = 0;
+            aW[i] = 0;
+        }
+        if (hetero && gm < a.M) {
+            // the row's segment sizes: uniform in a tile inside one segment,
+            // else gathered with scalar loads and selects like row_seg
+            int sH = a.seg[s_first].H, sW = a.seg[s_first].W, sHo = a.seg[s_first].Ho, sWo = a.seg[s_first].Wo;
+            if (!one_seg)
+                for (int k = 1; k < a.nseg; ++k) {
+                    const bool hit = gm >= a.seg[k].m_start;
+                    sH = hit ? a.seg[k].H : sH;
+                    sW = hit ? a.seg[k].W : sW;
+                    sHo = hit ? a.seg[k].Ho : sHo;
+                    sWo = hit ? a.seg[k].Wo : sWo;
+                }
+            const RowSeg sg = one_seg ? useg : row_seg(a, gm);
+            const int local = gm - sg.m_start, hw = sHo * sWo;
+            const int fl = local / hw, pix = local - fl * hw, ho = pix / sWo;
+            abase[i] = (const u16 *)sg.in + (size_t)fl * sH * sW * in_cs;
+            ahi[i] = ho * a.stride - a.pad;
+            awi[i] = (pix - ho * sWo) * a.stride - a.pad;
+            aH[i] = sH;
+            aW[i] = sW;
+        } else if (gm < a.M) {
             int fr, ho, wo;
             if constexpr (pool2) {
                 const int g = gm >> 2;
@@ -189,8 +218,9 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
 #pragma unroll
         for (int i = 0; i < AI; ++i) {
             const int hi = ahi[i] + lr, wi = awi[i] + ls;
-            const bool ok = (unsigned)hi < (unsigned)H && (unsigned)wi < (unsigned)W;
-            arow[i] = (ok ? abase[i] + (size_t)(hi * W + wi) * in_cs : zp) + acq[i] * 8;
+            const int Hr = hetero ? aH[hetero ? i : 0] : H, Wr = hetero ? aW[hetero ? i : 0] : W;
+            const bool ok = (unsigned)hi < (unsigned)Hr && (unsigned)wi < (unsigned)Wr;
+            arow[i] = (ok ? abase[i] + (size_t)(hi * Wr + wi) * in_cs : zp) + acq[i] * 8;
         }
     };
     set_tap();
@@ -508,11 +538,21 @@ hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) {
         return hipErrorInvalidValue;
     if (a.k_splits > 1 && (long)a.k_splits * a.M * a.N * 4 > 0x7fffffffL) return hipErrorInvalidValue;
     if ((long)a.k_per_split * a.k_splits < a.K) return hipErrorInvalidValue;
+    // mixed sizes: NHWC output, no fused pool; each segment whole frames of
+    // its own size, the rows of the segments back to back
+    if (a.hetero && a.out_mode != OUT_NHWC) return hipErrorInvalidValue;
     for (int i = 0; i < a.nseg; ++i) {
-        if (!a.seg[i].in || !a.seg[i].scale || !a.seg[i].shift) return hipErrorInvalidValue;
-        if ((a.k_splits <= 1 || a.counters) && !a.seg[i].out) return hipErrorInvalidValue;
-        if (a.has_res && !a.seg[i].res) return hipErrorInvalidValue;
-        if (a.seg[i].m_start != a.seg[i].f_start * a.Ho * a.Wo) return hipErrorInvalidValue;
+        const ConvSeg &s = a.seg[i];
+        if (!s.in || !s.scale || !s.shift) return hipErrorInvalidValue;
+        if ((a.k_splits <= 1 || a.counters) && !s.out) return hipErrorInvalidValue;
+        if (a.has_res && !s.res) return hipErrorInvalidValue;
+        if (!a.hetero) {
+            if (s.m_start != s.f_start * a.Ho * a.Wo) return hipErrorInvalidValue;
+            continue;
+        }
+        const long rows = (i + 1 < a.nseg ? a.seg[i + 1].m_start : a.M) - (long)s.m_start;
+        if (s.H <= 0 || s.W <= 0 || s.Ho <= 0 || s.Wo <= 0 || rows <= 0 || rows % ((long)s.Ho * s.Wo))
+            return hipErrorInvalidValue;
     }
     const int bm = conv_tile_bm(tile), bn = conv_tile_bn(tile);
     if (!bm) return hipErrorInvalidValue;
@@ -521,13 +561,14 @@ hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) {
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
     dim3 grid((unsigned)blocks, (unsigned)a.k_splits);
     hipError_t e = hipErrorInvalidValue;
-    const bool pool = a.out_mode == OUT_NHWC_POOL2;
-#define GEMEL_DMA_CASE(T, BM_, BN_, WM_, WN_, ST_, BK_, NT_)                                                    \
-    case T:                                                                                                     \
-        e = submit(sk,                                                                                          \
-                   pool ? reinterpret_cast<const void *>(&conv_dma_kernel<BM_, BN_, WM_, WN_, ST_, BK_, true>)  \
-                        : reinterpret_cast<const void *>(&conv_dma_kernel<BM_, BN_, WM_, WN_, ST_, BK_, false>), \
-                   grid, dim3(NT_), a);                                                                         \
+    const int mode = a.out_mode == OUT_NHWC_POOL2 ? 1 : a.hetero ? 2 : 0;
+#define GEMEL_DMA_CASE(T, BM_, BN_, WM_, WN_, ST_, BK_, NT_)                                                  \
+    case T:                                                                                                   \
+        e = submit(sk,                                                                                        \
+                   mode == 1   ? reinterpret_cast<const void *>(&conv_dma_kernel<BM_, BN_, WM_, WN_, ST_, BK_, 1>) \
+                   : mode == 2 ? reinterpret_cast<const void *>(&conv_dma_kernel<BM_, BN_, WM_, WN_, ST_, BK_, 2>) \
+                               : reinterpret_cast<const void *>(&conv_dma_kernel<BM_, BN_, WM_, WN_, ST_, BK_, 0>), \
+                   grid, dim3(NT_), a);                                                                       \
         break;
     switch (tile) {
         GEMEL_DMA_CASE(TILE_DMA_256x256, 256, 256, 2, 4, 4, 32, 512)

@@ -27,8 +27,9 @@ struct ConvSeg {
     void *out;            // NHWC [frames][Ho][Wo][out_cs] or NCHW f32 final
     const float *scale;   // [N] per output channel
     const float *shift;   // [N]
-    int32_t m_start;      // first GEMM row (= first frame * Ho * Wo)
+    int32_t m_start;      // first GEMM row (rows of the earlier segments)
     int32_t f_start;      // first frame of the segment in the launch
+    int32_t H, W, Ho, Wo; // the segment's input and output sizes (ConvArgs::hetero)
 };
 
 struct ConvArgs {
@@ -48,6 +49,11 @@ struct ConvArgs {
     int32_t out_mode;     // OUT_NHWC or OUT_NCHW_F32
     int32_t nseg;
     int32_t uni_affine;   // every segment uses the same scale/shift arrays
+    int32_t hetero;       // 1: segments of different spatial sizes (one weight
+                          // copy used at several positions or input sizes):
+                          // each row's sizes are its segment's H, W, Ho, Wo,
+                          // the launch-wide ones are unused (LDS-DMA kernel,
+                          // NHWC output, no fused pool)
     int32_t k_splits;     // >1: write fp32 partials to `partial`
     int32_t k_per_split;  // depth handled by one split (multiple of BK)
     float *partial;       // [k_splits][M][N] when k_splits > 1

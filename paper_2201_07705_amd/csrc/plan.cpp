@@ -341,16 +341,17 @@ struct ConvCand {
 
 // Every (tile, split-K) configuration the conv may use, fastest estimate
 // first. dma_depth: deepest LDS-DMA step the conv allows (0: no DMA tile,
-// 32 or 64); force >= 0 restricts the tile; pooled: the conv's 2x2 pool is
-// fused (LDS-DMA tiles, no split-K).
-std::vector<ConvCand> conv_candidates(int64_t M, int64_t N, int64_t K, int dma_depth, int force, bool pooled) {
+// 32 or 64); force >= 0 restricts the tile; dma_only: LDS-DMA tiles only
+// (a fused pool, segments of mixed sizes); no_split: no split-K (a fused
+// pool).
+std::vector<ConvCand> conv_candidates(int64_t M, int64_t N, int64_t K, int dma_depth, int force, bool dma_only,
+                                      bool no_split) {
     const double cu_flops = 4096.0 * 2.4e9;   // per CU, dense bf16
     std::vector<ConvCand> out;
     for (const TileCost &tc : kTileCost) {
         if (force >= 0 && tc.tile != force) continue;
         if (force < 0 && tile_is_dma(tc.tile) && tile_dma_depth(tc.tile) > dma_depth) continue;
-        // a fused pool runs in the LDS-DMA kernel without split-K
-        if (pooled && (!tile_is_dma(tc.tile) || tile_dma_depth(tc.tile) > dma_depth)) continue;
+        if (dma_only && (!tile_is_dma(tc.tile) || tile_dma_depth(tc.tile) > dma_depth)) continue;
         const int64_t bm = conv_tile_bm(tc.tile), bn = conv_tile_bn(tc.tile);
         const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
         int last = 0;
@@ -360,7 +361,7 @@ std::vector<ConvCand> conv_candidates(int64_t M, int64_t N, int64_t K, int dma_d
             const int64_t s_eff = (K + k_s - 1) / k_s;
             if (s_eff > 1 && s_eff * M * N * 4 > kMaxPartialBytes) break;
             if (s_eff == last) continue;
-            if (pooled && s_eff > 1) break;
+            if (no_split && s_eff > 1) break;
             last = (int)s_eff;
             const double waves = std::ceil((double)(tiles * s_eff) / (256.0 * tc.occ));
             double t = waves * (tc.occ * (2.0 * bm * bn * k_s) / (cu_flops * tc.eff) + tc.lat);
@@ -382,9 +383,9 @@ void conv_split_depth(int64_t K, int &splits, int &kps) {
 // Launch configuration of a bf16 implicit-GEMM conv of size M x N x K:
 // the candidate with the smallest estimated time (or the forced tile /
 // split count).
-void pick_conv_config(int64_t M, int64_t N, int64_t K, int dma_depth, int force, int force_splits, bool pooled,
-                      int &tile, int &splits, int &kps) {
-    const std::vector<ConvCand> c = conv_candidates(M, N, K, dma_depth, force, pooled);
+void pick_conv_config(int64_t M, int64_t N, int64_t K, int dma_depth, int force, int force_splits, bool dma_only,
+                      bool pooled, int &tile, int &splits, int &kps) {
+    const std::vector<ConvCand> c = conv_candidates(M, N, K, dma_depth, force, dma_only || pooled, pooled);
     tile = c.empty() ? (force >= 0 ? force : TILE_64x64) : c[0].tile;
     splits = c.empty() ? 1 : c[0].splits;
     if (force_splits > 0 && !pooled) splits = (int)std::min<int64_t>(force_splits, (K + CONV_BK - 1) / CONV_BK);
@@ -420,7 +421,8 @@ ReduceArgs reduce_args(const ConvArgs &a) {
 // (leaving tile/splits/kps alone) if nothing could be timed.
 bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int &tile, int &splits, int &kps) {
     std::vector<int64_t> key = {a0.M, a0.N, a0.K, a0.H, a0.W, a0.Cin, a0.in_cs, a0.kh, a0.kw, a0.stride, a0.pad,
-                                a0.out_cs, a0.has_res, a0.out_mode, a0.nseg > 1, dma_depth, ctx->opt.splitk_fused};
+                                a0.out_cs, a0.has_res, a0.out_mode, a0.nseg > 1, dma_depth, ctx->opt.splitk_fused,
+                                a0.hetero};
     auto hit = ctx->tune_cache.find(key);
     if (hit != ctx->tune_cache.end()) {
         tile = hit->second.first;
@@ -428,7 +430,8 @@ bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int
         conv_split_depth(a0.K, splits, kps);
         return true;
     }
-    std::vector<ConvCand> c = conv_candidates(a0.M, a0.N, a0.K, dma_depth, -1, a0.out_mode == OUT_NHWC_POOL2);
+    const bool pooled = a0.out_mode == OUT_NHWC_POOL2;
+    std::vector<ConvCand> c = conv_candidates(a0.M, a0.N, a0.K, dma_depth, -1, pooled || a0.hetero, pooled);
     if (c.empty()) return false;
     const double cut = 2.0 * c[0].est;
     size_t n = 0;
@@ -607,7 +610,14 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
             }
             int nid = -1;
             if (L.group >= 0 && !ctx->opt.split_merged) {
-                std::vector<int64_t> key = {L.group, L.in_h, L.in_w, L.in_c, L.act,
+                // members of different spatial sizes share a launch where the
+                // LDS-DMA kernel can take them (one weight copy, per-segment
+                // sizes): bf16 conv, internal NHWC output, no fused pool
+                const bool mixed = ctx->opt.mixed_sizes && bf16 && L.op == GEMEL_OP_CONV && !direct_output(L) &&
+                                   pool_of[(size_t)s][(size_t)l] < 0 && L.in_cp % 32 == 0 &&
+                                   (int64_t)L.in_cp * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES &&
+                                   (forced < 0 || (tile_is_dma(forced) && (tile_dma_depth(forced) == 32 || L.in_cp % 64 == 0)));
+                std::vector<int64_t> key = {L.group, mixed ? -1 : L.in_h, mixed ? -1 : L.in_w, L.in_c, L.act,
                                             (int64_t)(L.slope * 1e6f), L.res >= 0, L.res_mode,
                                             direct_output(L), L.src1_cp, pool_of[(size_t)s][(size_t)l] >= 0,
                                             occurrence[{s, L.group}]++};
@@ -977,9 +987,9 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     return fail(ctx, GEMEL_EBUDGET, "an output layer's weights exceed one staging slot");
                 for (int64_t r0 = 0; r0 < blob->rows; r0 += per) rows.push_back({r0, std::min(per, blob->rows - r0)});
             }
-            int64_t frames_in = 0;
-            for (auto [s, l] : nd.mem) frames_in += nfr[(size_t)s];
-            const double in_elems = (double)frames_in * L0.in_h * L0.in_w * L0.in_c;
+            double in_elems = 0;
+            for (auto [s, l] : nd.mem)
+                in_elems += (double)nfr[(size_t)s] * layer(s, l).in_h * layer(s, l).in_w * layer(s, l).in_c;
             const double kdepth = L0.op == GEMEL_OP_CONV ? (double)L0.kh * L0.kw * L0.cin : (double)L0.cin;
             for (auto [row0, nrows] : rows) {
                 Launch Lc;
@@ -1060,7 +1070,9 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 a.res_mode = L0.res_mode; a.has_res = L0.res >= 0;
                 a.out_mode = direct ? OUT_NCHW_F32 : pooled ? OUT_NHWC_POOL2 : OUT_NHWC;
                 a.nseg = 0;
+                a.hetero = 0;
                 int f = 0;
+                int64_t m_acc = 0;
                 for (auto [s, l] : nd.mem) {
                     if (!nfr[(size_t)s]) continue;
                     const Layer &L = layer(s, l);
@@ -1072,7 +1084,11 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     sg.scale = blob->aff_dev + row0;
                     sg.shift = blob->aff_dev + blob->rows + row0;
                     sg.f_start = f;
-                    sg.m_start = f * L.out_h * L.out_w;
+                    sg.m_start = (int32_t)m_acc;
+                    sg.H = L.in_h; sg.W = L.in_w; sg.Ho = L.out_h; sg.Wo = L.out_w;
+                    if (L.in_h != L0.in_h || L.in_w != L0.in_w || L.out_h != L0.out_h || L.out_w != L0.out_w)
+                        a.hetero = 1;
+                    m_acc += (int64_t)nfr[(size_t)s] * L.out_h * L.out_w;
                     if (direct) Lc.patches.push_back({Patch::OUTPUT, s, L.out_index, a.nseg});
                     f += nfr[(size_t)s];
                     a.nseg++;
@@ -1096,7 +1112,8 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                         a.k_per_split = a.K;
                     } else {
                         pick_conv_config(a.M, a.N, a.K, dma_depth, ctx->opt.conv_tile == TILE_STEM ? TILE_64x64 : ctx->opt.conv_tile,
-                                         ctx->opt.conv_splits, pooled, Lc.tile, a.k_splits, a.k_per_split);
+                                         ctx->opt.conv_splits, a.hetero != 0, pooled, Lc.tile, a.k_splits,
+                                         a.k_per_split);
                         // measured choice where nothing is forced and the
                         // launch's tensors all exist at plan time
                         if (ctx->opt.tune && can_tune && ctx->opt.conv_tile < 0 && (ctx->opt.conv_splits <= 0 || pooled) &&
@@ -1104,7 +1121,8 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                             tune_conv(ctx, a, dma_depth, bf16, Lc.tile, a.k_splits, a.k_per_split);
                     }
                     if (tile_is_dma(Lc.tile) && !conv_dma_supported(a, Lc.tile)) {
-                        if (pooled) return fail(ctx, GEMEL_ESTATE, "internal: fused pool without an LDS-DMA tile");
+                        if (pooled || a.hetero)
+                            return fail(ctx, GEMEL_ESTATE, "internal: fused pool or mixed sizes without an LDS-DMA tile");
                         Lc.tile = TILE_64x64;
                     }
                     Lc.type = L_CONV_BF16;

@@ -527,6 +527,11 @@ gemel_status gemel_set_option(gemel_ctx *ctx, int32_t key, int64_t value) {
         if (value > 1) ctx->opt.tune_candidates = (int)value;
         drop_plans(ctx);
         break;
+    case GEMEL_OPT_MIXED_SIZES:
+        if (value != 0 && value != 1) return fail(ctx, GEMEL_EINVAL, "mixed_sizes is 0 or 1");
+        ctx->opt.mixed_sizes = (int)value;
+        drop_plans(ctx);
+        break;
     case GEMEL_OPT_FUSE_POOL:
         if (value != 0 && value != 1) return fail(ctx, GEMEL_EINVAL, "fuse_pool is 0 or 1");
         ctx->opt.fuse_pool = (int)value;

@@ -39,7 +39,8 @@ Q_UNMERGED_BYTES, Q_MERGED_BYTES, Q_RESIDENT_BYTES, Q_PEAK_BYTES, \
 OPT_USE_GRAPH, OPT_SWAP_SLOT_BYTES, OPT_SWAP_SLOTS, OPT_FAIL_COPY_AT, \
     OPT_SPLIT_MERGED, OPT_WEIGHT_BUDGET, OPT_PROFILE, OPT_CONV_TILE, \
     OPT_CONV_SPLITS, OPT_STREAMS, OPT_GRAPH_DAG, OPT_FORK_US, \
-    OPT_AUTOTUNE, OPT_SPLITK_FUSED, OPT_TUNE, OPT_FUSE_POOL = range(16)
+    OPT_AUTOTUNE, OPT_SPLITK_FUSED, OPT_TUNE, OPT_FUSE_POOL, \
+    OPT_MIXED_SIZES = range(17)
 KERNEL_FAMILIES = ("conv_mfma", "conv_f32", "splitk_reduce", "fc", "pack",
                    "pool", "route", "export")
 

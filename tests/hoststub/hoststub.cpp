@@ -316,16 +316,25 @@ static hipError_t conv_common(const ConvArgs &a, int tile, int esz, const char *
     const long long hwo = (long long)a.Ho * a.Wo;
     ok &= chk(a.w, (long long)a.N * a.K * esz, "weights", kern);
     if (need_zero) ok &= chk(a.zero, GEMEL_ZERO_PAGE_BYTES, "zero page", kern);
+    if (a.hetero && (!tile_is_dma(tile) || a.out_mode != OUT_NHWC)) {
+        ++violations;
+        last = std::string(kern) + ": mixed sizes outside the LDS-DMA kernel's conditions";
+        return hipErrorInvalidValue;
+    }
     for (int i = 0; i < a.nseg; ++i) {
         const ConvSeg &s = a.seg[i];
         const long long rows = seg_rows(a.seg, a.nseg, i, a.M);
-        if (rows <= 0 || rows % hwo || s.m_start != (long long)s.f_start * hwo) {
+        // a segment's own sizes with mixed sizes, else the launch's
+        const long long shw = a.hetero ? (long long)s.Ho * s.Wo : hwo;
+        const long long sin = a.hetero ? (long long)s.H * s.W : (long long)a.H * a.W;
+        if (rows <= 0 || shw <= 0 || rows % shw || (!a.hetero && s.m_start != (long long)s.f_start * hwo) ||
+            (a.hetero && i && s.m_start <= a.seg[i - 1].m_start)) {
             ++violations;
             last = std::string(kern) + ": segment rows do not match frames";
             return hipErrorInvalidValue;
         }
-        const long long frames = rows / hwo;
-        ok &= chk(s.in, frames * a.H * a.W * a.in_cs * esz, "input", kern);
+        const long long frames = rows / shw;
+        ok &= chk(s.in, frames * sin * a.in_cs * esz, "input", kern);
         ok &= chk(s.scale, (long long)a.N * 4, "scale", kern) & chk(s.shift, (long long)a.N * 4, "shift", kern);
         if (a.has_res) ok &= chk(s.res, ((rows - 1) * a.out_cs + a.N) * esz, "residual", kern);
         if (a.k_splits <= 1 || a.counters) {

@@ -51,3 +51,36 @@ def test_all_candidate_groups_merged_match_oracle():
     finally:
         g.close()
     compare(wl, got, oracle_outputs(wl, params, frames), tag="variants-64px")
+
+
+def _run(wl, params, frames, **opts):
+    from paper_2201_07705_amd import gemel as G
+    g = GpuWorkload(wl, params)
+    try:
+        for k, v in opts.items():
+            g.ctx.set_option(getattr(G, k), v)
+        out = g.run(frames, repeat=2)
+        return out, g.ctx.query(G.Q_LAUNCHES)
+    finally:
+        g.close()
+
+
+@pytest.mark.parametrize("tile", [11, 18, 19])
+def test_mixed_size_launch_equals_one_launch_per_size(tile):
+    """Members of a merged group whose inputs differ in size (VGG-16's
+    conv5_1 at 4x4 with VGG-19's conv4_4 at 8x8, once pooling is not fused
+    into them) run as one launch whose segments keep their own sizes; with
+    the tile and split-K pinned, the bits equal one launch per size."""
+    import numpy as np
+    wl = _variants_workload()
+    params = [wl.params(i) for i in range(len(wl.models))]
+    frames = [wl.frames(i) for i in range(len(wl.models))]
+    log(f"mixed sizes tile {tile}")
+    pin = dict(OPT_FUSE_POOL=0, OPT_CONV_TILE=tile, OPT_CONV_SPLITS=1)
+    a, na = _run(wl, params, frames, OPT_MIXED_SIZES=0, **pin)
+    b, nb = _run(wl, params, frames, OPT_MIXED_SIZES=1, **pin)
+    assert nb < na
+    for x, y in zip(a, b):
+        for u, v in zip(x, y):
+            assert np.array_equal(u, v)
+    compare(wl, b, oracle_outputs(wl, params, frames), tag=f"variants-mixed-{tile}")
