@@ -335,7 +335,7 @@ enum {
     GEMEL_OPT_FORK_US = 11,      /* a branch gets a stream of its own when
                                     the work only it leads to is estimated
                                     at this many microseconds or more
-                                    (default 30), or spans 3 or more
+                                    (default 12), or spans 3 or more
                                     launch steps                           */
     GEMEL_OPT_AUTOTUNE = 12,     /* 1 (default): the first 12 rounds of a
                                     graphable plan over several streams try

@@ -175,7 +175,7 @@ struct Options {
     int use_graph = 1;
     int graph_dag = 0;
     int autotune = 1;
-    int fork_us = 30;
+    int fork_us = 12;
     int splitk_fused = 1;
     int tune = 1;             // measured conv configuration at plan time
     int tune_candidates = 4;  // configurations timed per conv shape
