@@ -337,16 +337,18 @@ enum {
                                     at this many microseconds or more
                                     (default 12), or spans 3 or more
                                     launch steps                           */
-    GEMEL_OPT_AUTOTUNE = 12,     /* 1 (default): the first 12 rounds of a
+    GEMEL_OPT_AUTOTUNE = 12,     /* 1 (default): the first 20 rounds of a
                                     graphable plan over several streams try
                                     the two graph forms of GEMEL_OPT_GRAPH_DAG,
                                     one graph with data edges plus each
-                                    stream's order, and direct enqueue, 3
-                                    rounds each (the first untimed), timing
+                                    stream's order, and direct enqueue: one
+                                    untimed round of each, then 4 timed
+                                    rounds of each, interleaved, timing
                                     each round with
                                     HIP events on the caller's stream (the
                                     timed rounds synchronise with it), and
-                                    later rounds use the fastest. Skipped
+                                    later rounds use the one with the
+                                    smallest median. Skipped
                                     while the caller's stream is being
                                     captured. 0: the mode set by
                                     GEMEL_OPT_GRAPH_DAG                    */

@@ -145,7 +145,7 @@ struct Plan {
     // execution mode of a multi-stream graphable plan, chosen by timing
     // each candidate over its first rounds (autotune)
     int tune_round = 0;
-    double tune_ms[4] = {0, 0, 0, 0};
+    double tune_ms[4][4] = {};   // timed rounds of each candidate mode
     int best_mode = -1;
     hipEvent_t tune_ev[2] = {nullptr, nullptr};
     std::vector<const void *> graph_frames;

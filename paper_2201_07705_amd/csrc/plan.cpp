@@ -1640,9 +1640,10 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
     }
     // mode of this round: a single-stream plan is one chain graph; a
     // multi-stream plan uses the mode set by the options, or, with autotune,
-    // each candidate mode for kTuneEach rounds (the first of them untimed)
-    // and then the fastest
-    constexpr int kTuneEach = 3;
+    // one untimed round of each candidate mode, then kTimed timed rounds of
+    // each with the modes interleaved (so that clock drift affects all
+    // alike), and then the mode with the smallest median
+    constexpr int kTimed = 4;
     constexpr int kNCand = 4;
     static const int kCand[kNCand] = {MODE_SEGMENTS, MODE_STREAMGRAPH, MODE_DAG, MODE_EAGER};
     int mode = ctx->opt.graph_dag ? MODE_DAG : MODE_SEGMENTS;
@@ -1656,8 +1657,8 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
             hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
             HIPCHK(hipStreamIsCapturing(stream, &cs), "hipStreamIsCapturing");
             if (cs == hipStreamCaptureStatusNone) {
-                mode = kCand[P.tune_round / kTuneEach];
-                timed = P.tune_round % kTuneEach != 0;
+                mode = kCand[P.tune_round % kNCand];
+                timed = P.tune_round >= kNCand;
                 tuning = true;
                 for (auto &ev : P.tune_ev)
                     if (!ev) HIPCHK(hipEventCreate(&ev), "hipEventCreate");
@@ -1708,13 +1709,22 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         HIPCHK(hipEventSynchronize(P.tune_ev[1]), "hipEventSynchronize");
         float ms = 0;
         HIPCHK(hipEventElapsedTime(&ms, P.tune_ev[0], P.tune_ev[1]), "hipEventElapsedTime");
-        P.tune_ms[P.tune_round / kTuneEach] += ms;
+        P.tune_ms[P.tune_round % kNCand][P.tune_round / kNCand - 1] = ms;
     }
     if (tuning) {
-        if (++P.tune_round == kNCand * kTuneEach) {
+        if (++P.tune_round == kNCand * (1 + kTimed)) {
+            static_assert(kTimed == 4, "median of four");
             int b = 0;
-            for (int c = 1; c < kNCand; ++c)
-                if (P.tune_ms[c] < P.tune_ms[b]) b = c;
+            double best = 0;
+            for (int c = 0; c < kNCand; ++c) {
+                double *t = P.tune_ms[c];
+                std::sort(t, t + kTimed);
+                const double med = 0.5 * (t[1] + t[2]);
+                if (c == 0 || med < best) {
+                    best = med;
+                    b = c;
+                }
+            }
             P.best_mode = kCand[b];
         }
     }

@@ -119,7 +119,7 @@ def test_autotuned_rounds_bitwise(r50vgg):
         dev = [torch.from_numpy(f).cuda() for f in frames]
         s = torch.cuda.Stream()
         outs = None
-        for r in range(14):
+        for r in range(22):
             with torch.cuda.stream(s):
                 outs = g.ctx.infer(g.ids, dev, stream=s, outputs=outs)
             s.synchronize()
