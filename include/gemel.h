@@ -137,7 +137,11 @@ typedef struct gemel_group {
 } gemel_group;
 
 /*
- * Create a context on HIP device `device`.
+ * Create a context on HIP device `device`: the GPU memory into which
+ * registered models are loaded. When a workload's models do not fit it,
+ * they are time-shared by swapping weights in from host memory over PCIe
+ * (Section 3.2); the paper evaluates each workload under fixed caps on
+ * that memory (Appendix A.3), which hbm_weight_budget stands for.
  *  dtype              GEMEL_F32 (float32 everywhere) or GEMEL_BF16 (bf16
  *                     weights and activations, float32 accumulation and
  *                     epilogue, float32 outputs).
@@ -216,7 +220,13 @@ gemel_status gemel_enumerate_groups(gemel_ctx *ctx, const int32_t *model_ids,
                                     int32_t *n_groups, int32_t *n_members);
 
 /*
- * Run one inference round over `n_models` registered models.
+ * Run one inference round over `n_models` registered models (the edge
+ * box's inference step, Section 3.2: each query's DNN processes its frames;
+ * with merging, Section 4, a shared layer is computed from its one stored
+ * copy, here once over the concatenated frames of all models that share it,
+ * and outputs are those of each model evaluated alone; with a weight budget,
+ * only layers that are not resident are loaded, Section 5.4 and Appendix
+ * A.4).
  *  model_ids   distinct model ids; their order does not change any output.
  *  frames      per model: device pointer to float32 NCHW
  *              [n_frames[i]][in_c][in_h][in_w].
@@ -227,10 +237,22 @@ gemel_status gemel_enumerate_groups(gemel_ctx *ctx, const int32_t *model_ids,
  *              [n][cout] (gemel_output_shape gives the dims).
  *  hip_stream  hipStream_t to enqueue on (NULL = the null stream).
  * Stream-ordered: the call enqueues work and returns; all buffers must stay
- * valid until the stream passes this point. Argument errors are returned
- * synchronously without enqueuing anything; an asynchronous device fault
- * surfaces as EDEVICE on this or a later call.
- * Errors: EINVAL, ESHAPE, ENOMEM, EBUDGET, EDEVICE.
+ * valid until the stream passes this point. Rounds of one context are
+ * ordered among themselves: a round on another stream than the previous
+ * round first waits (on the device) for the previous round to finish.
+ * Argument errors are returned synchronously without enqueuing anything.
+ * A failure part way through enqueuing (EDEVICE) leaves the work already
+ * enqueued joined back to hip_stream, so a synchronisation of that stream
+ * covers it; an asynchronous device fault surfaces as EDEVICE on this or a
+ * later call.
+ * Stream capture: a round may be enqueued while hip_stream is being
+ * captured into a graph once an earlier round outside capture has placed
+ * the weights and built the plan for the same model set and frame counts;
+ * the captured round then runs on hip_stream alone (no worker streams,
+ * events, allocations or synchronisation), and the caller orders the
+ * graph's replays against other rounds. Otherwise, and for rounds that
+ * stream weights or are profiled, the call returns ESTATE while capturing.
+ * Errors: EINVAL, ESHAPE, ENOMEM, EBUDGET, EDEVICE, ESTATE.
  */
 gemel_status gemel_infer(gemel_ctx *ctx, const int32_t *model_ids,
                          int32_t n_models, const void *const *frames,
@@ -263,10 +285,16 @@ enum {
     GEMEL_Q_N_MODELS = 7,       /* registered models                      */
     GEMEL_Q_GRAPH_REPLAYS = 8,  /* rounds served by a replayed HIP graph  */
     GEMEL_Q_STREAMS = 9,        /* GEMEL_OPT_STREAMS now in force         */
-    GEMEL_Q_ROUND_MODE = 10     /* how the last round ran: 0 enqueued
+    GEMEL_Q_ROUND_MODE = 10,    /* how the last round ran: 0 enqueued
                                    directly, 1 per-stream chain graphs,
                                    2 one graph with data edges, 3 one graph
-                                   with data edges and stream order       */
+                                   with data edges and stream order, 4 on
+                                   the caller's stream alone (a round
+                                   enqueued while that stream was being
+                                   captured)                             */
+    GEMEL_Q_ROUND_TUNING = 11   /* rounds the last plan's round-mode tuner
+                                   (GEMEL_OPT_AUTOTUNE) still runs before
+                                   its choice is fixed; 0 = settled      */
 };
 
 /* Read a counter. Errors: EINVAL (unknown key, null val). */
@@ -385,7 +413,7 @@ enum {
                                     full-size tensor disappear. Results are
                                     bit-identical to the separate pool. 0:
                                     off                                    */
-    GEMEL_OPT_MIXED_SIZES = 16   /* 1 (default): members of a merged group
+    GEMEL_OPT_MIXED_SIZES = 16,  /* 1 (default): members of a merged group
                                     whose inputs differ in spatial size
                                     (one weight copy at several positions
                                     or input sizes) run as one launch whose
@@ -394,6 +422,41 @@ enum {
                                     input channels a multiple of 32,
                                     internal output, no fused pool). 0: one
                                     launch per size                        */
+    GEMEL_OPT_PAIRED_ACTS = 17,  /* bf16 contexts: 1 = a tensor written by
+                                    an unmerged conv (not an output, not a
+                                    residual, input wider than 8 channels)
+                                    and read only by unmerged convs, either
+                                    directly or through upsample / concat,
+                                    is stored as pairs of bf16 (hi =
+                                    bf16(y), lo = bf16(y - hi)), and each
+                                    conv reading it multiplies both halves
+                                    by its weights (stored twice along the
+                                    input channels), so those activations
+                                    keep about 16 significant bits instead
+                                    of 8 (deep per-model chains, e.g.
+                                    detection heads, then drift less from
+                                    the float32 result). Costs twice the
+                                    bytes of those tensors and twice the
+                                    MFMA work of their consumers. 0
+                                    (default): bf16 activations            */
+    GEMEL_OPT_FAIL_ALLOC_AT = 18,/* test hook: the n-th (1-based) device or
+                                    pinned-host allocation the library makes
+                                    from now fails as if out of memory (the
+                                    call reports ENOMEM, or, for the scratch
+                                    of plan-time tuning, skips that tuning);
+                                    0 = off                                */
+    GEMEL_OPT_GROUP_UNMERGED = 19 /* 1: an unmerged bf16 conv that
+                                    appears with the same shape and epilogue
+                                    in several active models (their k-th such
+                                    layer each, e.g. per-model heads of one
+                                    architecture) runs as ONE grouped launch
+                                    whose segments keep their own weights and
+                                    scale/shift (output tiles never straddle
+                                    two segments), where the LDS-DMA kernel
+                                    can take it and the weights are resident.
+                                    Results are those of separate launches
+                                    of the same tile configuration. 0
+                                    (default): one launch per model        */
 };
 
 /* Set an option; takes effect at the next gemel_infer. Errors: EINVAL. */
@@ -409,7 +472,11 @@ enum {
     GEMEL_K_POOL = 5,        /* max and global average pooling              */
     GEMEL_K_ROUTE = 6,       /* upsample and concat                         */
     GEMEL_K_EXPORT = 7,      /* internal tensor -> NCHW f32 output          */
-    GEMEL_K_COUNT = 8
+    GEMEL_K_CONV_MERGED = 8, /* the GEMEL_K_CONV_MFMA launches that run a
+                                merged layer over the frames of several
+                                models (a subset: also counted in
+                                GEMEL_K_CONV_MFMA)                          */
+    GEMEL_K_COUNT = 9
 };
 
 /* Per-round statistics of one kernel family, averaged over the rounds run

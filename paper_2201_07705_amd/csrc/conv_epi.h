@@ -96,6 +96,24 @@ __device__ __forceinline__ u32x4 pack8_bf16(const float *y) {
     for (int q = 0; q < 4; ++q) o[q] = (uint32_t)f2bf(y[2 * q]) | ((uint32_t)f2bf(y[2 * q + 1]) << 16);
     return o;
 }
+// Stores 8 values y at out[off, off + 8) as bf16. With pair > 0 the
+// remainders y - bf16(y) (exact in fp32), rounded to bf16, are stored at
+// out[off + pair, off + pair + 8): the tensor then holds each value as a
+// pair of bf16 whose sum carries about 16 significant bits.
+__device__ __forceinline__ void store8_bf16(u16 *out, size_t off, const float *y, int pair) {
+    const u32x4 hi = pack8_bf16(y);
+    *(u32x4 *)(out + off) = hi;
+    if (pair) {
+        float lo[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const uint32_t w = hi[j >> 1];
+            lo[j] = y[j] - __uint_as_float((j & 1) ? (w & 0xffff0000u) : (w << 16));
+        }
+        *(u32x4 *)(out + off + pair) = pack8_bf16(lo);
+    }
+}
+
 // epi8_f32, rounded to bf16 and packed in channel order.
 __device__ __forceinline__ u32x4 epi8_bf16(const float *v, const float *sc, const float *sh, const u32x4 &r4,
                                            int kind, int has_res, int res_mode, int act, float slope) {
@@ -140,12 +158,13 @@ __device__ __forceinline__ RowSeg row_seg(const Args &a, int gm) {
 
 // Scalars of the fused epilogue.
 struct Epi {
-    int out_cs, cout, act, res_mode, has_res, HWo, kind;
+    int out_cs, cout, act, res_mode, has_res, HWo, kind, pair;
     float slope;
 };
 template <typename Args>
 __device__ __forceinline__ Epi epi_of(const Args &a, int HWo) {
     Epi e;
+    e.pair = a.out_pair;
     e.out_cs = a.out_cs; e.cout = a.cout; e.act = a.act; e.res_mode = a.res_mode;
     e.has_res = a.has_res; e.HWo = HWo; e.slope = a.slope;
     e.kind = epi_kind(a.act, a.has_res, a.res_mode, a.slope);
@@ -164,7 +183,9 @@ __device__ __forceinline__ void store8_nhwc_bf16(const RowSeg &sg, const Epi &e,
     const float sh[8] = {sh0.x, sh0.y, sh0.z, sh0.w, sh1.x, sh1.y, sh1.z, sh1.w};
     u32x4 r4 = {0u, 0u, 0u, 0u};
     if (e.has_res) r4 = *(const u32x4 *)((const u16 *)sg.res + off);
-    *(u32x4 *)((u16 *)sg.out + off) = epi8_bf16(v, sc, sh, r4, e.kind, e.has_res, e.res_mode, e.act, e.slope);
+    float y[8];
+    epi8_f32(v, sc, sh, r4, e.kind, e.has_res, e.res_mode, e.act, e.slope, y);
+    store8_bf16((u16 *)sg.out, off, y, e.pair);
 }
 
 // Epilogue of 8 consecutive channels of row gm into NHWC fp32.

@@ -49,6 +49,14 @@ struct Layer {
     int group = -1;              // index of the merge group containing it
     int out_index = -1;          // position among the model's outputs
     int consumers = 0;           // layers that read this layer's output
+    // storage of the tensors (assign_layouts, with the weight placement):
+    // physical channels per pixel of the src0 / src1 / output tensors, and
+    // whether the output holds bf16 (hi, lo) pairs: hi in channels
+    // [0, out_cp), lo in [out_cp, 2 * out_cp)
+    int in_phys = 0, src1_phys = 0, out_phys = 0;
+    bool out_paired = false;
+    std::shared_ptr<Blob> exec;  // parameters as the kernels read them: eff,
+                                 // or eff gathered to a paired input's channels
 };
 
 struct Model {
@@ -77,6 +85,7 @@ struct Launch {
     bool bf16 = true;
     // kernel family (GEMEL_K_*) and algorithmic work of this launch
     int kind = 0;
+    bool merged = false;  // runs a merged layer over several models' frames
     double flops = 0, bytes = 0;
     ConvArgs conv{};
     ReduceArgs red{};
@@ -158,6 +167,7 @@ struct Profile {
     struct Rec {
         hipEvent_t a, b;
         int kind;
+        int subset;   // GEMEL_K_CONV_MERGED for merged convs, else -1
     };
     std::vector<hipEvent_t> pool;    // free events
     std::vector<Rec> pending;        // recorded, not yet read
@@ -184,7 +194,10 @@ struct Options {
     int64_t slot_bytes = 32ll << 20;
     int slots = 3;
     int64_t fail_copy_at = 0;
+    int64_t fail_alloc_at = 0;
     int split_merged = 0;
+    int paired_acts = 0;      // unmerged conv chains keep bf16 (hi, lo) pairs
+    int group_unmerged = 0;   // same-shape unmerged convs of several models: one launch
 };
 
 }  // namespace gemel
@@ -212,8 +225,16 @@ struct gemel_ctx {
     std::vector<std::shared_ptr<gemel::Blob>> placed;  // blobs of the pool
     size_t resident_bytes = 0, peak_bytes = 0;
     int64_t copies_issued = 0;
+    int64_t allocs_issued = 0;
     int64_t graph_replays = 0;
     int last_mode = 0;   // execution mode of the last round (GEMEL_Q_ROUND_MODE)
+    int tuning_left = 0; // rounds the last plan's round-mode tuner still runs
+    // ordering between rounds: ev_round_done is recorded on a round's stream
+    // after its last work; a round on another stream first waits for it
+    hipEvent_t ev_round_done = nullptr;
+    hipStream_t round_stream = nullptr;
+    bool round_seen = false;
+    hipEvent_t ev_side_join = nullptr;   // side stream -> caller after a failed round
     std::map<std::vector<int>, std::unique_ptr<gemel::Plan>> plans;
     gemel::Plan *last_plan = nullptr;
     gemel::Profile prof;

@@ -318,7 +318,9 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_bf16_kernel(const ConvArgs a
                         else
                             r4 = *(const u32x4 *)(resp + off);
                     }
-                    *(u32x4 *)(outp + off) = epi8_bf16(v, sc, sh, r4, e.kind, e.has_res, e.res_mode, e.act, e.slope);
+                    float y[8];
+                    epi8_f32(v, sc, sh, r4, e.kind, e.has_res, e.res_mode, e.act, e.slope, y);
+                    store8_bf16(outp, off, y, e.pair);
                 } else if (one_seg) {
                     store8_nhwc_bf16(useg, e, gm, gn, v);
                 } else {
@@ -417,6 +419,7 @@ int conv_tile_threads(int tile) { return tile >= 0 && tile < TILE_COUNT ? kTiles
 
 static bool conv_args_ok(const ConvArgs &a) {
     if (a.M <= 0 || a.N <= 0 || a.K <= 0 || a.nseg < 1 || a.nseg > GEMEL_MAX_SEG) return false;
+    if (a.grouped) return false;   // the LDS-DMA kernel's form
     if (a.N % 8 || a.K % 8 || a.Cin % 8 || a.in_cs < a.Cin || a.in_cs % 8) return false;
     if (a.K != a.kh * a.kw * a.Cin || a.out_cs < a.N || a.out_cs % 8) return false;
     if (a.Ho <= 0 || a.Wo <= 0 || a.H <= 0 || a.W <= 0) return false;
@@ -432,6 +435,9 @@ static bool conv_args_ok(const ConvArgs &a) {
     if (a.k_splits > 1 && (long)a.k_splits * a.M * a.N * 4 > 0x7fffffffL) return false;
     if (a.k_per_split <= 0 || (long)a.k_per_split * a.k_splits < a.K) return false;
     if (a.out_mode == OUT_NCHW_F32 && a.cout > a.N) return false;
+    // bf16 pairs: internal NHWC output, both halves inside the pixel
+    if (a.out_pair && (a.out_mode != OUT_NHWC || a.out_pair < a.N || a.out_pair % 8 || a.out_cs < a.out_pair + a.N))
+        return false;
     // the fused 2x2 pool and segments of mixed sizes exist only in the
     // LDS-DMA kernel
     if ((a.out_mode != OUT_NHWC && a.out_mode != OUT_NCHW_F32) || a.hetero) return false;
@@ -470,7 +476,7 @@ hipError_t launch_conv_bf16(const ConvArgs &a, int tile, const Sink &sk) {
 }
 
 hipError_t launch_conv_f32(const ConvArgs &a, const Sink &sk) {
-    if (!conv_args_ok(a) || a.k_splits != 1) return hipErrorInvalidValue;
+    if (!conv_args_ok(a) || a.k_splits != 1 || a.out_pair) return hipErrorInvalidValue;
     const long n = (long)a.M * a.N;
     dim3 grid((unsigned)((n + 255) / 256)), block(256);
     return submit(sk, reinterpret_cast<const void *>(&conv_f32_kernel), grid, block, a);
@@ -480,6 +486,9 @@ hipError_t launch_conv_reduce(const ReduceArgs &a, bool bf16, const Sink &sk) {
     if (a.M <= 0 || a.N <= 0 || a.N % 8 || a.splits < 1 || !a.partial || a.nseg < 1 || a.nseg > GEMEL_MAX_SEG)
         return hipErrorInvalidValue;
     if (a.out_mode != OUT_NHWC && a.out_mode != OUT_NCHW_F32) return hipErrorInvalidValue;
+    if (a.out_pair && (!bf16 || a.out_mode != OUT_NHWC || a.out_pair < a.N || a.out_pair % 8 ||
+                       a.out_cs < a.out_pair + a.N))
+        return hipErrorInvalidValue;
     for (int i = 0; i < a.nseg; ++i)
         if (!a.seg[i].out || !a.seg[i].scale || !a.seg[i].shift || (a.has_res && !a.seg[i].res))
             return hipErrorInvalidValue;

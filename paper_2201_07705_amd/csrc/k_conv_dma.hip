@@ -104,11 +104,28 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / WN, wn = wave - (wave / WN) * WN;
     const int tiles_n = (a.N + BN - 1) / BN;
-    const int tiles = ((a.M + BM - 1) / BM) * tiles_n;
+    // grouped launches tile every segment on its own (a tile never
+    // straddles two segments' weights); seg[s].t_start is its first tile
+    const int tiles = a.grouped ? a.seg[a.nseg - 1].t_start +
+                                      ((a.M - a.seg[a.nseg - 1].m_start + BM - 1) / BM) * tiles_n
+                                : ((a.M + BM - 1) / BM) * tiles_n;
     const int G = gridDim.x;
     const int t = (G & 7) == 0 ? (int)(blockIdx.x & 7) * (G >> 3) + (int)(blockIdx.x >> 3) : (int)blockIdx.x;
     if (t >= tiles) return;
-    const int tm = t / tiles_n, tn = t - (t / tiles_n) * tiles_n;
+    // the tile's rows [m_lo, min(m_lo + BM, m_end)) and column tile tn
+    int m_lo, m_end = a.M, tn;
+    if (a.grouped) {
+        int sg = 0;
+        for (int i = 1; i < a.nseg; ++i) sg += t >= a.seg[i].t_start ? 1 : 0;
+        const int local = t - a.seg[sg].t_start, tml = local / tiles_n;
+        tn = local - tml * tiles_n;
+        m_lo = a.seg[sg].m_start + tml * BM;
+        if (sg + 1 < a.nseg) m_end = a.seg[sg + 1].m_start;
+    } else {
+        const int tm = t / tiles_n;
+        tn = t - tm * tiles_n;
+        m_lo = tm * BM;
+    }
     const int k_begin = blockIdx.y * a.k_per_split;
     const int k_end = min(a.K, k_begin + a.k_per_split);
     const int HWo = a.Ho * a.Wo;
@@ -118,7 +135,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
     // segment of the tile's first and last row (wave-uniform, scalar loads):
     // rows of a tile inside one segment take its fields as uniform values;
     // per-row lookups only for a tile that straddles segments
-    const int m_first = tm * BM, m_last = min(a.M, m_first + BM) - 1;
+    const int m_first = m_lo, m_last = min(m_end, m_first + BM) - 1;
     int s_first = 0, s_last = 0;
     for (int i = 1; i < a.nseg; ++i) {
         s_first += m_first >= a.seg[i].m_start ? 1 : 0;
@@ -145,7 +162,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
     for (int i = 0; i < AI; ++i) {
         const int rl = (i * NW + wave) * RPI + lane / CPR;
         acq[i] = (lane % CPR) ^ sw(rl);
-        const int gm = tm * BM + rl;
+        const int gm = m_lo + rl;
         abase[i] = zp;
         ahi[i] = -(1 << 28);
         awi[i] = 0;
@@ -153,7 +170,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
             aH[i] = 0;
             aW[i] = 0;
         }
-        if (hetero && gm < a.M) {
+        if (hetero && gm < m_end) {
             // the row's segment sizes: uniform in a tile inside one segment,
             // else gathered with scalar loads and selects like row_seg
             int sH = a.seg[s_first].H, sW = a.seg[s_first].W, sHo = a.seg[s_first].Ho, sWo = a.seg[s_first].Wo;
@@ -173,7 +190,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
             awi[i] = (pix - ho * sWo) * a.stride - a.pad;
             aH[i] = sH;
             aW[i] = sW;
-        } else if (gm < a.M) {
+        } else if (gm < m_end) {
             int fr, ho, wo;
             if constexpr (pool2) {
                 const int g = gm >> 2;
@@ -199,7 +216,8 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
     for (int i = 0; i < BI; ++i) {
         const int rl = (i * NW + wave) * RPI + lane / CPR;
         const int gn = tn * BN + rl;
-        bbase[i] = (const u16 *)a.w + (size_t)(gn < N ? gn : 0) * K + ((lane % CPR) ^ sw(rl)) * 8;
+        bbase[i] = (const u16 *)(a.grouped ? a.seg[s_first].w : a.w) + (size_t)(gn < N ? gn : 0) * K +
+                   ((lane % CPR) ^ sw(rl)) * 8;
     }
     // loader position (uniform): next step's tap (lr, ls) and channel base lc
     int kb = k_begin, lc, lr, ls;
@@ -293,7 +311,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
     const int my_gn = tn * BN + wn * TN + (lane % (TN / 8)) * 8;
     f32x4 sc0 = {1.f, 1.f, 1.f, 1.f}, sc1 = sc0, sh0 = {0.f, 0.f, 0.f, 0.f}, sh1 = sh0;
     if (a.k_splits <= 1 && my_gn < N) {
-        const float *scl = a.seg[0].scale + my_gn, *shl = a.seg[0].shift + my_gn;
+        const float *scl = useg.scale + my_gn, *shl = useg.shift + my_gn;
         sc0 = *(const f32x4 *)scl;
         sc1 = *(const f32x4 *)(scl + 4);
         sh0 = *(const f32x4 *)shl;
@@ -412,14 +430,14 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
     const float h8[8] = {sh0[0], sh0[1], sh0[2], sh0[3], sh1[0], sh1[1], sh1[2], sh1[3]};
 #pragma nounroll
     for (int grp = 0; grp < NGRP; ++grp) {
-        const int row0 = tm * BM + wm * TM + grp * PG * 16;
+        const int row0 = m_lo + wm * TM + grp * PG * 16;
         // residuals of the group's items, loaded ahead of the staging
         u32x4 rv[ITEMS];
 #pragma unroll
         for (int u = 0; u < ITEMS; ++u) {
             rv[u] = u32x4{0u, 0u, 0u, 0u};
             const int gm = row0 + (lane + u * 64) / CHW;
-            if (pre_res && col_ok && gm < a.M) {
+            if (pre_res && col_ok && gm < m_end) {
                 const RowSeg sg = one_seg ? useg : row_seg(a, gm);
                 rv[u] = *(const u32x4 *)((const u16 *)sg.res + (size_t)(gm - sg.m_start) * out_cs + gn);
             }
@@ -458,7 +476,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
                 const int idx = lane + u * 64;
                 const int pr = idx / CHW;
                 const int gm = row0 + 4 * pr;
-                if (idx >= NPI || !col_ok || gm >= a.M) continue;
+                if (idx >= NPI || !col_ok || gm >= m_end) continue;
                 float mx[8];
 #pragma unroll
                 for (int j = 0; j < 8; ++j) mx[j] = -INFINITY;
@@ -480,7 +498,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
         for (int u = 0; u < ITEMS; ++u) {
             const int rl = (lane + u * 64) / CHW;
             const int gm = row0 + rl;
-            if (!col_ok || gm >= a.M) continue;
+            if (!col_ok || gm >= m_end) continue;
             const float *src = ew + rl * EPI_LD + ch * 8;
             const float4 v0 = *(const float4 *)src, v1 = *(const float4 *)(src + 4);
             if (a.k_splits > 1) {
@@ -494,8 +512,9 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
             const int lr_ = gm - sg.m_start;
             if (a.out_mode == OUT_NHWC) {
                 const size_t off = (size_t)lr_ * out_cs + gn;
-                *(u32x4 *)((u16 *)sg.out + off) =
-                    epi8_bf16(v, s8, h8, rv[u], ekind, a.has_res, a.res_mode, a.act, a.slope);
+                float y[8];
+                epi8_f32(v, s8, h8, rv[u], ekind, a.has_res, a.res_mode, a.act, a.slope, y);
+                store8_bf16((u16 *)sg.out + off, 0, y, a.out_pair);
             } else {
                 const int f = lr_ / HWo, pix = lr_ - (lr_ / HWo) * HWo;
                 const u16 *resp = (const u16 *)sg.res;
@@ -513,13 +532,14 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
-    if (a.k_splits > 1 && a.counters) splitk_fixup<64 * WM * WN>(a, t, tm * BM, BM, tn * BN, BN, (int *)st2);
+    if (a.k_splits > 1 && a.counters)
+        splitk_fixup<64 * WM * WN>(a, t, m_lo, min(BM, m_end - m_lo), tn * BN, BN, (int *)st2);
 }
 
 bool conv_dma_supported(const ConvArgs &a) {
     // a row outside the image reads the zero page at its channel offset
     return a.Cin % 32 == 0 && a.in_cs % 8 == 0 && a.K % 32 == 0 && a.k_per_split % 32 == 0 && a.zero &&
-           a.uni_affine && (long)a.in_cs * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES;
+           (a.uni_affine || a.grouped) && (long)a.in_cs * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES;
 }
 bool conv_dma_supported(const ConvArgs &a, int tile) {
     if (!conv_dma_supported(a)) return false;
@@ -538,12 +558,17 @@ hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) {
         return hipErrorInvalidValue;
     if (a.k_splits > 1 && (long)a.k_splits * a.M * a.N * 4 > 0x7fffffffL) return hipErrorInvalidValue;
     if ((long)a.k_per_split * a.k_splits < a.K) return hipErrorInvalidValue;
+    // bf16 pairs: internal NHWC output, both halves inside the pixel
+    if (a.out_pair && (a.out_mode != OUT_NHWC || a.out_pair < a.N || a.out_pair % 8 || a.out_cs < a.out_pair + a.N))
+        return hipErrorInvalidValue;
     // mixed sizes: NHWC output, no fused pool; each segment whole frames of
     // its own size, the rows of the segments back to back
     if (a.hetero && a.out_mode != OUT_NHWC) return hipErrorInvalidValue;
+    if (a.grouped && a.hetero) return hipErrorInvalidValue;
     for (int i = 0; i < a.nseg; ++i) {
         const ConvSeg &s = a.seg[i];
         if (!s.in || !s.scale || !s.shift) return hipErrorInvalidValue;
+        if (a.grouped && (!s.w || (i && s.m_start <= a.seg[i - 1].m_start))) return hipErrorInvalidValue;
         if ((a.k_splits <= 1 || a.counters) && !s.out) return hipErrorInvalidValue;
         if (a.has_res && !s.res) return hipErrorInvalidValue;
         if (!a.hetero) {
@@ -556,7 +581,18 @@ hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) {
     }
     const int bm = conv_tile_bm(tile), bn = conv_tile_bn(tile);
     if (!bm) return hipErrorInvalidValue;
-    const long tiles = (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn);
+    // grouped: each segment tiled on its own, from tile seg[s].t_start
+    ConvArgs b = a;
+    long tiles = 0;
+    if (a.grouped) {
+        for (int i = 0; i < a.nseg; ++i) {
+            const long rows = (i + 1 < a.nseg ? a.seg[i + 1].m_start : a.M) - (long)a.seg[i].m_start;
+            b.seg[i].t_start = (int32_t)tiles;
+            tiles += (rows + bm - 1) / bm * ((a.N + bn - 1) / bn);
+        }
+    } else {
+        tiles = (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn);
+    }
     const long blocks = tiles >= 8 ? (tiles + 7) / 8 * 8 : tiles;
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
     dim3 grid((unsigned)blocks, (unsigned)a.k_splits);
@@ -568,7 +604,7 @@ hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) {
                    mode == 1   ? reinterpret_cast<const void *>(&conv_dma_kernel<BM_, BN_, WM_, WN_, ST_, BK_, 1>) \
                    : mode == 2 ? reinterpret_cast<const void *>(&conv_dma_kernel<BM_, BN_, WM_, WN_, ST_, BK_, 2>) \
                                : reinterpret_cast<const void *>(&conv_dma_kernel<BM_, BN_, WM_, WN_, ST_, BK_, 0>), \
-                   grid, dim3(NT_), a);                                                                       \
+                   grid, dim3(NT_), b);                                                                       \
         break;
     switch (tile) {
         GEMEL_DMA_CASE(TILE_DMA_256x256, 256, 256, 2, 4, 4, 32, 512)

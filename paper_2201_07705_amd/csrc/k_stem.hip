@@ -372,7 +372,7 @@ __global__ __launch_bounds__(256) void conv_stem_kernel(const ConvArgs a) {
 
 bool conv_stem_supported(const ConvArgs &a) {
     return a.Cin == 8 && a.in_cs == 8 && a.k_splits <= 1 && a.kh * a.kw <= STEM_MAX_TAPS && a.zero && a.uni_affine &&
-           !a.hetero && (a.out_mode == OUT_NHWC || a.out_mode == OUT_NCHW_F32);
+           !a.hetero && !a.grouped && !a.out_pair && (a.out_mode == OUT_NHWC || a.out_mode == OUT_NCHW_F32);
 }
 
 hipError_t launch_conv_stem(const ConvArgs &a, const Sink &sk) {

@@ -30,6 +30,9 @@ struct ConvSeg {
     int32_t m_start;      // first GEMM row (rows of the earlier segments)
     int32_t f_start;      // first frame of the segment in the launch
     int32_t H, W, Ho, Wo; // the segment's input and output sizes (ConvArgs::hetero)
+    const void *w;        // ConvArgs::grouped: this segment's weights [N][K]
+    int32_t t_start;      // ConvArgs::grouped: first output tile of the
+                          // segment (set by the launcher for its tile shape)
 };
 
 struct ConvArgs {
@@ -47,6 +50,9 @@ struct ConvArgs {
     int32_t res_mode;     // 0: act(z + r), 1: act(z) + r
     int32_t has_res;
     int32_t out_mode;     // OUT_NHWC or OUT_NCHW_F32
+    int32_t out_pair;     // 0, or (OUT_NHWC) the channel offset at which
+                          // the low halves of bf16 (hi, lo) pairs are
+                          // stored: hi = bf16(y), lo = bf16(y - hi)
     int32_t nseg;
     int32_t uni_affine;   // every segment uses the same scale/shift arrays
     int32_t hetero;       // 1: segments of different spatial sizes (one weight
@@ -54,6 +60,10 @@ struct ConvArgs {
                           // each row's sizes are its segment's H, W, Ho, Wo,
                           // the launch-wide ones are unused (LDS-DMA kernel,
                           // NHWC output, no fused pool)
+    int32_t grouped;      // 1: the segments are separate GEMMs of one shape
+                          // (the same layer of several models, each with its
+                          // own weights seg[s].w and scale/shift): output
+                          // tiles never straddle segments (LDS-DMA kernel)
     int32_t k_splits;     // >1: write fp32 partials to `partial`
     int32_t k_per_split;  // depth handled by one split (multiple of BK)
     float *partial;       // [k_splits][M][N] when k_splits > 1
@@ -73,6 +83,7 @@ struct ReduceArgs {
     int32_t act;
     float slope;
     int32_t res_mode, has_res, out_mode, nseg;
+    int32_t out_pair;     // as ConvArgs::out_pair
     ConvSeg seg[GEMEL_MAX_SEG];
 };
 

@@ -42,6 +42,27 @@ namespace gemel {
             return fail(ctx, GEMEL_EDEVICE, std::string(what) + ": " + hipGetErrorString(e_)); \
     } while (0)
 
+// Device and pinned-host allocations of the library, counted so that a
+// test can make the n-th one fail (GEMEL_OPT_FAIL_ALLOC_AT).
+static hipError_t alloc_device(gemel_ctx *ctx, void **p, size_t bytes) {
+    ctx->allocs_issued++;
+    if (ctx->opt.fail_alloc_at && ctx->allocs_issued == ctx->opt.fail_alloc_at) {
+        ctx->opt.fail_alloc_at = 0;
+        *p = nullptr;
+        return hipErrorOutOfMemory;
+    }
+    return hipMalloc(p, bytes);
+}
+static hipError_t alloc_pinned(gemel_ctx *ctx, void **p, size_t bytes) {
+    ctx->allocs_issued++;
+    if (ctx->opt.fail_alloc_at && ctx->allocs_issued == ctx->opt.fail_alloc_at) {
+        ctx->opt.fail_alloc_at = 0;
+        *p = nullptr;
+        return hipErrorOutOfMemory;
+    }
+    return hipHostMalloc(p, bytes, hipHostMallocDefault);
+}
+
 namespace {
 
 struct DeviceScope {
@@ -71,6 +92,10 @@ gemel_status ensure_device(gemel_ctx *ctx) {
         HIPCHK(hipStreamCreateWithFlags(&w, hipStreamNonBlocking), "hipStreamCreate");
         ctx->workers.push_back(w);
     }
+    HIPCHK(hipEventCreateWithFlags(&ctx->ev_round_done, hipEventDisableTiming), "hipEventCreate");
+    HIPCHK(hipEventCreateWithFlags(&ctx->ev_side_join, hipEventDisableTiming), "hipEventCreate");
+    ctx->round_seen = false;
+    ctx->round_stream = nullptr;
     ctx->dev_ready = true;
     return GEMEL_OK;
 }
@@ -138,9 +163,107 @@ void release_device(gemel_ctx *ctx) {
     ctx->tune_partial_bytes = ctx->tune_ctr_bytes = 0;
     if (ctx->side) (void)hipStreamDestroy(ctx->side);
     ctx->side = nullptr;
+    for (hipEvent_t *ev : {&ctx->ev_round_done, &ctx->ev_side_join}) {
+        if (*ev) (void)hipEventDestroy(*ev);
+        *ev = nullptr;
+    }
+    ctx->round_seen = false;
+    ctx->round_stream = nullptr;
     for (auto w : ctx->workers) (void)hipStreamDestroy(w);
     ctx->workers.clear();
     ctx->dev_ready = false;
+}
+
+// Tensor storage of every model under the current options and sharing
+// map: which conv outputs are kept as bf16 (hi, lo) pairs, the physical
+// channels per pixel of every tensor, and the parameters each conv reads
+// (its effective parameters, or a copy whose input-channel columns follow
+// the physical layout of a paired input).
+//
+// With GEMEL_OPT_PAIRED_ACTS, the output of an unmerged conv (not an output,
+// not a residual, not reading an 8-channel input) is paired when every
+// consumer can read pairs: an unmerged conv through its main input, or an
+// upsample / concat (not an output) whose own consumers all can. A conv
+// that reads a paired tensor multiplies both halves by the same weights
+// (its weight columns duplicated), so it sums hi * w + lo * w in fp32.
+static void assign_layouts(gemel_ctx *ctx) {
+    const bool on = ctx->opt.paired_acts && ctx->dtype == GEMEL_BF16;
+    for (auto &mp : ctx->models) {
+        Model &m = *mp;
+        const int n = (int)m.layers.size();
+        // consumers of each layer: (consumer, 0 = src0, 1 = src1, 2 = residual)
+        std::vector<std::vector<std::pair<int, int>>> cons((size_t)n);
+        for (int c = 0; c < n; ++c) {
+            const Layer &C = m.layers[(size_t)c];
+            if (C.src0 >= 0) cons[(size_t)C.src0].push_back({c, 0});
+            if (C.op == GEMEL_OP_CONCAT && C.src1 >= 0) cons[(size_t)C.src1].push_back({c, 1});
+            if (C.res >= 0) cons[(size_t)C.res].push_back({c, 2});
+        }
+        std::function<bool(int, int)> reads_pairs = [&](int c, int role) -> bool {
+            const Layer &C = m.layers[(size_t)c];
+            if (role == 2) return false;
+            if (C.op == GEMEL_OP_CONV) return role == 0 && C.group < 0;
+            if (C.op != GEMEL_OP_UPSAMPLE2X && C.op != GEMEL_OP_CONCAT) return false;
+            if (C.is_output || cons[(size_t)c].empty()) return false;
+            for (auto [d, r] : cons[(size_t)c])
+                if (!reads_pairs(d, r)) return false;
+            return true;
+        };
+        // logical channel held by each physical channel of a tensor (-1: padding)
+        auto plain = [](int c, int cp) {
+            std::vector<int> v((size_t)cp, -1);
+            for (int i = 0; i < c; ++i) v[(size_t)i] = i;
+            return v;
+        };
+        const std::vector<int> in_map = plain(m.in_c, m.in_cp);
+        std::vector<std::vector<int>> cmap((size_t)n);
+        for (int l = 0; l < n; ++l) {
+            Layer &L = m.layers[(size_t)l];
+            const std::vector<int> &m0 = L.src0 < 0 ? in_map : cmap[(size_t)L.src0];
+            L.in_phys = (int)m0.size();
+            L.src1_phys = 0;
+            L.out_paired = on && L.op == GEMEL_OP_CONV && L.group < 0 && !L.is_output && L.res < 0 &&
+                           L.in_phys != 8 && !cons[(size_t)l].empty();
+            for (auto [c, r] : cons[(size_t)l]) L.out_paired = L.out_paired && reads_pairs(c, r);
+            std::vector<int> &out = cmap[(size_t)l];
+            if (L.op == GEMEL_OP_UPSAMPLE2X) {
+                out = m0;
+            } else if (L.op == GEMEL_OP_CONCAT) {
+                const std::vector<int> &m1 = L.src1 < 0 ? in_map : cmap[(size_t)L.src1];
+                L.src1_phys = (int)m1.size();
+                out = m0;
+                for (int x : m1) out.push_back(x < 0 ? -1 : x + L.in_c);
+            } else {
+                out = plain(L.out_c, L.out_cp);
+                if (L.out_paired) {
+                    const std::vector<int> hi = out;
+                    out.insert(out.end(), hi.begin(), hi.end());
+                }
+            }
+            L.out_phys = (int)out.size();
+            L.exec = L.eff;
+            if (L.op == GEMEL_OP_CONV && L.eff && L.in_phys != L.in_cp) {
+                // weight columns gathered to the input's physical channels
+                const Blob &B = *L.eff;
+                auto nb = std::make_shared<Blob>();
+                nb->rows = B.rows;
+                nb->elem = B.elem;
+                nb->k = (int64_t)L.kh * L.kw * L.in_phys;
+                nb->scale = B.scale;
+                nb->shift = B.shift;
+                nb->w.assign((size_t)(nb->rows * nb->k) * nb->elem, 0);
+                for (int64_t o = 0; o < B.rows; ++o)
+                    for (int64_t t = 0; t < (int64_t)L.kh * L.kw; ++t)
+                        for (int j = 0; j < L.in_phys; ++j) {
+                            const int c = m0[(size_t)j];
+                            if (c < 0) continue;
+                            std::memcpy(&nb->w[(size_t)((o * nb->k + t * L.in_phys + j) * (int64_t)nb->elem)],
+                                        &B.w[(size_t)((o * B.k + t * L.in_cp + c) * (int64_t)B.elem)], B.elem);
+                        }
+                L.exec = nb;
+            }
+        }
+    }
 }
 
 gemel_status materialise(gemel_ctx *ctx) {
@@ -149,18 +272,19 @@ gemel_status materialise(gemel_ctx *ctx) {
     if (st) return st;
     drop_plans(ctx);
     free_placement(ctx);
+    assign_layouts(ctx);
 
     // distinct copies in use, in registration order, with their user counts
     std::vector<std::shared_ptr<Blob>> blobs;
     std::set<Blob *> seen;
     for (auto &m : ctx->models)
         for (auto &l : m->layers)
-            if (l.eff) {
-                if (seen.insert(l.eff.get()).second) {
-                    l.eff->users = 0;
-                    blobs.push_back(l.eff);
+            if (l.exec) {
+                if (seen.insert(l.exec.get()).second) {
+                    l.exec->users = 0;
+                    blobs.push_back(l.exec);
                 }
-                l.eff->users++;
+                l.exec->users++;
             }
     size_t w_total = 0, aff_total = 0, max_final = 0;
     for (auto &b : blobs) {
@@ -169,7 +293,7 @@ gemel_status materialise(gemel_ctx *ctx) {
     }
     for (auto &m : ctx->models)
         for (auto &l : m->layers)
-            if (l.eff && l.is_output && l.consumers == 0) max_final = std::max(max_final, l.eff->w_bytes());
+            if (l.exec && l.is_output && l.consumers == 0) max_final = std::max(max_final, l.exec->w_bytes());
 
     std::vector<char> resident(blobs.size(), 1);
     size_t staging_bytes = 0;
@@ -205,7 +329,7 @@ gemel_status materialise(gemel_ctx *ctx) {
     size_t pool = aff_total + GEMEL_ZERO_PAGE_BYTES;  // + zero page
     for (size_t i = 0; i < blobs.size(); ++i)
         if (resident[i]) pool += (size_t)round_up((int64_t)blobs[i]->w_bytes(), 256);
-    if (hipMalloc(&ctx->wpool, pool) != hipSuccess) {
+    if (alloc_device(ctx, &ctx->wpool, pool) != hipSuccess) {
         ctx->wpool = nullptr;
         (void)hipGetLastError();
         return fail(ctx, GEMEL_ENOMEM, "device allocation of the weight pool failed");
@@ -233,7 +357,7 @@ gemel_status materialise(gemel_ctx *ctx) {
             e = hipMemcpy(b.w_dev, b.w.data(), b.w_bytes(), hipMemcpyHostToDevice);
             off += (size_t)round_up((int64_t)b.w_bytes(), 256);
         } else if (e == hipSuccess) {
-            e = hipHostMalloc((void **)&b.w_pinned, b.w_bytes(), hipHostMallocDefault);
+            e = alloc_pinned(ctx, (void **)&b.w_pinned, b.w_bytes());
             if (e == hipSuccess) std::memcpy(b.w_pinned, b.w.data(), b.w_bytes());
             else b.w_pinned = nullptr;
         }
@@ -243,7 +367,7 @@ gemel_status materialise(gemel_ctx *ctx) {
         }
     }
     if (slots) {
-        if (hipMalloc(&ctx->staging, staging_bytes) != hipSuccess) {
+        if (alloc_device(ctx, &ctx->staging, staging_bytes) != hipSuccess) {
             ctx->staging = nullptr;
             free_placement(ctx);
             return fail(ctx, GEMEL_ENOMEM, "device allocation of the staging slots failed");
@@ -408,6 +532,7 @@ ReduceArgs reduce_args(const ConvArgs &a) {
     r.M = a.M; r.N = a.N; r.splits = a.k_splits; r.HWo = a.Ho * a.Wo;
     r.out_cs = a.out_cs; r.cout = a.cout; r.act = a.act; r.slope = a.slope;
     r.res_mode = a.res_mode; r.has_res = a.has_res; r.out_mode = a.out_mode;
+    r.out_pair = a.out_pair;
     r.nseg = a.nseg;
     for (int i = 0; i < a.nseg; ++i) r.seg[i] = a.seg[i];
     return r;
@@ -422,7 +547,7 @@ ReduceArgs reduce_args(const ConvArgs &a) {
 bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int &tile, int &splits, int &kps) {
     std::vector<int64_t> key = {a0.M, a0.N, a0.K, a0.H, a0.W, a0.Cin, a0.in_cs, a0.kh, a0.kw, a0.stride, a0.pad,
                                 a0.out_cs, a0.has_res, a0.out_mode, a0.nseg > 1, dma_depth, ctx->opt.splitk_fused,
-                                a0.hetero};
+                                a0.hetero, a0.grouped, a0.out_pair};
     auto hit = ctx->tune_cache.find(key);
     if (hit != ctx->tune_cache.end()) {
         tile = hit->second.first;
@@ -431,7 +556,7 @@ bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int
         return true;
     }
     const bool pooled = a0.out_mode == OUT_NHWC_POOL2;
-    std::vector<ConvCand> c = conv_candidates(a0.M, a0.N, a0.K, dma_depth, -1, pooled || a0.hetero, pooled);
+    std::vector<ConvCand> c = conv_candidates(a0.M, a0.N, a0.K, dma_depth, -1, pooled || a0.hetero || a0.grouped, pooled);
     if (c.empty()) return false;
     const double cut = 2.0 * c[0].est;
     size_t n = 0;
@@ -454,7 +579,7 @@ bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int
         if (ctx->tune_partial) (void)hipFree(ctx->tune_partial);
         ctx->tune_partial = nullptr;
         ctx->tune_partial_bytes = 0;
-        if (hipMalloc(&ctx->tune_partial, pbytes) != hipSuccess) {
+        if (alloc_device(ctx, &ctx->tune_partial, pbytes) != hipSuccess) {
             (void)hipGetLastError();
             return false;
         }
@@ -464,7 +589,7 @@ bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int
         if (ctx->tune_ctr) (void)hipFree(ctx->tune_ctr);
         ctx->tune_ctr = nullptr;
         ctx->tune_ctr_bytes = 0;
-        if (hipMalloc(&ctx->tune_ctr, cbytes) != hipSuccess) {
+        if (alloc_device(ctx, &ctx->tune_ctr, cbytes) != hipSuccess) {
             (void)hipGetLastError();
             return false;
         }
@@ -581,8 +706,8 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
             const int l = Pl.src0;
             const Layer &L = m.layers[(size_t)l];
             // the LDS-DMA kernel's requirements (as for its tiles below)
-            const bool dma = L.in_cp % 32 == 0 && (int64_t)L.in_cp * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES &&
-                             (forced < 0 || tile_dma_depth(forced) == 32 || L.in_cp % 64 == 0);
+            const bool dma = L.in_phys % 32 == 0 && (int64_t)L.in_phys * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES &&
+                             (forced < 0 || tile_dma_depth(forced) == 32 || L.in_phys % 64 == 0);
             if (L.op != GEMEL_OP_CONV || L.res >= 0 || L.is_output || L.consumers != 1 || !dma || L.out_h % 2 ||
                 L.out_w % 2 || L.out_h < 2 || L.out_w < 2)
                 continue;
@@ -598,6 +723,15 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
     std::vector<Node> nodes;
     std::map<std::vector<int64_t>, int> group_node;
     std::map<std::pair<int, int>, int> occurrence;   // (model slot, group) -> appearances so far
+    std::map<std::pair<int, std::vector<int64_t>>, int> ungrouped_seen;  // (slot, signature) -> appearances
+    // an unmerged bf16 conv that a grouped launch can take: the LDS-DMA
+    // kernel's input conditions, resident weights, no mixed sizes
+    auto groupable = [&](int s, int l) {
+        const Layer &L = layer(s, l);
+        return ctx->opt.group_unmerged && bf16 && L.op == GEMEL_OP_CONV && L.group < 0 && L.exec && L.exec->w_dev &&
+               L.in_phys % 32 == 0 && (int64_t)L.in_phys * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES &&
+               (forced < 0 || (tile_is_dma(forced) && (tile_dma_depth(forced) == 32 || L.in_phys % 64 == 0)));
+    };
     std::vector<std::vector<int>> node_of((size_t)S);
     for (int s = 0; s < S; ++s) {
         const Model &m = model(s);
@@ -614,12 +748,13 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 // LDS-DMA kernel can take them (one weight copy, per-segment
                 // sizes): bf16 conv, internal NHWC output, no fused pool
                 const bool mixed = ctx->opt.mixed_sizes && bf16 && L.op == GEMEL_OP_CONV && !direct_output(L) &&
-                                   pool_of[(size_t)s][(size_t)l] < 0 && L.in_cp % 32 == 0 &&
-                                   (int64_t)L.in_cp * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES &&
-                                   (forced < 0 || (tile_is_dma(forced) && (tile_dma_depth(forced) == 32 || L.in_cp % 64 == 0)));
+                                   pool_of[(size_t)s][(size_t)l] < 0 && L.in_phys % 32 == 0 &&
+                                   (int64_t)L.in_phys * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES &&
+                                   (forced < 0 || (tile_is_dma(forced) && (tile_dma_depth(forced) == 32 || L.in_phys % 64 == 0)));
                 std::vector<int64_t> key = {L.group, mixed ? -1 : L.in_h, mixed ? -1 : L.in_w, L.in_c, L.act,
                                             (int64_t)(L.slope * 1e6f), L.res >= 0, L.res_mode,
-                                            direct_output(L), L.src1_cp, pool_of[(size_t)s][(size_t)l] >= 0,
+                                            direct_output(L), L.src1_phys, L.in_phys, L.out_paired,
+                                            pool_of[(size_t)s][(size_t)l] >= 0,
                                             occurrence[{s, L.group}]++};
                 auto it = group_node.find(key);
                 if (it != group_node.end() && nodes[(size_t)it->second].mem.size() < GEMEL_MAX_SEG) {
@@ -628,6 +763,23 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     nid = (int)nodes.size();
                     nodes.push_back(Node{L.op, {}});
                     group_node[key] = nid;
+                }
+            } else if (groupable(s, l)) {
+                // the same unmerged conv of several models (same shape and
+                // epilogue, its k-th appearance in each): one grouped launch,
+                // each segment with its own weights
+                const int pooled = pool_of[(size_t)s][(size_t)l] >= 0;
+                std::vector<int64_t> sig = {-1, L.in_h, L.in_w, L.in_c, L.in_phys, L.out_c, L.out_phys, L.kh,
+                                            L.stride, L.pad, L.act, (int64_t)(L.slope * 1e6f), L.res >= 0,
+                                            L.res_mode, direct_output(L), L.out_paired, pooled};
+                sig.push_back(ungrouped_seen[{s, sig}]++);
+                auto it = group_node.find(sig);
+                if (it != group_node.end() && nodes[(size_t)it->second].mem.size() < GEMEL_MAX_SEG) {
+                    nid = it->second;
+                } else {
+                    nid = (int)nodes.size();
+                    nodes.push_back(Node{L.op, {}});
+                    group_node[sig] = nid;
                 }
             } else {
                 nid = (int)nodes.size();
@@ -716,7 +868,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
         {   // the node's weights are read once, whatever its member count
             const auto [s0, l0] = nodes[(size_t)order[(size_t)i]].mem[0];
             const Layer &L0 = layer(s0, l0);
-            if (L0.eff) est[(size_t)i] += (double)L0.eff->rows * L0.eff->k * L0.eff->elem / 4e12;
+            if (L0.exec) est[(size_t)i] += (double)L0.exec->rows * L0.exec->k * L0.exec->elem / 4e12;
         }
         for (auto [s, l] : nodes[(size_t)order[(size_t)i]].mem) {
             const Layer &L = layer(s, l);
@@ -727,7 +879,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
             const double kd = L.op == GEMEL_OP_CONV ? (double)L.kh * L.kw * L.cin : (double)L.cin;
             if (L.op == GEMEL_OP_CONV || L.op == GEMEL_OP_FC)
                 est[(size_t)i] += 2.0 * n * L.out_h * L.out_w * L.out_c * kd / 1e15;
-            est[(size_t)i] += n * L.out_h * L.out_w * L.out_cp * esz / 4e12;
+            est[(size_t)i] += n * L.out_h * L.out_w * L.out_phys * esz / 4e12;
         }
         preds[(size_t)i].assign(ps.begin(), ps.end());
     }
@@ -838,11 +990,11 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
             if (p >= 0) {   // the conv writes its pool's (pooled) tensor only
                 const Layer &Pl = layer(s, p);
                 TInfo &t = T[{s, p}];
-                t.bytes = (size_t)nfr[(size_t)s] * Pl.out_h * Pl.out_w * Pl.out_cp * esz;
+                t.bytes = (size_t)nfr[(size_t)s] * Pl.out_h * Pl.out_w * Pl.out_phys * esz;
                 t.prod = i;
             } else if (!direct_output(L)) {
                 TInfo &t = T[{s, l}];
-                t.bytes = (size_t)nfr[(size_t)s] * L.out_h * L.out_w * L.out_cp * esz;
+                t.bytes = (size_t)nfr[(size_t)s] * L.out_h * L.out_w * L.out_phys * esz;
                 t.prod = i;
             }
         }
@@ -886,7 +1038,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
         placed.push_back(t);
     }
     P.arena_bytes = arena;
-    if (arena && hipMalloc(&P.arena, arena) != hipSuccess) {
+    if (arena && alloc_device(ctx, &P.arena, arena) != hipSuccess) {
         P.arena = nullptr;
         (void)hipGetLastError();
         return fail(ctx, GEMEL_ENOMEM, "device allocation of the activation arena failed");
@@ -968,7 +1120,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
         const auto [s0, l0] = nd.mem[0];
         const Layer &L0 = layer(s0, l0);
         if (L0.op == GEMEL_OP_CONV || L0.op == GEMEL_OP_FC) {
-            Blob *blob = L0.eff.get();
+            Blob *blob = L0.exec.get();
             const bool pooled = pool_of[(size_t)s0][(size_t)l0] >= 0;   // alike for every member
             int64_t M = 0;
             for (auto [s, l] : nd.mem) M += (int64_t)nfr[(size_t)s] * layer(s, l).out_h * layer(s, l).out_w;
@@ -991,12 +1143,18 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
             for (auto [s, l] : nd.mem)
                 in_elems += (double)nfr[(size_t)s] * layer(s, l).in_h * layer(s, l).in_w * layer(s, l).in_c;
             const double kdepth = L0.op == GEMEL_OP_CONV ? (double)L0.kh * L0.kw * L0.cin : (double)L0.cin;
+            int members = 0;
+            for (auto [s, l] : nd.mem) members += nfr[(size_t)s] > 0 ? 1 : 0;
+            // unmerged layers of several models in one node: a grouped
+            // launch, every member with its own weights
+            const bool grouped = nd.mem.size() > 1 && L0.group < 0;
             for (auto [row0, nrows] : rows) {
                 Launch Lc;
                 Lc.bf16 = bf16;
+                Lc.merged = members > 1 && !grouped;
                 const double co = (double)std::max<int64_t>(0, std::min<int64_t>(nrows, L0.out_c - row0));
                 Lc.flops = 2.0 * (double)M * co * kdepth;
-                Lc.bytes = co * kdepth * esz + in_elems * esz +
+                Lc.bytes = co * kdepth * esz * (grouped ? members : 1) + in_elems * esz +
                            (double)M * co * (direct ? 4.0 : esz) / (pooled ? 4.0 : 1.0) +
                            (L0.res >= 0 ? (double)M * co * esz : 0.0);
                 if (!blob->w_dev) {
@@ -1009,7 +1167,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     FcArgs &a = Lc.fc;
                     a.w = wptr;
                     a.M = (int)M; a.N = (int)nrows; a.K = (int)blob->k;
-                    a.out_cs = L0.out_cp; a.cout = L0.out_c;
+                    a.out_cs = L0.out_phys; a.cout = L0.out_c;
                     a.act = L0.act; a.slope = L0.slope;
                     a.out_mode = direct ? OUT_NCHW_F32 : OUT_NHWC;
                     a.nseg = 0;
@@ -1056,7 +1214,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 a.zero = ctx->zero_page;
                 a.M = (int)M; a.N = (int)nrows; a.K = (int)blob->k;
                 if (L0.op == GEMEL_OP_CONV) {
-                    a.H = L0.in_h; a.W = L0.in_w; a.Cin = L0.in_cp; a.in_cs = L0.in_cp;
+                    a.H = L0.in_h; a.W = L0.in_w; a.Cin = L0.in_phys; a.in_cs = L0.in_phys;
                     a.Ho = L0.out_h; a.Wo = L0.out_w;
                     a.kh = L0.kh; a.kw = L0.kw; a.stride = L0.stride; a.pad = L0.pad;
                 } else {  // FC over many frames: a 1x1 conv on a 1x1 map with Cin = K
@@ -1064,7 +1222,8 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     a.Ho = a.Wo = 1;
                     a.kh = a.kw = 1; a.stride = 1; a.pad = 0;
                 }
-                a.out_cs = L0.out_cp;
+                a.out_cs = L0.out_phys;
+                a.out_pair = L0.out_paired ? L0.out_cp : 0;
                 a.cout = direct ? std::min<int>((int)nrows, L0.out_c - (int)row0) : L0.out_c;
                 a.act = L0.act; a.slope = L0.slope;
                 a.res_mode = L0.res_mode; a.has_res = L0.res >= 0;
@@ -1081,8 +1240,10 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     sg.res = L.res >= 0 ? (const void *)((char *)tptr(s, L.res) + row0 * esz) : nullptr;
                     const int wl = pooled ? pool_of[(size_t)s][(size_t)l] : l;   // the tensor written
                     sg.out = direct ? nullptr : (void *)((char *)tptr(s, wl) + row0 * esz);
-                    sg.scale = blob->aff_dev + row0;
-                    sg.shift = blob->aff_dev + blob->rows + row0;
+                    const Blob *mb = L.exec.get();   // the member's own parameters (grouped)
+                    sg.w = grouped ? mb->w_dev : nullptr;
+                    sg.scale = mb->aff_dev + row0;
+                    sg.shift = mb->aff_dev + mb->rows + row0;
                     sg.f_start = f;
                     sg.m_start = (int32_t)m_acc;
                     sg.H = L.in_h; sg.W = L.in_w; sg.Ho = L.out_h; sg.Wo = L.out_w;
@@ -1094,13 +1255,14 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     a.nseg++;
                 }
                 if (!a.nseg) continue;
+                a.grouped = grouped ? 1 : 0;
                 a.uni_affine = 1;
                 for (int i = 1; i < a.nseg; ++i)
                     if (a.seg[i].scale != a.seg[0].scale || a.seg[i].shift != a.seg[0].shift) a.uni_affine = 0;
                 if (bf16) {
                     // DMA tiles: masked rows read the zero page at their
                     // channel offset, so the pixel stride must fit it
-                    const bool dma_ok = a.in_cs % 8 == 0 && a.uni_affine &&
+                    const bool dma_ok = a.in_cs % 8 == 0 && (a.uni_affine || a.grouped) &&
                                         (int64_t)a.in_cs * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES;
                     const int dma_depth = !dma_ok ? 0 : a.Cin % 64 == 0 ? 64 : a.Cin % 32 == 0 ? 32 : 0;
                     // 8-channel inputs (the RGB stems) take the stem kernel
@@ -1112,7 +1274,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                         a.k_per_split = a.K;
                     } else {
                         pick_conv_config(a.M, a.N, a.K, dma_depth, ctx->opt.conv_tile == TILE_STEM ? TILE_64x64 : ctx->opt.conv_tile,
-                                         ctx->opt.conv_splits, a.hetero != 0, pooled, Lc.tile, a.k_splits,
+                                         ctx->opt.conv_splits, a.hetero != 0 || a.grouped != 0, pooled, Lc.tile, a.k_splits,
                                          a.k_per_split);
                         // measured choice where nothing is forced and the
                         // launch's tensors all exist at plan time
@@ -1121,8 +1283,9 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                             tune_conv(ctx, a, dma_depth, bf16, Lc.tile, a.k_splits, a.k_per_split);
                     }
                     if (tile_is_dma(Lc.tile) && !conv_dma_supported(a, Lc.tile)) {
-                        if (pooled || a.hetero)
-                            return fail(ctx, GEMEL_ESTATE, "internal: fused pool or mixed sizes without an LDS-DMA tile");
+                        if (pooled || a.hetero || a.grouped)
+                            return fail(ctx, GEMEL_ESTATE,
+                                        "internal: fused pool, mixed sizes or grouped launch without an LDS-DMA tile");
                         Lc.tile = TILE_64x64;
                     }
                     Lc.type = L_CONV_BF16;
@@ -1157,10 +1320,10 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
         Launch Le;
         Le.bf16 = bf16;
         EwArgs &a = Le.ew;
-        a.H = L0.in_h; a.W = L0.in_w; a.C = L0.in_cp;
-        a.Ho = L0.out_h; a.Wo = L0.out_w; a.Co = L0.out_cp;
+        a.H = L0.in_h; a.W = L0.in_w; a.C = L0.in_phys;
+        a.Ho = L0.out_h; a.Wo = L0.out_w; a.Co = L0.out_phys;
         a.k = L0.kh; a.stride = L0.stride; a.pad = L0.pad;
-        a.C1 = L0.src1_cp;
+        a.C1 = L0.src1_phys;
         a.nseg = 0;
         for (auto [s, l] : nd.mem) {
             if (!nfr[(size_t)s]) continue;
@@ -1195,7 +1358,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
         Le.bytes = (double)nfr[(size_t)s] * L.out_h * L.out_w * L.out_c * (esz + 4.0);
         Le.bf16 = bf16;
         EwArgs &a = Le.ew;
-        a.H = L.out_h; a.W = L.out_w; a.C = L.out_cp; a.c_logical = L.out_c;
+        a.H = L.out_h; a.W = L.out_w; a.C = L.out_phys; a.c_logical = L.out_c;
         a.nseg = 1;
         a.seg[0].in0 = tptr(s, l);
         a.seg[0].in1 = nullptr;
@@ -1246,7 +1409,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
             done.push_back(i);
         }
         if (total) {
-            if (hipMalloc((void **)&P.partial, total) != hipSuccess) {
+            if (alloc_device(ctx, (void **)&P.partial, total) != hipSuccess) {
                 P.partial = nullptr;
                 (void)hipGetLastError();
                 return fail(ctx, GEMEL_ENOMEM, "device allocation of the split-K buffer failed");
@@ -1268,7 +1431,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
         size_t total = 0;
         for (auto &L : P.launches) total += (size_t)L.ctr_n;
         if (total) {
-            if (hipMalloc((void **)&P.counters, total * sizeof(int32_t)) != hipSuccess) {
+            if (alloc_device(ctx, (void **)&P.counters, total * sizeof(int32_t)) != hipSuccess) {
                 P.counters = nullptr;
                 (void)hipGetLastError();
                 return fail(ctx, GEMEL_ENOMEM, "device allocation of the split-K counters failed");
@@ -1363,7 +1526,45 @@ hipError_t launch_one(Launch &L, const CallPtrs &cp, const Plan &P, void *wptr, 
 
 }  // namespace
 
+// After a failure part way through a round: the work already enqueued on
+// the worker streams and the side (weight copy) stream is joined back to
+// the caller's stream, best effort, so that a synchronisation of that
+// stream covers the partial round and the next round's launches are
+// ordered after it.
+static void join_partial_round(gemel_ctx *ctx, Plan &P, hipStream_t st) {
+    for (int k = 1; k < P.n_streams; ++k) {
+        if (hipEventRecord(P.ev_join[(size_t)k], ctx->workers[(size_t)k - 1]) == hipSuccess)
+            (void)hipStreamWaitEvent(st, P.ev_join[(size_t)k], 0);
+    }
+    if (ctx->side && hipEventRecord(ctx->ev_side_join, ctx->side) == hipSuccess)
+        (void)hipStreamWaitEvent(st, ctx->ev_side_join, 0);
+    (void)hipGetLastError();
+}
+
+// Every launch of the plan in plan order on one stream, with no event and
+// no other stream (a round captured into the caller's graph). Plan order is
+// a topological order of the launches' dependencies, and the plan's arena
+// and split-K regions are shared only between launches ordered by those
+// dependencies, so one stream is always a valid schedule.
+static gemel_status enqueue_serial(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStream_t st) {
+    for (Launch &L : P.launches) {
+        Sink sk;
+        sk.stream = st;
+        const hipError_t e = launch_one(L, cp, P, nullptr, sk);
+        if (e != hipSuccess) return fail(ctx, GEMEL_EDEVICE, std::string("kernel launch: ") + hipGetErrorString(e));
+    }
+    return GEMEL_OK;
+}
+
+static gemel_status enqueue_body(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStream_t st);
+
 static gemel_status enqueue(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStream_t st) {
+    const gemel_status s = enqueue_body(ctx, P, cp, st);
+    if (s) join_partial_round(ctx, P, st);
+    return s;
+}
+
+static gemel_status enqueue_body(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStream_t st) {
     const int nslots = ctx->staging_slots;
     const int nch = (int)P.chunks.size();
     int next_copy = 0;
@@ -1406,7 +1607,8 @@ static gemel_status enqueue(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStre
             HIPCHK(hipStreamWaitEvent(ls, ctx->ev_copied[(size_t)(L.chunk % nslots)], 0), "hipStreamWaitEvent");
             wptr = slot_ptr(L.chunk);
         }
-        Profile::Rec rec{nullptr, nullptr, L.kind};
+        const int subset = L.kind == GEMEL_K_CONV_MFMA && L.merged ? GEMEL_K_CONV_MERGED : -1;
+        Profile::Rec rec{nullptr, nullptr, L.kind, subset};
         if (ctx->opt.profile) {
             for (hipEvent_t *ev : {&rec.a, &rec.b}) {
                 if (ctx->prof.pool.empty()) {
@@ -1426,9 +1628,12 @@ static gemel_status enqueue(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStre
         if (e != hipSuccess) return fail(ctx, GEMEL_EDEVICE, std::string("kernel launch: ") + hipGetErrorString(e));
         if (ctx->opt.profile) {
             HIPCHK(hipEventRecord(rec.b, ls), "hipEventRecord");
-            ctx->prof.flops[L.kind] += L.flops;
-            ctx->prof.bytes[L.kind] += L.bytes;
-            ctx->prof.launches[L.kind] += 1;
+            for (int k : {L.kind, subset}) {
+                if (k < 0) continue;
+                ctx->prof.flops[k] += L.flops;
+                ctx->prof.bytes[k] += L.bytes;
+                ctx->prof.launches[k] += 1;
+            }
         }
         if (L.chunk >= 0) HIPCHK(hipEventRecord(ctx->ev_free[(size_t)(L.chunk % nslots)], ls), "hipEventRecord");
         if (L.record >= 0) HIPCHK(hipEventRecord(P.events[(size_t)L.record], ls), "hipEventRecord");
@@ -1532,12 +1737,20 @@ static void build_segments(Plan &P) {
 }
 
 // Execution modes of a round.
-enum RoundMode { MODE_EAGER = 0, MODE_SEGMENTS = 1, MODE_DAG = 2, MODE_STREAMGRAPH = 3 };
+enum RoundMode { MODE_EAGER = 0, MODE_SEGMENTS = 1, MODE_DAG = 2, MODE_STREAMGRAPH = 3, MODE_SERIAL = 4 };
 
 // One graph round of the per-stream segments, launched in plan order, each
 // after its cross-stream waits, worker streams forked after the packs and
 // joined at the end.
+static gemel_status launch_segments_body(gemel_ctx *ctx, Plan &P, hipStream_t st);
+
 static gemel_status launch_segments(gemel_ctx *ctx, Plan &P, hipStream_t st) {
+    const gemel_status s = launch_segments_body(ctx, P, st);
+    if (s) join_partial_round(ctx, P, st);
+    return s;
+}
+
+static gemel_status launch_segments_body(gemel_ctx *ctx, Plan &P, hipStream_t st) {
     hipStream_t streams[8] = {st};
     for (int k = 1; k < P.n_streams; ++k) streams[k] = ctx->workers[(size_t)k - 1];
     bool forked = P.n_streams == 1;
@@ -1593,6 +1806,18 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         key.push_back(n_frames[ci]);
     }
     DeviceScope scope(ctx->device);
+    // A round captured into the caller's graph may only enqueue work: the
+    // weight placement and the plan (allocations, synchronous copies, tuning
+    // runs) must come from an earlier round outside capture, and it runs on
+    // the caller's stream alone.
+    bool capturing = false;
+    if (stream) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        HIPCHK(hipStreamIsCapturing(stream, &cs), "hipStreamIsCapturing");
+        capturing = cs != hipStreamCaptureStatusNone;
+    }
+    if (capturing && !ctx->weights_ready)
+        return fail(ctx, GEMEL_ESTATE, "weights are not placed yet: run one round outside stream capture first");
     gemel_status st = materialise(ctx);
     if (st) return st;
     // The null stream gets a single-stream plan (its implicit synchronisation
@@ -1602,13 +1827,13 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
     key.push_back(nstreams);
     auto it = ctx->plans.find(key);
     if (it == ctx->plans.end()) {
+        if (capturing)
+            return fail(ctx, GEMEL_ESTATE,
+                        "no plan for this model set and frame counts yet: run one round outside stream capture first");
         auto P = std::make_unique<Plan>();
         const int saved = ctx->opt.streams;
         ctx->opt.streams = nstreams;
-        hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
-        const bool can_tune = stream == nullptr || (hipStreamIsCapturing(stream, &cap) == hipSuccess &&
-                                                    cap == hipStreamCaptureStatusNone);
-        st = build_plan(ctx, ids, nfr, *P, can_tune);
+        st = build_plan(ctx, ids, nfr, *P, true);
         ctx->opt.streams = saved;
         if (st) {
             if (P->arena) (void)hipFree(P->arena);
@@ -1631,12 +1856,30 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         const int no = (int)ctx->models[(size_t)id]->outputs.size();
         for (int o = 0; o < no; ++o) cp.outputs.push_back(outputs[caller_out_base[(size_t)ci] + o]);
     }
+    if (capturing) {
+        if (!P.chunks.empty()) return fail(ctx, GEMEL_ESTATE, "a round that streams weights cannot be captured");
+        if (ctx->opt.profile) return fail(ctx, GEMEL_ESTATE, "a profiled round cannot be captured");
+        ctx->last_mode = MODE_SERIAL;
+        return enqueue_serial(ctx, P, cp, stream);
+    }
+    // rounds share the plan's arena and split-K regions and the staging
+    // slots: a round on another stream than the previous one first waits
+    // for the previous round's work
+    if (ctx->round_seen && ctx->round_stream != stream)
+        HIPCHK(hipStreamWaitEvent(stream, ctx->ev_round_done, 0), "hipStreamWaitEvent");
+    auto round_done = [&]() -> gemel_status {
+        HIPCHK(hipEventRecord(ctx->ev_round_done, stream), "hipEventRecord");
+        ctx->round_stream = stream;
+        ctx->round_seen = true;
+        return GEMEL_OK;
+    };
     const bool graphable = will_graph && P.chunks.empty();
+    ctx->tuning_left = 0;
     if (!graphable) {
         ctx->last_mode = MODE_EAGER;
         st = enqueue(ctx, P, cp, stream);
         if (!st && ctx->opt.profile) ctx->prof.rounds++;
-        return st;
+        return st ? st : round_done();
     }
     // mode of this round: a single-stream plan is one chain graph; a
     // multi-stream plan uses the mode set by the options, or, with autotune,
@@ -1654,15 +1897,11 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         if (P.best_mode >= 0) {
             mode = P.best_mode;
         } else {
-            hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-            HIPCHK(hipStreamIsCapturing(stream, &cs), "hipStreamIsCapturing");
-            if (cs == hipStreamCaptureStatusNone) {
-                mode = kCand[P.tune_round % kNCand];
-                timed = P.tune_round >= kNCand;
-                tuning = true;
-                for (auto &ev : P.tune_ev)
-                    if (!ev) HIPCHK(hipEventCreate(&ev), "hipEventCreate");
-            }
+            mode = kCand[P.tune_round % kNCand];
+            timed = P.tune_round >= kNCand;
+            tuning = true;
+            for (auto &ev : P.tune_ev)
+                if (!ev) HIPCHK(hipEventCreate(&ev), "hipEventCreate");
         }
     }
     // graphs for this set of caller pointers (rebuilt when they change)
@@ -1727,8 +1966,9 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
             }
             P.best_mode = kCand[b];
         }
+        ctx->tuning_left = P.best_mode >= 0 ? 0 : kNCand * (1 + kTimed) - P.tune_round;
     }
-    return GEMEL_OK;
+    return round_done();
 }
 
 void profile_reset(gemel_ctx *ctx) {
@@ -1753,6 +1993,7 @@ gemel_status profile_read(gemel_ctx *ctx, gemel_kernel_stat *stats, int32_t *rou
         HIPCHK(hipEventSynchronize(r.b), "hipEventSynchronize");
         HIPCHK(hipEventElapsedTime(&ms, r.a, r.b), "hipEventElapsedTime");
         p.ms[r.kind] += ms;
+        if (r.subset >= 0) p.ms[r.subset] += ms;
         p.pool.push_back(r.a);
         p.pool.push_back(r.b);
     }

@@ -469,6 +469,7 @@ gemel_status gemel_query(gemel_ctx *ctx, int32_t key, int64_t *val) {
     case GEMEL_Q_GRAPH_REPLAYS: *val = ctx->graph_replays; break;
     case GEMEL_Q_STREAMS: *val = ctx->opt.streams; break;
     case GEMEL_Q_ROUND_MODE: *val = ctx->last_mode; break;
+    case GEMEL_Q_ROUND_TUNING: *val = ctx->tuning_left; break;
     default: return fail(ctx, GEMEL_EINVAL, "unknown query key");
     }
     return GEMEL_OK;
@@ -496,6 +497,15 @@ gemel_status gemel_set_option(gemel_ctx *ctx, int32_t key, int64_t value) {
     case GEMEL_OPT_FAIL_COPY_AT:
         if (value < 0) return fail(ctx, GEMEL_EINVAL, "fail_copy_at must be >= 0");
         ctx->opt.fail_copy_at = value ? ctx->copies_issued + value : 0;
+        break;
+    case GEMEL_OPT_GROUP_UNMERGED:
+        if (value != 0 && value != 1) return fail(ctx, GEMEL_EINVAL, "group_unmerged is 0 or 1");
+        ctx->opt.group_unmerged = (int)value;
+        drop_plans(ctx);
+        break;
+    case GEMEL_OPT_FAIL_ALLOC_AT:
+        if (value < 0) return fail(ctx, GEMEL_EINVAL, "fail_alloc_at must be >= 0");
+        ctx->opt.fail_alloc_at = value ? ctx->allocs_issued + value : 0;
         break;
     case GEMEL_OPT_SPLIT_MERGED:
         if (value != 0 && value != 1) return fail(ctx, GEMEL_EINVAL, "split_merged is 0 or 1");
@@ -536,6 +546,14 @@ gemel_status gemel_set_option(gemel_ctx *ctx, int32_t key, int64_t value) {
         if (value != 0 && value != 1) return fail(ctx, GEMEL_EINVAL, "fuse_pool is 0 or 1");
         ctx->opt.fuse_pool = (int)value;
         drop_plans(ctx);
+        break;
+    case GEMEL_OPT_PAIRED_ACTS:
+        if (value != 0 && value != 1) return fail(ctx, GEMEL_EINVAL, "paired_acts is 0 or 1");
+        if (ctx->opt.paired_acts != (int)value) {
+            ctx->opt.paired_acts = (int)value;
+            ctx->weights_ready = false;
+            drop_plans(ctx);
+        }
         break;
     case GEMEL_OPT_SPLITK_FUSED:
         if (value < 0 || value > 2) return fail(ctx, GEMEL_EINVAL, "splitk_fused is 0, 1 or 2");

@@ -35,14 +35,15 @@ LEAKY_SLOPE = 0.1
 
 Q_UNMERGED_BYTES, Q_MERGED_BYTES, Q_RESIDENT_BYTES, Q_PEAK_BYTES, \
     Q_STREAMED_BYTES, Q_ACTIVATION_BYTES, Q_LAUNCHES, Q_N_MODELS, \
-    Q_GRAPH_REPLAYS, Q_STREAMS, Q_ROUND_MODE = range(11)
+    Q_GRAPH_REPLAYS, Q_STREAMS, Q_ROUND_MODE, Q_ROUND_TUNING = range(12)
 OPT_USE_GRAPH, OPT_SWAP_SLOT_BYTES, OPT_SWAP_SLOTS, OPT_FAIL_COPY_AT, \
     OPT_SPLIT_MERGED, OPT_WEIGHT_BUDGET, OPT_PROFILE, OPT_CONV_TILE, \
     OPT_CONV_SPLITS, OPT_STREAMS, OPT_GRAPH_DAG, OPT_FORK_US, \
     OPT_AUTOTUNE, OPT_SPLITK_FUSED, OPT_TUNE, OPT_FUSE_POOL, \
-    OPT_MIXED_SIZES = range(17)
+    OPT_MIXED_SIZES, OPT_PAIRED_ACTS, OPT_FAIL_ALLOC_AT, \
+    OPT_GROUP_UNMERGED = range(20)
 KERNEL_FAMILIES = ("conv_mfma", "conv_f32", "splitk_reduce", "fc", "pack",
-                   "pool", "route", "export")
+                   "pool", "route", "export", "conv_merged")
 
 EXPORTED = ("gemel_create", "gemel_register_model", "gemel_merge",
             "gemel_enumerate_groups", "gemel_infer", "gemel_model_outputs", "gemel_output_shape",

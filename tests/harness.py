@@ -11,6 +11,11 @@ import numpy as np
 BF16_TOL = 2e-2      # normwise max relative error for bf16 workloads
 F32_TOL = 1e-4       # the same for float32 workloads
 
+# One record per compared output (tag, model, output, normwise error, argmax
+# vectors compared, near-tie exemptions, mismatches); printed at the end of
+# the session by tests/conftest.py.
+PARITY = []
+
 
 def log(msg):
     print(f"[{time.strftime('%H:%M:%S')}] {msg}", flush=True)
@@ -67,6 +72,9 @@ class GpuWorkload:
         if merge:
             self.ctx.merge([[(self.ids[a], b) for a, b in g]
                             for g in wl.groups])
+        from paper_2201_07705_amd import gemel as G
+        for name, value in wl.options.items():
+            self.ctx.set_option(getattr(G, "OPT_" + name.upper()), int(value))
         if budget == "auto" and wl.budget_frac:
             from paper_2201_07705_amd import gemel as G
             unmerged = self.ctx.query(G.Q_UNMERGED_BYTES)
@@ -99,10 +107,14 @@ def oracle_outputs(wl, params, frames, round_act=False):
     return om.run_workload(wl.models, params, frames, wl.groups, round_act)
 
 
-def compare(wl, got, ref, tol=None, check_argmax=True, tag=""):
-    """Assert normwise error per output and arg-max agreement."""
+def compare(wl, got, ref, tol=None, check_argmax=True, check_norm=True,
+            tag=""):
+    """Assert normwise error per output and arg-max agreement (classifier
+    logits per frame; YOLO class scores per anchor and cell). Every output
+    is checked and recorded before the first failure is raised."""
     tol = tol or (BF16_TOL if wl.bf16 else F32_TOL)
     worst = 0.0
+    errors = []
     for mi, (g_outs, r_outs) in enumerate(zip(got, ref)):
         assert len(g_outs) == len(r_outs)
         for oi, (g, r) in enumerate(zip(g_outs, r_outs)):
@@ -110,13 +122,28 @@ def compare(wl, got, ref, tol=None, check_argmax=True, tag=""):
             assert np.all(np.isfinite(g)), (tag, mi, oi)
             e = normwise(g, r)
             worst = max(worst, e)
-            assert e <= tol, f"{tag} model {mi} output {oi}: err {e:.3e}"
+            rec = {"tag": tag, "model": mi, "output": oi, "normwise": e,
+                   "vectors": 0, "near_ties": 0, "mismatches": 0}
+            if check_norm and e > tol:
+                errors.append(f"{tag} model {mi} output {oi}: normwise "
+                              f"error {e:.3e} > {tol:.0e}")
+            vec = None
             if check_argmax and g.ndim == 2:
-                bad, ties = argmax_check(g, r)
-                assert bad == 0, f"{tag} model {mi}: {bad} argmax mismatches"
+                vec = (g, r)
             if check_argmax and g.ndim == 4 and g.shape[1] == 255:
-                bad, ties = argmax_check(yolo_class_vectors(g),
-                                         yolo_class_vectors(r))
-                assert bad == 0, f"{tag} model {mi} output {oi}: {bad} " \
-                    "class argmax mismatches"
+                vec = (yolo_class_vectors(g), yolo_class_vectors(r))
+            if vec is not None:
+                bad, ties = argmax_check(*vec)
+                rec.update(vectors=int(vec[0].shape[0]), near_ties=ties,
+                           mismatches=bad)
+                if bad:
+                    errors.append(f"{tag} model {mi} output {oi}: {bad} "
+                                  "argmax mismatches beyond near ties")
+            PARITY.append(rec)
+            log(f"{tag} model {mi} output {oi}: normwise {e:.3e}"
+                + (f", argmax over {rec['vectors']} vectors, "
+                   f"{rec['near_ties']} near-tie exemptions, "
+                   f"{rec['mismatches']} mismatches"
+                   if rec["vectors"] else ""))
+    assert not errors, "; ".join(errors)
     return worst

@@ -20,63 +20,116 @@ def main():
     kw = json.loads(sys.argv[3]) if len(sys.argv) > 3 else {}
     opts = json.loads(sys.argv[4]) if len(sys.argv) > 4 else {}
     rounds = int(sys.argv[5]) if len(sys.argv) > 5 else 2
+    # per-round scenario: "streams" (stream index of each round), "capture"
+    # (rounds enqueued while their stream reports an active capture),
+    # "fail" ({round: n}: the n-th swap copy from that round on fails)
+    scen = json.loads(sys.argv[6]) if len(sys.argv) > 6 else {}
     L = G.load(libpath)
     L.hipMalloc.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t]
     L.hipMalloc.restype = ctypes.c_int
     for f in ("hoststub_violations", "hoststub_launches", "hoststub_live_bytes",
-              "hoststub_hazards", "hoststub_check_order", "hoststub_selftest"):
+              "hoststub_hazards", "hoststub_check_order", "hoststub_selftest",
+              "hoststub_allocs"):
         getattr(L, f).restype = ctypes.c_long
+    L.hoststub_set_capturing.argtypes = [ctypes.c_void_p]
+    L.hoststub_set_capturing.restype = None
     L.hoststub_last.restype = ctypes.c_char_p
     if name == "variants":   # every candidate group merged (tests/test_gpu_merging.py)
         sys.path.insert(0, os.path.join(ROOT, "tests"))
         from test_gpu_merging import _variants_workload
         wl = _variants_workload(**kw)
+    elif name == "chain":    # a deep unmerged chain (tests/test_gpu_layers.py)
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        from test_gpu_layers import _deep_chain
+        from workloads.configs import ModelSpec, Workload
+        wl = Workload("chain", 11, "bf16",
+                      [ModelSpec("m0", "custom",
+                                 _deep_chain(with_route=kw.get("route", True)),
+                                 kw.get("frames", 3), (3, 24, 24))],
+                      [], "uniform", options={"PAIRED_ACTS": 1})
     else:
         wl = configs.get(name, **kw)
-    ctx = G.Context(0, wl.dtype, 0, library=L)
-    ids = [ctx.register_model(m.layers, wl.params(i), m.in_chw)
-           for i, m in enumerate(wl.models)]
-    ctx.merge([[(ids[a], b) for a, b in g] for g in wl.groups])
-    if wl.budget_frac:
-        ctx.set_option(G.OPT_WEIGHT_BUDGET,
-                       int(wl.budget_frac * ctx.query(G.Q_UNMERGED_BYTES)))
-    for k, v in opts.items():
-        ctx.set_option(getattr(G, k), v)
+    params = [wl.params(i) for i in range(len(wl.models))]
 
     def dev(nbytes):
         p = ctypes.c_void_p()
         assert L.hipMalloc(ctypes.byref(p), max(nbytes, 1)) == 0
         return p.value
 
-    frames, nfr, outs = [], [], []
-    for i, m in enumerate(wl.models):
-        c, h, w = m.in_chw
-        frames.append(dev(m.n_frames * c * h * w * 4))
-        nfr.append(m.n_frames)
-        for o in range(ctx.n_outputs(ids[i])):
-            shp = ctx.output_shape(ids[i], o, m.n_frames)
-            n = 1
-            for d in shp:
-                n *= d
-            outs.append(dev(n * 4))
-    stream = dev(16)   # any non-null handle: enables graphs and streams
-    status = []
-    for _ in range(rounds):
-        status.append(ctx.infer_raw(ids, frames, nfr, outs, stream))
-    L.hoststub_check_order()
-    print(json.dumps({
-        "selftest": L.hoststub_selftest(),
-        "hazards": L.hoststub_hazards(),
-        "status": status,
-        "violations": L.hoststub_violations(),
-        "launches": L.hoststub_launches(),
-        "last": L.hoststub_last().decode(),
-        "plan_launches": ctx.query(G.Q_LAUNCHES),
-        "arena": ctx.query(G.Q_ACTIVATION_BYTES),
-        "streamed": ctx.query(G.Q_STREAMED_BYTES),
-        "error": L.gemel_last_error(ctx._h).decode(),
-    }), flush=True)
-    ctx.close()
+    def one(scen):
+        """One context through `rounds` rounds of scenario `scen`."""
+        ctx = G.Context(0, wl.dtype, 0, library=L)
+        ids = [ctx.register_model(m.layers, params[i], m.in_chw)
+               for i, m in enumerate(wl.models)]
+        ctx.merge([[(ids[a], b) for a, b in g] for g in wl.groups])
+        if wl.budget_frac:
+            ctx.set_option(G.OPT_WEIGHT_BUDGET,
+                           int(wl.budget_frac * ctx.query(G.Q_UNMERGED_BYTES)))
+        for k, v in wl.options.items():
+            ctx.set_option(getattr(G, "OPT_" + k.upper()), int(v))
+        for k, v in opts.items():
+            ctx.set_option(getattr(G, k), v)
+        frames, nfr, outs = [], [], []
+        for i, m in enumerate(wl.models):
+            c, h, w = m.in_chw
+            frames.append(dev(m.n_frames * c * h * w * 4))
+            nfr.append(m.n_frames)
+            for o in range(ctx.n_outputs(ids[i])):
+                shp = ctx.output_shape(ids[i], o, m.n_frames)
+                n = 1
+                for d in shp:
+                    n *= d
+                outs.append(dev(n * 4))
+        # any non-null handles: enable graphs and streams
+        streams = [dev(16) for _ in range(1 + max(scen.get("streams", [0])))]
+        status, launches = [], []
+        live_before = L.hoststub_live_bytes()
+        allocs_before = L.hoststub_allocs()
+        for r in range(rounds):
+            st = streams[scen["streams"][r]] if "streams" in scen else streams[0]
+            if str(r) in scen.get("fail", {}):
+                ctx.set_option(G.OPT_FAIL_COPY_AT, scen["fail"][str(r)])
+            if str(r) in scen.get("fail_alloc", {}):
+                ctx.set_option(G.OPT_FAIL_ALLOC_AT, scen["fail_alloc"][str(r)])
+            cap = r in scen.get("capture", [])
+            if cap:
+                L.hoststub_set_capturing(st)
+            before = L.hoststub_launches()
+            status.append(ctx.infer_raw(ids, frames, nfr, outs, st))
+            launches.append(L.hoststub_launches() - before)
+            if cap:
+                L.hoststub_set_capturing(None)
+        L.hoststub_check_order()
+        res = {
+            "status": status,
+            "round_launches": launches,
+            "allocs": L.hoststub_allocs() - allocs_before,
+            "error": L.gemel_last_error(ctx._h).decode(),
+            "plan_launches": ctx.query(G.Q_LAUNCHES),
+            "arena": ctx.query(G.Q_ACTIVATION_BYTES),
+            "streamed": ctx.query(G.Q_STREAMED_BYTES),
+            "round_mode": ctx.query(G.Q_ROUND_MODE),
+        }
+        ctx.close()
+        # device bytes the context still held after it was destroyed
+        res["leaked"] = L.hoststub_live_bytes() - live_before
+        return res
+
+    def totals(res):
+        return dict(res, **{
+            "selftest": L.hoststub_selftest(),
+            "hazards": L.hoststub_hazards(),
+            "violations": L.hoststub_violations(),
+            "launches": L.hoststub_launches(),
+            "last": L.hoststub_last().decode(),
+        })
+
+    if "each" in scen:
+        # several scenarios, each in a fresh context; counters accumulate
+        runs = [one(sc) for sc in scen["each"]]
+        print(json.dumps(totals({"runs": runs})), flush=True)
+    else:
+        print(json.dumps(totals(one(scen))), flush=True)
 
 
 if __name__ == "__main__":

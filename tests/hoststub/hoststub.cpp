@@ -34,7 +34,7 @@
 namespace {
 std::mutex mu;
 std::map<uintptr_t, size_t> live;     // base -> bytes
-long violations = 0, launches = 0, hazards = 0;
+long violations = 0, launches = 0, hazards = 0, allocs = 0;
 std::string last;
 
 bool inside(const void *p, size_t bytes) {
@@ -67,6 +67,22 @@ std::map<hipEvent_t, std::vector<int>> evstate;      // nodes an event's record 
 size_t synced = 0;
 std::vector<int> host_done;                          // nodes the host has waited for
 Node *cur = nullptr;                                 // node of the launch being checked
+// stream capture: while set, every operation must be enqueued on this
+// stream, and nothing may allocate or synchronise
+hipStream_t capturing = nullptr;
+
+void capture_check(hipStream_t s, const char *what) {
+    if (!capturing || s == capturing) return;
+    ++violations;
+    last = std::string("during capture: ") + what + " on another stream than the captured one";
+    std::fprintf(stderr, "hoststub violation: %s\n", last.c_str());
+}
+void capture_forbid(const char *what) {
+    if (!capturing) return;
+    ++violations;
+    last = std::string("during capture: ") + what;
+    std::fprintf(stderr, "hoststub violation: %s\n", last.c_str());
+}
 
 void begin_node(const gemel::Sink &sk, const char *kern) {
     Node n;
@@ -78,6 +94,7 @@ void begin_node(const gemel::Sink &sk, const char *kern) {
         if (sk.node) *sk.node = (hipGraphNode_t)(intptr_t)u.nodes.size();
         cur = &u.nodes.back();
     } else {
+        capture_check(sk.stream, kern);
         n.deps = frontier[sk.stream];
         n.deps.insert(n.deps.end(), host_done.begin(), host_done.end());
         n.synced = synced;
@@ -161,6 +178,7 @@ hipError_t verdict(bool ok) { return ok ? hipSuccess : hipErrorInvalidValue; }
 extern "C" {
 long hoststub_violations() { return violations; }
 long hoststub_launches() { return launches; }
+long hoststub_allocs() { return allocs; }
 long hoststub_hazards() { return hazards; }
 const char *hoststub_last() { return last.c_str(); }
 long hoststub_live_bytes() {
@@ -170,6 +188,8 @@ long hoststub_live_bytes() {
 }
 // Check every directly enqueued launch and copy recorded so far.
 long hoststub_check_order() { return check_universe(eager, "enqueue"); }
+// Report stream s as being captured (null: no capture).
+void hoststub_set_capturing(hipStream_t s) { capturing = s; }
 
 hipError_t hipGetDevice(int *d) { *d = 0; return hipSuccess; }
 hipError_t hipSetDevice(int) { return hipSuccess; }
@@ -183,22 +203,29 @@ hipError_t hipStreamDestroy(hipStream_t s) { frontier.erase(s); std::free(s); re
 hipError_t hipEventCreate(hipEvent_t *e) { *e = (hipEvent_t)std::malloc(16); return hipSuccess; }
 hipError_t hipEventCreateWithFlags(hipEvent_t *e, unsigned) { return hipEventCreate(e); }
 hipError_t hipEventDestroy(hipEvent_t e) { evstate.erase(e); std::free(e); return hipSuccess; }
-hipError_t hipEventRecord(hipEvent_t e, hipStream_t s) { evstate[e] = frontier[s]; return hipSuccess; }
+hipError_t hipEventRecord(hipEvent_t e, hipStream_t s) {
+    capture_check(s, "hipEventRecord");
+    evstate[e] = frontier[s];
+    return hipSuccess;
+}
 // A host wait orders every later operation after what the waited-for event
 // or stream had reached.
 hipError_t hipEventSynchronize(hipEvent_t e) {
+    capture_forbid("hipEventSynchronize");
     auto it = evstate.find(e);
     if (it != evstate.end()) host_done.insert(host_done.end(), it->second.begin(), it->second.end());
     return hipSuccess;
 }
 hipError_t hipStreamSynchronize(hipStream_t s) {
+    capture_forbid("hipStreamSynchronize");
     auto it = frontier.find(s);
     if (it != frontier.end()) host_done.insert(host_done.end(), it->second.begin(), it->second.end());
     return hipSuccess;
 }
 hipError_t hipEventElapsedTime(float *ms, hipEvent_t, hipEvent_t) { *ms = 0.001f; return hipSuccess; }
 hipError_t hipStreamWaitEvent(hipStream_t s, hipEvent_t e, unsigned) {
-    if (!s || !e) return hipErrorInvalidValue;
+    if (!e) return hipErrorInvalidValue;
+    capture_check(s, "hipStreamWaitEvent");
     auto it = evstate.find(e);
     if (it != evstate.end()) {
         auto &f = frontier[s];
@@ -207,6 +234,8 @@ hipError_t hipStreamWaitEvent(hipStream_t s, hipEvent_t e, unsigned) {
     return hipSuccess;
 }
 hipError_t hipMalloc(void **p, size_t n) {
+    capture_forbid("hipMalloc");
+    ++allocs;
     *p = std::malloc(n ? n : 1);
     if (!*p) return hipErrorOutOfMemory;
     std::lock_guard<std::mutex> g(mu);
@@ -229,6 +258,7 @@ hipError_t hipFree(void *p) {
 hipError_t hipHostMalloc(void **p, size_t n, unsigned) { return hipMalloc(p, n); }
 hipError_t hipHostFree(void *p) { return hipFree(p); }
 hipError_t hipMemcpy(void *d, const void *s, size_t n, hipMemcpyKind) {
+    capture_forbid("hipMemcpy");
     cur = nullptr;
     bool ok = chk(d, (long long)n, "memcpy dst", "hipMemcpy");
     if (ok) std::memcpy(d, s, n);
@@ -245,12 +275,23 @@ hipError_t hipMemcpyAsync(void *d, const void *s, size_t n, hipMemcpyKind k, hip
     (void)k;
     return verdict(ok);
 }
-hipError_t hipDeviceSynchronize() { synced = eager.nodes.size(); return hipSuccess; }
+hipError_t hipDeviceSynchronize() {
+    capture_forbid("hipDeviceSynchronize");
+    // everything issued so far has completed: check it, then start a new
+    // history (no later operation can overlap the completed ones)
+    check_universe(eager, "enqueue");
+    eager.nodes.clear();
+    frontier.clear();
+    evstate.clear();
+    host_done.clear();
+    synced = 0;
+    return hipSuccess;
+}
 hipError_t hipGetLastError() { return hipSuccess; }
 const char *hipGetErrorString(hipError_t e) { return e == hipSuccess ? "success" : "stub error"; }
 hipError_t hipLaunchKernel(const void *, dim3, dim3, void **, size_t, hipStream_t) { return hipErrorInvalidValue; }
 hipError_t hipStreamIsCapturing(hipStream_t s, hipStreamCaptureStatus *st) {
-    *st = hipStreamCaptureStatusNone;
+    *st = s && s == capturing ? hipStreamCaptureStatusActive : hipStreamCaptureStatusNone;
     return s ? hipSuccess : hipErrorInvalidValue;
 }
 hipError_t hipGraphCreate(hipGraph_t *g, unsigned) {
@@ -274,6 +315,7 @@ hipError_t hipGraphInstantiate(hipGraphExec_t *e, hipGraph_t g, hipGraphNode_t *
 hipError_t hipGraphDestroy(hipGraph_t g) { graphs.erase(g); std::free(g); return hipSuccess; }
 hipError_t hipGraphExecDestroy(hipGraphExec_t e) { execs.erase(e); std::free(e); return hipSuccess; }
 hipError_t hipGraphLaunch(hipGraphExec_t e, hipStream_t s) {
+    capture_check(s, "hipGraphLaunch");
     auto it = execs.find(e);
     if (it == execs.end() || !s) return hipErrorInvalidValue;
     Node n;
@@ -314,8 +356,20 @@ static hipError_t conv_common(const ConvArgs &a, int tile, int esz, const char *
         return hipErrorInvalidValue;
     }
     const long long hwo = (long long)a.Ho * a.Wo;
+    if (a.out_pair && (a.out_mode != OUT_NHWC || a.out_pair < a.N || a.out_pair % 8 ||
+                       a.out_cs < a.out_pair + a.N || esz != 2)) {
+        ++violations;
+        last = std::string(kern) + ": bf16 pairs outside their conditions";
+        return hipErrorInvalidValue;
+    }
     ok &= chk(a.w, (long long)a.N * a.K * esz, "weights", kern);
     if (need_zero) ok &= chk(a.zero, GEMEL_ZERO_PAGE_BYTES, "zero page", kern);
+    if (a.grouped && (!tile_is_dma(tile) || a.hetero)) {
+        ++violations;
+        last = std::string(kern) + ": grouped launch outside the LDS-DMA kernel's conditions";
+        return hipErrorInvalidValue;
+    }
+    for (int i = 0; a.grouped && i < a.nseg; ++i) ok &= chk(a.seg[i].w, (long long)a.N * a.K * esz, "segment weights", kern);
     if (a.hetero && (!tile_is_dma(tile) || a.out_mode != OUT_NHWC)) {
         ++violations;
         last = std::string(kern) + ": mixed sizes outside the LDS-DMA kernel's conditions";
@@ -339,7 +393,7 @@ static hipError_t conv_common(const ConvArgs &a, int tile, int esz, const char *
         if (a.has_res) ok &= chk(s.res, ((rows - 1) * a.out_cs + a.N) * esz, "residual", kern);
         if (a.k_splits <= 1 || a.counters) {
             if (a.out_mode == OUT_NHWC)
-                ok &= chk(s.out, ((rows - 1) * a.out_cs + a.N) * esz, "output", kern, true);
+                ok &= chk(s.out, ((rows - 1) * a.out_cs + a.out_pair + a.N) * esz, "output", kern, true);
             else if (a.out_mode == OUT_NHWC_POOL2)   // the pooled tensor: a quarter of the rows
                 ok &= chk(s.out, ((rows / 4 - 1) * a.out_cs + a.N) * esz, "pooled output", kern, true);
             else
@@ -361,7 +415,7 @@ static hipError_t conv_common(const ConvArgs &a, int tile, int esz, const char *
 
 bool conv_dma_supported(const ConvArgs &a) {
     return a.Cin % 32 == 0 && a.in_cs % 8 == 0 && a.K % 32 == 0 && a.k_per_split % 32 == 0 && a.zero &&
-           a.uni_affine && (long)a.in_cs * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES;
+           (a.uni_affine || a.grouped) && (long)a.in_cs * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES;
 }
 bool conv_dma_supported(const ConvArgs &a, int tile) {
     if (!conv_dma_supported(a)) return false;
@@ -370,6 +424,7 @@ bool conv_dma_supported(const ConvArgs &a, int tile) {
 hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) { return launch_conv_bf16(a, tile, sk); }
 bool conv_stem_supported(const ConvArgs &a) {
     return a.Cin == 8 && a.in_cs == 8 && a.k_splits <= 1 && a.kh * a.kw <= STEM_MAX_TAPS && a.zero && a.uni_affine &&
+           !a.out_pair && !a.grouped &&
            (a.out_mode == OUT_NHWC || a.out_mode == OUT_NCHW_F32);
 }
 hipError_t launch_conv_stem(const ConvArgs &a, const Sink &sk) {
@@ -401,7 +456,7 @@ hipError_t launch_conv_reduce(const ReduceArgs &a, bool bf16, const Sink &sk) {
         const ConvSeg &s = a.seg[i];
         const long long rows = seg_rows(a.seg, a.nseg, i, a.M);
         if (a.out_mode == OUT_NHWC)
-            ok &= chk(s.out, ((rows - 1) * a.out_cs + a.N) * esz, "output", "conv_reduce", true);
+            ok &= chk(s.out, ((rows - 1) * a.out_cs + a.out_pair + a.N) * esz, "output", "conv_reduce", true);
         else
             ok &= chk(s.out, rows * a.cout * 4, "output nchw", "conv_reduce", true);
         if (a.has_res) ok &= chk(s.res, ((rows - 1) * a.out_cs + a.N) * esz, "residual", "conv_reduce");

@@ -54,6 +54,19 @@ def test_header_enums_match_binding():
                       ("GEMEL_OPT_WEIGHT_BUDGET", G.OPT_WEIGHT_BUDGET)]:
         m = re.search(rf"{name}\s*=\s*(-?\d+)", txt)
         assert m and int(m.group(1)) == val, name
+    # every query key and option of the header, by name, in the binding
+    for prefix in ("Q", "OPT"):
+        found = re.findall(rf"GEMEL_{prefix}_(\w+)\s*=\s*(\d+)", txt)
+        assert found
+        for name, val in found:
+            assert getattr(G, f"{prefix}_{name}") == int(val), name
+    # kernel families: the binding's names in GEMEL_K_* order
+    fams = dict((int(v), n) for n, v in
+                re.findall(r"GEMEL_K_(\w+)\s*=\s*(\d+)", txt))
+    count = fams.pop(max(fams))
+    assert count == "COUNT" and len(G.KERNEL_FAMILIES) == len(fams)
+    for i, n in fams.items():
+        assert G.KERNEL_FAMILIES[i] == n.lower(), (i, n)
     assert ctypes.sizeof(G.LayerDesc) == 4 * 14 + 8 * 6 + 8
 
 

@@ -202,3 +202,82 @@ def test_merged_segments_with_different_frame_counts(dtype):
     models = [body + [h] for h in heads]
     groups = [[(0, i), (1, i), (2, i)] for i in range(4)]
     run_case(models, (3, 24, 24), [2, 5, 1], dtype, groups)
+
+
+def _deep_chain(depth=16, c=64, with_route=True):
+    """A per-model chain of 3x3 / 1x1 convs with batch norm and leaky ReLU
+    (the shape of a detection head), optionally with an upsample + concat
+    route, ending in a linear 1x1 output conv."""
+    lay = [conv("c0", -1, 3, c, 3, 1, 1, bn=True, act="leaky")]
+    for i in range(1, depth):
+        k = 3 if i % 2 else 1
+        lay.append(conv(f"c{i}", i - 1, c, c, k, 1, k // 2, bn=True,
+                        act="leaky"))
+    src = len(lay) - 1
+    if with_route:
+        # route: 1x1 conv, 2x2 max pool (a coarser scale), upsample, then
+        # concat with the chain's own output (a paired tap next to a plain
+        # bf16 tensor in one concat)
+        lay.append(conv("r", src, c, c // 2, 1, bn=True, act="leaky"))
+        lay.append(L("p", "maxpool", len(lay) - 1, cin=c // 2, cout=c // 2,
+                     kh=2, kw=2, stride=2))
+        lay.append(L("u", "upsample", len(lay) - 1, cin=c // 2, cout=c // 2))
+        lay.append(L("cat", "concat", len(lay) - 1, src1=src, cin=c // 2,
+                     cout=c // 2 + c))
+        lay.append(conv("m", len(lay) - 1, c // 2 + c, c, 3, 1, 1, bn=True,
+                        act="leaky"))
+        src = len(lay) - 1
+    lay.append(conv("out", src, c, 40, 1, bias=True, out=True))
+    return lay
+
+
+@pytest.mark.parametrize("with_route", [False, True])
+def test_paired_activations_cut_drift_of_deep_unmerged_chains(with_route):
+    """GEMEL_OPT_PAIRED_ACTS keeps unmerged activations as bf16 (hi, lo)
+    pairs: the output of a deep per-model chain then drifts from the
+    float32 oracle by far less than with bf16 activations. What remains is
+    mostly the one bf16 rounding of the first conv's output (it reads the
+    8-channel input and stays bf16; with the route, also the pooled route
+    tensor), which the chain's gain carries to the output: about a third of
+    the drift of 16 roundings or less."""
+    from paper_2201_07705_amd import gemel as G
+    lay = _deep_chain(with_route=with_route)
+    models = [ModelSpec("m0", "custom", lay, 3, (3, 24, 24))]
+    errs = {}
+    for paired in (0, 1):
+        wl = Workload("chain", 11, "bf16", models, [], "uniform",
+                      options={"PAIRED_ACTS": paired})
+        params = [wl.params(0)]
+        fr = [wl.frames(0)]
+        g = GpuWorkload(wl, params)
+        try:
+            got = g.run(fr)
+        finally:
+            g.close()
+        errs[paired] = compare(wl, got, oracle_outputs(wl, params, fr),
+                               tol=BF16_LAYER_TOL * 3, check_argmax=False,
+                               tag=f"chain-pairs{paired}")
+    log(f"deep chain normwise error: bf16 {errs[0]:.3e}, pairs {errs[1]:.3e}")
+    assert errs[1] <= 5e-3 and errs[1] * 3 <= errs[0], errs
+
+
+def test_paired_activations_leave_merged_layers_bitwise():
+    """Pairs apply only to tensors between unmerged layers: on a workload
+    whose every conv is merged (ResNet-18 x2, reduced), the outputs with
+    and without the option are bitwise equal."""
+    import numpy as np
+    from workloads import configs
+    wl = configs.resnet18x2(res=64, frames=2)
+    params = [wl.params(i) for i in range(len(wl.models))]
+    fr = [wl.frames(i) for i in range(len(wl.models))]
+    outs = []
+    for paired in (0, 1):
+        wl.options = {"PAIRED_ACTS": paired, "TUNE": 0}
+        g = GpuWorkload(wl, params)
+        try:
+            outs.append(g.run(fr))
+        finally:
+            g.close()
+    for a, b in zip(outs[0], outs[1]):
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)

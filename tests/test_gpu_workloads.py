@@ -1,12 +1,17 @@
 """End-to-end parity of the merged workloads against the oracle.
 
-Reduced-resolution variants are checked on every output element (the
-oracle finishes them in seconds); the full-size workloads run in the same
-launch configuration as the benchmark and are checked on sampled frames:
-the oracle evaluates only the sampled frames (frames are independent, so
-the outputs of a frame do not depend on the other frames in the batch)."""
+Reduced-resolution variants and the full-size workloads are checked on
+every output element of every frame, in the launch configuration the
+benchmark uses (the workload's own options, plan-time tuning on). The
+oracle evaluates each model alone on its frames with its effective
+weights; the full-size runs take 10-30 s of oracle time each on the host
+cores. The bar: normwise error max|g - r| / max|r| per output tensor
+within 2e-2 (bf16) or 1e-4 (float32), and the arg-max of every classifier
+frame and of every YOLO (anchor, cell) class vector equal to the oracle's
+except near ties (the oracle's top-2 gap within twice the frame's max abs
+error); the near-tie exemptions are counted and printed in the session's
+parity summary."""
 
-import numpy as np
 import pytest
 
 from harness import GpuWorkload, compare, log, oracle_outputs
@@ -15,43 +20,24 @@ from workloads import configs
 pytestmark = pytest.mark.gpu
 
 
-def _full_check(wl, budget=0, tag=""):
+def _run(wl, budget=0, tag=""):
+    """GPU outputs and oracle outputs of every frame of every model."""
     params = [wl.params(i) for i in range(len(wl.models))]
     fr = [wl.frames(i) for i in range(len(wl.models))]
-    log(f"{tag}: gpu run")
+    log(f"{tag}: gpu run ({wl.total_frames()} frames, options {wl.options})")
     g = GpuWorkload(wl, params, budget=budget)
     try:
         got = g.run(fr)
     finally:
         g.close()
-    log(f"{tag}: oracle")
+    log(f"{tag}: oracle on every frame")
     ref = oracle_outputs(wl, params, fr)
+    return got, ref
+
+
+def _full_check(wl, budget=0, tag=""):
+    got, ref = _run(wl, budget, tag)
     e = compare(wl, got, ref, tag=tag)
-    log(f"{tag}: worst normwise error {e:.3e}")
-
-
-def _sampled(wl, pick, budget=0, tag=""):
-    """GPU on every frame; oracle on frames ``pick(model_index, n)``.
-    Returns the sampled GPU outputs and the oracle's."""
-    params = [wl.params(i) for i in range(len(wl.models))]
-    fr = [wl.frames(i) for i in range(len(wl.models))]
-    log(f"{tag}: gpu run ({wl.total_frames()} frames)")
-    g = GpuWorkload(wl, params, budget=budget)
-    try:
-        got = g.run(fr)
-    finally:
-        g.close()
-    idx = [pick(i, m.n_frames) for i, m in enumerate(wl.models)]
-    log(f"{tag}: oracle on frames {idx}")
-    sub = [f[i] for f, i in zip(fr, idx)]
-    ref = oracle_outputs(wl, params, sub)
-    got_sub = [[o[i] for o in outs] for outs, i in zip(got, idx)]
-    return got_sub, ref
-
-
-def _sampled_check(wl, pick, budget=0, tag=""):
-    got_sub, ref = _sampled(wl, pick, budget, tag)
-    e = compare(wl, got_sub, ref, tag=tag)
     log(f"{tag}: worst normwise error {e:.3e}")
 
 
@@ -67,50 +53,12 @@ def test_resnet18x2_reduced():
     _full_check(configs.resnet18x2(res=96, frames=3), tag="r18x2-96px")
 
 
-def test_resnet18x2_full_size_sampled():
-    _sampled_check(configs.resnet18x2(),
-                   lambda i, n: [0, n - 1] if i == 0 else [1, 2],
-                   tag="r18x2")
-
-
 def test_r50_vgg16_reduced():
     _full_check(configs.r50x2_vgg16x2(res=64, frames=2), tag="r50vgg-64px")
 
 
-def test_r50_vgg16_full_size_sampled():
-    _sampled_check(configs.r50x2_vgg16x2(),
-                   lambda i, n: [(3 * i) % n, n - 1 - i],
-                   tag="r50vgg")
-
-
 def test_yolov3x3_reduced():
     _full_check(configs.yolov3x3(res=96, frames=2), tag="yolo-96px")
-
-
-@pytest.fixture(scope="module")
-def yolo_full():
-    wl = configs.yolov3x3()
-    return wl, _sampled(wl, lambda i, n: [(i + 1) % n], tag="yolo")
-
-
-def test_yolov3x3_full_size_sampled_argmax(yolo_full):
-    """Class argmax per (anchor, cell) identical on every sampled frame."""
-    wl, (got, ref) = yolo_full
-    e = compare(wl, got, ref, tol=1.0, tag="yolo")
-    log(f"yolo: class argmax identical; worst normwise error {e:.3e}")
-
-
-# The 52x52 head sits ~100 stored activations deep. An oracle that stores
-# every activation in bf16 (exact arithmetic otherwise) drifts from the fp64
-# oracle by up to 1.76e-2 on these frames, and the GPU (fp32 accumulation,
-# its own rounding flips) lands at 1.2e-2..2.02e-2 depending on the split-K
-# schedule: the 2e-2 bar is inside bf16 storage noise for this output.
-@pytest.mark.xfail(strict=False, reason="bf16 activation drift on the "
-                   "deepest YOLOv3 head reaches the 2e-2 normwise bar")
-def test_yolov3x3_full_size_sampled_normwise(yolo_full):
-    wl, (got, ref) = yolo_full
-    e = compare(wl, got, ref, check_argmax=False, tag="yolo")
-    log(f"yolo: worst normwise error {e:.3e}")
 
 
 def test_mix8_reduced_with_budget():
@@ -118,6 +66,37 @@ def test_mix8_reduced_with_budget():
                 tag="mix8-32px")
 
 
-def test_mix8_full_size_sampled_with_budget():
-    _sampled_check(configs.mix8_budget40(), lambda i, n: [(5 * i) % n],
-                   budget="auto", tag="mix8")
+# ---- full-size workloads, every frame ----
+
+def test_resnet18x2_full_size():
+    _full_check(configs.resnet18x2(), tag="r18x2")
+
+
+def test_r50_vgg16_full_size():
+    _full_check(configs.r50x2_vgg16x2(), tag="r50vgg")
+
+
+@pytest.fixture(scope="module")
+def yolo_full():
+    wl = configs.yolov3x3()
+    return wl, _run(wl, tag="yolo")
+
+
+def test_yolov3x3_full_size_normwise(yolo_full):
+    """Every output map of every frame of the three detectors within the
+    bf16 normwise tolerance (the per-model heads keep bf16-pair
+    activations, the workload's option)."""
+    wl, (got, ref) = yolo_full
+    e = compare(wl, got, ref, check_argmax=False, tag="yolo")
+    log(f"yolo: worst normwise error {e:.3e}")
+
+
+def test_yolov3x3_full_size_class_argmax(yolo_full):
+    """Class arg-max per (anchor, cell) of every frame equal to the
+    oracle's outside near ties."""
+    wl, (got, ref) = yolo_full
+    compare(wl, got, ref, check_norm=False, tag="yolo-argmax")
+
+
+def test_mix8_full_size_with_budget():
+    _full_check(configs.mix8_budget40(), budget="auto", tag="mix8")

@@ -34,12 +34,13 @@ def hostlib():
     return LIB
 
 
-def drive(lib, name, kw, opts, rounds=2):
+def drive(lib, name, kw, opts, rounds=2, scenario=None):
     asan = subprocess.check_output(["gcc", "-print-file-name=libasan.so"],
                                    text=True).strip()
     env = dict(os.environ, LD_PRELOAD=asan, ASAN_OPTIONS="detect_leaks=0")
     r = subprocess.run(["python", os.path.join(STUB, "drive.py"), lib, name,
-                        json.dumps(kw), json.dumps(opts), str(rounds)],
+                        json.dumps(kw), json.dumps(opts), str(rounds),
+                        json.dumps(scenario or {})],
                        capture_output=True, text=True, env=env, timeout=600)
     assert r.returncode == 0, r.stderr[-3000:]
     return json.loads(r.stdout.strip().splitlines()[-1])
@@ -72,6 +73,9 @@ CASES = [
     ("yolov3x3", {"res": 96, "frames": 2}, {"OPT_TUNE": 0}),
     ("mix8_budget40", {"res": 32, "frames": 2}, {}),
     ("variants", {"res": 32, "frames": 2}, {}),
+    ("chain", {"route": True}, {}),
+    ("chain", {"route": True}, {"OPT_CONV_SPLITS": 3, "OPT_SPLITK_FUSED": 0}),
+    ("chain", {"route": False}, {"OPT_CONV_SPLITS": 2, "OPT_SPLITK_FUSED": 2}),
     ("mix8_budget40", {"res": 32, "frames": 2},
      {"OPT_SWAP_SLOT_BYTES": 1 << 20, "OPT_SWAP_SLOTS": 2,
       "OPT_STREAMS": 3, "OPT_USE_GRAPH": 0}),
@@ -105,3 +109,105 @@ def test_all_groups_merged_still_batches_across_models(hostlib):
     for out in (merged, split):
         assert out["status"] == [0] and out["violations"] == 0 and out["hazards"] == 0, out
     assert merged["plan_launches"] < split["plan_launches"]
+
+
+ESTATE, EDEVICE = -7, -6
+
+
+@pytest.mark.parametrize("name,kw,opts", [
+    ("r50x2_vgg16x2", {"res": 64, "frames": 2}, {}),
+    ("r50x2_vgg16x2", {"res": 64, "frames": 2}, {"OPT_USE_GRAPH": 0}),
+    ("yolov3x3", {"res": 96, "frames": 2}, {"OPT_STREAMS": 8, "OPT_FORK_US": 0}),
+])
+def test_rounds_on_alternating_streams_are_ordered(hostlib, name, kw, opts):
+    """Rounds share the plan's arena, split-K regions and counters: a round
+    on another stream than the previous one waits for it, so no two
+    launches of different rounds touch common bytes unordered."""
+    out = drive(hostlib, name, kw, opts, 5, {"streams": [0, 1, 1, 0, 2]})
+    assert out["status"] == [0] * 5, out["error"]
+    assert out["hazards"] == 0 and out["violations"] == 0, out["last"]
+
+
+@pytest.mark.parametrize("opts", [{}, {"OPT_AUTOTUNE": 0},
+                                  {"OPT_USE_GRAPH": 0}, {"OPT_STREAMS": 1}])
+def test_captured_round_uses_the_callers_stream_only(hostlib, opts):
+    """While the caller's stream is being captured, a round whose plan and
+    weights exist enqueues every launch on that stream alone: no worker
+    stream, event, allocation or synchronisation (the stub flags each),
+    in a valid order (the ordering check covers the captured launches),
+    and as many launches as the plan has."""
+    out = drive(hostlib, "r50x2_vgg16x2", {"res": 64, "frames": 2}, opts, 3,
+                {"capture": [1]})
+    assert out["status"] == [0, 0, 0], out["error"]
+    assert out["hazards"] == 0 and out["violations"] == 0, out["last"]
+    assert out["round_launches"][1] == out["plan_launches"]
+
+
+def test_capture_before_the_first_round_is_refused(hostlib):
+    """A first round needs allocations and synchronous copies (weight
+    placement, plan): under capture it is refused with ESTATE before any
+    of them, and the next round outside capture still works."""
+    out = drive(hostlib, "resnet18x2", {"res": 64, "frames": 2}, {}, 2,
+                {"capture": [0]})
+    assert out["status"] == [ESTATE, 0], out["error"]
+    assert out["violations"] == 0 and out["hazards"] == 0, out["last"]
+    assert out["round_launches"][0] == 0
+
+
+def test_captured_round_that_streams_weights_is_refused(hostlib):
+    out = drive(hostlib, "mix8_budget40", {"res": 32, "frames": 2}, {}, 2,
+                {"capture": [1]})
+    assert out["status"] == [0, ESTATE], out["error"]
+    assert out["violations"] == 0 and out["hazards"] == 0, out["last"]
+
+
+@pytest.mark.parametrize("at", [1, 3, 7, 20])
+@pytest.mark.parametrize("opts", [{}, {"OPT_STREAMS": 1}])
+def test_copy_failure_part_way_leaves_rounds_ordered(hostlib, at, opts):
+    """A weight copy that fails after launches (and the fork to worker
+    streams) were enqueued: the round returns EDEVICE, its partial work is
+    joined back to the caller's stream, and the next rounds, on the same
+    and on another stream, are ordered after it (no hazard)."""
+    out = drive(hostlib, "mix8_budget40", {"res": 32, "frames": 2},
+                dict(opts, OPT_SWAP_SLOT_BYTES=1 << 20, OPT_SWAP_SLOTS=2), 4,
+                {"fail": {"1": at}, "streams": [0, 0, 0, 1]})
+    assert out["status"] == [0, EDEVICE, 0, 0], out["error"]
+    assert out["hazards"] == 0 and out["violations"] == 0, out["last"]
+
+
+ENOMEM = -2
+
+
+@pytest.mark.parametrize("name,kw,opts", [
+    ("resnet18x2", {"res": 64, "frames": 2}, {}),
+    # a weight budget: staging slots and pinned host copies as well
+    ("resnet18x2", {"res": 64, "frames": 2},
+     {"OPT_WEIGHT_BUDGET": 12000000, "OPT_SWAP_SLOT_BYTES": 1 << 20,
+      "OPT_SWAP_SLOTS": 2}),
+])
+def test_allocation_failures_report_enomem_and_leak_nothing(hostlib, name,
+                                                            kw, opts):
+    """The n-th device or pinned allocation of the first round fails, for
+    every n the round makes: the round reports ENOMEM (or, when the failed
+    allocation was the scratch of plan-time tuning, succeeds untuned), the
+    next round succeeds, nothing is left half-enqueued, and the destroyed
+    context holds no memory."""
+    base = drive(hostlib, name, kw, opts, 1)
+    assert base["status"] == [0] and base["leaked"] == 0
+    A = base["allocs"]
+    assert A >= 3
+    # every allocation when there are few; else the first and last ones
+    # (weight pool, staging, plan buffers) and a sample of the pinned copies
+    ns = sorted(set(range(1, A + 1)) if A <= 24 else
+                set(range(1, 6)) | set(range(A - 7, A + 1)) |
+                {A // 4, A // 2, 3 * A // 4})
+    out = drive(hostlib, name, kw, opts, 2,
+                {"each": [{"fail_alloc": {"0": n}} for n in ns]})
+    assert out["violations"] == 0 and out["hazards"] == 0, out["last"]
+    seen_enomem = 0
+    for n, r in zip(ns, out["runs"]):
+        assert r["status"][0] in (0, ENOMEM), (n, r["error"])
+        assert r["status"][1] == 0, (n, r["error"])
+        assert r["leaked"] == 0, n
+        seen_enomem += r["status"][0] == ENOMEM
+    assert seen_enomem >= 3

@@ -45,7 +45,7 @@ def test_resnet18_resnet34_share_41_of_73_layers():
 
 
 def test_vgg16_largest_layer_is_392_mb():
-    """Section 4.2, Observation 1: one VGG16 layer takes 392 MB (float32)."""
+    """Section 5.2, Observation 1: one VGG16 layer takes 392 MB (float32)."""
     v16 = zoo.vgg(16)
     groups = OM.candidate_groups([(0, v16, IN224), (1, v16, IN224)], 4)
     total, members = groups[0]
