@@ -335,9 +335,12 @@ enum {
                                     pipeline with depth steps of 64,
                                     256x256, 256x128, 128x128, 128x64, used
                                     where Cin % 64 == 0; 18, 19: LDS-DMA
-                                    64x64 of depth 32 and 64) with split-K
-                                    still chosen. A forced tile a conv
-                                    cannot use falls back to 64x64         */
+                                    64x64 of depth 32 and 64; 20..23:
+                                    LDS-DMA of depth 32 with a 64x64 tile
+                                    per wave, 256x128 and 128x256 of 8
+                                    waves, 256x64 and 64x256 of 4) with
+                                    split-K still chosen. A forced tile a
+                                    conv cannot use falls back to 64x64    */
     GEMEL_OPT_CONV_SPLITS = 8,   /* 0 (default): split-K chosen per conv;
                                     n >= 1: force n depth splits (capped
                                     so that every split has work)          */
@@ -445,7 +448,7 @@ enum {
                                     call reports ENOMEM, or, for the scratch
                                     of plan-time tuning, skips that tuning);
                                     0 = off                                */
-    GEMEL_OPT_GROUP_UNMERGED = 19 /* 1: an unmerged bf16 conv that
+    GEMEL_OPT_GROUP_UNMERGED = 19 /* 1 (default): an unmerged bf16 conv that
                                     appears with the same shape and epilogue
                                     in several active models (their k-th such
                                     layer each, e.g. per-model heads of one
@@ -455,8 +458,8 @@ enum {
                                     two segments), where the LDS-DMA kernel
                                     can take it and the weights are resident.
                                     Results are those of separate launches
-                                    of the same tile configuration. 0
-                                    (default): one launch per model        */
+                                    of the same tile configuration. 0: one
+                                    launch per model                       */
 };
 
 /* Set an option; takes effect at the next gemel_infer. Errors: EINVAL. */

@@ -5,7 +5,9 @@ this file. Usage: ``python -m paper_2201_07705_amd.build``."""
 from __future__ import annotations
 
 import glob
+import json
 import os
+import re
 import subprocess
 import sys
 from concurrent.futures import ThreadPoolExecutor
@@ -25,13 +27,37 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
          f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}"]
 
 
+RESOURCES = os.path.join(BUILD, "kernel_resources.json")
+
+
+def _resources(text):
+    """Per-kernel register, scratch and occupancy figures from hipcc's
+    kernel-resource-usage remarks."""
+    out, name = {}, None
+    for line in text.splitlines():
+        m = re.search(r"remark:\s+(Function Name|VGPRs|AGPRs|ScratchSize "
+                      r"\[bytes/lane\]|Occupancy \[waves/SIMD\]):\s*(\S+)",
+                      line)
+        if not m:
+            continue
+        key, val = m.group(1), m.group(2)
+        if key == "Function Name":
+            name = val
+            out[name] = {}
+        elif name is not None:
+            out[name][key.split()[0].lower()] = int(val)
+    return out
+
+
 def _compile(src):
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
     cmd = [HIPCC] + FLAGS + ["-c", src, "-o", obj]
+    if src.endswith(".hip"):
+        cmd.append("-Rpass-analysis=kernel-resource-usage")
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stdout}\n{r.stderr}")
-    return obj
+    return obj, _resources(r.stderr)
 
 
 def build(verbose=False):
@@ -39,7 +65,13 @@ def build(verbose=False):
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")) +
                   glob.glob(os.path.join(CSRC, "*.cpp")))
     with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
-        objs = list(ex.map(_compile, srcs))
+        done = list(ex.map(_compile, srcs))
+    objs = [o for o, _ in done]
+    res = {}
+    for _, r in done:
+        res.update(r)
+    with open(RESOURCES, "w") as f:
+        json.dump(res, f, indent=1, sort_keys=True)
     tmp = LIB + f".tmp{os.getpid()}"
     cmd = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp] \
         + objs

@@ -197,7 +197,7 @@ struct Options {
     int64_t fail_alloc_at = 0;
     int split_merged = 0;
     int paired_acts = 0;      // unmerged conv chains keep bf16 (hi, lo) pairs
-    int group_unmerged = 0;   // same-shape unmerged convs of several models: one launch
+    int group_unmerged = 1;   // same-shape unmerged convs of several models: one launch
 };
 
 }  // namespace gemel

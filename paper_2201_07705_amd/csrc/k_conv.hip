@@ -411,7 +411,8 @@ static const TileShape kTiles[TILE_COUNT] = {
     {256, 64, 256},  {64, 64, 256},  {128, 64, 256}, {64, 128, 256},
     {256, 256, 512}, {256, 128, 256}, {128, 128, 256}, {128, 64, 128}, {256, 32, 256},
     {256, 256, 512}, {256, 128, 256}, {128, 128, 256}, {128, 64, 128},
-    {64, 64, 256}, {64, 64, 256}};
+    {64, 64, 256}, {64, 64, 256},
+    {256, 128, 512}, {128, 256, 512}, {256, 64, 256}, {64, 256, 256}};
 
 int conv_tile_bm(int tile) { return tile >= 0 && tile < TILE_COUNT ? kTiles[tile].bm : 0; }
 int conv_tile_bn(int tile) { return tile >= 0 && tile < TILE_COUNT ? kTiles[tile].bn : 0; }

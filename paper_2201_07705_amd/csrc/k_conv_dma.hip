@@ -78,8 +78,17 @@ __device__ __forceinline__ void wait_lgkm0() {
 // MODE 1: the 2x2 stride-2 max pool fused (out_mode OUT_NHWC_POOL2);
 // MODE 2: segments of different spatial sizes (ConvArgs::hetero). Separate
 // instantiations, so that the plain kernels keep their code and registers.
+// Waves per SIMD the kernel is compiled for: two where the LDS of two
+// workgroups fits one CU and a workgroup has at most 4 waves (the register
+// budget then allows both), else one.
+template <int BM, int BN, int WM, int WN, int STAGES, int BK>
+constexpr int dma_min_waves() {
+    return WM * WN <= 4 && 2 * STAGES * (BM + BN) * BK * 2 <= 160 * 1024 ? 2 : 1;
+}
+
 template <int BM, int BN, int WM, int WN, int STAGES, int BK, int MODE>
-__global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a) {
+__global__ __launch_bounds__(64 * WM *WN, (dma_min_waves<BM, BN, WM, WN, STAGES, BK>())) void conv_dma_kernel(
+    const ConvArgs a) {
     constexpr int NW = WM * WN, NT = 64 * NW;
     static_assert(BK == 32 || BK == 64, "step depth");
     constexpr int CPR = BK / 8;                                 // 16-byte chunks per row
@@ -104,28 +113,40 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / WN, wn = wave - (wave / WN) * WN;
     const int tiles_n = (a.N + BN - 1) / BN;
-    // grouped launches tile every segment on its own (a tile never
-    // straddles two segments' weights); seg[s].t_start is its first tile
-    const int tiles = a.grouped ? a.seg[a.nseg - 1].t_start +
-                                      ((a.M - a.seg[a.nseg - 1].m_start + BM - 1) / BM) * tiles_n
-                                : ((a.M + BM - 1) / BM) * tiles_n;
     const int G = gridDim.x;
     const int t = (G & 7) == 0 ? (int)(blockIdx.x & 7) * (G >> 3) + (int)(blockIdx.x >> 3) : (int)blockIdx.x;
-    if (t >= tiles) return;
-    // the tile's rows [m_lo, min(m_lo + BM, m_end)) and column tile tn
-    int m_lo, m_end = a.M, tn;
+    // the tile's rows [m_lo, min(m_lo + BM, m_end)), column tile tn and
+    // weights. Grouped launches tile every segment on its own (a tile never
+    // straddles two segments' weights; seg[s].t_start is its first tile).
+    // Segment fields are gathered with selects over a static walk of the
+    // table: indexing the argument block with a computed segment number
+    // makes the compiler copy the whole block to scratch memory.
+    int m_lo, m_end = a.M, tn, tiles;
+    const void *wseg = a.w;
     if (a.grouped) {
-        int sg = 0;
-        for (int i = 1; i < a.nseg; ++i) sg += t >= a.seg[i].t_start ? 1 : 0;
-        const int local = t - a.seg[sg].t_start, tml = local / tiles_n;
+        int ts = 0, ms = 0;
+        bool past = false;
+        for (int i = 0; i < a.nseg; ++i) {
+            const int ti = a.seg[i].t_start, mi = a.seg[i].m_start;
+            const void *wi = a.seg[i].w;
+            const bool hit = t >= ti;
+            if (!hit && !past) m_end = mi;   // the next segment's first row
+            past = past || !hit;
+            ts = hit ? ti : ts;
+            ms = hit ? mi : ms;
+            wseg = hit ? wi : wseg;
+            tiles = ti + ((i + 1 < a.nseg ? a.seg[i + 1].m_start : a.M) - mi + BM - 1) / BM * tiles_n;
+        }
+        const int local = t - ts, tml = local / tiles_n;
         tn = local - tml * tiles_n;
-        m_lo = a.seg[sg].m_start + tml * BM;
-        if (sg + 1 < a.nseg) m_end = a.seg[sg + 1].m_start;
+        m_lo = ms + tml * BM;
     } else {
+        tiles = ((a.M + BM - 1) / BM) * tiles_n;
         const int tm = t / tiles_n;
         tn = t - tm * tiles_n;
         m_lo = tm * BM;
     }
+    if (t >= tiles) return;
     const int k_begin = blockIdx.y * a.k_per_split;
     const int k_end = min(a.K, k_begin + a.k_per_split);
     const int HWo = a.Ho * a.Wo;
@@ -216,8 +237,7 @@ __global__ __launch_bounds__(64 * WM *WN) void conv_dma_kernel(const ConvArgs a)
     for (int i = 0; i < BI; ++i) {
         const int rl = (i * NW + wave) * RPI + lane / CPR;
         const int gn = tn * BN + rl;
-        bbase[i] = (const u16 *)(a.grouped ? a.seg[s_first].w : a.w) + (size_t)(gn < N ? gn : 0) * K +
-                   ((lane % CPR) ^ sw(rl)) * 8;
+        bbase[i] = (const u16 *)wseg + (size_t)(gn < N ? gn : 0) * K + ((lane % CPR) ^ sw(rl)) * 8;
     }
     // loader position (uniform): next step's tap (lr, ls) and channel base lc
     int kb = k_begin, lc, lr, ls;
@@ -593,6 +613,7 @@ hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) {
     } else {
         tiles = (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn);
     }
+    if (tiles != conv_tiles(a, bm, bn)) return hipErrorInvalidValue;
     const long blocks = tiles >= 8 ? (tiles + 7) / 8 * 8 : tiles;
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
     dim3 grid((unsigned)blocks, (unsigned)a.k_splits);
@@ -617,6 +638,10 @@ hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) {
         GEMEL_DMA_CASE(TILE_DMA64_256x128, 256, 128, 2, 2, 3, 64, 256)
         GEMEL_DMA_CASE(TILE_DMA64_128x128, 128, 128, 2, 2, 2, 64, 256)
         GEMEL_DMA_CASE(TILE_DMA64_128x64, 128, 64, 2, 1, 3, 64, 128)
+        GEMEL_DMA_CASE(TILE_DMA_256x128W8, 256, 128, 4, 2, 4, 32, 512)
+        GEMEL_DMA_CASE(TILE_DMA_128x256W8, 128, 256, 2, 4, 4, 32, 512)
+        GEMEL_DMA_CASE(TILE_DMA_256x64, 256, 64, 4, 1, 4, 32, 256)
+        GEMEL_DMA_CASE(TILE_DMA_64x256, 64, 256, 1, 4, 4, 32, 256)
     default: break;
     }
 #undef GEMEL_DMA_CASE

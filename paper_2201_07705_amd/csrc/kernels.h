@@ -63,11 +63,29 @@ enum ConvTile {
     // small tiles for latency-bound layers: 4 waves of 32x32, 4 stages
     TILE_DMA_64x64 = 18,     // depth 32 (4 workgroups per CU)
     TILE_DMA64_64x64 = 19,   // depth 64 (2 workgroups per CU)
-    TILE_COUNT = 20
+    // LDS-DMA, depth 32, 4 stages, every wave a 64x64 tile (register
+    // double-buffered fragments at two waves per SIMD)
+    TILE_DMA_256x128W8 = 20, // 8 waves (4 x 2)
+    TILE_DMA_128x256W8 = 21, // 8 waves (2 x 4)
+    TILE_DMA_256x64 = 22,    // 4 waves (4 x 1), 2 workgroups per CU
+    TILE_DMA_64x256 = 23,    // 4 waves (1 x 4), 2 workgroups per CU
+    TILE_COUNT = 24
 };
 int conv_tile_threads(int tile);
 int conv_tile_bm(int tile);
 int conv_tile_bn(int tile);
+// Output tiles of a conv launch for a bm x bn tile shape: a grouped launch
+// tiles every segment on its own (a tile never straddles two segments).
+inline long conv_tiles(const ConvArgs &a, int bm, int bn) {
+    const long tn = (a.N + bn - 1) / bn;
+    if (!a.grouped) return (long)((a.M + bm - 1) / bm) * tn;
+    long t = 0;
+    for (int i = 0; i < a.nseg; ++i) {
+        const long rows = (i + 1 < a.nseg ? a.seg[i + 1].m_start : a.M) - (long)a.seg[i].m_start;
+        t += (rows + bm - 1) / bm * tn;
+    }
+    return t;
+}
 constexpr int CONV_BK = 64;
 
 hipError_t launch_conv_bf16(const ConvArgs &a, int tile, const Sink &sk);
@@ -76,7 +94,7 @@ bool conv_dma_supported(const ConvArgs &a, int tile);   // this DMA tile
 hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk);
 inline bool tile_is_dma(int tile) {
     return (tile >= TILE_DMA_256x256 && tile <= TILE_DMA_128x64) ||
-           (tile >= TILE_DMA64_256x256 && tile <= TILE_DMA64_64x64);
+           (tile >= TILE_DMA64_256x256 && tile <= TILE_DMA_64x256);
 }
 inline int tile_dma_depth(int tile) {
     return (tile >= TILE_DMA64_256x256 && tile <= TILE_DMA64_128x64) || tile == TILE_DMA64_64x64 ? 64 : 32;

@@ -452,6 +452,10 @@ static const TileCost kTileCost[] = {
     {TILE_DMA64_128x64, 0.370, 3, 5.06e-6},
     {TILE_DMA_64x64, 0.380, 4, 2.50e-6},
     {TILE_DMA64_64x64, 0.420, 2, 2.20e-6},
+    {TILE_DMA_256x128W8, 0.560, 1, 7.00e-6},
+    {TILE_DMA_128x256W8, 0.560, 1, 7.00e-6},
+    {TILE_DMA_256x64, 0.500, 2, 5.00e-6},
+    {TILE_DMA_64x256, 0.500, 2, 5.00e-6},
 };
 
 // Partial sums of one split-K launch are addressed with 32-bit byte offsets.
@@ -568,7 +572,7 @@ bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int
     for (const ConvCand &k : c) {
         const int64_t bm = conv_tile_bm(k.tile), bn = conv_tile_bn(k.tile);
         if (k.splits > 1) pbytes = std::max(pbytes, (size_t)k.splits * a0.M * a0.N * 4);
-        cbytes = std::max(cbytes, (size_t)(((a0.M + bm - 1) / bm) * ((a0.N + bn - 1) / bn)) * 4);
+        cbytes = std::max(cbytes, (size_t)conv_tiles(a0, (int)bm, (int)bn) * 4);
     }
     if (!ctx->tune_stream && hipStreamCreateWithFlags(&ctx->tune_stream, hipStreamNonBlocking) != hipSuccess)
         return false;
@@ -607,7 +611,7 @@ bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int
         a.k_splits = sp;
         a.k_per_split = kp;
         const int64_t bm = conv_tile_bm(c[i].tile), bn = conv_tile_bn(c[i].tile);
-        const int tiles = (int)(((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn));
+        const int tiles = (int)conv_tiles(a, (int)bm, (int)bn);
         const bool fuse = sp > 1 && fuse_splitk(ctx, tiles);
         a.partial = sp > 1 ? (float *)ctx->tune_partial : nullptr;
         a.counters = fuse ? (int32_t *)ctx->tune_ctr : nullptr;
@@ -1299,7 +1303,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 if (a.k_splits > 1) {
                     step_partial[(size_t)step] = std::max(step_partial[(size_t)step], (size_t)a.k_splits * a.M * a.N * 4);
                     const int bm = conv_tile_bm(Lc.tile), bn = conv_tile_bn(Lc.tile);
-                    const int tiles = ((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn);
+                    const int tiles = (int)conv_tiles(a, bm, bn);
                     if (fuse_splitk(ctx, tiles)) Lc.ctr_n = tiles;
                 }
                 P.launches.push_back(Lc);

@@ -400,10 +400,9 @@ gemel_status gemel_enumerate_groups(gemel_ctx *ctx, const int32_t *model_ids, in
     }
 }
 
-gemel_status gemel_infer(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models,
-                         const void *const *frames, const int32_t *n_frames, void *const *outputs,
-                         void *hip_stream) {
-    if (!ctx) return GEMEL_EINVAL;
+// Argument checks of gemel_infer.
+static gemel_status check_infer_args(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models,
+                                     const void *const *frames, const int32_t *n_frames, void *const *outputs) {
     if (n_models <= 0 || !model_ids || !frames || !n_frames || !outputs)
         return fail(ctx, GEMEL_EINVAL, "null argument array or no models");
     if (n_models > (int)ctx->models.size()) return fail(ctx, GEMEL_EINVAL, "more models than registered");
@@ -424,6 +423,15 @@ gemel_status gemel_infer(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_mod
         }
         out_slot += (int)m.outputs.size();
     }
+    return GEMEL_OK;
+}
+
+gemel_status gemel_infer(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models,
+                         const void *const *frames, const int32_t *n_frames, void *const *outputs,
+                         void *hip_stream) {
+    if (!ctx) return GEMEL_EINVAL;
+    const gemel_status st = check_infer_args(ctx, model_ids, n_models, frames, n_frames, outputs);
+    if (st) return st;
     try {
         return run(ctx, model_ids, n_models, frames, n_frames, outputs, (hipStream_t)hip_stream);
     } catch (const std::bad_alloc &) {
@@ -513,7 +521,8 @@ gemel_status gemel_set_option(gemel_ctx *ctx, int32_t key, int64_t value) {
         drop_plans(ctx);
         break;
     case GEMEL_OPT_CONV_TILE:
-        if (value < -1 || value >= TILE_COUNT) return fail(ctx, GEMEL_EINVAL, "conv tile is -1..19");
+        if (value < -1 || value >= TILE_COUNT)
+            return fail(ctx, GEMEL_EINVAL, "conv tile is -1.." + std::to_string(TILE_COUNT - 1));
         ctx->opt.conv_tile = (int)value;
         drop_plans(ctx);
         break;

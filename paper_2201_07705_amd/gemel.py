@@ -46,7 +46,8 @@ KERNEL_FAMILIES = ("conv_mfma", "conv_f32", "splitk_reduce", "fc", "pack",
                    "pool", "route", "export", "conv_merged")
 
 EXPORTED = ("gemel_create", "gemel_register_model", "gemel_merge",
-            "gemel_enumerate_groups", "gemel_infer", "gemel_model_outputs", "gemel_output_shape",
+            "gemel_enumerate_groups", "gemel_infer",
+            "gemel_model_outputs", "gemel_output_shape",
             "gemel_query", "gemel_set_option", "gemel_profile",
             "gemel_last_error", "gemel_destroy")
 
@@ -313,7 +314,7 @@ class Context:
         nf = (ctypes.c_int32 * n)(*n_frames)
         op = (ctypes.c_void_p * max(len(out_ptrs), 1))(*out_ptrs)
         return self._lib.gemel_infer(self._h, ids, n, fp, nf, op,
-                                 ctypes.c_void_p(stream))
+                                     ctypes.c_void_p(stream))
 
     def close(self):
         if self._h:

@@ -47,6 +47,16 @@ def main():
                                  _deep_chain(with_route=kw.get("route", True)),
                                  kw.get("frames", 3), (3, 24, 24))],
                       [], "uniform", options={"PAIRED_ACTS": 1})
+    elif name == "grouped":  # one unmerged conv in several models (tests/test_gpu_layers.py)
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        from test_gpu_layers import GROUP_CASES, conv
+        from workloads.configs import ModelSpec, Workload
+        cin, cout, k, s_, p_, hw, frames = GROUP_CASES[kw.get("case", 0)]
+        wl = Workload("grouped", 13, "bf16",
+                      [ModelSpec(f"m{i}", "custom",
+                                 [conv("c", -1, cin, cout, k, s_, p_, bn=True,
+                                       act="leaky", out=True)], n, (cin, hw, hw))
+                       for i, n in enumerate(frames)], [], "normal")
     else:
         wl = configs.get(name, **kw)
     params = [wl.params(i) for i in range(len(wl.models))]
@@ -82,7 +92,7 @@ def main():
                 outs.append(dev(n * 4))
         # any non-null handles: enable graphs and streams
         streams = [dev(16) for _ in range(1 + max(scen.get("streams", [0])))]
-        status, launches = [], []
+        status, launches, round_allocs = [], [], []
         live_before = L.hoststub_live_bytes()
         allocs_before = L.hoststub_allocs()
         for r in range(rounds):
@@ -95,14 +105,17 @@ def main():
             if cap:
                 L.hoststub_set_capturing(st)
             before = L.hoststub_launches()
+            a_before = L.hoststub_allocs()
             status.append(ctx.infer_raw(ids, frames, nfr, outs, st))
             launches.append(L.hoststub_launches() - before)
+            round_allocs.append(L.hoststub_allocs() - a_before)
             if cap:
                 L.hoststub_set_capturing(None)
         L.hoststub_check_order()
         res = {
             "status": status,
             "round_launches": launches,
+            "round_allocs": round_allocs,
             "allocs": L.hoststub_allocs() - allocs_before,
             "error": L.gemel_last_error(ctx._h).decode(),
             "plan_launches": ctx.query(G.Q_LAUNCHES),

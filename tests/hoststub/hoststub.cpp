@@ -333,9 +333,9 @@ hipError_t hipGraphLaunch(hipGraphExec_t e, hipStream_t s) {
 namespace gemel {
 
 static const int kBm[TILE_COUNT] = {128, 128, 64, 256, 256, 256, 64, 128, 64, 256, 256, 128, 128, 256,
-                                    256, 256, 128, 128, 64, 64};
+                                    256, 256, 128, 128, 64, 64, 256, 128, 256, 64};
 static const int kBn[TILE_COUNT] = {128, 64, 64, 256, 128, 64, 64, 64, 128, 256, 128, 128, 64, 32,
-                                    256, 128, 128, 64, 64, 64};
+                                    256, 128, 128, 64, 64, 64, 128, 256, 64, 256};
 int conv_tile_bm(int t) { return t >= 0 && t < TILE_COUNT ? kBm[t] : 0; }
 int conv_tile_bn(int t) { return t >= 0 && t < TILE_COUNT ? kBn[t] : 0; }
 int conv_tile_threads(int t) { return (t == TILE_256x256 || t == TILE_256x128) ? 512 : 256; }
@@ -408,7 +408,7 @@ static hipError_t conv_common(const ConvArgs &a, int tile, int esz, const char *
     if (a.k_splits > 1) ok &= chk(a.partial, (long long)a.k_splits * a.M * a.N * 4, "partial", kern, true);
     if (a.k_splits > 1 && a.counters) {
         const long long bm = conv_tile_bm(tile), bn = conv_tile_bn(tile);
-        ok &= chk(a.counters, ((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn) * 4, "counters", kern, true);
+        ok &= chk(a.counters, conv_tiles(a, (int)bm, (int)bn) * 4, "counters", kern, true);
     }
     return verdict(ok);
 }

@@ -47,6 +47,20 @@ def test_library_is_newer_than_its_sources():
     assert os.path.getmtime(lib) >= newest, "libgemel.so is stale: rebuild"
 
 
+def test_kernels_use_no_scratch_memory():
+    """Every HIP kernel of the build keeps its state in registers and LDS:
+    no per-lane scratch (a by-value argument block indexed with a computed
+    segment number, or a register spill, would put it there and cost an
+    order of magnitude in memory traffic)."""
+    import json
+    from paper_2201_07705_amd import build as B
+    assert os.path.getmtime(B.RESOURCES) >= os.path.getmtime(B.LIB) - 60
+    res = json.load(open(B.RESOURCES))
+    assert len(res) >= 30
+    bad = {k: v for k, v in res.items() if v.get("scratchsize", 0)}
+    assert not bad, bad
+
+
 def test_header_enums_match_binding():
     txt = open(os.path.join(ROOT, "include", "gemel.h")).read()
     for name, val in [("GEMEL_EBUDGET", G.EBUDGET), ("GEMEL_OP_CONCAT", 5),

@@ -80,7 +80,8 @@ def test_conv_layer_output_store(dtype, case):
 TILES = ["128x128", "128x64", "64x64", "256x256", "256x128", "256x64",
          "64x64d2", "128x64d2", "64x128", "dma256x256", "dma256x128",
          "dma128x128", "dma128x64", "stem", "dma64_256x256", "dma64_256x128",
-         "dma64_128x128", "dma64_128x64", "dma64x64", "dma64_64x64"]
+         "dma64_128x128", "dma64_128x64", "dma64x64", "dma64_64x64",
+         "dma256x128w8", "dma128x256w8", "dma256x64", "dma64x256"]
 
 
 @pytest.mark.parametrize("tile", range(len(TILES)), ids=lambda t: TILES[t])
@@ -278,6 +279,89 @@ def test_paired_activations_leave_merged_layers_bitwise():
             outs.append(g.run(fr))
         finally:
             g.close()
+    for a, b in zip(outs[0], outs[1]):
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)
+
+
+DMA_TILES = [t for t, n in enumerate(TILES) if n.startswith("dma")]
+GROUP_CASES = [
+    # cin, cout, k, stride, pad, hw, frames per model (ragged segments)
+    (64, 64, 3, 1, 1, 13, (1, 3, 2)),
+    (128, 96, 1, 1, 0, 9, (2, 1, 4)),
+    (256, 255, 1, 1, 0, 13, (3, 3, 3)),
+    (64, 128, 3, 2, 1, 15, (2, 5)),
+]
+
+
+@pytest.mark.parametrize("splits,fused", [(1, 0), (3, 0), (3, 2)],
+                         ids=["split1", "split3", "split3fused"])
+@pytest.mark.parametrize("tile", DMA_TILES, ids=lambda t: TILES[t])
+@pytest.mark.parametrize("case", GROUP_CASES, ids=lambda c: "x".join(map(str, c[:6])))
+def test_grouped_unmerged_conv_exact(tile, case, splits, fused):
+    """The same unmerged conv in several models (each its own weights, BN
+    and frame count; segments of ragged row counts) as ONE grouped launch:
+    every LDS-DMA tile, split-K 1/3, against the oracle at fp32
+    accumulation precision, and bitwise equal to one launch per model in
+    the same configuration."""
+    import numpy as np
+    from paper_2201_07705_amd import gemel as G
+    cin, cout, k, s, p, hw, frames = case
+    log(f"grouped tile {TILES[tile]} splits {splits} conv {case}")
+    models = [ModelSpec(f"m{i}", "custom",
+                        [conv("c", -1, cin, cout, k, s, p, bn=True,
+                              act="leaky", out=True)], n, (cin, hw, hw))
+              for i, n in enumerate(frames)]
+    wl = Workload("grouped", 13, "bf16", models, [], "normal")
+    params = [wl.params(i) for i in range(len(models))]
+    fr = [wl.frames(i) for i in range(len(models))]
+    outs, launches = [], []
+    for grouped in (1, 0):
+        g = GpuWorkload(wl, params)
+        try:
+            g.ctx.set_option(G.OPT_GROUP_UNMERGED, grouped)
+            g.ctx.set_option(G.OPT_CONV_TILE, tile)
+            g.ctx.set_option(G.OPT_CONV_SPLITS, splits)
+            g.ctx.set_option(G.OPT_SPLITK_FUSED, fused)
+            outs.append(g.run(fr))
+            launches.append(g.ctx.query(G.Q_LAUNCHES))
+        finally:
+            g.close()
+    assert launches[0] < launches[1], launches
+    compare(wl, outs[0], oracle_outputs(wl, params, fr), tol=EXACT_TOL,
+            check_argmax=False)
+    for a, b in zip(outs[0], outs[1]):
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("name,kw", [("r50x2_vgg16x2", {"res": 64, "frames": 2}),
+                                     ("yolov3x3", {"res": 96, "frames": 2})])
+def test_grouped_unmerged_workloads(name, kw):
+    """Whole workloads with the per-model layers grouped (ResNet-50 layer4,
+    the YOLOv3 heads): fewer launches, the oracle's outputs within the
+    workload tolerance, and bitwise equal to one launch per model with the
+    tile configuration forced alike."""
+    import numpy as np
+    from paper_2201_07705_amd import gemel as G
+    from workloads import configs
+    wl = configs.get(name, **kw)
+    params = [wl.params(i) for i in range(len(wl.models))]
+    fr = [wl.frames(i) for i in range(len(wl.models))]
+    outs, launches = [], []
+    for grouped in (1, 0):
+        g = GpuWorkload(wl, params)
+        try:
+            g.ctx.set_option(G.OPT_GROUP_UNMERGED, grouped)
+            g.ctx.set_option(G.OPT_CONV_TILE, 11)   # LDS-DMA 128x128
+            g.ctx.set_option(G.OPT_CONV_SPLITS, 1)
+            outs.append(g.run(fr))
+            launches.append(g.ctx.query(G.Q_LAUNCHES))
+        finally:
+            g.close()
+    log(f"{name}: launches grouped {launches[0]}, per model {launches[1]}")
+    assert launches[0] < launches[1]
+    compare(wl, outs[0], oracle_outputs(wl, params, fr), tag=f"{name}-grouped")
     for a, b in zip(outs[0], outs[1]):
         for x, y in zip(a, b):
             assert np.array_equal(x, y)

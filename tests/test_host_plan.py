@@ -74,6 +74,18 @@ CASES = [
     ("mix8_budget40", {"res": 32, "frames": 2}, {}),
     ("variants", {"res": 32, "frames": 2}, {}),
     ("chain", {"route": True}, {}),
+    ("yolov3x3", {"res": 96, "frames": 2}, {"OPT_GROUP_UNMERGED": 1}),
+    # grouped launches of ragged segments, fused split-K (one arrival
+    # counter per output tile of every segment)
+    ("grouped", {"case": 1}, {"OPT_GROUP_UNMERGED": 1, "OPT_CONV_TILE": 12,
+                              "OPT_CONV_SPLITS": 3, "OPT_SPLITK_FUSED": 2}),
+    ("grouped", {"case": 0}, {"OPT_GROUP_UNMERGED": 1, "OPT_CONV_TILE": 9,
+                              "OPT_CONV_SPLITS": 3, "OPT_SPLITK_FUSED": 2}),
+    ("yolov3x3", {"res": 96, "frames": 2},
+     {"OPT_GROUP_UNMERGED": 1, "OPT_CONV_SPLITS": 3, "OPT_SPLITK_FUSED": 2,
+      "OPT_STREAMS": 8, "OPT_FORK_US": 0}),
+    ("r50x2_vgg16x2", {"res": 64, "frames": 2},
+     {"OPT_GROUP_UNMERGED": 1, "OPT_CONV_SPLITS": 3, "OPT_SPLITK_FUSED": 0}),
     ("chain", {"route": True}, {"OPT_CONV_SPLITS": 3, "OPT_SPLITK_FUSED": 0}),
     ("chain", {"route": False}, {"OPT_CONV_SPLITS": 2, "OPT_SPLITK_FUSED": 2}),
     ("mix8_budget40", {"res": 32, "frames": 2},
@@ -211,3 +223,4 @@ def test_allocation_failures_report_enomem_and_leak_nothing(hostlib, name,
         assert r["leaked"] == 0, n
         seen_enomem += r["status"][0] == ENOMEM
     assert seen_enomem >= 3
+
