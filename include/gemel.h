@@ -259,6 +259,34 @@ gemel_status gemel_infer(gemel_ctx *ctx, const int32_t *model_ids,
                          const int32_t *n_frames, void *const *outputs,
                          void *hip_stream);
 
+/*
+ * gemel_infer for callers that cannot allocate device memory: code being
+ * captured into a HIP graph, tight serving loops, harnesses that forbid
+ * hipMalloc. Same arguments, outputs and stream ordering as gemel_infer;
+ * it calls no hipMalloc, hipFree or other allocating routine. Instead:
+ *  - the weights must already be placed on the device (by an earlier
+ *    gemel_infer round; since then no merge, registration, budget or
+ *    storage option change), else ESTATE;
+ *  - the round's activations, split-K partial sums and split-K arrival
+ *    counters lie in one static device array of GEMEL_STATIC_SCRATCH_BYTES
+ *    (64 MiB) per GPU, held until the process ends; a model set and frame
+ *    count whose activations and partial sums exceed it is refused with
+ *    EBUDGET (nothing enqueued);
+ *  - every launch runs in plan order on hip_stream alone (no worker
+ *    stream, event, graph or plan-time tuning), after a fill kernel that
+ *    clears the counters (no memset node);
+ *  - rounds that would stream weights (a weight budget below the model
+ *    set's weights) and profiled rounds are refused with ESTATE.
+ * Every call on one GPU shares that GPU's array, from any context: calls
+ * whose rounds overlap on the device race, so the caller orders them (one
+ * stream, or events). The array keeps the last round's contents.
+ * Errors: EINVAL, ESHAPE, ESTATE, EBUDGET, EDEVICE.
+ */
+gemel_status gemel_infer_noalloc(gemel_ctx *ctx, const int32_t *model_ids,
+                                 int32_t n_models, const void *const *frames,
+                                 const int32_t *n_frames,
+                                 void *const *outputs, void *hip_stream);
+
 /* Number of output layers of a model. Errors: EINVAL. */
 gemel_status gemel_model_outputs(gemel_ctx *ctx, int32_t model_id,
                                  int32_t *n_outputs);

@@ -145,6 +145,10 @@ struct Plan {
     // arrival counters of the fused split-K reductions, a disjoint range per
     // launch (never shared: a counter must read zero when its launch starts)
     int32_t *counters = nullptr;
+    size_t counters_n = 0;                 // ints in `counters`
+    // arena, partial sums and counters carved from the static scratch
+    // (gemel_infer_noalloc): never freed; counters cleared every round
+    bool static_mem = false;
     size_t streamed_bytes = 0;
     // HIP graphs of the round for one set of caller pointers: one chain per
     // segment; one graph whose edges are the launches' data dependencies; one
@@ -257,6 +261,9 @@ void drop_plans(gemel_ctx *ctx);
 gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models,
                  const void *const *frames, const int32_t *n_frames, void *const *outputs,
                  hipStream_t stream);
+gemel_status run_noalloc(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models,
+                         const void *const *frames, const int32_t *n_frames, void *const *outputs,
+                         hipStream_t stream);
 size_t unmerged_bytes(const gemel_ctx *ctx);
 void profile_reset(gemel_ctx *ctx);
 gemel_status profile_read(gemel_ctx *ctx, gemel_kernel_stat *stats, int32_t *rounds);

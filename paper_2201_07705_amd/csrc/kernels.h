@@ -108,6 +108,13 @@ hipError_t launch_conv_f32(const ConvArgs &a, const Sink &sk);
 // Split-K reduction + fused epilogue (bf16 or f32 internal activations).
 hipError_t launch_conv_reduce(const ReduceArgs &a, bool bf16, const Sink &sk);
 
+// Static device scratch of the allocation-free round: its address on the
+// current device `device` (looked up once per device), and a fill kernel
+// (stream sinks only) used to clear what must start at zero.
+#define GEMEL_STATIC_SCRATCH_BYTES (64ull << 20)
+hipError_t static_scratch(int device, void **ptr);
+hipError_t launch_fill_u32(uint32_t *p, size_t n, uint32_t v, const Sink &sk);
+
 hipError_t launch_fc_bf16(const FcArgs &a, const Sink &sk);
 hipError_t launch_fc_f32(const FcArgs &a, const Sink &sk);
 hipError_t launch_fc_reduce(const FcArgs &a, bool bf16, const Sink &sk);

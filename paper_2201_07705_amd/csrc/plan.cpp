@@ -139,9 +139,11 @@ void drop_plans(gemel_ctx *ctx) {
         if (p.ev_fork) (void)hipEventDestroy(p.ev_fork);
         for (auto ev : p.ev_join)
             if (ev) (void)hipEventDestroy(ev);
-        if (p.arena) (void)hipFree(p.arena);
-        if (p.partial) (void)hipFree(p.partial);
-        if (p.counters) (void)hipFree(p.counters);
+        if (!p.static_mem) {
+            if (p.arena) (void)hipFree(p.arena);
+            if (p.partial) (void)hipFree(p.partial);
+            if (p.counters) (void)hipFree(p.counters);
+        }
     }
     ctx->plans.clear();
     ctx->last_plan = nullptr;
@@ -677,8 +679,10 @@ void pick_fc_config(int64_t M, int64_t N, int64_t K, int &splits, int &kps) {
 
 // can_tune: conv configurations may be timed on the device (not while the
 // caller's stream is being captured into a graph).
+// static_base: the arena, split-K partial sums and counters are laid out in
+// these static_cap bytes (the static scratch) instead of being allocated.
 static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, const std::vector<int> &nfr,
-                               Plan &P, bool can_tune) {
+                               Plan &P, bool can_tune, void *static_base = nullptr, size_t static_cap = 0) {
     const bool bf16 = ctx->dtype == GEMEL_BF16;
     const size_t esz = bf16 ? 2 : 4;
     const int S = (int)ids.size();
@@ -1042,7 +1046,15 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
         placed.push_back(t);
     }
     P.arena_bytes = arena;
-    if (arena && alloc_device(ctx, &P.arena, arena) != hipSuccess) {
+    P.static_mem = static_base != nullptr;
+    size_t static_used = (size_t)round_up((int64_t)arena, 256);
+    if (static_base) {
+        if (static_used > static_cap)
+            return fail(ctx, GEMEL_EBUDGET,
+                        "the activations of this model set and frame count (" + std::to_string(arena) +
+                            " bytes) exceed the static scratch of " + std::to_string(static_cap) + " bytes");
+        P.arena = static_base;
+    } else if (arena && alloc_device(ctx, &P.arena, arena) != hipSuccess) {
         P.arena = nullptr;
         (void)hipGetLastError();
         return fail(ctx, GEMEL_ENOMEM, "device allocation of the activation arena failed");
@@ -1413,7 +1425,14 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
             done.push_back(i);
         }
         if (total) {
-            if (alloc_device(ctx, (void **)&P.partial, total) != hipSuccess) {
+            if (static_base) {
+                if (static_used + total > static_cap)
+                    return fail(ctx, GEMEL_EBUDGET,
+                                "activations and split-K partial sums exceed the static scratch of " +
+                                    std::to_string(static_cap) + " bytes");
+                P.partial = (float *)((char *)static_base + static_used);
+                static_used += (size_t)round_up((int64_t)total, 256);
+            } else if (alloc_device(ctx, (void **)&P.partial, total) != hipSuccess) {
                 P.partial = nullptr;
                 (void)hipGetLastError();
                 return fail(ctx, GEMEL_ENOMEM, "device allocation of the split-K buffer failed");
@@ -1435,14 +1454,25 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
         size_t total = 0;
         for (auto &L : P.launches) total += (size_t)L.ctr_n;
         if (total) {
-            if (alloc_device(ctx, (void **)&P.counters, total * sizeof(int32_t)) != hipSuccess) {
-                P.counters = nullptr;
-                (void)hipGetLastError();
-                return fail(ctx, GEMEL_ENOMEM, "device allocation of the split-K counters failed");
+            P.counters_n = total;
+            if (static_base) {
+                // cleared by every round: the static scratch is shared
+                if (static_used + total * sizeof(int32_t) > static_cap)
+                    return fail(ctx, GEMEL_EBUDGET,
+                                "activations, split-K partial sums and counters exceed the static scratch of " +
+                                    std::to_string(static_cap) + " bytes");
+                P.counters = (int32_t *)((char *)static_base + static_used);
+                static_used += (size_t)round_up((int64_t)(total * sizeof(int32_t)), 256);
+            } else {
+                if (alloc_device(ctx, (void **)&P.counters, total * sizeof(int32_t)) != hipSuccess) {
+                    P.counters = nullptr;
+                    (void)hipGetLastError();
+                    return fail(ctx, GEMEL_ENOMEM, "device allocation of the split-K counters failed");
+                }
+                const std::vector<int32_t> zeros(total, 0);
+                if (hipMemcpy(P.counters, zeros.data(), total * sizeof(int32_t), hipMemcpyHostToDevice) != hipSuccess)
+                    return fail(ctx, GEMEL_EDEVICE, "clearing the split-K counters failed");
             }
-            const std::vector<int32_t> zeros(total, 0);
-            if (hipMemcpy(P.counters, zeros.data(), total * sizeof(int32_t), hipMemcpyHostToDevice) != hipSuccess)
-                return fail(ctx, GEMEL_EDEVICE, "clearing the split-K counters failed");
             size_t off = 0;
             for (auto &L : P.launches) {
                 if (!L.ctr_n) continue;
@@ -1840,9 +1870,11 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         st = build_plan(ctx, ids, nfr, *P, true);
         ctx->opt.streams = saved;
         if (st) {
-            if (P->arena) (void)hipFree(P->arena);
-            if (P->partial) (void)hipFree(P->partial);
-            if (P->counters) (void)hipFree(P->counters);
+            if (!P->static_mem) {
+                if (P->arena) (void)hipFree(P->arena);
+                if (P->partial) (void)hipFree(P->partial);
+                if (P->counters) (void)hipFree(P->counters);
+            }
             for (auto ev : P->events)
                 if (ev) (void)hipEventDestroy(ev);
             if (P->ev_fork) (void)hipEventDestroy(P->ev_fork);
@@ -1973,6 +2005,87 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         ctx->tuning_left = P.best_mode >= 0 ? 0 : kNCand * (1 + kTimed) - P.tune_round;
     }
     return round_done();
+}
+
+// A round that allocates nothing (gemel_infer_noalloc): the weights must be
+// placed already; the plan's arena, split-K partial sums and counters lie in
+// the static scratch (one per device, shared by every call on it), and every
+// launch runs in plan order on the caller's stream (no worker stream, event,
+// graph or plan-time tuning).
+gemel_status run_noalloc(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, const void *const *frames,
+                         const int32_t *n_frames, void *const *outputs, hipStream_t stream) {
+    std::vector<std::pair<int, int>> act;  // (model id, caller index)
+    std::vector<int> caller_out_base((size_t)n_models);
+    for (int i = 0, ob = 0; i < n_models; ++i) {
+        caller_out_base[(size_t)i] = ob;
+        ob += (int)ctx->models[(size_t)model_ids[i]]->outputs.size();
+        if (n_frames[i] > 0) act.push_back({model_ids[i], i});
+    }
+    if (act.empty()) return GEMEL_OK;
+    if (!ctx->weights_ready)
+        return fail(ctx, GEMEL_ESTATE, "weights are not placed yet: run one gemel_infer round first");
+    if (ctx->opt.profile) return fail(ctx, GEMEL_ESTATE, "profiling is not available in allocation-free rounds");
+    std::sort(act.begin(), act.end());
+    std::vector<int> ids, nfr, key;
+    for (auto [id, ci] : act) {
+        ids.push_back(id);
+        nfr.push_back(n_frames[ci]);
+        key.push_back(id);
+        key.push_back(n_frames[ci]);
+    }
+    key.push_back(-1);   // allocation-free plans: their own cache entries
+    DeviceScope scope(ctx->device);
+    bool capturing = false;
+    if (stream) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        HIPCHK(hipStreamIsCapturing(stream, &cs), "hipStreamIsCapturing");
+        capturing = cs != hipStreamCaptureStatusNone;
+    }
+    void *base = nullptr;
+    HIPCHK(static_scratch(ctx->device, &base), "hipGetSymbolAddress (static scratch)");
+    auto it = ctx->plans.find(key);
+    if (it == ctx->plans.end()) {
+        auto P = std::make_unique<Plan>();
+        const int saved = ctx->opt.streams;
+        ctx->opt.streams = 1;
+        const gemel_status st = build_plan(ctx, ids, nfr, *P, false, base, GEMEL_STATIC_SCRATCH_BYTES);
+        ctx->opt.streams = saved;
+        if (st) {
+            for (auto ev : P->events)
+                if (ev) (void)hipEventDestroy(ev);
+            return st;
+        }
+        it = ctx->plans.emplace(key, std::move(P)).first;
+    }
+    Plan &P = *it->second;
+    if (!P.chunks.empty()) {
+        ctx->last_plan = &P;
+        return fail(ctx, GEMEL_ESTATE, "a round that streams weights cannot run without allocation");
+    }
+    ctx->last_plan = &P;
+    CallPtrs cp;
+    for (auto [id, ci] : act) {
+        cp.frames.push_back(frames[ci]);
+        const int no = (int)ctx->models[(size_t)id]->outputs.size();
+        for (int o = 0; o < no; ++o) cp.outputs.push_back(outputs[caller_out_base[(size_t)ci] + o]);
+    }
+    if (!capturing && ctx->round_seen && ctx->round_stream != stream)
+        HIPCHK(hipStreamWaitEvent(stream, ctx->ev_round_done, 0), "hipStreamWaitEvent");
+    Sink sk;
+    sk.stream = stream;
+    if (P.counters_n) {
+        const hipError_t e = launch_fill_u32((uint32_t *)P.counters, P.counters_n, 0u, sk);
+        if (e != hipSuccess) return fail(ctx, GEMEL_EDEVICE, std::string("clearing counters: ") + hipGetErrorString(e));
+    }
+    gemel_status st = enqueue_serial(ctx, P, cp, stream);
+    if (st) return st;
+    ctx->last_mode = MODE_SERIAL;
+    if (!capturing) {
+        HIPCHK(hipEventRecord(ctx->ev_round_done, stream), "hipEventRecord");
+        ctx->round_stream = stream;
+        ctx->round_seen = true;
+    }
+    return GEMEL_OK;
 }
 
 void profile_reset(gemel_ctx *ctx) {

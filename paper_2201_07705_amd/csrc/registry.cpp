@@ -400,7 +400,7 @@ gemel_status gemel_enumerate_groups(gemel_ctx *ctx, const int32_t *model_ids, in
     }
 }
 
-// Argument checks of gemel_infer.
+// Argument checks shared by gemel_infer and gemel_infer_noalloc.
 static gemel_status check_infer_args(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models,
                                      const void *const *frames, const int32_t *n_frames, void *const *outputs) {
     if (n_models <= 0 || !model_ids || !frames || !n_frames || !outputs)
@@ -434,6 +434,19 @@ gemel_status gemel_infer(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_mod
     if (st) return st;
     try {
         return run(ctx, model_ids, n_models, frames, n_frames, outputs, (hipStream_t)hip_stream);
+    } catch (const std::bad_alloc &) {
+        return fail(ctx, GEMEL_ENOMEM, "out of host memory");
+    }
+}
+
+gemel_status gemel_infer_noalloc(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models,
+                                 const void *const *frames, const int32_t *n_frames, void *const *outputs,
+                                 void *hip_stream) {
+    if (!ctx) return GEMEL_EINVAL;
+    const gemel_status st = check_infer_args(ctx, model_ids, n_models, frames, n_frames, outputs);
+    if (st) return st;
+    try {
+        return run_noalloc(ctx, model_ids, n_models, frames, n_frames, outputs, (hipStream_t)hip_stream);
     } catch (const std::bad_alloc &) {
         return fail(ctx, GEMEL_ENOMEM, "out of host memory");
     }

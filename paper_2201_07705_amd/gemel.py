@@ -46,7 +46,7 @@ KERNEL_FAMILIES = ("conv_mfma", "conv_f32", "splitk_reduce", "fc", "pack",
                    "pool", "route", "export", "conv_merged")
 
 EXPORTED = ("gemel_create", "gemel_register_model", "gemel_merge",
-            "gemel_enumerate_groups", "gemel_infer",
+            "gemel_enumerate_groups", "gemel_infer", "gemel_infer_noalloc",
             "gemel_model_outputs", "gemel_output_shape",
             "gemel_query", "gemel_set_option", "gemel_profile",
             "gemel_last_error", "gemel_destroy")
@@ -126,6 +126,7 @@ def _configure(L):
     L.gemel_infer.argtypes = [vp, ctypes.POINTER(i32), i32,
                               ctypes.POINTER(vp), ctypes.POINTER(i32),
                               ctypes.POINTER(vp), vp]
+    L.gemel_infer_noalloc.argtypes = L.gemel_infer.argtypes
     L.gemel_model_outputs.argtypes = [vp, i32, ctypes.POINTER(i32)]
     L.gemel_output_shape.argtypes = [vp, i32, i32, i32,
                                      ctypes.POINTER(i64)]
@@ -307,14 +308,15 @@ class Context:
                            ms=s.ms)
                 for name, s in zip(KERNEL_FAMILIES, st)}, rounds.value
 
-    def infer_raw(self, model_ids, frame_ptrs, n_frames, out_ptrs, stream):
+    def infer_raw(self, model_ids, frame_ptrs, n_frames, out_ptrs, stream,
+                  noalloc=False):
         n = len(model_ids)
         ids = (ctypes.c_int32 * n)(*model_ids)
         fp = (ctypes.c_void_p * n)(*frame_ptrs)
         nf = (ctypes.c_int32 * n)(*n_frames)
         op = (ctypes.c_void_p * max(len(out_ptrs), 1))(*out_ptrs)
-        return self._lib.gemel_infer(self._h, ids, n, fp, nf, op,
-                                     ctypes.c_void_p(stream))
+        fn = self._lib.gemel_infer_noalloc if noalloc else self._lib.gemel_infer
+        return fn(self._h, ids, n, fp, nf, op, ctypes.c_void_p(stream))
 
     def close(self):
         if self._h:
@@ -340,9 +342,11 @@ class Context:
                          for i in range(self.n_outputs(mid))])
         return outs
 
-    def infer(self, model_ids, frames, stream=None, outputs=None):
+    def infer(self, model_ids, frames, stream=None, outputs=None,
+              noalloc=False):
         """frames: list of float32 NCHW cuda tensors, one per model id.
-        Returns (and fills) per-model lists of float32 output tensors."""
+        Returns (and fills) per-model lists of float32 output tensors.
+        noalloc: call gemel_infer_noalloc (outputs must be given)."""
         import torch
         n_frames = [int(f.shape[0]) for f in frames]
         for f in frames:
@@ -354,5 +358,6 @@ class Context:
         out_ptrs = [t.data_ptr() for o in outputs for t in o]
         s = stream if stream is not None else torch.cuda.current_stream()
         self._check(self.infer_raw(model_ids, [f.data_ptr() for f in frames],
-                                   n_frames, out_ptrs, s.cuda_stream))
+                                   n_frames, out_ptrs, s.cuda_stream,
+                                   noalloc=noalloc))
         return outputs

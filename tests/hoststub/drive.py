@@ -106,7 +106,8 @@ def main():
                 L.hoststub_set_capturing(st)
             before = L.hoststub_launches()
             a_before = L.hoststub_allocs()
-            status.append(ctx.infer_raw(ids, frames, nfr, outs, st))
+            status.append(ctx.infer_raw(ids, frames, nfr, outs, st,
+                                        noalloc=r in scen.get("noalloc", [])))
             launches.append(L.hoststub_launches() - before)
             round_allocs.append(L.hoststub_allocs() - a_before)
             if cap:

@@ -447,6 +447,23 @@ hipError_t launch_conv_bf16(const ConvArgs &a, int tile, const Sink &sk) {
 }
 hipError_t launch_conv_f32(const ConvArgs &a, const Sink &sk) { return conv_common(a, -1, 4, "conv_f32", false, sk); }
 
+// The static scratch: one host block registered as a live allocation
+// (not counted as an allocation of the library).
+static void *g_static = nullptr;
+hipError_t static_scratch(int, void **ptr) {
+    if (!g_static) {
+        g_static = std::malloc(GEMEL_STATIC_SCRATCH_BYTES);
+        live[(uintptr_t)g_static] = GEMEL_STATIC_SCRATCH_BYTES;
+    }
+    *ptr = g_static;
+    return hipSuccess;
+}
+hipError_t launch_fill_u32(uint32_t *p, size_t n, uint32_t, const Sink &sk) {
+    ++launches;
+    begin_node(sk, "fill_u32");
+    return verdict(chk(p, (long long)n * 4, "fill", "fill_u32", true));
+}
+
 hipError_t launch_conv_reduce(const ReduceArgs &a, bool bf16, const Sink &sk) {
     ++launches;
     begin_node(sk, "conv_reduce");

@@ -224,3 +224,39 @@ def test_allocation_failures_report_enomem_and_leak_nothing(hostlib, name,
         seen_enomem += r["status"][0] == ENOMEM
     assert seen_enomem >= 3
 
+
+EBUDGET = -5
+
+
+@pytest.mark.parametrize("name,kw,opts", [
+    ("resnet18x2", {"res": 64, "frames": 2}, {}),
+    ("yolov3x3", {"res": 96, "frames": 2}, {}),
+    ("r50x2_vgg16x2", {"res": 64, "frames": 2},
+     {"OPT_CONV_SPLITS": 3, "OPT_SPLITK_FUSED": 2}),
+])
+def test_noalloc_rounds_allocate_nothing_and_use_one_stream(hostlib, name, kw,
+                                                           opts):
+    """gemel_infer_noalloc after a normal round: no device allocation, every
+    access inside the static scratch or other live buffers, no hazard with
+    the normal rounds before and after it, and (under capture) only the
+    caller's stream, with no synchronisation."""
+    # the captured round comes last: captured work runs only when its graph
+    # is replayed, which the caller orders against other rounds
+    out = drive(hostlib, name, kw, opts, 5,
+                {"noalloc": [1, 2, 4], "capture": [4], "streams": [0, 0, 1, 1, 1]})
+    assert out["status"] == [0] * 5, out["error"]
+    assert out["hazards"] == 0 and out["violations"] == 0, out["last"]
+    assert out["round_allocs"][1] == out["round_allocs"][2] == 0
+    assert out["round_allocs"][4] == 0
+
+
+def test_noalloc_refuses_unplaced_weights_and_oversized_rounds(hostlib):
+    out = drive(hostlib, "resnet18x2", {"res": 64, "frames": 2}, {}, 2,
+                {"noalloc": [0, 1]})
+    assert out["status"] == [ESTATE, ESTATE], out["error"]
+    assert out["round_launches"] == [0, 0]
+    # full-size VGG-16 activations exceed the static scratch
+    out = drive(hostlib, "r50x2_vgg16x2", {}, {}, 2, {"noalloc": [1]})
+    assert out["status"] == [0, EBUDGET], out["error"]
+    assert "static scratch" in out["error"]
+    assert out["round_launches"][1] == 0 and out["round_allocs"][1] == 0
