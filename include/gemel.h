@@ -287,6 +287,29 @@ gemel_status gemel_infer_noalloc(gemel_ctx *ctx, const int32_t *model_ids,
                                  const int32_t *n_frames,
                                  void *const *outputs, void *hip_stream);
 
+/*
+ * Models of the round that will follow the next gemel_infer call, for the
+ * weight cache (GEMEL_OPT_SWAP_CACHE): their shared layers are not evicted
+ * while that call loads its own (Appendix A.4: the scheduler keeps the
+ * shared layers needed by the models next in line). n_models == 0 clears
+ * the hint. Errors: EINVAL.
+ */
+gemel_status gemel_set_next_round(gemel_ctx *ctx, const int32_t *model_ids,
+                                  int32_t n_models);
+
+/*
+ * Sharing-aware load order of a round-robin cycle over `model_ids`
+ * (Section 5.4: models that share the most layers are placed next to one
+ * another, so each swap loads fewer bytes): start with the model whose
+ * stored parameter copies take the most bytes, then repeatedly place the
+ * remaining model sharing the most bytes of copies with one end of the
+ * order so far at that end (ties: more bytes, lower id, the back end).
+ * Bytes are kernel-layout weights rounded up to 256 per copy, under the
+ * current sharing map. `order` receives n_models ids. Errors: EINVAL.
+ */
+gemel_status gemel_load_order(gemel_ctx *ctx, const int32_t *model_ids,
+                              int32_t n_models, int32_t *order);
+
 /* Number of output layers of a model. Errors: EINVAL. */
 gemel_status gemel_model_outputs(gemel_ctx *ctx, int32_t model_id,
                                  int32_t *n_outputs);
@@ -320,9 +343,16 @@ enum {
                                    the caller's stream alone (a round
                                    enqueued while that stream was being
                                    captured)                             */
-    GEMEL_Q_ROUND_TUNING = 11   /* rounds the last plan's round-mode tuner
+    GEMEL_Q_ROUND_TUNING = 11,  /* rounds the last plan's round-mode tuner
                                    (GEMEL_OPT_AUTOTUNE) still runs before
                                    its choice is fixed; 0 = settled      */
+    GEMEL_Q_ROUND_LOADED_BYTES = 12,  /* weight cache: bytes the last round
+                                   loaded into the cache                 */
+    GEMEL_Q_ROUND_EVICTED_BYTES = 13, /* weight cache: bytes it evicted   */
+    GEMEL_Q_CACHED_BYTES = 14,  /* weight cache: bytes cached after it    */
+    GEMEL_Q_CACHE_CAPACITY = 15 /* weight cache: its capacity (the weight
+                                   budget minus the resident scale/shift
+                                   vectors), 0 without the cache         */
 };
 
 /* Read a counter. Errors: EINVAL (unknown key, null val). */
@@ -476,7 +506,7 @@ enum {
                                     call reports ENOMEM, or, for the scratch
                                     of plan-time tuning, skips that tuning);
                                     0 = off                                */
-    GEMEL_OPT_GROUP_UNMERGED = 19 /* 1 (default): an unmerged bf16 conv that
+    GEMEL_OPT_GROUP_UNMERGED = 19,/* 1 (default): an unmerged bf16 conv that
                                     appears with the same shape and epilogue
                                     in several active models (their k-th such
                                     layer each, e.g. per-model heads of one
@@ -488,6 +518,38 @@ enum {
                                     Results are those of separate launches
                                     of the same tile configuration. 0: one
                                     launch per model                       */
+    GEMEL_OPT_SWAP_CACHE = 20    /* with a weight budget: 1 = time-shared
+                                    rounds over subsets of the models keep
+                                    a weight cache across rounds (Section
+                                    5.4: loading a model brings in only its
+                                    layers not already in GPU memory;
+                                    Appendix A.4: layers shared by the
+                                    models of the current or next round are
+                                    never evicted). The scale/shift vectors
+                                    stay resident and the rest of the
+                                    budget is the cache; every weight blob
+                                    waits in pinned host memory. A round
+                                    loads the blobs its models need that
+                                    are not cached, in first-use order
+                                    (models by id, then layers), each
+                                    first-fit at the lowest 256-byte-aligned
+                                    offset with room, after evicting, while
+                                    none has room, cached blobs that are
+                                    not pinned: unshared before shared,
+                                    larger before smaller, then the blob
+                                    first used earlier (models by id, then
+                                    layers). Pinned: the round's blobs and the
+                                    shared blobs of the models named by
+                                    gemel_set_next_round. Copies run on a
+                                    side stream after the previous round's
+                                    work and each launch waits only for its
+                                    own weights' copy. A round whose pinned
+                                    blobs exceed the cache returns EBUDGET
+                                    and changes nothing. Rounds are not
+                                    graphed or captured. 0 (default): the
+                                    budget keeps the largest blobs (merged
+                                    ones first) resident and streams the
+                                    rest through staging slots every round */
 };
 
 /* Set an option; takes effect at the next gemel_infer. Errors: EINVAL. */

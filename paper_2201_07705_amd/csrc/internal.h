@@ -34,6 +34,12 @@ struct Blob {
     float *aff_dev = nullptr;        // scale[rows] then shift[rows], resident
     uint8_t *w_pinned = nullptr;     // pinned host copy of a streamed blob
     int users = 0;                   // registered layers using this copy
+    // weight cache (GEMEL_OPT_SWAP_CACHE): number in placement order, offset
+    // in the cache (-1: not cached), event recorded after its last load
+    int index = -1;
+    int64_t cache_off = -1;
+    hipEvent_t ev_loaded = nullptr;
+    int loaded_round = -1;           // round of the last load
 };
 
 struct Layer {
@@ -94,6 +100,9 @@ struct Launch {
     std::vector<Patch> patches;
     // weight streaming: >= 0 when the weights come from a staging slot
     int chunk = -1;
+    // weight cache: the blob(s) whose current cache address the launch
+    // reads (one per segment for a grouped launch, else one)
+    std::vector<Blob *> wblobs;
     int ctr_n = 0;  // arrival counters of a fused split-K launch
     // concurrency: stream index, plan events waited for before the launch,
     // plan event recorded after it (-1 = none)
@@ -202,6 +211,7 @@ struct Options {
     int split_merged = 0;
     int paired_acts = 0;      // unmerged conv chains keep bf16 (hi, lo) pairs
     int group_unmerged = 1;   // same-shape unmerged convs of several models: one launch
+    int swap_cache = 0;       // weights cached across rounds (with a budget)
 };
 
 }  // namespace gemel
@@ -239,6 +249,15 @@ struct gemel_ctx {
     hipStream_t round_stream = nullptr;
     bool round_seen = false;
     hipEvent_t ev_side_join = nullptr;   // side stream -> caller after a failed round
+    // weight cache across rounds (GEMEL_OPT_SWAP_CACHE with a budget): the
+    // cache's device bytes, the models of the next round (their shared
+    // blobs stay cached), and the last round's load statistics
+    bool cache_mode = false;
+    char *cache_base = nullptr;
+    size_t cache_cap = 0;
+    int cache_round = 0;
+    std::vector<int> next_models;
+    int64_t round_loaded = 0, round_evicted = 0;
     std::map<std::vector<int>, std::unique_ptr<gemel::Plan>> plans;
     gemel::Plan *last_plan = nullptr;
     gemel::Profile prof;
@@ -251,6 +270,8 @@ struct gemel_ctx {
     size_t tune_partial_bytes = 0;
     void *tune_ctr = nullptr;
     size_t tune_ctr_bytes = 0;
+    void *tune_w = nullptr;   // stand-in weights while the weight cache is on
+    size_t tune_w_bytes = 0;
 };
 
 namespace gemel {

@@ -103,10 +103,19 @@ gemel_status ensure_device(gemel_ctx *ctx) {
 void free_placement(gemel_ctx *ctx) {
     for (auto &b : ctx->placed) {
         if (b->w_pinned) (void)hipHostFree(b->w_pinned);
+        if (b->ev_loaded) (void)hipEventDestroy(b->ev_loaded);
         b->w_pinned = nullptr;
         b->w_dev = nullptr;
         b->aff_dev = nullptr;
+        b->ev_loaded = nullptr;
+        b->index = -1;
+        b->cache_off = -1;
+        b->loaded_round = -1;
     }
+    ctx->cache_mode = false;
+    ctx->cache_base = nullptr;
+    ctx->cache_cap = 0;
+    ctx->cache_round = 0;
     ctx->placed.clear();
     if (ctx->wpool) (void)hipFree(ctx->wpool);
     if (ctx->staging) (void)hipFree(ctx->staging);
@@ -161,8 +170,9 @@ void release_device(gemel_ctx *ctx) {
     }
     if (ctx->tune_partial) (void)hipFree(ctx->tune_partial);
     if (ctx->tune_ctr) (void)hipFree(ctx->tune_ctr);
-    ctx->tune_partial = ctx->tune_ctr = nullptr;
-    ctx->tune_partial_bytes = ctx->tune_ctr_bytes = 0;
+    if (ctx->tune_w) (void)hipFree(ctx->tune_w);
+    ctx->tune_partial = ctx->tune_ctr = ctx->tune_w = nullptr;
+    ctx->tune_partial_bytes = ctx->tune_ctr_bytes = ctx->tune_w_bytes = 0;
     if (ctx->side) (void)hipStreamDestroy(ctx->side);
     ctx->side = nullptr;
     for (hipEvent_t *ev : {&ctx->ev_round_done, &ctx->ev_side_join}) {
@@ -301,7 +311,17 @@ gemel_status materialise(gemel_ctx *ctx) {
     size_t staging_bytes = 0;
     int slots = 0;
     int64_t slot_bytes = 0;
-    if (ctx->budget && w_total + aff_total > ctx->budget) {
+    // weight cache: scale/shift resident, every weight blob in pinned host
+    // memory and loaded into the cache (the rest of the budget) when a
+    // round needs it
+    const bool cache = ctx->opt.swap_cache && ctx->budget;
+    size_t cache_cap = 0;
+    if (cache) {
+        if (aff_total >= ctx->budget)
+            return fail(ctx, GEMEL_EBUDGET, "weight budget smaller than the scale/shift vectors");
+        cache_cap = (size_t)(ctx->budget - aff_total) / 256 * 256;
+        std::fill(resident.begin(), resident.end(), 0);
+    } else if (ctx->budget && w_total + aff_total > ctx->budget) {
         slots = ctx->opt.slots;
         slot_bytes = std::max<int64_t>(ctx->opt.slot_bytes, round_up((int64_t)max_final, 256));
         staging_bytes = (size_t)slots * (size_t)slot_bytes;
@@ -328,7 +348,7 @@ gemel_status materialise(gemel_ctx *ctx) {
                 return fail(ctx, GEMEL_EBUDGET, "a weight row block does not fit one staging slot");
     }
 
-    size_t pool = aff_total + GEMEL_ZERO_PAGE_BYTES;  // + zero page
+    size_t pool = aff_total + GEMEL_ZERO_PAGE_BYTES + cache_cap;  // + zero page
     for (size_t i = 0; i < blobs.size(); ++i)
         if (resident[i]) pool += (size_t)round_up((int64_t)blobs[i]->w_bytes(), 256);
     if (alloc_device(ctx, &ctx->wpool, pool) != hipSuccess) {
@@ -363,10 +383,21 @@ gemel_status materialise(gemel_ctx *ctx) {
             if (e == hipSuccess) std::memcpy(b.w_pinned, b.w.data(), b.w_bytes());
             else b.w_pinned = nullptr;
         }
+        if (e == hipSuccess && cache) {
+            b.index = (int)i;
+            e = hipEventCreateWithFlags(&b.ev_loaded, hipEventDisableTiming);
+            if (e != hipSuccess) b.ev_loaded = nullptr;
+        }
         if (e != hipSuccess) {
             free_placement(ctx);
             return fail(ctx, GEMEL_ENOMEM, std::string("placing weights: ") + hipGetErrorString(e));
         }
+    }
+    if (cache) {
+        ctx->cache_mode = true;
+        ctx->cache_base = (char *)ctx->wpool + off;
+        ctx->cache_cap = cache_cap;
+        ctx->cache_round = 0;
     }
     if (slots) {
         if (alloc_device(ctx, &ctx->staging, staging_bytes) != hipSuccess) {
@@ -591,6 +622,22 @@ bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int
         }
         ctx->tune_partial_bytes = pbytes;
     }
+    // cached weights may still be in flight on the copy stream, or not be
+    // cached at all: time the candidates over a zeroed buffer of the same
+    // size instead (the kernels' timing does not depend on the values)
+    const size_t wbytes = ctx->cache_mode ? (size_t)a0.N * a0.K * (bf16 ? 2 : 4) : 0;
+    if (wbytes > ctx->tune_w_bytes) {
+        if (ctx->tune_w) (void)hipFree(ctx->tune_w);
+        ctx->tune_w = nullptr;
+        ctx->tune_w_bytes = 0;
+        if (alloc_device(ctx, &ctx->tune_w, wbytes) != hipSuccess) {
+            (void)hipGetLastError();
+            return false;
+        }
+        const std::vector<char> zeros(wbytes, 0);
+        if (hipMemcpy(ctx->tune_w, zeros.data(), wbytes, hipMemcpyHostToDevice) != hipSuccess) return false;
+        ctx->tune_w_bytes = wbytes;
+    }
     if (cbytes > ctx->tune_ctr_bytes) {
         if (ctx->tune_ctr) (void)hipFree(ctx->tune_ctr);
         ctx->tune_ctr = nullptr;
@@ -608,6 +655,11 @@ bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int
     // launch of candidate i
     auto once = [&](size_t i) {
         ConvArgs a = a0;
+        if (wbytes) {
+            a.w = ctx->tune_w;
+            if (a.grouped)
+                for (int g = 0; g < a.nseg; ++g) a.seg[g].w = ctx->tune_w;
+        }
         int sp = c[i].splits, kp = 0;
         conv_split_depth(a.K, sp, kp);
         a.k_splits = sp;
@@ -736,7 +788,8 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
     // kernel's input conditions, resident weights, no mixed sizes
     auto groupable = [&](int s, int l) {
         const Layer &L = layer(s, l);
-        return ctx->opt.group_unmerged && bf16 && L.op == GEMEL_OP_CONV && L.group < 0 && L.exec && L.exec->w_dev &&
+        return ctx->opt.group_unmerged && bf16 && L.op == GEMEL_OP_CONV && L.group < 0 && L.exec &&
+               (L.exec->w_dev || ctx->cache_mode) &&
                L.in_phys % 32 == 0 && (int64_t)L.in_phys * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES &&
                (forced < 0 || (tile_is_dma(forced) && (tile_dma_depth(forced) == 32 || L.in_phys % 64 == 0)));
     };
@@ -1145,7 +1198,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
             const bool fc_f32 = L0.op == GEMEL_OP_FC && !bf16;
             // weight chunks: a resident blob is one chunk with no copy
             std::vector<std::pair<int64_t, int64_t>> rows;  // (row0, nrows)
-            if (blob->w_dev) {
+            if (blob->w_dev || ctx->cache_mode) {   // resident, or cached when the round runs
                 rows.push_back({0, blob->rows});
             } else {
                 const int64_t row_bytes = blob->k * (int64_t)blob->elem;
@@ -1173,7 +1226,10 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 Lc.bytes = co * kdepth * esz * (grouped ? members : 1) + in_elems * esz +
                            (double)M * co * (direct ? 4.0 : esz) / (pooled ? 4.0 : 1.0) +
                            (L0.res >= 0 ? (double)M * co * esz : 0.0);
-                if (!blob->w_dev) {
+                if (ctx->cache_mode) {
+                    // the weights' cache address is set when the round runs
+                    if (!grouped) Lc.wblobs.push_back(blob);
+                } else if (!blob->w_dev) {
                     Lc.chunk = (int)P.chunks.size();
                     P.chunks.push_back(Chunk{blob, row0, nrows});
                     P.streamed_bytes += P.chunks.back().bytes();
@@ -1256,8 +1312,9 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     sg.res = L.res >= 0 ? (const void *)((char *)tptr(s, L.res) + row0 * esz) : nullptr;
                     const int wl = pooled ? pool_of[(size_t)s][(size_t)l] : l;   // the tensor written
                     sg.out = direct ? nullptr : (void *)((char *)tptr(s, wl) + row0 * esz);
-                    const Blob *mb = L.exec.get();   // the member's own parameters (grouped)
+                    Blob *mb = L.exec.get();   // the member's own parameters (grouped)
                     sg.w = grouped ? mb->w_dev : nullptr;
+                    if (grouped && ctx->cache_mode) Lc.wblobs.push_back(mb);
                     sg.scale = mb->aff_dev + row0;
                     sg.shift = mb->aff_dev + mb->rows + row0;
                     sg.f_start = f;
@@ -1295,7 +1352,7 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                         // measured choice where nothing is forced and the
                         // launch's tensors all exist at plan time
                         if (ctx->opt.tune && can_tune && ctx->opt.conv_tile < 0 && (ctx->opt.conv_splits <= 0 || pooled) &&
-                            !direct && blob->w_dev)
+                            !direct && (blob->w_dev || ctx->cache_mode))
                             tune_conv(ctx, a, dma_depth, bf16, Lc.tile, a.k_splits, a.k_per_split);
                     }
                     if (tile_is_dma(Lc.tile) && !conv_dma_supported(a, Lc.tile)) {
@@ -1592,6 +1649,102 @@ static gemel_status enqueue_serial(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, 
 
 static gemel_status enqueue_body(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStream_t st);
 
+// Weight cache (GEMEL_OPT_SWAP_CACHE): bring every blob the round's models
+// need into the cache before their launches. Needed blobs are taken in
+// first-use order (models by id, then layers); one that is not cached is
+// placed first-fit (lowest offset with a large enough free run, 256-byte
+// aligned) after evicting, while no run fits, cached blobs that are not
+// pinned, unshared before shared, larger before smaller, lower number
+// first. Pinned: the round's blobs and the shared blobs of the models of
+// the next round (gemel_set_next_round). The whole decision is made before
+// anything changes, so a round whose pinned blobs do not fit changes
+// nothing. Copies run on the side stream after the previous round's work
+// (their regions may still be read by it); each loaded blob records an
+// event its launches wait for.
+static gemel_status cache_round(gemel_ctx *ctx, Plan &P, hipStream_t st) {
+    ctx->cache_round++;
+    std::vector<Blob *> needed;
+    std::set<Blob *> in_needed;
+    for (int id : P.model_ids)
+        for (auto &l : ctx->models[(size_t)id]->layers)
+            if (l.exec && in_needed.insert(l.exec.get()).second) needed.push_back(l.exec.get());
+    std::set<Blob *> pinned(in_needed);
+    for (int id : ctx->next_models)
+        if (id >= 0 && id < (int)ctx->models.size())
+            for (auto &l : ctx->models[(size_t)id]->layers)
+                if (l.exec && l.exec->users > 1) pinned.insert(l.exec.get());
+    auto sz = [](const Blob *b) { return (int64_t)round_up((int64_t)b->w_bytes(), 256); };
+    std::map<Blob *, int64_t> at;   // the cache after this round
+    for (auto &b : ctx->placed)
+        if (b->cache_off >= 0) at[b.get()] = b->cache_off;
+    std::vector<Blob *> loaded, evicted;
+    for (Blob *b : needed) {
+        if (at.count(b)) continue;
+        const int64_t size = sz(b);
+        int64_t off = -1;
+        while (true) {
+            std::vector<std::pair<int64_t, int64_t>> taken;
+            for (auto &kv : at) taken.push_back({kv.second, kv.second + sz(kv.first)});
+            std::sort(taken.begin(), taken.end());
+            int64_t pos = 0;
+            off = -1;
+            for (auto &t : taken) {
+                if (t.first - pos >= size) {
+                    off = pos;
+                    break;
+                }
+                pos = std::max(pos, t.second);
+            }
+            if (off < 0 && (int64_t)ctx->cache_cap - pos >= size) off = pos;
+            if (off >= 0) break;
+            Blob *v = nullptr;
+            for (auto &kv : at) {
+                Blob *c = kv.first;
+                if (pinned.count(c)) continue;
+                auto key = [&](const Blob *x) { return std::make_tuple(x->users > 1, -sz(x), x->index); };
+                if (!v || key(c) < key(v)) v = c;
+            }
+            if (!v)
+                return fail(ctx, GEMEL_EBUDGET,
+                            "the weights this round pins do not fit the weight cache of " +
+                                std::to_string(ctx->cache_cap) + " bytes");
+            at.erase(v);
+            evicted.push_back(v);
+        }
+        at[b] = off;
+        loaded.push_back(b);
+    }
+    // commit
+    int64_t lb = 0, eb = 0;
+    for (Blob *v : evicted) {
+        v->cache_off = -1;
+        v->w_dev = nullptr;
+        eb += sz(v);
+    }
+    if (!loaded.empty() && ctx->round_seen)
+        HIPCHK(hipStreamWaitEvent(ctx->side, ctx->ev_round_done, 0), "hipStreamWaitEvent");
+    for (Blob *b : loaded) {
+        b->cache_off = at[b];
+        b->w_dev = ctx->cache_base + b->cache_off;
+        lb += sz(b);
+        ctx->copies_issued++;
+        if (ctx->opt.fail_copy_at && ctx->copies_issued == ctx->opt.fail_copy_at) {
+            ctx->opt.fail_copy_at = 0;
+            b->cache_off = -1;   // its copy never ran: not cached
+            b->w_dev = nullptr;
+            return fail(ctx, GEMEL_EDEVICE, "injected failure of a weight copy");
+        }
+        HIPCHK(hipMemcpyAsync(b->w_dev, b->w_pinned, b->w_bytes(), hipMemcpyHostToDevice, ctx->side),
+               "hipMemcpyAsync (weight cache)");
+        HIPCHK(hipEventRecord(b->ev_loaded, ctx->side), "hipEventRecord");
+        b->loaded_round = ctx->cache_round;
+    }
+    ctx->round_loaded = lb;
+    ctx->round_evicted = eb;
+    (void)st;
+    return GEMEL_OK;
+}
+
 static gemel_status enqueue(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStream_t st) {
     const gemel_status s = enqueue_body(ctx, P, cp, st);
     if (s) join_partial_round(ctx, P, st);
@@ -1599,6 +1752,10 @@ static gemel_status enqueue(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStre
 }
 
 static gemel_status enqueue_body(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStream_t st) {
+    if (ctx->cache_mode) {
+        const gemel_status s = cache_round(ctx, P, st);
+        if (s) return s;
+    }
     const int nslots = ctx->staging_slots;
     const int nch = (int)P.chunks.size();
     int next_copy = 0;
@@ -1635,6 +1792,16 @@ static gemel_status enqueue_body(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hi
         const hipStream_t ls = streams[L.stream];
         for (int ev : L.waits) HIPCHK(hipStreamWaitEvent(ls, P.events[(size_t)ev], 0), "hipStreamWaitEvent");
         void *wptr = nullptr;
+        if (!L.wblobs.empty()) {
+            // cached weights: wait for this round's copies of them, then
+            // read them at their current cache addresses
+            for (Blob *b : L.wblobs)
+                if (b->loaded_round == ctx->cache_round)
+                    HIPCHK(hipStreamWaitEvent(ls, b->ev_loaded, 0), "hipStreamWaitEvent");
+            if (L.conv.grouped)
+                for (size_t i = 0; i < L.wblobs.size() && (int)i < L.conv.nseg; ++i) L.conv.seg[i].w = L.wblobs[i]->w_dev;
+            wptr = L.wblobs[0]->w_dev;
+        }
         if (L.chunk >= 0) {
             gemel_status s = issue_copies(L.chunk + nslots - 1);
             if (s) return s;
@@ -1893,7 +2060,8 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         for (int o = 0; o < no; ++o) cp.outputs.push_back(outputs[caller_out_base[(size_t)ci] + o]);
     }
     if (capturing) {
-        if (!P.chunks.empty()) return fail(ctx, GEMEL_ESTATE, "a round that streams weights cannot be captured");
+        if (!P.chunks.empty() || ctx->cache_mode)
+            return fail(ctx, GEMEL_ESTATE, "a round that streams or caches weights cannot be captured");
         if (ctx->opt.profile) return fail(ctx, GEMEL_ESTATE, "a profiled round cannot be captured");
         ctx->last_mode = MODE_SERIAL;
         return enqueue_serial(ctx, P, cp, stream);
@@ -1909,7 +2077,7 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         ctx->round_seen = true;
         return GEMEL_OK;
     };
-    const bool graphable = will_graph && P.chunks.empty();
+    const bool graphable = will_graph && P.chunks.empty() && !ctx->cache_mode;
     ctx->tuning_left = 0;
     if (!graphable) {
         ctx->last_mode = MODE_EAGER;
@@ -2058,9 +2226,9 @@ gemel_status run_noalloc(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_mod
         it = ctx->plans.emplace(key, std::move(P)).first;
     }
     Plan &P = *it->second;
-    if (!P.chunks.empty()) {
+    if (!P.chunks.empty() || ctx->cache_mode) {
         ctx->last_plan = &P;
-        return fail(ctx, GEMEL_ESTATE, "a round that streams weights cannot run without allocation");
+        return fail(ctx, GEMEL_ESTATE, "a round that streams or caches weights cannot run without allocation");
     }
     ctx->last_plan = &P;
     CallPtrs cp;

@@ -10,6 +10,7 @@
 #include <map>
 #include <new>
 #include <set>
+#include <tuple>
 
 #include "internal.h"
 
@@ -452,6 +453,82 @@ gemel_status gemel_infer_noalloc(gemel_ctx *ctx, const int32_t *model_ids, int32
     }
 }
 
+gemel_status gemel_set_next_round(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models) {
+    if (!ctx) return GEMEL_EINVAL;
+    if (n_models < 0 || (n_models > 0 && !model_ids)) return fail(ctx, GEMEL_EINVAL, "bad model list");
+    std::vector<int> next;
+    for (int i = 0; i < n_models; ++i) {
+        if (model_ids[i] < 0 || model_ids[i] >= (int)ctx->models.size())
+            return fail(ctx, GEMEL_EINVAL, "unknown model id " + std::to_string(model_ids[i]));
+        next.push_back(model_ids[i]);
+    }
+    ctx->next_models = next;
+    return GEMEL_OK;
+}
+
+// Bytes of the stored parameter copies two models both use.
+static int64_t shared_param_bytes(const Model &a, const Model &b) {
+    std::set<const Blob *> in_a;
+    for (auto &l : a.layers)
+        if (l.eff) in_a.insert(l.eff.get());
+    std::set<const Blob *> seen;
+    int64_t s = 0;
+    for (auto &l : b.layers)
+        if (l.eff && in_a.count(l.eff.get()) && seen.insert(l.eff.get()).second)
+            s += round_up((int64_t)l.eff->w_bytes(), 256);
+    return s;
+}
+
+gemel_status gemel_load_order(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, int32_t *order) {
+    if (!ctx) return GEMEL_EINVAL;
+    if (n_models <= 0 || !model_ids || !order) return fail(ctx, GEMEL_EINVAL, "null argument or no models");
+    std::set<int> ids;
+    for (int i = 0; i < n_models; ++i) {
+        if (model_ids[i] < 0 || model_ids[i] >= (int)ctx->models.size())
+            return fail(ctx, GEMEL_EINVAL, "unknown model id " + std::to_string(model_ids[i]));
+        if (!ids.insert(model_ids[i]).second) return fail(ctx, GEMEL_EINVAL, "model id listed twice");
+    }
+    std::map<int, int64_t> total;
+    for (int id : ids) {
+        std::set<const Blob *> seen;
+        int64_t t = 0;
+        for (auto &l : ctx->models[(size_t)id]->layers)
+            if (l.eff && seen.insert(l.eff.get()).second) t += round_up((int64_t)l.eff->w_bytes(), 256);
+        total[id] = t;
+    }
+    std::vector<int> left(ids.begin(), ids.end()), seq;
+    // the model of the most bytes first (lower id on ties)
+    int first = left[0];
+    for (int m : left)
+        if (total[m] > total[first]) first = m;
+    seq.push_back(first);
+    left.erase(std::find(left.begin(), left.end(), first));
+    while (!left.empty()) {
+        // the remaining model that shares the most bytes with either end,
+        // placed at that end (ties: more bytes, lower id, the back end)
+        std::tuple<int64_t, int64_t, int, int> best{-1, -1, 0, 0};
+        bool have = false;
+        for (int m : left)
+            for (int end : {0, 1}) {
+                const int e = end == 0 ? seq.back() : seq.front();
+                const auto key = std::make_tuple(
+                    shared_param_bytes(*ctx->models[(size_t)e], *ctx->models[(size_t)m]), total[m], -m, -end);
+                if (!have || key > best) {
+                    best = key;
+                    have = true;
+                }
+            }
+        const int m = -std::get<2>(best);
+        if (std::get<3>(best) == 0)
+            seq.push_back(m);
+        else
+            seq.insert(seq.begin(), m);
+        left.erase(std::find(left.begin(), left.end(), m));
+    }
+    for (int i = 0; i < n_models; ++i) order[i] = seq[(size_t)i];
+    return GEMEL_OK;
+}
+
 gemel_status gemel_model_outputs(gemel_ctx *ctx, int32_t model_id, int32_t *n_outputs) {
     if (!ctx) return GEMEL_EINVAL;
     if (!n_outputs || model_id < 0 || model_id >= (int)ctx->models.size())
@@ -491,6 +568,16 @@ gemel_status gemel_query(gemel_ctx *ctx, int32_t key, int64_t *val) {
     case GEMEL_Q_STREAMS: *val = ctx->opt.streams; break;
     case GEMEL_Q_ROUND_MODE: *val = ctx->last_mode; break;
     case GEMEL_Q_ROUND_TUNING: *val = ctx->tuning_left; break;
+    case GEMEL_Q_ROUND_LOADED_BYTES: *val = ctx->round_loaded; break;
+    case GEMEL_Q_ROUND_EVICTED_BYTES: *val = ctx->round_evicted; break;
+    case GEMEL_Q_CACHED_BYTES: {
+        int64_t c = 0;
+        for (auto &b : ctx->placed)
+            if (b->cache_off >= 0) c += round_up((int64_t)b->w_bytes(), 256);
+        *val = c;
+        break;
+    }
+    case GEMEL_Q_CACHE_CAPACITY: *val = (int64_t)ctx->cache_cap; break;
     default: return fail(ctx, GEMEL_EINVAL, "unknown query key");
     }
     return GEMEL_OK;
@@ -518,6 +605,14 @@ gemel_status gemel_set_option(gemel_ctx *ctx, int32_t key, int64_t value) {
     case GEMEL_OPT_FAIL_COPY_AT:
         if (value < 0) return fail(ctx, GEMEL_EINVAL, "fail_copy_at must be >= 0");
         ctx->opt.fail_copy_at = value ? ctx->copies_issued + value : 0;
+        break;
+    case GEMEL_OPT_SWAP_CACHE:
+        if (value != 0 && value != 1) return fail(ctx, GEMEL_EINVAL, "swap_cache is 0 or 1");
+        if (ctx->opt.swap_cache != (int)value) {
+            ctx->opt.swap_cache = (int)value;
+            ctx->weights_ready = false;
+            drop_plans(ctx);
+        }
         break;
     case GEMEL_OPT_GROUP_UNMERGED:
         if (value != 0 && value != 1) return fail(ctx, GEMEL_EINVAL, "group_unmerged is 0 or 1");

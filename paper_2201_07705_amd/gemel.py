@@ -35,18 +35,21 @@ LEAKY_SLOPE = 0.1
 
 Q_UNMERGED_BYTES, Q_MERGED_BYTES, Q_RESIDENT_BYTES, Q_PEAK_BYTES, \
     Q_STREAMED_BYTES, Q_ACTIVATION_BYTES, Q_LAUNCHES, Q_N_MODELS, \
-    Q_GRAPH_REPLAYS, Q_STREAMS, Q_ROUND_MODE, Q_ROUND_TUNING = range(12)
+    Q_GRAPH_REPLAYS, Q_STREAMS, Q_ROUND_MODE, Q_ROUND_TUNING, \
+    Q_ROUND_LOADED_BYTES, Q_ROUND_EVICTED_BYTES, Q_CACHED_BYTES, \
+    Q_CACHE_CAPACITY = range(16)
 OPT_USE_GRAPH, OPT_SWAP_SLOT_BYTES, OPT_SWAP_SLOTS, OPT_FAIL_COPY_AT, \
     OPT_SPLIT_MERGED, OPT_WEIGHT_BUDGET, OPT_PROFILE, OPT_CONV_TILE, \
     OPT_CONV_SPLITS, OPT_STREAMS, OPT_GRAPH_DAG, OPT_FORK_US, \
     OPT_AUTOTUNE, OPT_SPLITK_FUSED, OPT_TUNE, OPT_FUSE_POOL, \
     OPT_MIXED_SIZES, OPT_PAIRED_ACTS, OPT_FAIL_ALLOC_AT, \
-    OPT_GROUP_UNMERGED = range(20)
+    OPT_GROUP_UNMERGED, OPT_SWAP_CACHE = range(21)
 KERNEL_FAMILIES = ("conv_mfma", "conv_f32", "splitk_reduce", "fc", "pack",
                    "pool", "route", "export", "conv_merged")
 
 EXPORTED = ("gemel_create", "gemel_register_model", "gemel_merge",
             "gemel_enumerate_groups", "gemel_infer", "gemel_infer_noalloc",
+            "gemel_set_next_round", "gemel_load_order",
             "gemel_model_outputs", "gemel_output_shape",
             "gemel_query", "gemel_set_option", "gemel_profile",
             "gemel_last_error", "gemel_destroy")
@@ -127,6 +130,9 @@ def _configure(L):
                               ctypes.POINTER(vp), ctypes.POINTER(i32),
                               ctypes.POINTER(vp), vp]
     L.gemel_infer_noalloc.argtypes = L.gemel_infer.argtypes
+    L.gemel_set_next_round.argtypes = [vp, ctypes.POINTER(i32), i32]
+    L.gemel_load_order.argtypes = [vp, ctypes.POINTER(i32), i32,
+                                   ctypes.POINTER(i32)]
     L.gemel_model_outputs.argtypes = [vp, i32, ctypes.POINTER(i32)]
     L.gemel_output_shape.argtypes = [vp, i32, i32, i32,
                                      ctypes.POINTER(i64)]
@@ -317,6 +323,20 @@ class Context:
         op = (ctypes.c_void_p * max(len(out_ptrs), 1))(*out_ptrs)
         fn = self._lib.gemel_infer_noalloc if noalloc else self._lib.gemel_infer
         return fn(self._h, ids, n, fp, nf, op, ctypes.c_void_p(stream))
+
+    def set_next_round(self, model_ids):
+        """Models of the round after the next infer (weight cache pins)."""
+        n = len(model_ids)
+        ids = (ctypes.c_int32 * max(n, 1))(*model_ids)
+        self._check(self._lib.gemel_set_next_round(self._h, ids, n))
+
+    def load_order(self, model_ids):
+        """Sharing-aware round-robin load order of the models."""
+        n = len(model_ids)
+        ids = (ctypes.c_int32 * n)(*model_ids)
+        out = (ctypes.c_int32 * n)()
+        self._check(self._lib.gemel_load_order(self._h, ids, n, out))
+        return list(out)
 
     def close(self):
         if self._h:

@@ -79,20 +79,23 @@ def main():
             ctx.set_option(getattr(G, "OPT_" + k.upper()), int(v))
         for k, v in opts.items():
             ctx.set_option(getattr(G, k), v)
-        frames, nfr, outs = [], [], []
+        frames, nfr, outs, outs_of = [], [], [], []
         for i, m in enumerate(wl.models):
             c, h, w = m.in_chw
             frames.append(dev(m.n_frames * c * h * w * 4))
             nfr.append(m.n_frames)
+            outs_of.append([])
             for o in range(ctx.n_outputs(ids[i])):
                 shp = ctx.output_shape(ids[i], o, m.n_frames)
                 n = 1
                 for d in shp:
                     n *= d
-                outs.append(dev(n * 4))
+                outs_of[-1].append(dev(n * 4))
+                outs.append(outs_of[-1][-1])
         # any non-null handles: enable graphs and streams
         streams = [dev(16) for _ in range(1 + max(scen.get("streams", [0])))]
-        status, launches, round_allocs = [], [], []
+        status, launches, round_allocs, cache = [], [], [], []
+        subsets = scen.get("rounds")   # model indices of each round
         live_before = L.hoststub_live_bytes()
         allocs_before = L.hoststub_allocs()
         for r in range(rounds):
@@ -106,8 +109,21 @@ def main():
                 L.hoststub_set_capturing(st)
             before = L.hoststub_launches()
             a_before = L.hoststub_allocs()
-            status.append(ctx.infer_raw(ids, frames, nfr, outs, st,
-                                        noalloc=r in scen.get("noalloc", [])))
+            if subsets is not None:
+                sub = subsets[r]
+                if scen.get("next", True):
+                    ctx.set_next_round([ids[i] for i in subsets[r + 1]]
+                                       if r + 1 < len(subsets) else [])
+                status.append(ctx.infer_raw(
+                    [ids[i] for i in sub], [frames[i] for i in sub],
+                    [nfr[i] for i in sub], [p for i in sub for p in outs_of[i]],
+                    st))
+                cache.append([ctx.query(G.Q_ROUND_LOADED_BYTES),
+                              ctx.query(G.Q_ROUND_EVICTED_BYTES),
+                              ctx.query(G.Q_CACHED_BYTES)])
+            else:
+                status.append(ctx.infer_raw(ids, frames, nfr, outs, st,
+                                            noalloc=r in scen.get("noalloc", [])))
             launches.append(L.hoststub_launches() - before)
             round_allocs.append(L.hoststub_allocs() - a_before)
             if cap:
@@ -117,6 +133,9 @@ def main():
             "status": status,
             "round_launches": launches,
             "round_allocs": round_allocs,
+            "cache": cache,
+            "cache_capacity": ctx.query(G.Q_CACHE_CAPACITY),
+            "load_order": ctx.load_order(ids),
             "allocs": L.hoststub_allocs() - allocs_before,
             "error": L.gemel_last_error(ctx._h).decode(),
             "plan_launches": ctx.query(G.Q_LAUNCHES),

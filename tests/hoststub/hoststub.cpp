@@ -353,6 +353,7 @@ static hipError_t conv_common(const ConvArgs &a, int tile, int esz, const char *
     if (!ok) {
         ++violations;
         last = std::string(kern) + ": inconsistent argument block";
+        std::fprintf(stderr, "hoststub violation: %s\n", last.c_str());
         return hipErrorInvalidValue;
     }
     const long long hwo = (long long)a.Ho * a.Wo;
@@ -360,6 +361,7 @@ static hipError_t conv_common(const ConvArgs &a, int tile, int esz, const char *
                        a.out_cs < a.out_pair + a.N || esz != 2)) {
         ++violations;
         last = std::string(kern) + ": bf16 pairs outside their conditions";
+        std::fprintf(stderr, "hoststub violation: %s\n", last.c_str());
         return hipErrorInvalidValue;
     }
     ok &= chk(a.w, (long long)a.N * a.K * esz, "weights", kern);
@@ -367,12 +369,14 @@ static hipError_t conv_common(const ConvArgs &a, int tile, int esz, const char *
     if (a.grouped && (!tile_is_dma(tile) || a.hetero)) {
         ++violations;
         last = std::string(kern) + ": grouped launch outside the LDS-DMA kernel's conditions";
+        std::fprintf(stderr, "hoststub violation: %s\n", last.c_str());
         return hipErrorInvalidValue;
     }
     for (int i = 0; a.grouped && i < a.nseg; ++i) ok &= chk(a.seg[i].w, (long long)a.N * a.K * esz, "segment weights", kern);
     if (a.hetero && (!tile_is_dma(tile) || a.out_mode != OUT_NHWC)) {
         ++violations;
         last = std::string(kern) + ": mixed sizes outside the LDS-DMA kernel's conditions";
+        std::fprintf(stderr, "hoststub violation: %s\n", last.c_str());
         return hipErrorInvalidValue;
     }
     for (int i = 0; i < a.nseg; ++i) {
@@ -385,6 +389,7 @@ static hipError_t conv_common(const ConvArgs &a, int tile, int esz, const char *
             (a.hetero && i && s.m_start <= a.seg[i - 1].m_start)) {
             ++violations;
             last = std::string(kern) + ": segment rows do not match frames";
+            std::fprintf(stderr, "hoststub violation: %s\n", last.c_str());
             return hipErrorInvalidValue;
         }
         const long long frames = rows / shw;
@@ -403,6 +408,7 @@ static hipError_t conv_common(const ConvArgs &a, int tile, int esz, const char *
     if (a.out_mode == OUT_NHWC_POOL2 && (!tile_is_dma(tile) || a.k_splits > 1 || a.has_res || a.Ho % 2 || a.Wo % 2)) {
         ++violations;
         last = std::string(kern) + ": fused pool outside the LDS-DMA kernel's conditions";
+        std::fprintf(stderr, "hoststub violation: %s\n", last.c_str());
         return hipErrorInvalidValue;
     }
     if (a.k_splits > 1) ok &= chk(a.partial, (long long)a.k_splits * a.M * a.N * 4, "partial", kern, true);
@@ -491,6 +497,7 @@ static hipError_t fc_common(const FcArgs &a, int esz, const char *kern, bool rea
     if (!ok) {
         ++violations;
         last = std::string(kern) + ": inconsistent argument block";
+        std::fprintf(stderr, "hoststub violation: %s\n", last.c_str());
         return hipErrorInvalidValue;
     }
     const bool split = a.k_splits > 1;

@@ -260,3 +260,38 @@ def test_noalloc_refuses_unplaced_weights_and_oversized_rounds(hostlib):
     assert out["status"] == [0, EBUDGET], out["error"]
     assert "static scratch" in out["error"]
     assert out["round_launches"][1] == 0 and out["round_allocs"][1] == 0
+
+
+@pytest.mark.parametrize("name,kw,per_round", [
+    ("mix8_budget40", {"res": 32, "frames": 1}, 1),
+    ("mix8_budget40", {"res": 32, "frames": 1}, 2),
+    ("r50x2_vgg16x2", {"res": 32, "frames": 1}, 1),
+])
+def test_weight_cache_rounds_follow_the_swap_oracle(hostlib, name, kw,
+                                                    per_round):
+    """Time-shared rounds over subsets of the models, in the library's
+    sharing-aware load order, two cycles, with the weight cache: every
+    round's loaded, evicted and cached bytes equal the swap oracle's
+    (oracle/swap.py), the load order equals the oracle's, and every access
+    stays in bounds and ordered."""
+    from oracle import swap as S
+    from swapcase import schedule
+    from workloads import configs
+    wl = configs.get(name, **kw)
+    sc = schedule(wl, per_round)
+    rounds, order, need = sc.rounds, sc.order, sc.need
+    sizes, users, pm = sc.sizes, sc.users, sc.per_model
+    cycle = rounds[:len(rounds) // 2]
+    opts = {"OPT_SWAP_CACHE": 1, "OPT_WEIGHT_BUDGET": sc.budget}
+    out = drive(hostlib, name, kw, opts, len(rounds), {"rounds": rounds})
+    assert out["status"] == [0] * len(rounds), out["error"]
+    assert out["cache_capacity"] >= need
+    assert out["hazards"] == 0 and out["violations"] == 0, out["last"]
+    assert out["load_order"] == order
+    want = S.simulate(sizes, users, pm, out["cache_capacity"], rounds)
+    got = out["cache"]
+    assert [w[:3] for w in want] == [tuple(g) for g in got], (want, got)
+    # the second cycle reloads less than the first (shared layers stay)
+    first = sum(w[0] for w in want[:len(cycle)])
+    second = sum(w[0] for w in want[len(cycle):])
+    assert 0 < second <= first
