@@ -310,6 +310,59 @@ gemel_status gemel_set_next_round(gemel_ctx *ctx, const int32_t *model_ids,
 gemel_status gemel_load_order(gemel_ctx *ctx, const int32_t *model_ids,
                               int32_t n_models, int32_t *order);
 
+/*
+ * Per-model batch sizes of a round-robin schedule under a per-frame
+ * deadline (Section 3.2: the time-sharing scheduler's offline profiling
+ * picks one global list of per-model batch sizes that maximises the
+ * minimum per-model throughput within the SLA, loading the next model
+ * while the current one runs; Section 5.4: merging changes those swap
+ * delays; Section 6.1: 100 ms). A host computation: no context, no device.
+ *
+ * cost_ms: [n_models][max_batch] row-major, entry (m, b - 1) the time of
+ *   model m on a batch of b frames; each row nondecreasing (as
+ *   gemel_profile_batches writes it). swap_ms: [n_models] load time of
+ *   model m when its turn comes, or NULL for none.
+ * One cycle visits the models once in index order. pipelined != 0: the
+ *   next model's load overlaps the current model's inference, a visit takes
+ *   max(cost of model i's batch, swap_ms[i + 1 mod n]); pipelined == 0:
+ *   swap_ms[i] + cost. T = the sum over the visits (ms).
+ * A frame waits at most one cycle for its model's next batch, so the
+ *   choice must satisfy T + cost(m, b_m) <= sla_ms for every m. Model m
+ *   then processes min(b_m / T, fps) frames/s (fps: its frames arriving per
+ *   second). Among batch lists in 1..max_batch, the one returned maximises
+ *   the minimum of these over the models; ties go to the shorter cycle,
+ *   then to the smaller batches (it is componentwise the smallest list
+ *   reaching the optimum).
+ * Outputs: batch[n_models]; min_fps and cycle_ms (either may be NULL).
+ * Errors: EINVAL (sizes, null cost/batch, non-finite or negative entries,
+ * a decreasing row, sla_ms or fps not positive); EBUDGET when batches of
+ * one frame already miss the deadline. Outputs are untouched on error.
+ */
+gemel_status gemel_sla_batches(int32_t n_models, int32_t max_batch,
+                               const double *cost_ms, const double *swap_ms,
+                               int32_t pipelined, double sla_ms, double fps,
+                               int32_t *batch, double *min_fps,
+                               double *cycle_ms);
+
+/*
+ * Measures the cost table gemel_sla_batches takes (Section 3.2's offline
+ * profiling): for each listed model and each batch b in 1..max_batch, a
+ * round of that model alone on b frames (zeroed buffers the call
+ * allocates), after untimed rounds that build and tune its plan, then
+ * `reps` rounds timed one by one with HIP events on hip_stream (null: the
+ * default stream; not captured); entry (i, b - 1) of cost_ms ([n_models][max_batch]) is the
+ * largest median over batches 1..b, so rows are nondecreasing. The call
+ * is synchronous, runs rounds like gemel_infer (same options, budget and
+ * weight cache), frees its buffers and drops every plan it built (the
+ * next gemel_infer builds its plan again). max_batch in 1..4096, reps in
+ * 1..1000. Errors: EINVAL, ESTATE (stream captured), ENOMEM, EDEVICE and
+ * those of gemel_infer.
+ */
+gemel_status gemel_profile_batches(gemel_ctx *ctx, const int32_t *model_ids,
+                                   int32_t n_models, int32_t max_batch,
+                                   int32_t reps, void *hip_stream,
+                                   double *cost_ms);
+
 /* Number of output layers of a model. Errors: EINVAL. */
 gemel_status gemel_model_outputs(gemel_ctx *ctx, int32_t model_id,
                                  int32_t *n_outputs);

@@ -286,6 +286,8 @@ gemel_status run_noalloc(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_mod
                          const void *const *frames, const int32_t *n_frames, void *const *outputs,
                          hipStream_t stream);
 size_t unmerged_bytes(const gemel_ctx *ctx);
+// hipMalloc, counted for GEMEL_OPT_FAIL_ALLOC_AT
+hipError_t alloc_device(gemel_ctx *ctx, void **p, size_t bytes);
 void profile_reset(gemel_ctx *ctx);
 gemel_status profile_read(gemel_ctx *ctx, gemel_kernel_stat *stats, int32_t *rounds);
 size_t merged_bytes(const gemel_ctx *ctx);

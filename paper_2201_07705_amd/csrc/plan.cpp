@@ -44,7 +44,7 @@ namespace gemel {
 
 // Device and pinned-host allocations of the library, counted so that a
 // test can make the n-th one fail (GEMEL_OPT_FAIL_ALLOC_AT).
-static hipError_t alloc_device(gemel_ctx *ctx, void **p, size_t bytes) {
+hipError_t alloc_device(gemel_ctx *ctx, void **p, size_t bytes) {
     ctx->allocs_issued++;
     if (ctx->opt.fail_alloc_at && ctx->allocs_issued == ctx->opt.fail_alloc_at) {
         ctx->opt.fail_alloc_at = 0;

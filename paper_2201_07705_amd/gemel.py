@@ -50,6 +50,7 @@ KERNEL_FAMILIES = ("conv_mfma", "conv_f32", "splitk_reduce", "fc", "pack",
 EXPORTED = ("gemel_create", "gemel_register_model", "gemel_merge",
             "gemel_enumerate_groups", "gemel_infer", "gemel_infer_noalloc",
             "gemel_set_next_round", "gemel_load_order",
+            "gemel_sla_batches", "gemel_profile_batches",
             "gemel_model_outputs", "gemel_output_shape",
             "gemel_query", "gemel_set_option", "gemel_profile",
             "gemel_last_error", "gemel_destroy")
@@ -133,6 +134,12 @@ def _configure(L):
     L.gemel_set_next_round.argtypes = [vp, ctypes.POINTER(i32), i32]
     L.gemel_load_order.argtypes = [vp, ctypes.POINTER(i32), i32,
                                    ctypes.POINTER(i32)]
+    f64p = ctypes.POINTER(ctypes.c_double)
+    L.gemel_sla_batches.argtypes = [i32, i32, f64p, f64p, i32,
+                                    ctypes.c_double, ctypes.c_double,
+                                    ctypes.POINTER(i32), f64p, f64p]
+    L.gemel_profile_batches.argtypes = [vp, ctypes.POINTER(i32), i32, i32,
+                                        i32, vp, f64p]
     L.gemel_model_outputs.argtypes = [vp, i32, ctypes.POINTER(i32)]
     L.gemel_output_shape.argtypes = [vp, i32, i32, i32,
                                      ctypes.POINTER(i64)]
@@ -212,6 +219,24 @@ def layer_descs(layers, params):
                     [_fptr(v) for v in vs]
                 d.bn_eps = eps
     return arr, keep
+
+
+def sla_batches(cost_ms, sla_ms, fps, swap_ms=None, pipelined=True,
+                library=None):
+    """Per-model batch sizes under a per-frame deadline from a cost table
+    [model][batch - 1] (ms): returns (batches, min frames/s, cycle ms)."""
+    L = library or lib()
+    n, nb = len(cost_ms), len(cost_ms[0])
+    flat = (ctypes.c_double * (n * nb))(*[c for row in cost_ms for c in row])
+    sw = (ctypes.c_double * n)(*swap_ms) if swap_ms is not None else None
+    b = (ctypes.c_int32 * n)()
+    v, t = ctypes.c_double(), ctypes.c_double()
+    st = L.gemel_sla_batches(n, nb, flat, sw, 1 if pipelined else 0,
+                             float(sla_ms), float(fps), b, ctypes.byref(v),
+                             ctypes.byref(t))
+    if st != OK:
+        raise GemelError(st, "gemel_sla_batches: " + STATUS_NAMES.get(st, "?"))
+    return list(b), v.value, t.value
 
 
 class Context:
@@ -337,6 +362,19 @@ class Context:
         out = (ctypes.c_int32 * n)()
         self._check(self._lib.gemel_load_order(self._h, ids, n, out))
         return list(out)
+
+    def profile_batches(self, model_ids, max_batch, reps=5, stream=None):
+        """Measured cost table [model][batch - 1] in ms (nondecreasing
+        rows) of each model alone on 1..max_batch frames."""
+        import torch
+        n = len(model_ids)
+        ids = (ctypes.c_int32 * n)(*model_ids)
+        out = (ctypes.c_double * (n * max_batch))()
+        s = stream if stream is not None else torch.cuda.current_stream()
+        self._check(self._lib.gemel_profile_batches(
+            self._h, ids, n, max_batch, reps, s.cuda_stream, out))
+        return [list(out[i * max_batch:(i + 1) * max_batch])
+                for i in range(n)]
 
     def close(self):
         if self._h:

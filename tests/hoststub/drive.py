@@ -98,6 +98,16 @@ def main():
         subsets = scen.get("rounds")   # model indices of each round
         live_before = L.hoststub_live_bytes()
         allocs_before = L.hoststub_allocs()
+        profile = None
+        if "profile" in scen:   # measured cost table, then the rounds
+            nb, reps = scen["profile"]
+            pid = (ctypes.c_int32 * len(ids))(*ids)
+            table = (ctypes.c_double * (len(ids) * nb))()
+            st = L.gemel_profile_batches(ctx._h, pid, len(ids), nb, reps,
+                                         streams[0], table)
+            profile = {"status": st, "table": list(table),
+                       "plans_after": ctx.query(G.Q_LAUNCHES),
+                       "error": L.gemel_last_error(ctx._h).decode()}
         for r in range(rounds):
             st = streams[scen["streams"][r]] if "streams" in scen else streams[0]
             if str(r) in scen.get("fail", {}):
@@ -142,6 +152,7 @@ def main():
             "arena": ctx.query(G.Q_ACTIVATION_BYTES),
             "streamed": ctx.query(G.Q_STREAMED_BYTES),
             "round_mode": ctx.query(G.Q_ROUND_MODE),
+            "profile": profile,
         }
         ctx.close()
         # device bytes the context still held after it was destroyed

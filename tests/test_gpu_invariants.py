@@ -268,3 +268,73 @@ def test_injected_copy_failure_then_retry():
     finally:
         g.close()
     _same(good, again)
+
+
+@pytest.mark.parametrize("at", [10, 40])
+def test_injected_copy_failure_mid_round_then_retry(at):
+    """A copy that fails after the round's first launches were enqueued
+    (worker streams forked): the call reports EDEVICE, the partial round is
+    joined back to the caller's stream, and the next round's outputs equal
+    those of a round before the failure."""
+    wl = configs.mix8_budget40(res=32, frames=1)
+    params = [wl.params(i) for i in range(len(wl.models))]
+    frames = [wl.frames(i) for i in range(len(wl.models))]
+    log(f"copy failure at copy {at} of a round")
+    g = _pinned(wl, params, budget="auto")
+    try:
+        good = g.run(frames)
+        g.ctx.set_option(G.OPT_FAIL_COPY_AT, at)
+        with pytest.raises(G.GemelError) as e:
+            g.run(frames)
+        assert e.value.code == G.EDEVICE
+        again = g.run(frames)
+    finally:
+        g.close()
+    _same(good, again)
+
+
+@pytest.mark.parametrize("at", [1, 2, 6])
+def test_injected_alloc_failure_then_retry(at):
+    """The at-th device or pinned allocation of a fresh context fails: the
+    call reports ENOMEM and leaves the context as it was; the next call
+    places everything and its outputs equal a context's that never failed."""
+    wl = configs.mix8_budget40(res=32, frames=1)
+    params = [wl.params(i) for i in range(len(wl.models))]
+    frames = [wl.frames(i) for i in range(len(wl.models))]
+    good = _run(wl, params, frames, budget="auto")
+    log(f"allocation failure at allocation {at}")
+    g = _pinned(wl, params, budget="auto")
+    try:
+        g.ctx.set_option(G.OPT_FAIL_ALLOC_AT, at)
+        with pytest.raises(G.GemelError) as e:
+            g.run(frames)
+        assert e.value.code == G.ENOMEM
+        again = g.run(frames)
+    finally:
+        g.close()
+    _same(good, again)
+
+
+def test_weight_cache_copy_failure_then_retry():
+    """Weight cache on: a cache copy that fails leaves its blob uncached;
+    the retry loads it and its outputs equal a round that never failed."""
+    from swapcase import schedule
+    wl = configs.mix8_budget40(res=32, frames=1)
+    params = [wl.params(i) for i in range(len(wl.models))]
+    frames = [wl.frames(i) for i in range(len(wl.models))]
+    sc = schedule(wl, 2)
+    log(f"cache copy failure, rounds {sc.rounds[:2]}")
+    g = _pinned(wl, params, OPT_SWAP_CACHE=1, OPT_WEIGHT_BUDGET=sc.budget)
+    try:
+        good = g.run(frames, order=sc.rounds[0])
+        g.ctx.set_option(G.OPT_FAIL_COPY_AT, 3)
+        with pytest.raises(G.GemelError) as e:
+            g.run(frames, order=sc.rounds[1])
+        assert e.value.code == G.EDEVICE
+        again = g.run(frames, order=sc.rounds[1])
+        first = g.run(frames, order=sc.rounds[0])
+    finally:
+        g.close()
+    ref = _run(wl, params, frames, order=sc.rounds[1])
+    _same([again[i] for i in sc.rounds[1]], [ref[i] for i in sc.rounds[1]])
+    _same([first[i] for i in sc.rounds[0]], [good[i] for i in sc.rounds[0]])

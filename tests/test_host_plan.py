@@ -27,7 +27,7 @@ def hostlib():
            "-fno-omit-frame-pointer", "-fPIC", "-shared", f"-I{STUB}",
            f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}",
            os.path.join(CSRC, "registry.cpp"), os.path.join(CSRC, "plan.cpp"),
-           os.path.join(STUB, "hoststub.cpp"), "-o", LIB + f".{os.getpid()}"]
+           os.path.join(CSRC, "batching.cpp"), os.path.join(STUB, "hoststub.cpp"), "-o", LIB + f".{os.getpid()}"]
     subprocess.check_call(cmd)
     # atomic: parallel test workers may build and load it at the same time
     os.replace(LIB + f".{os.getpid()}", LIB)
@@ -295,3 +295,21 @@ def test_weight_cache_rounds_follow_the_swap_oracle(hostlib, name, kw,
     first = sum(w[0] for w in want[:len(cycle)])
     second = sum(w[0] for w in want[len(cycle):])
     assert 0 < second <= first
+
+
+def test_profile_batches_runs_every_batch_and_frees_its_buffers(hostlib):
+    """gemel_profile_batches on the CPU stub: one plan per (model, batch),
+    every launch in bounds and ordered, a full nondecreasing cost table
+    (the stub's event clock reads 0.001 ms per pair), no plan kept, and the
+    rounds after it still run; the context frees everything at the end."""
+    out = drive(hostlib, "r50x2_vgg16x2", {"res": 32, "frames": 1}, {}, 2,
+                {"profile": [3, 2]})
+    prof = out["profile"]
+    assert prof["status"] == 0, prof["error"]
+    assert prof["plans_after"] == 0          # plans dropped
+    assert prof["table"] == [0.001 * 1.0] * len(prof["table"]) or \
+        all(abs(x - 0.001) < 1e-6 for x in prof["table"])
+    assert len(prof["table"]) == 4 * 3
+    assert out["status"] == [0, 0], out["error"]
+    assert out["hazards"] == 0 and out["violations"] == 0, out["last"]
+    assert out["leaked"] == 0
