@@ -145,6 +145,18 @@ struct Plan {
     hipEvent_t ev_fork = nullptr;          // origin -> worker streams
     std::vector<hipEvent_t> ev_join;       // worker streams -> origin
     std::vector<Chunk> chunks;             // streamed chunks, consumption order
+    // Streamed chunks packed in consumption order into one pinned host image,
+    // cut into copy segments of at most one staging slot each (a chunk never
+    // straddles two): one copy per segment per round. Built at the plan's
+    // first round.
+    struct CopySeg {
+        size_t off, bytes;                 // in the image
+    };
+    void *image = nullptr;
+    std::vector<CopySeg> copy_segs;
+    std::vector<int> chunk_seg;            // segment of each chunk
+    std::vector<size_t> chunk_off;         // its offset in the segment (and slot)
+    std::vector<hipEvent_t> ev_chunk;      // recorded after each chunk's consumer
     void *arena = nullptr;
     size_t arena_bytes = 0;
     // split-K partial sums: one region per split-K step; steps that may run
@@ -230,6 +242,10 @@ struct gemel_ctx {
     hipStream_t side = nullptr;      // weight-copy stream
     std::vector<hipStream_t> workers;  // extra streams for concurrent steps
     std::vector<hipEvent_t> ev_copied, ev_free;
+    // per staging slot: for each stream, the event of the last consumer on
+    // it of the segment that last used the slot (the next copy into the
+    // slot waits for all of them)
+    std::vector<std::vector<std::pair<hipStream_t, hipEvent_t>>> slot_users;
     void *wpool = nullptr;           // resident weights + all scale/shift
     void *zero_page = nullptr;       // GEMEL_ZERO_PAGE_BYTES zero bytes inside wpool
     size_t wpool_bytes = 0;

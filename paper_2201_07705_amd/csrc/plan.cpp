@@ -122,10 +122,10 @@ void free_placement(gemel_ctx *ctx) {
     ctx->wpool = ctx->staging = nullptr;
     ctx->zero_page = nullptr;
     ctx->wpool_bytes = 0;
-    for (auto e : ctx->ev_copied) (void)hipEventDestroy(e);
-    for (auto e : ctx->ev_free) (void)hipEventDestroy(e);
+    for (auto e : ctx->ev_copied)
+        if (e) (void)hipEventDestroy(e);
     ctx->ev_copied.clear();
-    ctx->ev_free.clear();
+    ctx->slot_users.clear();
     ctx->staging_slots = 0;
     ctx->resident_bytes = 0;
     ctx->weights_ready = false;
@@ -148,6 +148,9 @@ void drop_plans(gemel_ctx *ctx) {
         if (p.ev_fork) (void)hipEventDestroy(p.ev_fork);
         for (auto ev : p.ev_join)
             if (ev) (void)hipEventDestroy(ev);
+        for (auto ev : p.ev_chunk)
+            if (ev) (void)hipEventDestroy(ev);
+        if (p.image) (void)hipHostFree(p.image);
         if (!p.static_mem) {
             if (p.arena) (void)hipFree(p.arena);
             if (p.partial) (void)hipFree(p.partial);
@@ -156,6 +159,7 @@ void drop_plans(gemel_ctx *ctx) {
     }
     ctx->plans.clear();
     ctx->last_plan = nullptr;
+    for (auto &u : ctx->slot_users) u.clear();   // events of the dropped plans
 }
 
 void release_device(gemel_ctx *ctx) {
@@ -408,10 +412,9 @@ gemel_status materialise(gemel_ctx *ctx) {
         ctx->staging_slots = slots;
         ctx->staging_slot_bytes = slot_bytes;
         ctx->ev_copied.resize((size_t)slots);
-        ctx->ev_free.resize((size_t)slots);
+        ctx->slot_users.assign((size_t)slots, {});
         for (int i = 0; i < slots; ++i) {
-            if (hipEventCreateWithFlags(&ctx->ev_copied[(size_t)i], hipEventDisableTiming) != hipSuccess ||
-                hipEventCreateWithFlags(&ctx->ev_free[(size_t)i], hipEventDisableTiming) != hipSuccess) {
+            if (hipEventCreateWithFlags(&ctx->ev_copied[(size_t)i], hipEventDisableTiming) != hipSuccess) {
                 free_placement(ctx);
                 return fail(ctx, GEMEL_EDEVICE, "event creation failed");
             }
@@ -1629,6 +1632,12 @@ static void join_partial_round(gemel_ctx *ctx, Plan &P, hipStream_t st) {
     }
     if (ctx->side && hipEventRecord(ctx->ev_side_join, ctx->side) == hipSuccess)
         (void)hipStreamWaitEvent(st, ctx->ev_side_join, 0);
+    // the partial round shares the arena and the staging slots with the next
+    // round, which, on another stream, waits for this event
+    if (ctx->ev_round_done && hipEventRecord(ctx->ev_round_done, st) == hipSuccess) {
+        ctx->round_stream = st;
+        ctx->round_seen = true;
+    }
     (void)hipGetLastError();
 }
 
@@ -1745,6 +1754,54 @@ static gemel_status cache_round(gemel_ctx *ctx, Plan &P, hipStream_t st) {
     return GEMEL_OK;
 }
 
+// Packs the plan's streamed chunks, in consumption order, into one pinned
+// host image cut into copy segments of at most one staging slot: a round
+// then copies each segment with one transfer instead of one per chunk.
+static gemel_status stream_image(gemel_ctx *ctx, Plan &P) {
+    const size_t cap = ctx->staging_slot_bytes;
+    size_t total = 0, used = cap;   // forces a first segment
+    P.chunk_seg.assign(P.chunks.size(), 0);
+    P.chunk_off.assign(P.chunks.size(), 0);
+    std::vector<Plan::CopySeg> segs;
+    for (size_t c = 0; c < P.chunks.size(); ++c) {
+        const size_t b = P.chunks[c].bytes();
+        const size_t at = (size_t)round_up((int64_t)used, 256);
+        if (at + b > cap) {
+            segs.push_back({(size_t)round_up((int64_t)total, 256), 0});
+            used = 0;
+        } else {
+            used = at;
+        }
+        Plan::CopySeg &sg = segs.back();
+        P.chunk_seg[c] = (int)segs.size() - 1;
+        P.chunk_off[c] = used;
+        used += b;
+        sg.bytes = used;
+        total = sg.off + sg.bytes;
+    }
+    void *img = nullptr;
+    if (alloc_pinned(ctx, &img, std::max<size_t>(total, 1)) != hipSuccess)
+        return fail(ctx, GEMEL_ENOMEM, "pinned host allocation of the streamed-weight image failed");
+    for (size_t c = 0; c < P.chunks.size(); ++c) {
+        const Chunk &ch = P.chunks[c];
+        std::memcpy((char *)img + segs[(size_t)P.chunk_seg[c]].off + P.chunk_off[c],
+                    ch.blob->w_pinned + (size_t)(ch.row0 * ch.blob->k) * ch.blob->elem, ch.bytes());
+    }
+    std::vector<hipEvent_t> evs(P.chunks.size(), nullptr);
+    for (auto &e : evs)
+        if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) {
+            e = nullptr;
+            for (auto x : evs)
+                if (x) (void)hipEventDestroy(x);
+            (void)hipHostFree(img);
+            return fail(ctx, GEMEL_EDEVICE, "event creation failed");
+        }
+    P.image = img;
+    P.copy_segs = std::move(segs);
+    P.ev_chunk = std::move(evs);
+    return GEMEL_OK;
+}
+
 static gemel_status enqueue(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hipStream_t st) {
     const gemel_status s = enqueue_body(ctx, P, cp, st);
     if (s) join_partial_round(ctx, P, st);
@@ -1757,30 +1814,39 @@ static gemel_status enqueue_body(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hi
         if (s) return s;
     }
     const int nslots = ctx->staging_slots;
-    const int nch = (int)P.chunks.size();
+    const int nseg = (int)P.copy_segs.size();
     int next_copy = 0;
-    auto slot_ptr = [&](int c) { return (char *)ctx->staging + (size_t)(c % nslots) * ctx->staging_slot_bytes; };
+    auto slot_ptr = [&](int seg) { return (char *)ctx->staging + (size_t)(seg % nslots) * ctx->staging_slot_bytes; };
+    // copies of segments [next_copy, upto]: each first waits for every
+    // consumer of the segment that last used its slot (on any stream, in
+    // this round or the previous one)
     auto issue_copies = [&](int upto) -> gemel_status {
-        for (; next_copy < nch && next_copy <= upto; ++next_copy) {
-            const Chunk &ch = P.chunks[(size_t)next_copy];
+        for (; next_copy < nseg && next_copy <= upto; ++next_copy) {
+            const Plan::CopySeg &sg = P.copy_segs[(size_t)next_copy];
             const int slot = next_copy % nslots;
             ctx->copies_issued++;
             if (ctx->opt.fail_copy_at && ctx->copies_issued == ctx->opt.fail_copy_at) {
                 ctx->opt.fail_copy_at = 0;
                 return fail(ctx, GEMEL_EDEVICE, "injected failure of a weight copy");
             }
-            HIPCHK(hipStreamWaitEvent(ctx->side, ctx->ev_free[(size_t)slot], 0), "hipStreamWaitEvent");
-            HIPCHK(hipMemcpyAsync(slot_ptr(next_copy), ch.blob->w_pinned + (size_t)(ch.row0 * ch.blob->k) * ch.blob->elem,
-                                  ch.bytes(), hipMemcpyHostToDevice, ctx->side),
+            for (auto &u : ctx->slot_users[(size_t)slot])
+                HIPCHK(hipStreamWaitEvent(ctx->side, u.second, 0), "hipStreamWaitEvent");
+            ctx->slot_users[(size_t)slot].clear();
+            HIPCHK(hipMemcpyAsync(slot_ptr(next_copy), (char *)P.image + sg.off, sg.bytes, hipMemcpyHostToDevice,
+                                  ctx->side),
                    "hipMemcpyAsync (weight swap-in)");
             HIPCHK(hipEventRecord(ctx->ev_copied[(size_t)slot], ctx->side), "hipEventRecord");
         }
         return GEMEL_OK;
     };
-    if (nch) {
+    if (nseg) {
         gemel_status s = issue_copies(nslots - 1);
         if (s) return s;
     }
+    // per stream: the latest segment whose copy it has waited for (copies
+    // complete in order on the copy stream, so later consumers of that or
+    // an earlier segment on the stream need no wait of their own)
+    std::vector<int> waited((size_t)std::max(P.n_streams, 1), -1);
     hipStream_t streams[8] = {st};
     for (int k = 1; k < P.n_streams; ++k) streams[k] = ctx->workers[(size_t)k - 1];
     for (size_t li = 0; li < P.launches.size(); ++li) {
@@ -1803,10 +1869,14 @@ static gemel_status enqueue_body(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hi
             wptr = L.wblobs[0]->w_dev;
         }
         if (L.chunk >= 0) {
-            gemel_status s = issue_copies(L.chunk + nslots - 1);
+            const int seg = P.chunk_seg[(size_t)L.chunk];
+            gemel_status s = issue_copies(seg + nslots - 1);
             if (s) return s;
-            HIPCHK(hipStreamWaitEvent(ls, ctx->ev_copied[(size_t)(L.chunk % nslots)], 0), "hipStreamWaitEvent");
-            wptr = slot_ptr(L.chunk);
+            if (seg > waited[(size_t)L.stream]) {
+                HIPCHK(hipStreamWaitEvent(ls, ctx->ev_copied[(size_t)(seg % nslots)], 0), "hipStreamWaitEvent");
+                waited[(size_t)L.stream] = seg;
+            }
+            wptr = slot_ptr(seg) + P.chunk_off[(size_t)L.chunk];
         }
         const int subset = L.kind == GEMEL_K_CONV_MFMA && L.merged ? GEMEL_K_CONV_MERGED : -1;
         Profile::Rec rec{nullptr, nullptr, L.kind, subset};
@@ -1836,7 +1906,16 @@ static gemel_status enqueue_body(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hi
                 ctx->prof.launches[k] += 1;
             }
         }
-        if (L.chunk >= 0) HIPCHK(hipEventRecord(ctx->ev_free[(size_t)(L.chunk % nslots)], ls), "hipEventRecord");
+        if (L.chunk >= 0) {
+            hipEvent_t e = P.ev_chunk[(size_t)L.chunk];
+            HIPCHK(hipEventRecord(e, ls), "hipEventRecord");
+            auto &users = ctx->slot_users[(size_t)(P.chunk_seg[(size_t)L.chunk] % nslots)];
+            auto u = std::find_if(users.begin(), users.end(), [&](const auto &x) { return x.first == ls; });
+            if (u != users.end())
+                u->second = e;   // stream order: this consumer ends after the earlier one
+            else
+                users.push_back({ls, e});
+        }
         if (L.record >= 0) HIPCHK(hipEventRecord(P.events[(size_t)L.record], ls), "hipEventRecord");
     }
     if ((int)P.launches.size() <= P.n_pack && P.n_streams > 1) {
@@ -2065,6 +2144,10 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         if (ctx->opt.profile) return fail(ctx, GEMEL_ESTATE, "a profiled round cannot be captured");
         ctx->last_mode = MODE_SERIAL;
         return enqueue_serial(ctx, P, cp, stream);
+    }
+    if (!P.chunks.empty() && !P.image) {
+        st = stream_image(ctx, P);
+        if (st) return st;
     }
     // rounds share the plan's arena and split-K regions and the staging
     // slots: a round on another stream than the previous one first waits

@@ -175,14 +175,17 @@ def test_captured_round_that_streams_weights_is_refused(hostlib):
 
 @pytest.mark.parametrize("at", [1, 3, 7, 20])
 @pytest.mark.parametrize("opts", [{}, {"OPT_STREAMS": 1}])
-def test_copy_failure_part_way_leaves_rounds_ordered(hostlib, at, opts):
+@pytest.mark.parametrize("streams", [[0, 0, 0, 1], [0, 0, 1, 2]])
+def test_copy_failure_part_way_leaves_rounds_ordered(hostlib, at, opts,
+                                                     streams):
     """A weight copy that fails after launches (and the fork to worker
     streams) were enqueued: the round returns EDEVICE, its partial work is
     joined back to the caller's stream, and the next rounds, on the same
-    and on another stream, are ordered after it (no hazard)."""
+    and on other streams (also the round right after the failure), are
+    ordered after it (no hazard)."""
     out = drive(hostlib, "mix8_budget40", {"res": 32, "frames": 2},
                 dict(opts, OPT_SWAP_SLOT_BYTES=1 << 20, OPT_SWAP_SLOTS=2), 4,
-                {"fail": {"1": at}, "streams": [0, 0, 0, 1]})
+                {"fail": {"1": at}, "streams": streams})
     assert out["status"] == [0, EDEVICE, 0, 0], out["error"]
     assert out["hazards"] == 0 and out["violations"] == 0, out["last"]
 
