@@ -24,6 +24,7 @@
 namespace gemel {
 
 typedef unsigned short u16;
+typedef __attribute__((address_space(3))) unsigned char fc_lds_u8;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -42,6 +43,17 @@ __device__ __forceinline__ int fc_seg(const FcArgs &a, int f) {
     return s;
 }
 
+// Input row of launch frame f. A select walk over the segments with
+// constant indices: indexing the kernel-argument array with a computed
+// index would copy it to scratch memory.
+__device__ __forceinline__ const u16 *fc_in_row(const FcArgs &a, int f) {
+    const u16 *p = (const u16 *)a.seg[0].in + (size_t)f * a.K;
+#pragma unroll
+    for (int i = 1; i < GEMEL_MAX_SEG; ++i)
+        if (i < a.nseg && f >= a.seg[i].f_start) p = (const u16 *)a.seg[i].in + (size_t)(f - a.seg[i].f_start) * a.K;
+    return p;
+}
+
 __device__ __forceinline__ void fc_store(const FcArgs &a, int f, int n, float acc, bool bf16) {
     const FcSeg &sg = a.seg[fc_seg(a, f)];
     const int lf = f - sg.f_start;
@@ -56,73 +68,117 @@ __device__ __forceinline__ void fc_store(const FcArgs &a, int f, int n, float ac
     }
 }
 
-// Elements of the LDS input slice: frames (16 per block) x (depth per split
-// + 8). The planner keeps MB * 16 * (k_per_split + 8) within it.
+// Elements of the LDS input slice: (depth per split) x (frames padded to
+// 16 per block), frame-minor, in runs of 64 16-byte slots. The planner
+// keeps MB * 16 * k_per_split within it with room for the last run.
 constexpr int FC_X_ELEMS = 32768;
+
+// vmcnt(0) only: expcnt and lgkmcnt left at their maxima (gfx9 encoding).
+__device__ __forceinline__ void fc_wait_vm0() { __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8)); }
 
 template <int MB>  // frame blocks of 16
 __global__ __launch_bounds__(256) void fc_bf16_kernel(const FcArgs a) {
+    constexpr int RB = 1;           // row blocks of 16 neurons per wave
+    constexpr int COLS = 64 * RB;   // neurons of a workgroup
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int n0 = blockIdx.x * 64 + wave * 16;
+    const int n0 = blockIdx.x * COLS + wave * 16 * RB;
     const int k_begin = blockIdx.y * a.k_per_split;
     const int k_end = min(a.K, k_begin + a.k_per_split);
-    const int row = n0 + (lane & 15);
     const int g = lane >> 4;
-    const bool row_ok = row < a.N;
-    const u16 *wrow = (const u16 *)a.w + (size_t)(row_ok ? row : 0) * a.K;
-    // the workgroup's slice of the inputs, [frame][k_begin, k_end), staged
-    // in LDS once: every wave reads it, and from LDS its reads need no wait
-    // on a global round trip inside the depth loop. Rows are padded by 16
-    // bytes so that the 16 frames of a fragment fall on distinct banks.
-    // Frames beyond M are left unset: they only feed output columns that are
-    // never stored.
-    __shared__ __attribute__((aligned(16))) u16 xs[FC_X_ELEMS];
-    const int kn = k_end - k_begin;
-    const int pitch = kn + 8;
-    {
-        const int chunks = kn / 8;
-        for (int idx = threadIdx.x; idx < a.M * chunks; idx += 256) {
-            const int f = idx / chunks, c = idx - (idx / chunks) * chunks;
-            const FcSeg &sg = a.seg[fc_seg(a, f)];
-            *(uint4 *)(xs + f * pitch + c * 8) =
-                *(const uint4 *)((const u16 *)sg.in + (size_t)(f - sg.f_start) * a.K + k_begin + c * 8);
+    // frames [f0, f1) of this grid slice and their weights: every frame of
+    // the launch, or (grouped) segment blockIdx.z alone. A select walk with
+    // constant indices: indexing the kernel-argument array with a computed
+    // index would copy it to scratch memory.
+    const void *wsrc = a.w;
+    int f0 = 0, f1 = a.M;
+    if (a.grouped) {
+        const int z = blockIdx.z;
+#pragma unroll
+        for (int i = 0; i < GEMEL_MAX_SEG; ++i) {
+            if (i == z) {
+                wsrc = a.seg[i].w;
+                f0 = a.seg[i].f_start;
+            }
+            if (i == z + 1 && i < a.nseg) f1 = a.seg[i].f_start;
         }
     }
-    __syncthreads();
-    f32x4 acc[MB];
+    const int mz = f1 - f0;
+    const u16 *wrow[RB];
+    bool row_ok[RB];
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    // depth steps of 256: 8 weight chunks of 16 bytes per lane (lane g of a
-    // row covers 32 contiguous bytes of every 128), the next step's weights
-    // loaded while the current step's MFMAs run
+    for (int r = 0; r < RB; ++r) {
+        const int row = n0 + r * 16 + (lane & 15);
+        row_ok[r] = row < a.N;
+        wrow[r] = (const u16 *)wsrc + (size_t)(row_ok[r] ? row : 0) * a.K;
+    }
+    // depth steps of 256: per row block 8 weight chunks of 16 bytes per lane
+    // (lane g of a row covers 32 contiguous bytes of every 128), the next
+    // step's weights loaded while the current step's MFMAs run. The first
+    // step is requested before the input slice is staged, so that its
+    // latency overlaps the staging.
     constexpr int KS = 256, WJ = KS / 32;
-    auto wload = [&](int k, uint4 (&wv)[WJ]) __attribute__((always_inline)) {
+    auto wload = [&](int k, uint4 (&wv)[RB][WJ]) __attribute__((always_inline)) {
 #pragma unroll
-        for (int j = 0; j < WJ; ++j) {
-            const int kk = k + j * 32 + g * 8;
-            wv[j] = (row_ok && kk < k_end) ? *(const uint4 *)(wrow + kk) : make_uint4(0, 0, 0, 0);
-        }
-    };
-    auto step = [&](int k, const uint4 (&wv)[WJ]) __attribute__((always_inline)) {
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-            uint4 xv[WJ];
-            const u16 *xr = xs + (mb * 16 + (lane & 15)) * pitch - k_begin;
+        for (int r = 0; r < RB; ++r)
 #pragma unroll
             for (int j = 0; j < WJ; ++j) {
                 const int kk = k + j * 32 + g * 8;
-                xv[j] = kk < k_end ? *(const uint4 *)(xr + kk) : make_uint4(0, 0, 0, 0);
+                wv[r][j] = (row_ok[r] && kk < k_end) ? *(const uint4 *)(wrow[r] + kk) : make_uint4(0, 0, 0, 0);
+            }
+    };
+    uint4 w0[RB][WJ], w1[RB][WJ];
+    if (n0 < a.N) wload(k_begin, w0);
+    // the workgroup's slice of the inputs, [k_begin, k_end) x frames, staged
+    // in LDS once: every wave reads it, and from LDS its reads need no wait
+    // on a global round trip inside the depth loop. With MP frames staged
+    // (M rounded up to a power of two up to 16, else 16 per frame block),
+    // chunk c (8 elements) of frame f sits in 16-byte slot c * MP + f, so
+    // the frames of a fragment are contiguous (no bank conflicts; lanes of
+    // frames beyond MP read a staged frame again, for output columns that
+    // are never stored). The slots are filled by direct global-to-LDS loads
+    // (each wave instruction writes 64 consecutive slots), all in flight at
+    // once; staged frames beyond M repeat frame M - 1.
+    const int MP = mz > 16 ? 16 * MB : mz > 8 ? 16 : mz > 4 ? 8 : mz > 2 ? 4 : mz;
+    __shared__ __attribute__((aligned(16))) u16 xs[FC_X_ELEMS];
+    const int kn = k_end - k_begin;
+    {
+        const int slots = (kn / 8) * MP;
+        for (int s0 = wave * 64; s0 < slots; s0 += 256) {
+            const int sl = min(s0 + lane, slots - 1);
+            const int c = sl / MP, f = f0 + min(sl - c * MP, mz - 1);
+            __builtin_amdgcn_global_load_lds((const void *)(fc_in_row(a, f) + k_begin + c * 8),
+                                             (fc_lds_u8 *)(xs + s0 * 8), 16, 0, 0);
+        }
+        fc_wait_vm0();
+    }
+    __syncthreads();
+    f32x4 acc[MB][RB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int r = 0; r < RB; ++r) acc[mb][r] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // one input fragment from LDS feeds the MFMAs of every row block
+    auto step = [&](int k, const uint4 (&wv)[RB][WJ]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            uint4 xv[WJ];
+            const int fr = mb * 16 + (lane & 15);
+            const u16 *xr = xs + (fr < MP ? fr : (fr & (MP - 1))) * 8;
+#pragma unroll
+            for (int j = 0; j < WJ; ++j) {
+                const int kk = k + j * 32 + g * 8;
+                xv[j] = kk < k_end ? *(const uint4 *)(xr + ((kk - k_begin) >> 3) * MP * 8) : make_uint4(0, 0, 0, 0);
             }
 #pragma unroll
             for (int j = 0; j < WJ; ++j)
-                acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    __builtin_bit_cast(bf16x8, wv[j]), __builtin_bit_cast(bf16x8, xv[j]), acc[mb], 0, 0, 0);
+#pragma unroll
+                for (int r = 0; r < RB; ++r)
+                    acc[mb][r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(bf16x8, wv[r][j]), __builtin_bit_cast(bf16x8, xv[j]), acc[mb][r], 0, 0, 0);
         }
     };
     if (n0 < a.N) {
-        uint4 w0[WJ], w1[WJ];
-        wload(k_begin, w0);
         for (int k = k_begin; k < k_end; k += 2 * KS) {
             if (k + KS < k_end) wload(k + KS, w1);
             step(k, w0);
@@ -132,36 +188,39 @@ __global__ __launch_bounds__(256) void fc_bf16_kernel(const FcArgs a) {
             }
         }
     }
-    // D[neuron = n0 + 4 g + v][frame = mb*16 + lane%16]
+    // D[neuron = n0 + 16 r + 4 g + v][frame = mb*16 + lane%16]
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
-        const int f = mb * 16 + (lane & 15);
-        if (f >= a.M) continue;
+        const int f = f0 + mb * 16 + (lane & 15);
+        if (f >= f1) continue;
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int n = n0 + g * 4 + v;
-            if (n >= a.N) continue;
-            if (a.k_splits > 1)
-                store_partial1(a.partial + ((size_t)blockIdx.y * a.M + f) * a.N + n, acc[mb][v]);
-            else
-                fc_store(a, f, n, acc[mb][v], true);
-        }
+        for (int r = 0; r < RB; ++r)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int n = n0 + r * 16 + g * 4 + v;
+                if (n >= a.N) continue;
+                if (a.k_splits > 1)
+                    store_partial1(a.partial + ((size_t)blockIdx.y * a.M + f) * a.N + n, acc[mb][r][v]);
+                else
+                    fc_store(a, f, n, acc[mb][r][v], true);
+            }
     }
-    // fused split-K reduction: the last split of this column of 64 neurons
+    // fused split-K reduction: the last split of this column of neurons
     // sums the partials in split order, as fc_reduce does
     if (a.k_splits > 1 && a.counters) {
         __shared__ int flag;
-        if (!splitk_arrive(a.counters + blockIdx.x, a.k_splits, &flag)) return;
-        // four items per thread, eight splits per batch of loads
-        for (int i0 = threadIdx.x; i0 < a.M * 64; i0 += 4 * 256) {
+        if (!splitk_arrive(a.counters + (a.grouped ? blockIdx.z * gridDim.x : 0) + blockIdx.x, a.k_splits, &flag))
+            return;
+        // four items per thread, sixteen splits per batch of loads
+        for (int i0 = threadIdx.x; i0 < mz * COLS; i0 += 4 * 256) {
             float sum[4] = {0.f, 0.f, 0.f, 0.f};
             bool ok[4];
             const float *base[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int item = i0 + u * 256;
-                const int f = item >> 6, n = blockIdx.x * 64 + (item & 63);
-                ok[u] = item < a.M * 64 && n < a.N;
+                const int f = f0 + item / COLS, n = blockIdx.x * COLS + (item % COLS);
+                ok[u] = item < mz * COLS && n < a.N;
                 base[u] = a.partial + (ok[u] ? (size_t)f * a.N + n : 0);
             }
             const size_t split_elems = (size_t)a.M * a.N;
@@ -181,7 +240,7 @@ __global__ __launch_bounds__(256) void fc_bf16_kernel(const FcArgs a) {
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int item = i0 + u * 256;
-                if (ok[u]) fc_store(a, item >> 6, blockIdx.x * 64 + (item & 63), sum[u], true);
+                if (ok[u]) fc_store(a, f0 + item / COLS, blockIdx.x * COLS + (item % COLS), sum[u], true);
             }
         }
     }
@@ -220,26 +279,43 @@ static bool fc_args_ok(const FcArgs &a) {
     for (int i = 0; i < a.nseg; ++i)
         if (!a.seg[i].in || !a.seg[i].out || !a.seg[i].scale || !a.seg[i].shift) return false;
     if (a.k_splits > 1 && !a.partial) return false;
+    if (a.grouped)
+        for (int i = 0; i < a.nseg; ++i)
+            if (!a.seg[i].w || (i > 0 && a.seg[i].f_start <= a.seg[i - 1].f_start)) return false;
     return true;
 }
 
+// Frames of the largest grid slice: the whole launch, or (grouped) the
+// largest segment.
+static int fc_slice_frames(const FcArgs &a) {
+    if (!a.grouped) return a.M;
+    int m = 0;
+    for (int i = 0; i < a.nseg; ++i) m = std::max(m, (i + 1 < a.nseg ? a.seg[i + 1].f_start : a.M) - a.seg[i].f_start);
+    return m;
+}
+
 hipError_t launch_fc_bf16(const FcArgs &a, const Sink &sk) {
-    if (!fc_args_ok(a) || a.M > 64 || (a.k_splits > 1 && a.k_per_split % 128)) return hipErrorInvalidValue;
-    if (((a.M + 15) / 16) * 16 * (long)(std::min(a.K, a.k_per_split) + 8) > FC_X_ELEMS) return hipErrorInvalidValue;
-    dim3 grid((unsigned)((a.N + 63) / 64), (unsigned)a.k_splits), block(256);
-    const int mb = (a.M + 15) / 16;
-    hipError_t e;
-    switch (mb) {
-    case 1: e = submit(sk, reinterpret_cast<const void *>(&fc_bf16_kernel<1>), grid, block, a); break;
-    case 2: e = submit(sk, reinterpret_cast<const void *>(&fc_bf16_kernel<2>), grid, block, a); break;
-    case 3: e = submit(sk, reinterpret_cast<const void *>(&fc_bf16_kernel<3>), grid, block, a); break;
-    default: e = submit(sk, reinterpret_cast<const void *>(&fc_bf16_kernel<4>), grid, block, a); break;
+    if (!fc_args_ok(a) || (a.k_splits > 1 && a.k_per_split % 128)) return hipErrorInvalidValue;
+    const int ms = fc_slice_frames(a);
+    if (ms < 1 || ms > 64) return hipErrorInvalidValue;
+    {
+        // LDS slots of the input slice, rounded up to whole 64-slot runs
+        const int mp = ms > 16 ? (ms + 15) / 16 * 16 : ms > 8 ? 16 : ms > 4 ? 8 : ms > 2 ? 4 : ms;
+        const long slots = (long)std::min(a.K, a.k_per_split) / 8 * mp;
+        if ((slots + 63) / 64 * 64 * 8 > FC_X_ELEMS) return hipErrorInvalidValue;
     }
-    return e;
+    dim3 grid((unsigned)((a.N + 63) / 64), (unsigned)a.k_splits, (unsigned)(a.grouped ? a.nseg : 1)), block(256);
+    const int mb = (ms + 15) / 16;
+    const void *t[4] = {reinterpret_cast<const void *>(&fc_bf16_kernel<1>),
+                        reinterpret_cast<const void *>(&fc_bf16_kernel<2>),
+                        reinterpret_cast<const void *>(&fc_bf16_kernel<3>),
+                        reinterpret_cast<const void *>(&fc_bf16_kernel<4>)};
+    const void *fn = t[mb - 1];
+    return submit(sk, fn, grid, block, a);
 }
 
 hipError_t launch_fc_f32(const FcArgs &a, const Sink &sk) {
-    if (!fc_args_ok(a) || a.k_splits != 1) return hipErrorInvalidValue;
+    if (!fc_args_ok(a) || a.k_splits != 1 || a.grouped) return hipErrorInvalidValue;
     const long n = (long)a.M * a.N;
     return submit(sk, reinterpret_cast<const void *>(&fc_f32_kernel), dim3((unsigned)((n + 255) / 256)), dim3(256), a);
 }

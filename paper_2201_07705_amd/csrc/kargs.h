@@ -91,6 +91,7 @@ struct FcSeg {
     const void *in;       // [frames][K] (the producer tensor, NHWC-flat)
     void *out;            // [frames][out_cs] internal, or [frames][cout] f32
     const float *scale, *shift;
+    const void *w;        // grouped launch: this segment's weights [N][K]
     int32_t f_start;      // first frame of the segment in the launch
 };
 
@@ -105,7 +106,11 @@ struct FcArgs {
     int32_t k_splits, k_per_split;
     float *partial;       // [k_splits][M][N]
     int32_t *counters;    // split-K: one arrival counter per workgroup
-                          // column (64 neurons), as in ConvArgs
+                          // column (64 neurons) and grid slice, as in
+                          // ConvArgs
+    int32_t grouped;      // bf16 kernel: every segment has its own weights
+                          // (seg[i].w; the same N, K and epilogue), one
+                          // grid slice (blockIdx.z) per segment
     FcSeg seg[GEMEL_MAX_SEG];
 };
 

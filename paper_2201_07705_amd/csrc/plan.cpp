@@ -719,11 +719,16 @@ bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int
 // (about 1024), with each split's input slice (16-frame blocks x depth) fitting
 // the kernel's 64 KB of LDS.
 void pick_fc_config(int64_t M, int64_t N, int64_t K, int &splits, int &kps) {
+    // M: frames of the largest grid slice (a grouped launch takes the
+    // configuration of one member's launch, so that its results are those
+    // of separate launches)
     const int64_t blocks = (N + 63) / 64;
     const int64_t want = (1024 + blocks - 1) / blocks;
     const int64_t maxs = std::max<int64_t>(1, K / 1024);
-    const int64_t fb = (M + 15) / 16 * 16;
-    const int64_t kps_cap = std::max<int64_t>(128, (32768 / fb - 8) / 128 * 128);
+    // frames staged in LDS (as the kernel computes them) and the depth that
+    // fits: kps * mp elements plus the last 64-slot run
+    const int64_t mp = M > 16 ? (M + 15) / 16 * 16 : M > 8 ? 16 : M > 4 ? 8 : M > 2 ? 4 : M;
+    const int64_t kps_cap = std::max<int64_t>(128, (32768 / mp - 64) / 128 * 128);
     splits = (int)std::max<int64_t>(1, std::min(want, maxs));
     splits = (int)std::max<int64_t>(splits, (K + kps_cap - 1) / kps_cap);
     kps = (int)round_up((K + splits - 1) / splits, 128);
@@ -791,11 +796,15 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
     // kernel's input conditions, resident weights, no mixed sizes
     auto groupable = [&](int s, int l) {
         const Layer &L = layer(s, l);
-        return ctx->opt.group_unmerged && bf16 && L.op == GEMEL_OP_CONV && L.group < 0 && L.exec &&
-               (L.exec->w_dev || ctx->cache_mode) &&
-               L.in_phys % 32 == 0 && (int64_t)L.in_phys * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES &&
+        if (!ctx->opt.group_unmerged || !bf16 || L.group >= 0 || !L.exec || !(L.exec->w_dev || ctx->cache_mode))
+            return false;
+        // the FC kernel over at most 64 frames in all; a layer whose weights
+        // alone fill the GPU's memory bandwidth keeps its own launch
+        if (L.op == GEMEL_OP_FC) return L.exec->w_bytes() <= ((size_t)64 << 20);
+        return L.op == GEMEL_OP_CONV && L.in_phys % 32 == 0 && (int64_t)L.in_phys * 2 + 128 <= GEMEL_ZERO_PAGE_BYTES &&
                (forced < 0 || (tile_is_dma(forced) && (tile_dma_depth(forced) == 32 || L.in_phys % 64 == 0)));
     };
+    std::map<int, int64_t> node_frames;   // frames of a grouped FC node so far
     std::vector<std::vector<int>> node_of((size_t)S);
     for (int s = 0; s < S; ++s) {
         const Model &m = model(s);
@@ -833,18 +842,22 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                 // epilogue, its k-th appearance in each): one grouped launch,
                 // each segment with its own weights
                 const int pooled = pool_of[(size_t)s][(size_t)l] >= 0;
-                std::vector<int64_t> sig = {-1, L.in_h, L.in_w, L.in_c, L.in_phys, L.out_c, L.out_phys, L.kh,
-                                            L.stride, L.pad, L.act, (int64_t)(L.slope * 1e6f), L.res >= 0,
-                                            L.res_mode, direct_output(L), L.out_paired, pooled};
+                std::vector<int64_t> sig = {-1, L.op, L.in_h, L.in_w, L.in_c, L.in_phys, L.out_c, L.out_phys,
+                                            L.kh, L.stride, L.pad, L.act, (int64_t)(L.slope * 1e6f), L.res >= 0,
+                                            L.res_mode, direct_output(L), L.out_paired, pooled,
+                                            (int64_t)L.exec->k};
                 sig.push_back(ungrouped_seen[{s, sig}]++);
                 auto it = group_node.find(sig);
-                if (it != group_node.end() && nodes[(size_t)it->second].mem.size() < GEMEL_MAX_SEG) {
+                const bool fits = L.op != GEMEL_OP_FC ||
+                                  (it != group_node.end() && node_frames[it->second] + nfr[(size_t)s] <= 64);
+                if (it != group_node.end() && nodes[(size_t)it->second].mem.size() < GEMEL_MAX_SEG && fits) {
                     nid = it->second;
                 } else {
                     nid = (int)nodes.size();
                     nodes.push_back(Node{L.op, {}});
                     group_node[sig] = nid;
                 }
+                node_frames[nid] += nfr[(size_t)s];
             } else {
                 nid = (int)nodes.size();
                 nodes.push_back(Node{L.op, {}});
@@ -1247,29 +1260,38 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
                     a.out_mode = direct ? OUT_NCHW_F32 : OUT_NHWC;
                     a.nseg = 0;
                     int f = 0;
+                    int64_t slice_frames = 0;
                     for (auto [s, l] : nd.mem) {
                         if (!nfr[(size_t)s]) continue;
                         FcSeg &sg = a.seg[a.nseg];
+                        // a grouped launch: each member with its own weights
+                        // and scale/shift
+                        Blob *mb = grouped ? layer(s, l).exec.get() : blob;
+                        if (grouped && ctx->cache_mode) Lc.wblobs.push_back(mb);
                         sg.in = in_ptr(s, layer(s, l).src0);
                         sg.out = direct ? nullptr : (void *)((char *)tptr(s, l) + row0 * esz);
-                        sg.scale = blob->aff_dev + row0;
-                        sg.shift = blob->aff_dev + blob->rows + row0;
+                        sg.scale = mb->aff_dev + row0;
+                        sg.shift = mb->aff_dev + mb->rows + row0;
+                        sg.w = grouped ? mb->w_dev : nullptr;
                         sg.f_start = f;
+                        slice_frames = grouped ? std::max<int64_t>(slice_frames, nfr[(size_t)s]) : M;
                         if (direct) Lc.patches.push_back({Patch::OUTPUT, s, layer(s, l).out_index, a.nseg});
                         f += nfr[(size_t)s];
                         a.nseg++;
                     }
                     Lc.kind = GEMEL_K_FC;
+                    a.grouped = grouped ? 1 : 0;
                     if (fc_f32) {
                         a.k_splits = 1;
                         a.k_per_split = a.K;
                         Lc.type = L_FC_F32;
                     } else {
-                        pick_fc_config(a.M, a.N, a.K, a.k_splits, a.k_per_split);
+                        pick_fc_config(slice_frames, a.N, a.K, a.k_splits, a.k_per_split);
                         Lc.type = L_FC_BF16;
                         if (a.k_splits > 1) {
                             step_partial[(size_t)step] = std::max(step_partial[(size_t)step], (size_t)a.k_splits * a.M * a.N * 4);
-                            if (ctx->opt.splitk_fused) Lc.ctr_n = (a.N + 63) / 64;
+                            if (ctx->opt.splitk_fused)
+                                Lc.ctr_n = (a.N + 63) / 64 * (grouped ? a.nseg : 1);
                         }
                     }
                     P.launches.push_back(Lc);
@@ -1864,8 +1886,11 @@ static gemel_status enqueue_body(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hi
             for (Blob *b : L.wblobs)
                 if (b->loaded_round == ctx->cache_round)
                     HIPCHK(hipStreamWaitEvent(ls, b->ev_loaded, 0), "hipStreamWaitEvent");
-            if (L.conv.grouped)
+            const bool fcl = L.type == L_FC_BF16 || L.type == L_FC_REDUCE;
+            if (!fcl && L.conv.grouped)
                 for (size_t i = 0; i < L.wblobs.size() && (int)i < L.conv.nseg; ++i) L.conv.seg[i].w = L.wblobs[i]->w_dev;
+            if (fcl && L.fc.grouped)
+                for (size_t i = 0; i < L.wblobs.size() && (int)i < L.fc.nseg; ++i) L.fc.seg[i].w = L.wblobs[i]->w_dev;
             wptr = L.wblobs[0]->w_dev;
         }
         if (L.chunk >= 0) {

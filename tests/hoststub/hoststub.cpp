@@ -502,7 +502,12 @@ static hipError_t fc_common(const FcArgs &a, int esz, const char *kern, bool rea
     }
     const bool split = a.k_splits > 1;
     const bool writes_out = !reads_w || !split || a.counters;
-    if (reads_w) ok &= chk(a.w, (long long)a.N * a.K * esz, "weights", kern);
+    if (a.grouped && esz != 2) ok = false;
+    if (reads_w && esz == 2 && split && a.counters)
+        ok &= chk(a.counters, (long long)(a.N + 63) / 64 * (a.grouped ? a.nseg : 1) * 4, "counters", kern, true);
+    if (reads_w && !a.grouped) ok &= chk(a.w, (long long)a.N * a.K * esz, "weights", kern);
+    for (int i = 0; reads_w && a.grouped && i < a.nseg; ++i)
+        ok &= chk(a.seg[i].w, (long long)a.N * a.K * esz, "segment weights", kern);
     for (int i = 0; i < a.nseg; ++i) {
         const FcSeg &s = a.seg[i];
         const long long frames = (i + 1 < a.nseg ? a.seg[i + 1].f_start : a.M) - s.f_start;

@@ -365,3 +365,54 @@ def test_grouped_unmerged_workloads(name, kw):
     for a, b in zip(outs[0], outs[1]):
         for x, y in zip(a, b):
             assert np.array_equal(x, y)
+
+
+FC_GROUP_CASES = [
+    # producer C x H x W, FC widths, frames per model
+    ((64, 7, 7), (520, 1000), (3, 5)),
+    ((512, 7, 7), (4096, 1000), (8, 8)),
+    ((32, 4, 4), (264,), (20, 30, 40)),   # more than 64 frames: two nodes
+]
+
+
+@pytest.mark.parametrize("fused", [0, 1], ids=["reduce", "fused"])
+@pytest.mark.parametrize("case", FC_GROUP_CASES, ids=lambda c: f"{c[0][0]}x{c[0][1]}-{'-'.join(map(str, c[2]))}")
+def test_grouped_unmerged_fc_exact(case, fused):
+    """The same unmerged FC stack in several models (each its own weights,
+    bias and frame count) as grouped FC launches (one grid slice per model):
+    against the oracle, and bitwise equal to one launch per model (the
+    grouped launch takes one member's split configuration)."""
+    import numpy as np
+    from paper_2201_07705_amd import gemel as G
+    (c, h, w), widths, frames = case
+    log(f"grouped fc {case} fused {fused}")
+    lay = [conv("c", -1, 8, c, 1, 1, 0, bias=True, act="relu")]
+    k = c * h * w
+    for i, n in enumerate(widths):
+        lay.append(L(f"fc{i}", "fc", i, cin=k, cout=n, bias=True,
+                     act="relu" if i + 1 < len(widths) else "none",
+                     out=i + 1 == len(widths)))
+        k = n
+    models = [ModelSpec(f"m{i}", "custom", lay, n, (8, h, w))
+              for i, n in enumerate(frames)]
+    wl = Workload("fcgroup", 17, "bf16", models, [], "normal")
+    params = [wl.params(i) for i in range(len(models))]
+    fr = [wl.frames(i) for i in range(len(models))]
+    outs, launches = [], []
+    for grouped in (1, 0):
+        g = GpuWorkload(wl, params)
+        try:
+            g.ctx.set_option(G.OPT_GROUP_UNMERGED, grouped)
+            g.ctx.set_option(G.OPT_SPLITK_FUSED, fused)
+            g.ctx.set_option(G.OPT_TUNE, 0)
+            outs.append(g.run(fr))
+            launches.append(g.ctx.query(G.Q_LAUNCHES))
+        finally:
+            g.close()
+    log(f"launches grouped {launches[0]}, per model {launches[1]}")
+    assert launches[0] < launches[1], launches
+    compare(wl, outs[0], oracle_outputs(wl, params, fr), tol=BF16_LAYER_TOL,
+            check_argmax=False, tag="fc-grouped")
+    for a, b in zip(outs[0], outs[1]):
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)
