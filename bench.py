@@ -242,6 +242,199 @@ def run_workload(wl, args, options, G, P, torch, steps, warmup,
     }
 
 
+def host_link_gbs(torch, mib=256, reps=10):
+    """Pinned host to device copy rate (GB/s) of one large transfer."""
+    src = torch.empty(mib << 20, dtype=torch.uint8).pin_memory()
+    dst = torch.empty(mib << 20, dtype=torch.uint8, device="cuda")
+    for _ in range(2):
+        dst.copy_(src, non_blocking=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        dst.copy_(src, non_blocking=True)
+    torch.cuda.synchronize()
+    return reps * (mib << 20) / (time.perf_counter() - t0) / 1e9
+
+
+def swap_leg(wl, G, P, torch, steps):
+    """Weight swapping on a budget (Section 3.2; Section 5.4 and Appendix
+    A.4 for the weight cache): round times with swapping against the same
+    rounds with every weight resident, the bytes each round copies, and the
+    ideal round time max(resident round, bytes / measured host-link rate)
+    that perfect overlap of copies and compute would reach. How much of
+    the copies actually overlaps kernels comes from a trace
+    (--trace-summary)."""
+    log(f"swap leg on {wl.name}: seeded inputs")
+    params = [wl.params(i) for i in range(len(wl.models))]
+    frames = [wl.frames(i) for i in range(len(wl.models))]
+    dev = [torch.from_numpy(f).cuda() for f in frames]
+    rate = host_link_gbs(torch)
+    log(f"host link {rate:.1f} GB/s")
+
+    def context(opts):
+        ctx = P.Context(0, wl.dtype)
+        ids = [ctx.register_model(m.layers, params[i], m.in_chw)
+               for i, m in enumerate(wl.models)]
+        ctx.merge([[(ids[a], b) for a, b in g] for g in wl.groups])
+        for k, v in dict(wl.options, **opts).items():
+            ctx.set_option(getattr(G, "OPT_" + k.upper()), int(v))
+        return ctx, ids
+
+    def timed(ctx, ids, rounds, reps):
+        """ms per round of the round list (model index lists), after two
+        untimed passes; loaded bytes per round of the last pass."""
+        stream = torch.cuda.Stream()
+        outs = {i: ctx.alloc_outputs([ids[i]], [wl.models[i].n_frames])[0]
+                for i in range(len(ids))}
+
+        def one_pass(record):
+            loaded = []
+            for r, sub in enumerate(rounds):
+                nxt = rounds[(r + 1) % len(rounds)]
+                if ctx.query(G.Q_CACHE_CAPACITY):
+                    ctx.set_next_round([ids[i] for i in nxt])
+                ctx.infer([ids[i] for i in sub], [dev[i] for i in sub],
+                          stream=stream, outputs=[outs[i] for i in sub])
+                if record:
+                    loaded.append(ctx.query(G.Q_ROUND_LOADED_BYTES))
+            return loaded
+        with torch.cuda.stream(stream):
+            for _ in range(2):
+                one_pass(False)
+            while ctx.query(G.Q_ROUND_TUNING) > 0:
+                one_pass(False)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        loaded = []
+        with torch.cuda.stream(stream):
+            for _ in range(reps):
+                loaded = one_pass(True)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / (reps * len(rounds)), loaded
+
+    out = {"workload": wl.name, "host_link_gbs": rate}
+    all_models = [list(range(len(wl.models)))]
+    # streaming: every model in one round, the budget's non-resident
+    # weights copied through the staging slots every round
+    ctx, ids = context({})
+    unmerged = ctx.query(G.Q_UNMERGED_BYTES)
+    budget = int(wl.budget_frac * unmerged)
+    ctx.close()
+    ctx, ids = context({"WEIGHT_BUDGET": budget})
+    ms_s, _ = timed(ctx, ids, all_models, steps)
+    streamed = ctx.query(G.Q_STREAMED_BYTES)
+    ctx.close()
+    ctx, ids = context({})
+    ms_r, _ = timed(ctx, ids, all_models, steps)
+    ctx.close()
+    copy_ms = streamed / rate / 1e6
+    out["streaming"] = {
+        "budget_bytes": budget, "round_ms": ms_s, "resident_round_ms": ms_r,
+        "copied_bytes_per_round": streamed, "copy_ms_at_link_rate": copy_ms,
+        "ideal_round_ms": max(ms_r, copy_ms),
+        "frames_per_s": wl.total_frames() / ms_s * 1e3}
+    log(f"streaming {ms_s:.2f} ms/round vs resident {ms_r:.2f}, "
+        f"{streamed / 1e6:.0f} MB copied")
+    # weight cache: round-robin rounds over subsets in the library's
+    # sharing-aware load order; the budget grows by quarters from the
+    # streaming one until the rounds' pinned weights fit the cache
+    for per in (1, 2):
+        b = budget
+        while True:
+            ctx, ids = context({"WEIGHT_BUDGET": b, "SWAP_CACHE": 1})
+            order = ctx.load_order(ids)
+            idx = [ids.index(i) for i in order]
+            rounds = [idx[i:i + per] for i in range(0, len(idx), per)]
+            try:
+                ms_c, loaded = timed(ctx, ids, rounds, max(2, steps // 10))
+                cap = ctx.query(G.Q_CACHE_CAPACITY)
+                ctx.close()
+                break
+            except G.GemelError as e:
+                ctx.close()
+                if e.code != G.EBUDGET or b > 4 * budget:
+                    raise
+                b = b * 5 // 4
+        ctx, ids = context({})
+        ms_rr, _ = timed(ctx, ids, rounds, max(2, steps // 10))
+        ctx.close()
+        lb = sum(loaded) / len(loaded)
+        cms = lb / rate / 1e6
+        out[f"cache_{per}_per_round"] = {
+            "budget_bytes": b, "cache_bytes": cap, "rounds_per_cycle": len(rounds),
+            "round_ms": ms_c, "resident_round_ms": ms_rr,
+            "loaded_bytes_per_round": lb, "copy_ms_at_link_rate": cms,
+            "ideal_round_ms": max(ms_rr, cms)}
+        log(f"cache, {per} model(s) per round: {ms_c:.2f} ms/round vs "
+            f"resident {ms_rr:.2f}, {lb / 1e6:.0f} MB loaded per round")
+    return out
+
+
+def trace_summary(path, gap_ms=50.0):
+    """Copy/compute overlap from a rocprofv3 CSV trace directory (kernel and
+    memory-copy traces): the run is cut into phases at idle gaps longer
+    than gap_ms; per phase, host-to-device copy count, bytes unknown to the
+    trace, busy time of the copy engine and of the kernels, and the time
+    both were busy (the copy time hidden behind compute)."""
+    import csv
+    import glob
+
+    def intervals(pattern, pred):
+        out = []
+        for f in glob.glob(os.path.join(path, pattern)):
+            for r in csv.DictReader(open(f)):
+                if pred(r):
+                    out.append((int(r["Start_Timestamp"]),
+                                int(r["End_Timestamp"])))
+        return sorted(out)
+
+    def union(iv):
+        out = []
+        for a, b in iv:
+            if out and a <= out[-1][1]:
+                out[-1][1] = max(out[-1][1], b)
+            else:
+                out.append([a, b])
+        return out
+
+    def length(u):
+        return sum(b - a for a, b in u)
+
+    def inter(u, v):
+        i = j = 0
+        t = 0
+        while i < len(u) and j < len(v):
+            a, b = max(u[i][0], v[j][0]), min(u[i][1], v[j][1])
+            t += max(0, b - a)
+            if u[i][1] < v[j][1]:
+                i += 1
+            else:
+                j += 1
+        return t
+
+    cp = intervals("*memory_copy_trace.csv",
+                   lambda r: "HOST_TO_DEVICE" in r.get("Direction", ""))
+    kn = intervals("*kernel_trace.csv", lambda r: True)
+    everything = union(sorted(cp + kn))
+    phases = [[everything[0][0], everything[0][1]]]
+    for a, b in everything[1:]:
+        if a - phases[-1][1] > gap_ms * 1e6:
+            phases.append([a, b])
+        else:
+            phases[-1][1] = b
+    rows = []
+    for a, b in phases:
+        c = union([x for x in cp if a <= x[0] < b])
+        k = union([x for x in kn if a <= x[0] < b])
+        if not c:
+            continue
+        rows.append({"span_ms": (b - a) / 1e6, "copies": sum(1 for x in cp if a <= x[0] < b),
+                     "copy_busy_ms": length(c) / 1e6, "kernel_busy_ms": length(k) / 1e6,
+                     "copy_hidden_ms": inter(c, k) / 1e6,
+                     "copy_hidden_fraction": inter(c, k) / max(1, length(c))})
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -254,6 +447,12 @@ def main():
                          "reported under 'also' (the other configuration "
                          "the conv target is quoted on); 'none' to skip")
     ap.add_argument("--also-steps", type=int, default=100)
+    ap.add_argument("--swap", default="mix8_budget40",
+                    help="workload with a weight budget measured under "
+                         "'swap' (streaming every round, and the weight "
+                         "cache over one- and two-model rounds); 'none' to "
+                         "skip")
+    ap.add_argument("--swap-steps", type=int, default=20)
     ap.add_argument("--profile-steps", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -266,9 +465,17 @@ def main():
                          "SPLITK_FUSED=0 (repeatable)")
     ap.add_argument("--sources-hash", action="store_true",
                     help="print the hash recorded with traffic figures")
+    ap.add_argument("--trace-summary", metavar="DIR",
+                    help="only summarise copy/compute overlap of a rocprofv3 "
+                         "CSV trace directory (kernel and memory-copy "
+                         "traces), one JSON line per phase")
     args = ap.parse_args()
     if args.sources_hash:
         print(sources_hash())
+        return
+    if args.trace_summary:
+        for row in trace_summary(args.trace_summary):
+            print(json.dumps(row))
         return
     if args.calibrate_copy:
         import torch
@@ -314,6 +521,10 @@ def main():
             "kernels": a["kern"],
         }
 
+    swap = None
+    if args.swap != "none":
+        swap = swap_leg(configs.get(args.swap), G, P, torch, args.swap_steps)
+
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle on host cores)")
@@ -343,6 +554,7 @@ def main():
         "launches_per_step": main_r["launches"],
         "options": main_r["options"],
         "also": also,
+        "swap": swap,
     }
     print(json.dumps(line), flush=True)
 

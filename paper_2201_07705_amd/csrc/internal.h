@@ -40,6 +40,7 @@ struct Blob {
     int64_t cache_off = -1;
     hipEvent_t ev_loaded = nullptr;
     int loaded_round = -1;           // round of the last load
+    int used_round = -1;             // last round that needed it
 };
 
 struct Layer {
@@ -272,6 +273,18 @@ struct gemel_ctx {
     char *cache_base = nullptr;
     size_t cache_cap = 0;
     int cache_round = 0;
+    // end of the last two cache rounds (slot r % 2 holds round
+    // cache_done_round[r % 2]): a copy waits only for the rounds that last
+    // used the bytes it overwrites, so the next round's loads can overlap
+    // the current round's compute
+    hipEvent_t ev_cache_done[2] = {nullptr, nullptr};
+    int cache_done_round[2] = {-1, -1};
+    // cache bytes freed by evictions and the last round that used them
+    struct Freed {
+        int64_t off, size;
+        int round;
+    };
+    std::vector<Freed> cache_freed;
     std::vector<int> next_models;
     int64_t round_loaded = 0, round_evicted = 0;
     std::map<std::vector<int>, std::unique_ptr<gemel::Plan>> plans;

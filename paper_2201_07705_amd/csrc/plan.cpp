@@ -111,7 +111,14 @@ void free_placement(gemel_ctx *ctx) {
         b->index = -1;
         b->cache_off = -1;
         b->loaded_round = -1;
+        b->used_round = -1;
     }
+    for (int i = 0; i < 2; ++i) {
+        if (ctx->ev_cache_done[i]) (void)hipEventDestroy(ctx->ev_cache_done[i]);
+        ctx->ev_cache_done[i] = nullptr;
+        ctx->cache_done_round[i] = -1;
+    }
+    ctx->cache_freed.clear();
     ctx->cache_mode = false;
     ctx->cache_base = nullptr;
     ctx->cache_cap = 0;
@@ -402,6 +409,12 @@ gemel_status materialise(gemel_ctx *ctx) {
         ctx->cache_base = (char *)ctx->wpool + off;
         ctx->cache_cap = cache_cap;
         ctx->cache_round = 0;
+        for (int k = 0; k < 2; ++k)
+            if (hipEventCreateWithFlags(&ctx->ev_cache_done[k], hipEventDisableTiming) != hipSuccess) {
+                ctx->ev_cache_done[k] = nullptr;
+                free_placement(ctx);
+                return fail(ctx, GEMEL_EDEVICE, "event creation failed");
+            }
     }
     if (slots) {
         if (alloc_device(ctx, &ctx->staging, staging_bytes) != hipSuccess) {
@@ -1659,6 +1672,10 @@ static void join_partial_round(gemel_ctx *ctx, Plan &P, hipStream_t st) {
     if (ctx->ev_round_done && hipEventRecord(ctx->ev_round_done, st) == hipSuccess) {
         ctx->round_stream = st;
         ctx->round_seen = true;
+        const int slot = ctx->cache_round & 1;
+        if (ctx->cache_mode && ctx->ev_cache_done[slot] &&
+            hipEventRecord(ctx->ev_cache_done[slot], st) == hipSuccess)
+            ctx->cache_done_round[slot] = ctx->cache_round;
     }
     (void)hipGetLastError();
 }
@@ -1746,17 +1763,41 @@ static gemel_status cache_round(gemel_ctx *ctx, Plan &P, hipStream_t st) {
         loaded.push_back(b);
     }
     // commit
+    const int R = ctx->cache_round;
     int64_t lb = 0, eb = 0;
     for (Blob *v : evicted) {
+        ctx->cache_freed.push_back({v->cache_off, sz(v), v->used_round});
         v->cache_off = -1;
         v->w_dev = nullptr;
         eb += sz(v);
     }
-    if (!loaded.empty() && ctx->round_seen)
-        HIPCHK(hipStreamWaitEvent(ctx->side, ctx->ev_round_done, 0), "hipStreamWaitEvent");
+    for (Blob *b : needed) b->used_round = R;
+    // a copy overwrites bytes that earlier rounds may still read: it waits
+    // for the end of the latest round that used them (the previous round
+    // only if it did; rounds further back are done by then or are waited
+    // for through the end of a later round, which follows them)
+    auto done_event = [&](int round) -> hipEvent_t {
+        const int slot = round & 1;
+        return ctx->cache_done_round[slot] == round ? ctx->ev_cache_done[slot] : ctx->ev_round_done;
+    };
+    int waited = 0;   // the side stream has waited for every round < waited + 1
+    auto wait_for = [&](int round) -> gemel_status {
+        if (round < 1 || round <= waited || !ctx->round_seen) return GEMEL_OK;
+        HIPCHK(hipStreamWaitEvent(ctx->side, done_event(round), 0), "hipStreamWaitEvent");
+        waited = round;
+        return GEMEL_OK;
+    };
     for (Blob *b : loaded) {
         b->cache_off = at[b];
         b->w_dev = ctx->cache_base + b->cache_off;
+        // the latest round that used any freed bytes this copy overwrites
+        int last = 0;
+        for (const auto &f : ctx->cache_freed)
+            if (f.off < b->cache_off + sz(b) && b->cache_off < f.off + f.size) last = std::max(last, f.round);
+        {
+            const gemel_status ws = wait_for(std::max(last, R - 2));
+            if (ws) return ws;
+        }
         lb += sz(b);
         ctx->copies_issued++;
         if (ctx->opt.fail_copy_at && ctx->copies_issued == ctx->opt.fail_copy_at) {
@@ -1770,6 +1811,17 @@ static gemel_status cache_round(gemel_ctx *ctx, Plan &P, hipStream_t st) {
         HIPCHK(hipEventRecord(b->ev_loaded, ctx->side), "hipEventRecord");
         b->loaded_round = ctx->cache_round;
     }
+    // freed bytes now occupied by this round's blobs need no record; the
+    // rest keep theirs (entries older than two rounds only ever ask for a
+    // wait on a round the side stream has passed)
+    std::vector<gemel_ctx::Freed> keep;
+    for (const auto &f : ctx->cache_freed) {
+        bool covered = false;
+        for (Blob *b : loaded)
+            if (b->cache_off <= f.off && f.off + f.size <= b->cache_off + sz(b)) covered = true;
+        if (!covered && f.round >= R - 2) keep.push_back(f);
+    }
+    ctx->cache_freed.swap(keep);
     ctx->round_loaded = lb;
     ctx->round_evicted = eb;
     (void)st;
@@ -2183,6 +2235,11 @@ gemel_status run(gemel_ctx *ctx, const int32_t *model_ids, int32_t n_models, con
         HIPCHK(hipEventRecord(ctx->ev_round_done, stream), "hipEventRecord");
         ctx->round_stream = stream;
         ctx->round_seen = true;
+        if (ctx->cache_mode) {
+            const int slot = ctx->cache_round & 1;
+            HIPCHK(hipEventRecord(ctx->ev_cache_done[slot], stream), "hipEventRecord");
+            ctx->cache_done_round[slot] = ctx->cache_round;
+        }
         return GEMEL_OK;
     };
     const bool graphable = will_graph && P.chunks.empty() && !ctx->cache_mode;
