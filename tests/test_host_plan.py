@@ -58,8 +58,6 @@ CASES = [
     ("yolov3x3", {"res": 96, "frames": 2},
      {"OPT_STREAMS": 8, "OPT_USE_GRAPH": 0}),
     ("yolov3x3", {"res": 96, "frames": 2}, {}),
-    ("yolov3x3", {"res": 96, "frames": 2},
-     {"OPT_STREAMS": 8, "OPT_FORK_US": 0}),
     ("r50x2_vgg16x2", {"res": 64, "frames": 2},
      {"OPT_STREAMS": 8, "OPT_FORK_US": 0, "OPT_GRAPH_DAG": 1,
       "OPT_AUTOTUNE": 0}),
@@ -72,9 +70,11 @@ CASES = [
       "OPT_SPLITK_FUSED": 0}),
     ("yolov3x3", {"res": 96, "frames": 2}, {"OPT_TUNE": 0}),
     ("mix8_budget40", {"res": 32, "frames": 2}, {}),
+    # small staging slots: many segments per round, slots reused in a round
+    ("mix8_budget40", {"res": 32, "frames": 1},
+     {"OPT_SWAP_SLOT_BYTES": 1 << 20, "OPT_SWAP_SLOTS": 2}),
     ("variants", {"res": 32, "frames": 2}, {}),
     ("chain", {"route": True}, {}),
-    ("yolov3x3", {"res": 96, "frames": 2}, {"OPT_GROUP_UNMERGED": 1}),
     # grouped launches of ragged segments, fused split-K (one arrival
     # counter per output tile of every segment)
     ("grouped", {"case": 1}, {"OPT_GROUP_UNMERGED": 1, "OPT_CONV_TILE": 12,
@@ -88,9 +88,6 @@ CASES = [
      {"OPT_GROUP_UNMERGED": 1, "OPT_CONV_SPLITS": 3, "OPT_SPLITK_FUSED": 0}),
     ("chain", {"route": True}, {"OPT_CONV_SPLITS": 3, "OPT_SPLITK_FUSED": 0}),
     ("chain", {"route": False}, {"OPT_CONV_SPLITS": 2, "OPT_SPLITK_FUSED": 2}),
-    ("mix8_budget40", {"res": 32, "frames": 2},
-     {"OPT_SWAP_SLOT_BYTES": 1 << 20, "OPT_SWAP_SLOTS": 2,
-      "OPT_STREAMS": 3, "OPT_USE_GRAPH": 0}),
 ]
 
 
@@ -173,9 +170,13 @@ def test_captured_round_that_streams_weights_is_refused(hostlib):
     assert out["violations"] == 0 and out["hazards"] == 0, out["last"]
 
 
-@pytest.mark.parametrize("at", [1, 3, 7, 20])
-@pytest.mark.parametrize("opts", [{}, {"OPT_STREAMS": 1}])
-@pytest.mark.parametrize("streams", [[0, 0, 0, 1], [0, 0, 1, 2]])
+@pytest.mark.parametrize("at,opts,streams", [
+    (1, {}, [0, 0, 0, 1]),                      # before the first launch
+    (7, {}, [0, 0, 0, 1]),
+    (20, {"OPT_STREAMS": 1}, [0, 0, 0, 1]),
+    (3, {}, [0, 0, 1, 2]),                      # next round on another stream
+    (20, {}, [0, 0, 1, 2]),
+])
 def test_copy_failure_part_way_leaves_rounds_ordered(hostlib, at, opts,
                                                      streams):
     """A weight copy that fails after launches (and the fork to worker
