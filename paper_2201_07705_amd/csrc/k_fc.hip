@@ -78,10 +78,9 @@ __device__ __forceinline__ void fc_wait_vm0() { __builtin_amdgcn_s_waitcnt((0x7 
 
 template <int MB>  // frame blocks of 16
 __global__ __launch_bounds__(256) void fc_bf16_kernel(const FcArgs a) {
-    constexpr int RB = 1;           // row blocks of 16 neurons per wave
-    constexpr int COLS = 64 * RB;   // neurons of a workgroup
+    constexpr int COLS = 64;   // neurons of a workgroup, 16 per wave
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int n0 = blockIdx.x * COLS + wave * 16 * RB;
+    const int n0 = blockIdx.x * COLS + wave * 16;
     const int k_begin = blockIdx.y * a.k_per_split;
     const int k_end = min(a.K, k_begin + a.k_per_split);
     const int g = lane >> 4;
@@ -103,30 +102,23 @@ __global__ __launch_bounds__(256) void fc_bf16_kernel(const FcArgs a) {
         }
     }
     const int mz = f1 - f0;
-    const u16 *wrow[RB];
-    bool row_ok[RB];
-#pragma unroll
-    for (int r = 0; r < RB; ++r) {
-        const int row = n0 + r * 16 + (lane & 15);
-        row_ok[r] = row < a.N;
-        wrow[r] = (const u16 *)wsrc + (size_t)(row_ok[r] ? row : 0) * a.K;
-    }
-    // depth steps of 256: per row block 8 weight chunks of 16 bytes per lane
+    const int row = n0 + (lane & 15);
+    const bool row_ok = row < a.N;
+    const u16 *wrow = (const u16 *)wsrc + (size_t)(row_ok ? row : 0) * a.K;
+    // depth steps of 256: 8 weight chunks of 16 bytes per lane
     // (lane g of a row covers 32 contiguous bytes of every 128), the next
     // step's weights loaded while the current step's MFMAs run. The first
     // step is requested before the input slice is staged, so that its
     // latency overlaps the staging.
     constexpr int KS = 256, WJ = KS / 32;
-    auto wload = [&](int k, uint4 (&wv)[RB][WJ]) __attribute__((always_inline)) {
+    auto wload = [&](int k, uint4 (&wv)[WJ]) __attribute__((always_inline)) {
 #pragma unroll
-        for (int r = 0; r < RB; ++r)
-#pragma unroll
-            for (int j = 0; j < WJ; ++j) {
-                const int kk = k + j * 32 + g * 8;
-                wv[r][j] = (row_ok[r] && kk < k_end) ? *(const uint4 *)(wrow[r] + kk) : make_uint4(0, 0, 0, 0);
-            }
+        for (int j = 0; j < WJ; ++j) {
+            const int kk = k + j * 32 + g * 8;
+            wv[j] = (row_ok && kk < k_end) ? *(const uint4 *)(wrow + kk) : make_uint4(0, 0, 0, 0);
+        }
     };
-    uint4 w0[RB][WJ], w1[RB][WJ];
+    uint4 w0[WJ], w1[WJ];
     if (n0 < a.N) wload(k_begin, w0);
     // the workgroup's slice of the inputs, [k_begin, k_end) x frames, staged
     // in LDS once: every wave reads it, and from LDS its reads need no wait
@@ -152,14 +144,11 @@ __global__ __launch_bounds__(256) void fc_bf16_kernel(const FcArgs a) {
         fc_wait_vm0();
     }
     __syncthreads();
-    f32x4 acc[MB][RB];
+    f32x4 acc[MB];
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int r = 0; r < RB; ++r) acc[mb][r] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // one input fragment from LDS feeds the MFMAs of every row block
-    auto step = [&](int k, const uint4 (&wv)[RB][WJ]) __attribute__((always_inline)) {
+    auto step = [&](int k, const uint4 (&wv)[WJ]) __attribute__((always_inline)) {
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
             uint4 xv[WJ];
@@ -172,10 +161,8 @@ __global__ __launch_bounds__(256) void fc_bf16_kernel(const FcArgs a) {
             }
 #pragma unroll
             for (int j = 0; j < WJ; ++j)
-#pragma unroll
-                for (int r = 0; r < RB; ++r)
-                    acc[mb][r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        __builtin_bit_cast(bf16x8, wv[r][j]), __builtin_bit_cast(bf16x8, xv[j]), acc[mb][r], 0, 0, 0);
+                acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    __builtin_bit_cast(bf16x8, wv[j]), __builtin_bit_cast(bf16x8, xv[j]), acc[mb], 0, 0, 0);
         }
     };
     if (n0 < a.N) {
@@ -188,22 +175,20 @@ __global__ __launch_bounds__(256) void fc_bf16_kernel(const FcArgs a) {
             }
         }
     }
-    // D[neuron = n0 + 16 r + 4 g + v][frame = mb*16 + lane%16]
+    // D[neuron = n0 + 4 g + v][frame = mb*16 + lane%16]
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
         const int f = f0 + mb * 16 + (lane & 15);
         if (f >= f1) continue;
 #pragma unroll
-        for (int r = 0; r < RB; ++r)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int n = n0 + r * 16 + g * 4 + v;
-                if (n >= a.N) continue;
-                if (a.k_splits > 1)
-                    store_partial1(a.partial + ((size_t)blockIdx.y * a.M + f) * a.N + n, acc[mb][r][v]);
-                else
-                    fc_store(a, f, n, acc[mb][r][v], true);
-            }
+        for (int v = 0; v < 4; ++v) {
+            const int n = n0 + g * 4 + v;
+            if (n >= a.N) continue;
+            if (a.k_splits > 1)
+                store_partial1(a.partial + ((size_t)blockIdx.y * a.M + f) * a.N + n, acc[mb][v]);
+            else
+                fc_store(a, f, n, acc[mb][v], true);
+        }
     }
     // fused split-K reduction: the last split of this column of neurons
     // sums the partials in split order, as fc_reduce does
@@ -211,7 +196,7 @@ __global__ __launch_bounds__(256) void fc_bf16_kernel(const FcArgs a) {
         __shared__ int flag;
         if (!splitk_arrive(a.counters + (a.grouped ? blockIdx.z * gridDim.x : 0) + blockIdx.x, a.k_splits, &flag))
             return;
-        // four items per thread, sixteen splits per batch of loads
+        // four items per thread, eight splits per batch of loads
         for (int i0 = threadIdx.x; i0 < mz * COLS; i0 += 4 * 256) {
             float sum[4] = {0.f, 0.f, 0.f, 0.f};
             bool ok[4];
