@@ -15,6 +15,29 @@ from paper_2201_07705_amd import gemel as G  # noqa: E402
 from workloads import configs  # noqa: E402
 
 
+def stub_params(layers):
+    """Parameter dicts of the shapes the workload generator makes, with
+    constant values."""
+    import numpy as np
+    out = []
+    for l in layers:
+        if l["op"] not in ("conv", "fc"):
+            out.append(None)
+            continue
+        shape = (l["cout"], l["cin"], l["kh"], l["kw"]) if l["op"] == "conv" \
+            else (l["cout"], l["cin"])
+        p = {"w": np.zeros(shape, np.float32), "b": None, "bn": None}
+        if l["bias"]:
+            p["b"] = np.zeros(l["cout"], np.float32)
+        if l["bn"]:
+            p["bn"] = (np.ones(l["cout"], np.float32),
+                       np.zeros(l["cout"], np.float32),
+                       np.zeros(l["cout"], np.float32),
+                       np.ones(l["cout"], np.float32), 1e-5)
+        out.append(p)
+    return out
+
+
 def main():
     libpath, name = sys.argv[1], sys.argv[2]
     kw = json.loads(sys.argv[3]) if len(sys.argv) > 3 else {}
@@ -59,7 +82,9 @@ def main():
                        for i, n in enumerate(frames)], [], "normal")
     else:
         wl = configs.get(name, **kw)
-    params = [wl.params(i) for i in range(len(wl.models))]
+    # the stub computes nothing: constant parameters of the right shapes
+    # (generating the seeded ones dominated the run time of large workloads)
+    params = [stub_params(m.layers) for m in wl.models]
 
     def dev(nbytes):
         p = ctypes.c_void_p()
