@@ -2,6 +2,7 @@
 // that the argument block matches what its kernel and grid assume and
 // returns hipErrorInvalidValue instead of launching otherwise.
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "kargs.h"
@@ -10,13 +11,17 @@ namespace gemel {
 
 // Where a launcher puts its kernel: enqueued on a stream, or, when graph is
 // set, added to that HIP graph as a kernel node that runs after the ndeps
-// nodes in deps (the new node is returned in *node).
+// nodes in deps (the new node is returned in *node). On a stream, ev_start
+// and ev_stop (if set) take the start and end time of the kernel's own
+// execution (hipExtLaunchKernel), not of its place in the stream.
 struct Sink {
     hipStream_t stream = nullptr;
     hipGraph_t graph = nullptr;
     const hipGraphNode_t *deps = nullptr;
     size_t ndeps = 0;
     hipGraphNode_t *node = nullptr;
+    hipEvent_t ev_start = nullptr;
+    hipEvent_t ev_stop = nullptr;
 };
 
 // Launch kernel fn (one by-value argument block of type A, no dynamic LDS)
@@ -24,6 +29,8 @@ struct Sink {
 template <typename A>
 inline hipError_t submit(const Sink &sk, const void *fn, dim3 grid, dim3 block, const A &args) {
     void *params[] = {const_cast<A *>(&args)};
+    if (!sk.graph && (sk.ev_start || sk.ev_stop))
+        return hipExtLaunchKernel(fn, grid, block, params, 0, sk.stream, sk.ev_start, sk.ev_stop, 0);
     if (!sk.graph) return hipLaunchKernel(fn, grid, block, params, 0, sk.stream);
     hipKernelNodeParams p{};
     p.func = const_cast<void *>(fn);

@@ -1968,14 +1968,15 @@ static gemel_status enqueue_body(gemel_ctx *ctx, Plan &P, const CallPtrs &cp, hi
                 ctx->prof.pool.pop_back();
             }
             ctx->prof.pending.push_back(rec);
-            HIPCHK(hipEventRecord(rec.a, ls), "hipEventRecord");
         }
         Sink sk;
         sk.stream = ls;
+        // profiled: the events take the kernel's own start and end times
+        sk.ev_start = rec.a;
+        sk.ev_stop = rec.b;
         hipError_t e = launch_one(L, cp, P, wptr, sk);
         if (e != hipSuccess) return fail(ctx, GEMEL_EDEVICE, std::string("kernel launch: ") + hipGetErrorString(e));
         if (ctx->opt.profile) {
-            HIPCHK(hipEventRecord(rec.b, ls), "hipEventRecord");
             for (int k : {L.kind, subset}) {
                 if (k < 0) continue;
                 ctx->prof.flops[k] += L.flops;

@@ -98,9 +98,14 @@ void begin_node(const gemel::Sink &sk, const char *kern) {
         n.deps = frontier[sk.stream];
         n.deps.insert(n.deps.end(), host_done.begin(), host_done.end());
         n.synced = synced;
+        const std::vector<int> before = frontier[sk.stream];
         eager.nodes.push_back(n);
         frontier[sk.stream] = {(int)eager.nodes.size() - 1};
         cur = &eager.nodes.back();
+        // kernel-timed events: the start follows what preceded the kernel
+        // on its stream, the stop follows the kernel
+        if (sk.ev_start) evstate[sk.ev_start] = before;
+        if (sk.ev_stop) evstate[sk.ev_stop] = frontier[sk.stream];
     }
 }
 
@@ -290,6 +295,9 @@ hipError_t hipDeviceSynchronize() {
 hipError_t hipGetLastError() { return hipSuccess; }
 const char *hipGetErrorString(hipError_t e) { return e == hipSuccess ? "success" : "stub error"; }
 hipError_t hipLaunchKernel(const void *, dim3, dim3, void **, size_t, hipStream_t) { return hipErrorInvalidValue; }
+hipError_t hipExtLaunchKernel(const void *, dim3, dim3, void **, size_t, hipStream_t, hipEvent_t, hipEvent_t, int) {
+    return hipErrorInvalidValue;
+}
 hipError_t hipStreamIsCapturing(hipStream_t s, hipStreamCaptureStatus *st) {
     *st = s && s == capturing ? hipStreamCaptureStatusActive : hipStreamCaptureStatusNone;
     return s ? hipSuccess : hipErrorInvalidValue;
