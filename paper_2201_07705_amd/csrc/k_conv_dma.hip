@@ -213,16 +213,21 @@ __global__ __launch_bounds__(64 * WM *WN, (dma_min_waves<BM, BN, WM, WN, STAGES,
             aW[i] = sW;
         } else if (gm < m_end) {
             int fr, ho, wo;
+            // quotients by multiply-high (the launcher's magic numbers): a
+            // per-lane integer division costs dozens of instructions
+            auto qdiv = [&](int n, int q) __attribute__((always_inline)) {
+                return (int)((__umulhi((uint32_t)n, a.dv_m[q]) + (uint32_t)n) >> a.dv_l[q]);
+            };
             if constexpr (pool2) {
                 const int g = gm >> 2;
-                fr = g / HWp;
-                const int pp = g - fr * HWp, hp = pp / Wp;
+                fr = qdiv(g, 0);
+                const int pp = g - fr * HWp, hp = qdiv(pp, 1);
                 ho = 2 * hp + ((gm >> 1) & 1);
                 wo = 2 * (pp - hp * Wp) + (gm & 1);
             } else {
-                fr = gm / HWo;
+                fr = qdiv(gm, 0);
                 const int pix = gm - fr * HWo;
-                ho = pix / a.Wo;
+                ho = qdiv(pix, 1);
                 wo = pix - ho * a.Wo;
             }
             const RowSeg sg = one_seg ? useg : row_seg(a, gm);
@@ -616,6 +621,23 @@ hipError_t launch_conv_dma(const ConvArgs &a, int tile, const Sink &sk) {
     if (tiles != conv_tiles(a, bm, bn)) return hipErrorInvalidValue;
     const long blocks = tiles >= 8 ? (tiles + 7) / 8 * 8 : tiles;
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
+    // magic numbers of the row decomposition (exact for rows below 2^31:
+    // m = floor(2^32 (2^l - d) / d) + 1 with l = ceil(log2 d))
+    {
+        const bool pool = a.out_mode == OUT_NHWC_POOL2;
+        const long d[2] = {pool ? (long)(a.Ho / 2) * (a.Wo / 2) : (long)a.Ho * a.Wo, pool ? a.Wo / 2 : a.Wo};
+        for (int q = 0; q < 2; ++q) {
+            if (d[q] <= 0) {
+                b.dv_m[q] = 1;
+                b.dv_l[q] = 0;
+                continue;
+            }
+            int l = 0;
+            while ((1L << l) < d[q]) ++l;
+            b.dv_m[q] = (uint32_t)(((uint64_t)1 << 32) * (uint64_t)((1L << l) - d[q]) / (uint64_t)d[q] + 1);
+            b.dv_l[q] = l;
+        }
+    }
     dim3 grid((unsigned)blocks, (unsigned)a.k_splits);
     hipError_t e = hipErrorInvalidValue;
     const int mode = a.out_mode == OUT_NHWC_POOL2 ? 1 : a.hetero ? 2 : 0;

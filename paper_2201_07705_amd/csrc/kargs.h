@@ -71,6 +71,11 @@ struct ConvArgs {
                           // zero between launches; the last split of a tile
                           // reduces the partials. Null: a separate reduce
                           // launch does.
+    uint32_t dv_m[2];     // LDS-DMA kernel (set by its launcher): row n of a
+    int32_t dv_l[2];      // frame splits as n / d = (umulhi(n, m) + n) >> l
+                          // for d = pixels per frame [0] and per row [1] of
+                          // the output (of the pooled output with a fused
+                          // pool)
     ConvSeg seg[GEMEL_MAX_SEG];
 };
 
