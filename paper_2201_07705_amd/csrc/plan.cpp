@@ -594,7 +594,9 @@ ReduceArgs reduce_args(const ConvArgs &a) {
 // Measured choice among the best-estimated configurations of one conv
 // launch: each candidate runs on the context's tuning stream over the
 // plan's own tensors (their contents are overwritten by every round), timed
-// launch by launch with HIP events; the smallest median wins. Results
+// launch by launch with HIP events bound to the kernels' own start and end
+// (hipExtLaunchKernel: the gap before the dispatch is not counted); the
+// smallest median wins. Results
 // are cached per conv shape for the life of the context. Returns false
 // (leaving tile/splits/kps alone) if nothing could be timed.
 bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int &tile, int &splits, int &kps) {
@@ -668,8 +670,9 @@ bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int
     }
     Sink sk;
     sk.stream = ctx->tune_stream;
-    // launch of candidate i
-    auto once = [&](size_t i) {
+    // launch of candidate i; timed: the events take the kernels' own start
+    // and end (the reduction's end where a separate launch reduces)
+    auto once = [&](size_t i, bool timed = false) {
         ConvArgs a = a0;
         if (wbytes) {
             a.w = ctx->tune_w;
@@ -685,8 +688,14 @@ bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int
         const bool fuse = sp > 1 && fuse_splitk(ctx, tiles);
         a.partial = sp > 1 ? (float *)ctx->tune_partial : nullptr;
         a.counters = fuse ? (int32_t *)ctx->tune_ctr : nullptr;
-        hipError_t e = launch_conv_bf16(a, c[i].tile, sk);
-        if (e == hipSuccess && sp > 1 && !fuse) e = launch_conv_reduce(reduce_args(a), bf16, sk);
+        const bool two = sp > 1 && !fuse;
+        Sink s1 = sk, s2 = sk;
+        if (timed) {
+            s1.ev_start = ctx->tune_ev[0];
+            (two ? s2 : s1).ev_stop = ctx->tune_ev[1];
+        }
+        hipError_t e = launch_conv_bf16(a, c[i].tile, s1);
+        if (e == hipSuccess && two) e = launch_conv_reduce(reduce_args(a), bf16, s2);
         return e;
     };
     // one untimed pass over every candidate, then kTuneReps passes timing
@@ -701,9 +710,7 @@ bool tune_conv(gemel_ctx *ctx, const ConvArgs &a0, int dma_depth, bool bf16, int
         for (size_t i = 0; i < c.size(); ++i) {
             if (!ok[i]) continue;
             float t = 0.f;
-            ok[i] = hipEventRecord(ctx->tune_ev[0], sk.stream) == hipSuccess && once(i) == hipSuccess &&
-                    hipEventRecord(ctx->tune_ev[1], sk.stream) == hipSuccess &&
-                    hipEventSynchronize(ctx->tune_ev[1]) == hipSuccess &&
+            ok[i] = once(i, true) == hipSuccess && hipEventSynchronize(ctx->tune_ev[1]) == hipSuccess &&
                     hipEventElapsedTime(&t, ctx->tune_ev[0], ctx->tune_ev[1]) == hipSuccess;
             if (ok[i]) ms[i].push_back(t);
         }
