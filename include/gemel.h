@@ -429,7 +429,8 @@ enum {
     GEMEL_OPT_WEIGHT_BUDGET = 5, /* replace the hbm_weight_budget given to
                                     gemel_create (bytes, 0 = unlimited)    */
     GEMEL_OPT_PROFILE = 6,       /* 1: time every kernel launch with HIP
-                                    events on the launch stream (disables
+                                    events bound to the kernel's own start
+                                    and end (hipExtLaunchKernel; disables
                                     graph replay); 0 (default): off. Setting
                                     it clears the collected statistics.    */
     GEMEL_OPT_CONV_TILE = 7,     /* -1 (default): pick each conv's tile
@@ -634,7 +635,8 @@ typedef struct gemel_kernel_stat {
     int32_t launches;    /* launches per round                              */
     double flops;        /* algorithmic FLOPs per round                     */
     double bytes;        /* algorithmic bytes per round                     */
-    double ms;           /* summed kernel time per round (HIP events)       */
+    double ms;           /* summed kernel time per round (HIP events on
+                            each kernel's own start and end)                */
 } gemel_kernel_stat;
 
 /*
