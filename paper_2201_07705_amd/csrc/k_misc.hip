@@ -193,7 +193,7 @@ static bool ew_ok(const EwArgs &a, bool need_in1) {
 
 static hipError_t ew_launch(const void *kern, long items_per_frame, const EwArgs &a, const Sink &sk) {
     const long items = items_per_frame * a.max_frames;
-    if (items <= 0) return hipSuccess;
+    if (items <= 0) return submit_nothing(sk);
     const long blocks = (items + 255) / 256;
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
     return submit(sk, kern, dim3((unsigned)blocks, (unsigned)a.nseg), dim3(256), a);
@@ -216,7 +216,7 @@ hipError_t launch_maxpool(const EwArgs &a, bool bf16, const Sink &sk) {
 hipError_t launch_avgpool(const EwArgs &a, bool bf16, const Sink &sk) {
     if (!ew_ok(a, false) || a.C % 8 || a.H <= 0 || a.W <= 0) return hipErrorInvalidValue;
     const long blocks = (long)a.max_frames * ((a.C / 8 + 63) / 64);
-    if (blocks <= 0) return hipSuccess;
+    if (blocks <= 0) return submit_nothing(sk);
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
     const void *k = bf16 ? reinterpret_cast<const void *>(&avgpool_kernel<u16>)
                          : reinterpret_cast<const void *>(&avgpool_kernel<float>);

@@ -252,6 +252,42 @@ def test_zero_frame_model_is_skipped(r18):
     assert outs[1][0].shape[0] == 0
 
 
+def test_profiled_round_times_every_kernel(r18):
+    """A profiled round (events bound to each kernel's own start and end)
+    over one model with frames and one without: every family that ran has a
+    positive time, the round's outputs equal the unprofiled ones bit for
+    bit, and the statistics read back after the zero-frame round as well."""
+    wl, params, frames = r18
+    log("profiled round with a zero-frame model")
+    g = _pinned(wl, params)
+    try:
+        import torch
+        full = g.run(frames)
+        g.ctx.set_option(G.OPT_PROFILE, 1)
+        s = torch.cuda.Stream()
+        dev = [torch.from_numpy(frames[0]).cuda(),
+               torch.empty((0, 3, 64, 64), device="cuda")]
+        for _ in range(2):
+            with torch.cuda.stream(s):
+                outs = g.ctx.infer(g.ids, dev, stream=s)
+        s.synchronize()
+        stats, rounds = g.ctx.profile()
+        prof = g.run(frames)
+        stats2, rounds2 = g.ctx.profile()
+    finally:
+        g.close()
+    assert rounds == 2 and rounds2 == 3
+    ran = {k: v for k, v in stats.items() if v["launches"]}
+    assert "conv_mfma" in ran
+    for k, v in ran.items():
+        assert np.isfinite(v["ms"]) and v["ms"] > 0, (k, v)
+    assert np.array_equal(outs[0][0].cpu().numpy(), full[0][0])
+    assert outs[1][0].shape[0] == 0
+    for a, b in zip(prof, full):
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)
+
+
 def test_injected_copy_failure_then_retry():
     wl = configs.mix8_budget40(res=32, frames=1)
     params = [wl.params(i) for i in range(len(wl.models))]
