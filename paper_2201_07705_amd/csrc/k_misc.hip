@@ -182,6 +182,18 @@ __global__ __launch_bounds__(256) void export_kernel(const EwArgs a) {
         if (cc * 8 + j < a.c_logical) o[j * hw] = v[j];
 }
 
+// A launcher with nothing to launch (no frames): the sink's timing events,
+// if any, are recorded on its stream where the kernel would have run, so
+// that they bound an empty interval instead of staying unrecorded.
+static hipError_t submit_nothing(const Sink &sk) {
+    if (sk.graph) return hipSuccess;
+    if (sk.ev_start) {
+        const hipError_t e = hipEventRecord(sk.ev_start, sk.stream);
+        if (e != hipSuccess) return e;
+    }
+    return sk.ev_stop ? hipEventRecord(sk.ev_stop, sk.stream) : hipSuccess;
+}
+
 static bool ew_ok(const EwArgs &a, bool need_in1) {
     if (a.nseg < 1 || a.nseg > GEMEL_MAX_SEG || a.max_frames < 0) return false;
     for (int i = 0; i < a.nseg; ++i) {

@@ -42,18 +42,6 @@ inline hipError_t submit(const Sink &sk, const void *fn, dim3 grid, dim3 block, 
     return hipGraphAddKernelNode(sk.node, sk.graph, sk.deps, sk.ndeps, &p);
 }
 
-// A launcher with nothing to launch (no frames): the sink's timing events,
-// if any, are recorded on its stream where the kernel would have run, so
-// that they bound an empty interval instead of staying unrecorded.
-inline hipError_t submit_nothing(const Sink &sk) {
-    if (sk.graph) return hipSuccess;
-    if (sk.ev_start) {
-        const hipError_t e = hipEventRecord(sk.ev_start, sk.stream);
-        if (e != hipSuccess) return e;
-    }
-    return sk.ev_stop ? hipEventRecord(sk.ev_stop, sk.stream) : hipSuccess;
-}
-
 // Tile configurations of the bf16 implicit-GEMM convolution.
 enum ConvTile {
     TILE_128x128 = 0,  // 4 waves, 64x64 per wave
