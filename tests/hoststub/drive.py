@@ -61,6 +61,10 @@ def main():
         sys.path.insert(0, os.path.join(ROOT, "tests"))
         from test_gpu_merging import _variants_workload
         wl = _variants_workload(**kw)
+    elif name == "many":     # more merged members than a launch holds (tests/test_gpu_merging.py)
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        from test_gpu_merging import _many_tiny
+        wl = _many_tiny(kw.get("n", 18), kw.get("dtype", "bf16"))
     elif name == "chain":    # a deep unmerged chain (tests/test_gpu_layers.py)
         sys.path.insert(0, os.path.join(ROOT, "tests"))
         from test_gpu_layers import _deep_chain

@@ -84,3 +84,45 @@ def test_mixed_size_launch_equals_one_launch_per_size(tile):
         for u, v in zip(x, y):
             assert np.array_equal(u, v)
     compare(wl, b, oracle_outputs(wl, params, frames), tag=f"variants-mixed-{tile}")
+
+
+def _many_tiny(n, dtype):
+    chw = (3, 24, 24)
+    models = [configs.ModelSpec(f"t{i}", "tiny", zoo.tiny(10), 1 + i % 3, chw)
+              for i in range(n)]
+    groups = configs.share_by_name(models, list(range(n)),
+                                   lambda name: name in ("conv1", "conv2"))
+    return configs.Workload(f"tiny{n}", 9, dtype, models, groups, "uniform")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_more_members_than_one_launch_holds(dtype):
+    """18 small CNNs share their first two convs: a merged layer has more
+    members than one launch's segment table holds (16), so it runs as
+    several launches over the one weight copy, and the input packs go 16
+    models at a time. Ragged frame counts (1-3 per model). Every output
+    against the oracle; with the tile pinned, bitwise equal to running
+    every merged layer per model."""
+    import numpy as np
+    from paper_2201_07705_amd import gemel as G
+    wl = _many_tiny(18, dtype)
+    params = [wl.params(i) for i in range(len(wl.models))]
+    fr = [wl.frames(i) for i in range(len(wl.models))]
+    log(f"18 merged members, {dtype}")
+    outs, launches = [], []
+    for split in (0, 1):
+        g = GpuWorkload(wl, params)
+        try:
+            if dtype == "bf16":
+                g.ctx.set_option(G.OPT_CONV_TILE, 2)
+                g.ctx.set_option(G.OPT_CONV_SPLITS, 1)
+            g.ctx.set_option(G.OPT_SPLIT_MERGED, split)
+            outs.append(g.run(fr))
+            launches.append(g.ctx.query(G.Q_LAUNCHES))
+        finally:
+            g.close()
+    assert launches[0] < launches[1], launches
+    compare(wl, outs[0], oracle_outputs(wl, params, fr), tag=f"tiny18-{dtype}")
+    for a, b in zip(outs[0], outs[1]):
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)

@@ -74,6 +74,8 @@ CASES = [
     ("mix8_budget40", {"res": 32, "frames": 1},
      {"OPT_SWAP_SLOT_BYTES": 1 << 20, "OPT_SWAP_SLOTS": 2}),
     ("variants", {"res": 32, "frames": 2}, {}),
+    ("many", {"n": 18, "dtype": "bf16"}, {}),
+    ("many", {"n": 18, "dtype": "f32"}, {"OPT_STREAMS": 4, "OPT_USE_GRAPH": 0}),
     ("chain", {"route": True}, {}),
     # grouped launches of ragged segments, fused split-K (one arrival
     # counter per output tile of every segment)
