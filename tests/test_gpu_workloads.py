@@ -100,3 +100,39 @@ def test_yolov3x3_full_size_class_argmax(yolo_full):
 
 def test_mix8_full_size_with_budget():
     _full_check(configs.mix8_budget40(), budget="auto", tag="mix8")
+
+
+# ---- three times the benchmark batch, sampled frames against the oracle ----
+
+def _sampled_check(wl, picks, tag):
+    """The whole batch through the library; the oracle on frames `picks` of
+    every model (each frame's outputs depend on that frame alone)."""
+    import numpy as np
+    params = [wl.params(i) for i in range(len(wl.models))]
+    fr = [wl.frames(i) for i in range(len(wl.models))]
+    log(f"{tag}: gpu run ({wl.total_frames()} frames)")
+    g = GpuWorkload(wl, params)
+    try:
+        got = g.run(fr)
+    finally:
+        g.close()
+    sub = [np.ascontiguousarray(f[picks]) for f in fr]
+    log(f"{tag}: oracle on frames {picks} of every model")
+    ref = oracle_outputs(wl, params, sub)
+    got_sub = [[o[picks] for o in m] for m in got]
+    e = compare(wl, got_sub, ref, tag=tag)
+    log(f"{tag}: worst normwise error {e:.3e}")
+
+
+def test_r50_vgg16_triple_batch_sampled():
+    """24 frames per model at 224x224 (merged launches over 48 frames, VGG's
+    first convs at 2.4 M GEMM rows): the first, a middle and the last frame
+    of every model against the oracle."""
+    _sampled_check(configs.r50x2_vgg16x2(frames=24), [0, 11, 23],
+                   "r50vgg-24f")
+
+
+def test_yolov3x3_triple_batch_sampled():
+    """12 frames per model at 416x416 (the merged backbone over 36 frames):
+    the first and the last frame of every model against the oracle."""
+    _sampled_check(configs.yolov3x3(frames=12), [0, 11], "yolo-12f")
