@@ -340,10 +340,12 @@ hipError_t hipGraphLaunch(hipGraphExec_t e, hipStream_t s) {
 
 namespace gemel {
 
-static const int kBm[TILE_COUNT] = {128, 128, 64, 256, 256, 256, 64, 128, 64, 256, 256, 128, 128, 256,
-                                    256, 256, 128, 128, 64, 64, 256, 128, 256, 64};
-static const int kBn[TILE_COUNT] = {128, 64, 64, 256, 128, 64, 64, 64, 128, 256, 128, 128, 64, 32,
-                                    256, 128, 128, 64, 64, 64, 128, 256, 64, 256};
+static const int kBm[] = {128, 128, 64, 256, 256, 256, 64, 128, 64, 256, 256, 128, 128, 256,
+                          256, 256, 128, 128, 64, 64, 256, 128, 256, 64};
+static const int kBn[] = {128, 64, 64, 256, 128, 64, 64, 64, 128, 256, 128, 128, 64, 32,
+                          256, 128, 128, 64, 64, 64, 128, 256, 64, 256};
+static_assert(sizeof(kBm) == TILE_COUNT * sizeof(int) && sizeof(kBn) == TILE_COUNT * sizeof(int),
+              "one entry per conv tile");
 int conv_tile_bm(int t) { return t >= 0 && t < TILE_COUNT ? kBm[t] : 0; }
 int conv_tile_bn(int t) { return t >= 0 && t < TILE_COUNT ? kBn[t] : 0; }
 int conv_tile_threads(int t) { return (t == TILE_256x256 || t == TILE_256x128) ? 512 : 256; }
