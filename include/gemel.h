@@ -572,7 +572,7 @@ enum {
                                     Results are those of separate launches
                                     of the same tile configuration. 0: one
                                     launch per model                       */
-    GEMEL_OPT_SWAP_CACHE = 20    /* with a weight budget: 1 = time-shared
+    GEMEL_OPT_SWAP_CACHE = 20,   /* with a weight budget: 1 = time-shared
                                     rounds over subsets of the models keep
                                     a weight cache across rounds (Section
                                     5.4: loading a model brings in only its
@@ -604,6 +604,15 @@ enum {
                                     budget keeps the largest blobs (merged
                                     ones first) resident and streams the
                                     rest through staging slots every round */
+    GEMEL_OPT_PREFETCH = 21      /* 1 (default): an LDS-DMA conv launch,
+                                    after its own tiles, reads the resident
+                                    weights (up to 16 MiB) of the next conv
+                                    launch of its stream into the L2 and
+                                    memory-side caches, so that launch's
+                                    depth loop starts on cache hits instead
+                                    of HBM reads (ungrouped, resident
+                                    weights only). Results are unchanged.
+                                    0: no prefetch                         */
 };
 
 /* Set an option; takes effect at the next gemel_infer. Errors: EINVAL. */

@@ -559,6 +559,18 @@ __global__ __launch_bounds__(64 * WM *WN, (dma_min_waves<BM, BN, WM, WN, STAGES,
     }
     if (a.k_splits > 1 && a.counters)
         splitk_fixup<64 * WM * WN>(a, t, m_lo, min(BM, m_end - m_lo), tn * BN, BN, (int *)st2);
+    if (a.pf) {
+        // the next conv's weights into L2 and the memory-side cache: the
+        // workgroups share them out in 1 KB wave loads into a stage buffer
+        // no longer read (after every wave's epilogue)
+        __builtin_amdgcn_s_barrier();
+        const uint64_t stride = (uint64_t)gridDim.x * gridDim.y * NW * 1024u;
+        for (uint64_t off = (((uint64_t)blockIdx.y * gridDim.x + blockIdx.x) * NW + wave) * 1024u + lane * 16u;
+             off + 16u <= a.pf_bytes; off += stride)
+            __builtin_amdgcn_global_load_lds((const void *)((const char *)a.pf + off),
+                                             (lds_u8 *)(st0 + wave * 1024), 16, 0, 0);
+        wait_vm<0>();
+    }
 }
 
 bool conv_dma_supported(const ConvArgs &a) {

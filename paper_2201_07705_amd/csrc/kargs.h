@@ -76,6 +76,9 @@ struct ConvArgs {
                           // for d = pixels per frame [0] and per row [1] of
                           // the output (of the pooled output with a fused
                           // pool)
+    const void *pf;       // or null: bytes [0, pf_bytes) read (into the
+    uint32_t pf_bytes;    // caches) once the tiles are done, the weights of
+    int32_t pf_pad;       // the conv that follows on the stream
     ConvSeg seg[GEMEL_MAX_SEG];
 };
 

@@ -1585,6 +1585,28 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
         }
     }
 
+    // ---- prefetch: each conv launch reads the weights of the next conv
+    // launch of its stream into the caches after its own tiles (resident,
+    // ungrouped weights; at most 16 MiB). Weights last read a round ago
+    // come from HBM, and the latency of those first reads holds up every
+    // early depth step of a launch with few steps in flight. ----
+    for (size_t i = 0; i < P.launches.size(); ++i) {
+        Launch &L = P.launches[i];
+        if (L.type != L_CONV_BF16) continue;
+        L.conv.pf = nullptr;
+        L.conv.pf_bytes = 0;
+        if (!ctx->opt.prefetch) continue;
+        for (size_t j = i + 1; j < P.launches.size(); ++j) {
+            const Launch &M = P.launches[j];
+            if (M.stream != L.stream || M.type != L_CONV_BF16) continue;
+            if (M.chunk < 0 && M.wblobs.empty() && !M.conv.grouped && M.conv.w) {
+                L.conv.pf = M.conv.w;
+                L.conv.pf_bytes = (uint32_t)std::min<int64_t>((int64_t)M.conv.N * M.conv.K * 2, 16 << 20) & ~15u;
+            }
+            break;
+        }
+    }
+
     // ---- dependencies of each launch (the edges of a graph round) ----
     {
         std::vector<std::vector<int>> tails((size_t)NS);  // launches that complete step i

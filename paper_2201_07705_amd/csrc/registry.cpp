@@ -672,6 +672,11 @@ gemel_status gemel_set_option(gemel_ctx *ctx, int32_t key, int64_t value) {
             drop_plans(ctx);
         }
         break;
+    case GEMEL_OPT_PREFETCH:
+        if (value != 0 && value != 1) return fail(ctx, GEMEL_EINVAL, "prefetch is 0 or 1");
+        ctx->opt.prefetch = (int)value;
+        drop_plans(ctx);
+        break;
     case GEMEL_OPT_SPLITK_FUSED:
         if (value < 0 || value > 2) return fail(ctx, GEMEL_EINVAL, "splitk_fused is 0, 1 or 2");
         ctx->opt.splitk_fused = (int)value;

@@ -43,7 +43,7 @@ OPT_USE_GRAPH, OPT_SWAP_SLOT_BYTES, OPT_SWAP_SLOTS, OPT_FAIL_COPY_AT, \
     OPT_CONV_SPLITS, OPT_STREAMS, OPT_GRAPH_DAG, OPT_FORK_US, \
     OPT_AUTOTUNE, OPT_SPLITK_FUSED, OPT_TUNE, OPT_FUSE_POOL, \
     OPT_MIXED_SIZES, OPT_PAIRED_ACTS, OPT_FAIL_ALLOC_AT, \
-    OPT_GROUP_UNMERGED, OPT_SWAP_CACHE = range(21)
+    OPT_GROUP_UNMERGED, OPT_SWAP_CACHE, OPT_PREFETCH = range(22)
 KERNEL_FAMILIES = ("conv_mfma", "conv_f32", "splitk_reduce", "fc", "pack",
                    "pool", "route", "export", "conv_merged")
 

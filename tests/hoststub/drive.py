@@ -52,7 +52,7 @@ def main():
     L.hipMalloc.restype = ctypes.c_int
     for f in ("hoststub_violations", "hoststub_launches", "hoststub_live_bytes",
               "hoststub_hazards", "hoststub_check_order", "hoststub_selftest",
-              "hoststub_allocs"):
+              "hoststub_allocs", "hoststub_prefetches"):
         getattr(L, f).restype = ctypes.c_long
     L.hoststub_set_capturing.argtypes = [ctypes.c_void_p]
     L.hoststub_set_capturing.restype = None
@@ -194,6 +194,7 @@ def main():
             "hazards": L.hoststub_hazards(),
             "violations": L.hoststub_violations(),
             "launches": L.hoststub_launches(),
+            "prefetches": L.hoststub_prefetches(),
             "last": L.hoststub_last().decode(),
         })
 

@@ -34,7 +34,7 @@
 namespace {
 std::mutex mu;
 std::map<uintptr_t, size_t> live;     // base -> bytes
-long violations = 0, launches = 0, hazards = 0, allocs = 0;
+long violations = 0, launches = 0, hazards = 0, allocs = 0, prefetches = 0;
 std::string last;
 
 bool inside(const void *p, size_t bytes) {
@@ -183,6 +183,7 @@ hipError_t verdict(bool ok) { return ok ? hipSuccess : hipErrorInvalidValue; }
 extern "C" {
 long hoststub_violations() { return violations; }
 long hoststub_launches() { return launches; }
+long hoststub_prefetches() { return prefetches; }
 long hoststub_allocs() { return allocs; }
 long hoststub_hazards() { return hazards; }
 const char *hoststub_last() { return last.c_str(); }
@@ -375,6 +376,10 @@ static hipError_t conv_common(const ConvArgs &a, int tile, int esz, const char *
         return hipErrorInvalidValue;
     }
     ok &= chk(a.w, (long long)a.N * a.K * esz, "weights", kern);
+    if (a.pf) {
+        ++prefetches;
+        ok &= a.pf_bytes > 0 && chk(a.pf, (long long)a.pf_bytes, "prefetched weights", kern);
+    }
     if (need_zero) ok &= chk(a.zero, GEMEL_ZERO_PAGE_BYTES, "zero page", kern);
     if (a.grouped && (!tile_is_dma(tile) || a.hetero)) {
         ++violations;

@@ -149,6 +149,19 @@ def test_all_groups_merged_still_batches_across_models(hostlib):
     assert merged["plan_launches"] < split["plan_launches"]
 
 
+def test_conv_launches_prefetch_the_next_conv_weights(hostlib):
+    """By default a conv launch names the weights of the next conv launch on
+    its stream as its prefetch region, checked like every other access (a
+    live allocation, in bounds); with OPT_PREFETCH 0 none does."""
+    kw = {"res": 64, "frames": 2}
+    on = drive(hostlib, "r50x2_vgg16x2", kw, {}, 1)
+    off = drive(hostlib, "r50x2_vgg16x2", kw, {"OPT_PREFETCH": 0}, 1)
+    for out in (on, off):
+        assert out["status"] == [0] and out["violations"] == 0 and out["hazards"] == 0, out["last"]
+    assert on["prefetches"] > 0 and off["prefetches"] == 0
+    assert on["launches"] == off["launches"]
+
+
 ESTATE, EDEVICE = -7, -6
 
 
