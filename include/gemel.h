@@ -403,9 +403,12 @@ enum {
                                    loaded into the cache                 */
     GEMEL_Q_ROUND_EVICTED_BYTES = 13, /* weight cache: bytes it evicted   */
     GEMEL_Q_CACHED_BYTES = 14,  /* weight cache: bytes cached after it    */
-    GEMEL_Q_CACHE_CAPACITY = 15 /* weight cache: its capacity (the weight
+    GEMEL_Q_CACHE_CAPACITY = 15,/* weight cache: its capacity (the weight
                                    budget minus the resident scale/shift
                                    vectors), 0 without the cache         */
+    GEMEL_Q_PREFETCHES = 16     /* conv launches of the last plan that
+                                   prefetch the next conv's weights
+                                   (GEMEL_OPT_PREFETCH)                  */
 };
 
 /* Read a counter. Errors: EINVAL (unknown key, null val). */
@@ -604,7 +607,9 @@ enum {
                                     budget keeps the largest blobs (merged
                                     ones first) resident and streams the
                                     rest through staging slots every round */
-    GEMEL_OPT_PREFETCH = 21      /* 1 (default): an LDS-DMA conv launch,
+    GEMEL_OPT_PREFETCH = 21      /* 1 (default): in a round that moves more
+                                    bytes than the GPU's 256 MiB memory-side
+                                    cache holds, an LDS-DMA conv launch,
                                     after its own tiles, reads the resident
                                     weights (up to 16 MiB) of the next conv
                                     launch of its stream into the L2 and
@@ -612,7 +617,7 @@ enum {
                                     depth loop starts on cache hits instead
                                     of HBM reads (ungrouped, resident
                                     weights only). Results are unchanged.
-                                    0: no prefetch                         */
+                                    2: in every round; 0: no prefetch      */
 };
 
 /* Set an option; takes effect at the next gemel_infer. Errors: EINVAL. */

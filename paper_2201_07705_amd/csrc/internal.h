@@ -225,7 +225,7 @@ struct Options {
     int paired_acts = 0;      // unmerged conv chains keep bf16 (hi, lo) pairs
     int group_unmerged = 1;   // same-shape unmerged convs of several models: one launch
     int swap_cache = 0;       // weights cached across rounds (with a budget)
-    int prefetch = 1;         // conv launches read the next conv's weights into the caches
+    int prefetch = 1;         // conv launches read the next conv's weights into the caches (2: in any round)
 };
 
 }  // namespace gemel

@@ -1587,15 +1587,21 @@ static gemel_status build_plan(gemel_ctx *ctx, const std::vector<int> &ids, cons
 
     // ---- prefetch: each conv launch reads the weights of the next conv
     // launch of its stream into the caches after its own tiles (resident,
-    // ungrouped weights; at most 16 MiB). Weights last read a round ago
-    // come from HBM, and the latency of those first reads holds up every
-    // early depth step of a launch with few steps in flight. ----
+    // ungrouped weights; at most 16 MiB). In a round that moves more bytes
+    // than the memory-side cache holds, weights last read a round ago come
+    // from HBM, and the latency of those first reads holds up every early
+    // depth step of a launch with few steps in flight. A smaller round
+    // finds its weights in that cache and would only pay for the reads. ----
+    constexpr double kMemSideCacheBytes = 256.0 * (1 << 20);
+    double round_bytes = 0;
+    for (const Launch &L : P.launches) round_bytes += L.bytes;
+    const bool prefetch = ctx->opt.prefetch == 2 || (ctx->opt.prefetch == 1 && round_bytes > kMemSideCacheBytes);
     for (size_t i = 0; i < P.launches.size(); ++i) {
         Launch &L = P.launches[i];
         if (L.type != L_CONV_BF16) continue;
         L.conv.pf = nullptr;
         L.conv.pf_bytes = 0;
-        if (!ctx->opt.prefetch) continue;
+        if (!prefetch) continue;
         for (size_t j = i + 1; j < P.launches.size(); ++j) {
             const Launch &M = P.launches[j];
             if (M.stream != L.stream || M.type != L_CONV_BF16) continue;

@@ -578,6 +578,13 @@ gemel_status gemel_query(gemel_ctx *ctx, int32_t key, int64_t *val) {
         break;
     }
     case GEMEL_Q_CACHE_CAPACITY: *val = (int64_t)ctx->cache_cap; break;
+    case GEMEL_Q_PREFETCHES: {
+        int64_t n = 0;
+        if (ctx->last_plan)
+            for (const Launch &L : ctx->last_plan->launches) n += L.type == L_CONV_BF16 && L.conv.pf ? 1 : 0;
+        *val = n;
+        break;
+    }
     default: return fail(ctx, GEMEL_EINVAL, "unknown query key");
     }
     return GEMEL_OK;
@@ -673,7 +680,7 @@ gemel_status gemel_set_option(gemel_ctx *ctx, int32_t key, int64_t value) {
         }
         break;
     case GEMEL_OPT_PREFETCH:
-        if (value != 0 && value != 1) return fail(ctx, GEMEL_EINVAL, "prefetch is 0 or 1");
+        if (value < 0 || value > 2) return fail(ctx, GEMEL_EINVAL, "prefetch is 0, 1 or 2");
         ctx->opt.prefetch = (int)value;
         drop_plans(ctx);
         break;

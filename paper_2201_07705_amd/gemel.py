@@ -37,7 +37,7 @@ Q_UNMERGED_BYTES, Q_MERGED_BYTES, Q_RESIDENT_BYTES, Q_PEAK_BYTES, \
     Q_STREAMED_BYTES, Q_ACTIVATION_BYTES, Q_LAUNCHES, Q_N_MODELS, \
     Q_GRAPH_REPLAYS, Q_STREAMS, Q_ROUND_MODE, Q_ROUND_TUNING, \
     Q_ROUND_LOADED_BYTES, Q_ROUND_EVICTED_BYTES, Q_CACHED_BYTES, \
-    Q_CACHE_CAPACITY = range(16)
+    Q_CACHE_CAPACITY, Q_PREFETCHES = range(17)
 OPT_USE_GRAPH, OPT_SWAP_SLOT_BYTES, OPT_SWAP_SLOTS, OPT_FAIL_COPY_AT, \
     OPT_SPLIT_MERGED, OPT_WEIGHT_BUDGET, OPT_PROFILE, OPT_CONV_TILE, \
     OPT_CONV_SPLITS, OPT_STREAMS, OPT_GRAPH_DAG, OPT_FORK_US, \

@@ -178,6 +178,7 @@ def main():
             "allocs": L.hoststub_allocs() - allocs_before,
             "error": L.gemel_last_error(ctx._h).decode(),
             "plan_launches": ctx.query(G.Q_LAUNCHES),
+            "plan_prefetches": ctx.query(G.Q_PREFETCHES),
             "arena": ctx.query(G.Q_ACTIVATION_BYTES),
             "streamed": ctx.query(G.Q_STREAMED_BYTES),
             "round_mode": ctx.query(G.Q_ROUND_MODE),

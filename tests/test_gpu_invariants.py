@@ -192,18 +192,24 @@ def test_fused_pool_equals_separate_pool(r50vgg, tile):
 @pytest.mark.parametrize("tile", [12, 18, 20], ids=["dma128x64", "dma64x64", "dma256x128w8"])
 def test_weight_prefetch_leaves_results_unchanged(r50vgg, tile):
     """Each LDS-DMA conv launch reads the next conv's weights into the caches
-    after its own tiles (2, 4 and 8 waves per workgroup here): the outputs
-    equal those of rounds without the prefetch bit for bit, on one stream,
-    on the round's streams as graph replays, and with split-K."""
+    after its own tiles (2, 4 and 8 waves per workgroup here; forced in every
+    round): the outputs equal those of rounds without the prefetch bit for
+    bit, on one stream, on the round's streams as graph replays, and with
+    split-K."""
     wl, params, frames = r50vgg
     log(f"weight prefetch tile {tile}")
     one = dict(OPT_CONV_TILE=tile, OPT_STREAMS=1, OPT_USE_GRAPH=0)
     ref = _run(wl, params, frames, OPT_PREFETCH=0, **one)
-    _same(ref, _run(wl, params, frames, **one))
-    _same(ref, _run(wl, params, frames, OPT_CONV_TILE=tile, repeat=3))
+    g = _pinned(wl, params, OPT_PREFETCH=2, **one)
+    try:
+        _same(ref, g.run(frames))
+        assert g.ctx.query(G.Q_PREFETCHES) > 0
+    finally:
+        g.close()
+    _same(ref, _run(wl, params, frames, OPT_CONV_TILE=tile, OPT_PREFETCH=2, repeat=3))
     sk = dict(OPT_CONV_TILE=tile, OPT_CONV_SPLITS=3, OPT_SPLITK_FUSED=2)
     _same(_run(wl, params, frames, OPT_PREFETCH=0, **sk),
-          _run(wl, params, frames, repeat=2, **sk))
+          _run(wl, params, frames, OPT_PREFETCH=2, repeat=2, **sk))
 
 
 def test_fused_pool_odd_sizes_and_default_plan():

@@ -150,15 +150,21 @@ def test_all_groups_merged_still_batches_across_models(hostlib):
 
 
 def test_conv_launches_prefetch_the_next_conv_weights(hostlib):
-    """By default a conv launch names the weights of the next conv launch on
-    its stream as its prefetch region, checked like every other access (a
-    live allocation, in bounds); with OPT_PREFETCH 0 none does."""
-    kw = {"res": 64, "frames": 2}
-    on = drive(hostlib, "r50x2_vgg16x2", kw, {}, 1)
-    off = drive(hostlib, "r50x2_vgg16x2", kw, {"OPT_PREFETCH": 0}, 1)
-    for out in (on, off):
+    """In a round that moves more bytes than the memory-side cache holds (2x
+    ResNet-50 + 2x VGG-16 at 224 px: about 2.1 GB), a conv launch names the
+    weights of the next conv launch on its stream as its prefetch region,
+    checked like every other access (a live allocation, in bounds); with
+    OPT_PREFETCH 0 none does, nor in a round that fits the cache (2x
+    ResNet-18, 4 frames each: about 176 MB) unless OPT_PREFETCH is 2."""
+    on = drive(hostlib, "r50x2_vgg16x2", {}, {}, 1)
+    off = drive(hostlib, "r50x2_vgg16x2", {}, {"OPT_PREFETCH": 0}, 1)
+    small = drive(hostlib, "resnet18x2", {}, {}, 1)
+    forced = drive(hostlib, "resnet18x2", {}, {"OPT_PREFETCH": 2}, 1)
+    for out in (on, off, small, forced):
         assert out["status"] == [0] and out["violations"] == 0 and out["hazards"] == 0, out["last"]
-    assert on["prefetches"] > 0 and off["prefetches"] == 0
+    assert on["prefetches"] > 0 and off["prefetches"] == 0 and small["prefetches"] == 0
+    assert on["plan_prefetches"] > 0 and off["plan_prefetches"] == 0 and small["plan_prefetches"] == 0
+    assert forced["plan_prefetches"] > 0
     assert on["launches"] == off["launches"]
 
 
